@@ -1,0 +1,284 @@
+"""Pins of the float64 oracle against facts fixed outside the oracle.
+
+Each test checks the oracle against something it does not compute itself:
+brute-force enumeration of every bracketing (the definitions of Sec. 2.1 and
+Eq. partial-derivative), closed forms (Catalan counts), invariants every
+marginal vector must satisfy, finite differences of log Z, and the worked
+CNF tree of Fig. 1b.  A dropped term, a wrong sign or index, or a transposed
+operand anywhere in the oracle breaks at least one of them.
+"""
+import math
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+from oracle import bruteforce as bf
+from oracle import oracle as orc
+from paper_2008_03736_amd import workloads as W
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def catalan(m):
+    return math.comb(2 * m, m) // (m + 1)
+
+
+def _one(n, s_dense):
+    """Wrap one sentence's dense score matrix as a batch of 1."""
+    n1 = n + 1
+    sc = np.full((1, n1, n1), np.nan, np.float32)
+    for i in range(n):
+        for j in range(i + 1, n + 1):
+            sc[0, i, j] = s_dense[i][j]
+    return sc, np.array([n], np.int32)
+
+
+def _valid_cells(n):
+    return [(i, j) for i in range(n) for j in range(i + 1, n + 1)]
+
+
+# --------------------------------------------------------------------------
+# Brute force over all C_{n-1} bracketings (n <= 8)
+
+
+@pytest.mark.parametrize("n", [1, 2, 3, 4, 5, 6, 7, 8])
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_bruteforce_logz_marginals_argmax(n, seed):
+    b = W.custom([n], seed=seed, sd=1.5)
+    s = b.scores[0]
+    lz_bf = bf.log_z(s, n)
+    mu_bf = bf.marginals(s, n)
+    best_bf, tree_bf = bf.best_tree(s, n)
+
+    lz = orc.logz(b.scores, b.lengths)[0]
+    assert abs(lz - lz_bf) <= 1e-12 * max(1.0, abs(lz_bf))
+    for method in ("adjoint", "outside"):
+        lz2, mu = orc.marginals(b.scores, b.lengths, method=method)
+        assert abs(lz2[0] - lz_bf) <= 1e-12 * max(1.0, abs(lz_bf))
+        for (i, j), v in mu_bf.items():
+            assert abs(mu[0, i, j] - v) <= 1e-12, (method, i, j)
+    spans, best = orc.cky(b.scores, b.lengths)
+    assert [tuple(r) for r in spans[0, : 2 * n - 1]] == tree_bf
+    assert (spans[0, 2 * n - 1:] == -1).all()
+    assert abs(best[0] - best_bf) <= 1e-12 * max(1.0, abs(best_bf))
+
+
+def test_bruteforce_tree_counts_are_catalan():
+    # |T(x)| = C_{n-1}: the enumerator itself is checked against the closed form.
+    for n in range(1, 10):
+        assert sum(1 for _ in bf.trees(0, n)) == catalan(n - 1)
+        for spans, splits in bf.trees(0, n):
+            assert len(spans) == 2 * n - 1 and len(splits) == n - 1
+            assert (0, n) in spans and all((i, i + 1) in spans for i in range(n))
+
+
+@pytest.mark.parametrize("n", [2, 3, 4, 5, 6, 7, 8])
+def test_cky_ties_lowest_split(n):
+    # Integer scores make many trees tie exactly; the oracle's DP (lowest k at
+    # every node) must return the optimal tree whose preorder split sequence is
+    # lexicographically smallest.
+    for seed in range(40):
+        b = W.custom([n], seed=100 + seed, integer=(-1, 1))
+        best_bf, tree_bf = bf.best_tree(b.scores[0], n)
+        spans, best = orc.cky(b.scores, b.lengths)
+        assert [tuple(r) for r in spans[0, : 2 * n - 1]] == tree_bf, seed
+        assert best[0] == best_bf
+
+
+@pytest.mark.parametrize("n", [1, 2, 3, 4])
+def test_bruteforce_labeled(n):
+    L = 3
+    b = W.custom([n], seed=7 + n, sd=1.0, labels=L)
+    lz_bf, mu_bf = bf.labeled(b.scores[0], n, L)
+    lz, mu = orc.labeled(b.scores, b.lengths)
+    assert abs(lz[0] - lz_bf) <= 1e-12 * max(1.0, abs(lz_bf))
+    for (i, j, l), v in mu_bf.items():
+        assert abs(mu[0, i, j, l] - v) <= 1e-12
+
+
+# --------------------------------------------------------------------------
+# Closed forms at sizes brute force cannot reach
+
+
+@pytest.mark.parametrize("n", [1, 2, 3, 10, 57, 140, 256])
+def test_zero_scores_logz_is_log_catalan(n):
+    b = W.custom([n], sd=0.0)
+    lz = orc.logz(b.scores, b.lengths)[0]
+    assert abs(lz - math.log(catalan(n - 1))) <= 1e-12 * max(1.0, math.log(catalan(n - 1)))
+
+
+@pytest.mark.parametrize("n,c", [(5, 0.75), (40, -1.25), (200, 2.0)])
+def test_constant_scores_logz(n, c):
+    # every tree has 2n-1 spans, so log Z = (2n-1)c + ln C_{n-1}
+    sc = np.full((1, n + 1, n + 1), np.float32(c))
+    lz = orc.logz(sc, [n])[0]
+    ref = (2 * n - 1) * c + math.log(catalan(n - 1))
+    assert abs(lz - ref) <= 1e-12 * max(1.0, abs(ref))
+
+
+@pytest.mark.parametrize("n", [5, 20, 60])
+def test_zero_scores_marginals_closed_form(n):
+    # trees containing (i,j) of width w: C_{w-1} inside times C_{n-w} outside
+    b = W.custom([n], sd=0.0)
+    _, mu = orc.marginals(b.scores, b.lengths)
+    for i, j in _valid_cells(n):
+        w = j - i
+        ref = float(Fraction(catalan(w - 1) * catalan(n - w), catalan(n - 1)))
+        assert abs(mu[0, i, j] - ref) <= 1e-12, (i, j)
+
+
+@pytest.mark.parametrize("n", [2, 9, 100, 256])
+def test_zero_scores_cky_right_branching(n):
+    # all trees tie; the lowest split at every node gives {(i,n)} + {(i,i+1)}
+    b = W.custom([n], sd=0.0)
+    spans, best = orc.cky(b.scores, b.lengths)
+    exp = []
+    for i in range(n - 1):
+        exp += [(i, n), (i, i + 1)]
+    exp.append((n - 1, n))
+    assert [tuple(r) for r in spans[0, : 2 * n - 1]] == exp
+    assert best[0] == 0.0
+
+
+# --------------------------------------------------------------------------
+# Invariants on workload-shaped inputs
+
+
+def _invariants(b, mu, lz, best, atol):
+    for bi, n in enumerate(b.lengths):
+        n = int(n)
+        m = mu[bi]
+        tri = np.array([m[i, j] for i, j in _valid_cells(n)])
+        assert np.all(tri >= -atol) and np.all(tri <= 1 + atol)
+        assert abs(m[0, n] - 1.0) <= atol
+        assert all(abs(m[i, i + 1] - 1.0) <= atol for i in range(n))
+        assert abs(tri.sum() - (2 * n - 1)) <= atol * n * n
+        # the best tree is one term of Z, and Z has C_{n-1} terms
+        assert best[bi] <= lz[bi] + 1e-9 * abs(lz[bi])
+        assert lz[bi] <= best[bi] + math.log(catalan(n - 1)) + 1e-9 * abs(lz[bi])
+
+
+def test_invariants_tiny_workload():
+    b = W.make("tiny")
+    lz, mu = orc.marginals(b.scores, b.lengths, threads=4)
+    _, best = orc.cky(b.scores, b.lengths, threads=4)
+    _invariants(b, mu, lz, best, 1e-10)
+
+
+def test_invariants_near_forbidden_spans():
+    # stress-style scores (sd 3, 5% of spans at -1e4) at a size the oracle
+    # finishes quickly
+    b = W.custom([1, 2, 3, 17, 64], seed=3, sd=3.0, forbid=0.05)
+    lz, mu = orc.marginals(b.scores, b.lengths)
+    _, best = orc.cky(b.scores, b.lengths)
+    _invariants(b, mu, lz, best, 1e-9)
+
+
+def test_outside_and_adjoint_agree():
+    b = W.custom([31, 47, 60], seed=11, sd=2.0)
+    lz1, mu1 = orc.marginals(b.scores, b.lengths, method="adjoint")
+    lz2, mu2 = orc.marginals(b.scores, b.lengths, method="outside")
+    assert np.array_equal(lz1, lz2)
+    v = W.valid_mask(b.lengths, b.n1)
+    assert np.max(np.abs(mu1[v] - mu2[v])) <= 1e-12
+
+
+def test_finite_differences():
+    # d log Z / d s(i,j) by central differences of the float64 log Z
+    n = 12
+    rng = np.random.default_rng(5)
+    s = rng.standard_normal((n + 1, n + 1))
+    _, mu = orc.marginals(*_one(n, s))
+
+    def lz_of(s2):
+        sc, ln = _one(n, s2)
+        return orc.logz(sc.astype(np.float32), ln)[0]
+
+    # float32 storage of the perturbed score limits h; use h that is exact in f32
+    h = 2.0 ** -10
+    for i, j in [(0, 12), (0, 1), (3, 9), (5, 6), (2, 11), (7, 12)]:
+        base = np.float32(s[i][j])
+        sp = s.copy(); sp[i][j] = float(base) + h
+        sm = s.copy(); sm[i][j] = float(base) - h
+        s0 = s.copy(); s0[i][j] = float(base)
+        fd = (lz_of(sp) - lz_of(sm)) / (2 * h)
+        _, mu0 = orc.marginals(*_one(n, s0))
+        assert abs(fd - mu0[0, i, j]) <= 2e-7, (i, j, fd, mu0[0, i, j])
+
+
+def test_forced_span_shift_identity():
+    # every tree holds all width-1 spans and the root: shifting those scores
+    # shifts log Z by the total shift and leaves every marginal unchanged
+    b = W.custom([23], seed=9, sd=2.0)
+    n = 23
+    lz0, mu0 = orc.marginals(b.scores, b.lengths)
+    sc = b.scores.copy()
+    for i in range(n):
+        sc[0, i, i + 1] += np.float32(0.5)
+    sc[0, 0, n] += np.float32(-1.5)
+    lz1, mu1 = orc.marginals(sc, b.lengths)
+    shift = sum(float(sc[0, i, i + 1]) - float(b.scores[0, i, i + 1]) for i in range(n))
+    shift += float(sc[0, 0, n]) - float(b.scores[0, 0, n])
+    assert abs(lz1[0] - lz0[0] - shift) <= 1e-12 * abs(lz0[0])
+    v = W.valid_mask(b.lengths, b.n1)
+    assert np.max(np.abs(mu1[v] - mu0[v])) <= 1e-12
+
+
+def test_upstream_gradient_scales_marginals():
+    b = W.custom([15, 8], seed=4, sd=1.0)
+    g = np.array([2.5, -0.75])
+    _, mu1 = orc.marginals(b.scores, b.lengths)
+    _, mug = orc.marginals(b.scores, b.lengths, grad=g)
+    v = W.valid_mask(b.lengths, b.n1)
+    ref = (mu1 * g[:, None, None])[v]
+    assert np.max(np.abs(mug[v] - ref)) <= 1e-12
+
+
+def test_labeled_sums_to_unlabeled():
+    # sum_l p((i,j,l)|x) = p((i,j)|x) of the label-reduced scores, and the
+    # reduction is log-sum-exp over labels
+    b = W.custom([9, 14], seed=2, sd=1.0, labels=5)
+    lz, mu4 = orc.labeled(b.scores, b.lengths)
+    red = np.log(np.exp(b.scores.astype(np.float64)).sum(-1))
+    lz2, mu = orc.marginals(red.astype(np.float32), b.lengths)
+    v = W.valid_mask(b.lengths, b.n1)
+    assert np.max(np.abs(mu4.sum(-1)[v] - mu[v])) <= 1e-6
+    assert np.max(np.abs(lz - lz2)) <= 1e-5
+
+
+# --------------------------------------------------------------------------
+# Worked example: the CNF tree of Fig. 1b
+
+
+def _read_fig1b():
+    rows = []
+    with open(os.path.join(GOLDEN, "fig1b_cnf_tree.txt")) as f:
+        for line in f:
+            if line.startswith("#") or not line.strip():
+                continue
+            i, j, _lab = line.split()
+            rows.append((int(i), int(j)))
+    return rows
+
+
+def test_fig1b_tree_is_decoded_and_dominates():
+    gold = _read_fig1b()
+    n = 5
+    assert len(gold) == 2 * n - 1
+    rng = np.random.default_rng(0)
+    s = 0.1 * rng.standard_normal((n + 1, n + 1))
+    for i, j in gold:
+        s[i][j] += 4.0
+    sc, ln = _one(n, s)
+    spans, best = orc.cky(sc, ln)
+    assert [tuple(r) for r in spans[0, : 2 * n - 1]] == gold
+    assert abs(best[0] - sum(float(sc[0, i, j]) for i, j in gold)) <= 1e-12
+    _, mu = orc.marginals(sc, ln)
+    gold_set = set(gold)
+    for i, j in _valid_cells(n):
+        if (i, j) in gold_set:
+            assert mu[0, i, j] > 0.95
+        else:
+            assert mu[0, i, j] < 0.05
