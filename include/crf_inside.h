@@ -1,0 +1,154 @@
+/*
+ * crf_inside.h -- C ABI of the MI355X (gfx950) batched tree-CRF library.
+ *
+ * Method: Zhang, Zhou & Li, "Fast and Accurate Neural CRF Constituency
+ * Parsing" (IJCAI 2020).  For every sentence of a batch, given span scores
+ * s(i,j), the library computes
+ *   - log Z(x), the log partition function over all binary bracketings
+ *     (Sec. 2.1, Eq. tree-prob), by the inside recursion of Sec. 3.1
+ *     (Algorithm 1);
+ *   - the span marginals p((i,j)|x) = d log Z / d s(i,j) (Sec. 3.2,
+ *     Eq. partial-derivative) by differentiating that recursion in reverse;
+ *   - the 1-best tree argmax_y s(x,y) (Sec. 2.1, Eq. tree-argmax) by CKY,
+ *     the same recursion with max in place of sum (Sec. 3.3);
+ *   - for the one-stage labelled CRF (Sec. 4.2, Eq. tree-label-score),
+ *     log Z and the per-label span marginals p((i,j,l)|x).
+ *
+ * Conventions
+ *   Fence posts.  A sentence of n words has boundaries 0..n; span (i,j),
+ *   0 <= i < j <= n, covers words i..j-1 (the paper's inclusive (i, j-1)).
+ *   Every legal tree contains all n width-1 spans and the root (0,n) and has
+ *   2n-1 spans in all (Sec. 2.1; Fig. 1b); width-1 spans are scored.
+ *
+ *   Layout.  scores is float32, row-major [B][N1][N1] (unlabelled) or
+ *   [B][N1][N1][L] (labelled), N1 = the padded side (>= max length + 1).
+ *   s(i,j) of sentence b is scores[(b*N1 + i)*N1 + j] (times L, plus l, when
+ *   labelled).  Only cells 0 <= i < j <= n_b are read; every other cell may
+ *   hold anything, NaN included.  marginals has the layout of scores and only
+ *   its valid cells are written: the rest of the buffer is left untouched.
+ *   Outputs are in the caller's sentence order.
+ *
+ *   Memory.  Every float/int pointer passed to a compute call is device memory
+ *   owned by the caller; the library never frees it.  lengths_host in
+ *   crf_plan_create is host memory, read only during the call.  The plan owns
+ *   its device copies of the lengths and schedule and a workspace for
+ *   sentences whose chart does not fit in LDS; they are allocated by
+ *   crf_plan_create and freed by crf_plan_destroy.  Compute calls allocate
+ *   nothing.
+ *
+ *   Streams.  `stream` is a hipStream_t (NULL = the null stream).  Compute
+ *   calls only enqueue work and never synchronise.  Calls on one plan may run
+ *   concurrently on different streams, except that two calls touching
+ *   sentences that use the workspace (crf_plan_info: spill_count > 0) race.
+ *
+ *   Errors.  Every call returns a status (CRF_OK = 0).  Arguments are checked
+ *   on the host before any HIP call is made, so a rejected call has no effect
+ *   on the device.  crf_last_error() gives a message for the last failure on
+ *   the calling thread.  Scores must be finite inside the valid region; NaN
+ *   or infinities there give unspecified (but memory-safe) results.
+ */
+#ifndef CRF_INSIDE_H
+#define CRF_INSIDE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+    CRF_OK = 0,
+    CRF_EINVAL = 1,        /* bad argument: null pointer, size or length out of range */
+    CRF_ENOMEM = 2,        /* host or device allocation failed (crf_plan_create only) */
+    CRF_EHIP = 3,          /* HIP runtime or launch error (see crf_last_error) */
+    CRF_EUNSUPPORTED = 4   /* valid but not implemented, e.g. decode of labelled scores */
+};
+
+#define CRF_MAX_LEN 1023      /* longest sentence, in words */
+#define CRF_MAX_LABELS 4096   /* most labels per span */
+
+/* Plan flags. */
+#define CRF_FORCE_SPILL 0x1u  /* run every sentence on the workspace-chart kernels */
+
+typedef struct crf_plan crf_plan;
+
+typedef struct {
+    int32_t batch;           /* B */
+    int32_t n1;              /* padded side N1 */
+    int32_t num_labels;      /* L (1 = unlabelled) */
+    int32_t max_len;         /* longest sentence */
+    int32_t lds_count;       /* sentences whose chart lives in LDS */
+    int32_t spill_count;     /* sentences whose chart lives in the workspace */
+    int64_t workspace_bytes; /* device workspace owned by the plan */
+    int32_t lds_bytes_inside;/* dynamic LDS per workgroup, inside kernels */
+    int32_t lds_bytes_cky;   /* dynamic LDS per workgroup, CKY kernel */
+} crf_plan_stats;
+
+/*
+ * crf_plan_create -- validate a batch shape and build its schedule.
+ *   out          receives the plan (set to NULL on failure).
+ *   lengths_host host int32[batch]: sentence lengths n_b, 1 <= n_b <= n1-1.
+ *   batch        B >= 1.
+ *   n1           padded side of the score block, 2 <= n1 <= CRF_MAX_LEN+1.
+ *   num_labels   L, 1 <= L <= CRF_MAX_LABELS; 1 = unlabelled scores.
+ *   flags        0 or CRF_FORCE_SPILL.
+ * Uses the current HIP device; later calls must run with that device current.
+ * Returns CRF_EINVAL (nothing allocated), CRF_ENOMEM or CRF_EHIP.
+ */
+int crf_plan_create(crf_plan **out, const int32_t *lengths_host, int32_t batch, int32_t n1,
+                    int32_t num_labels, uint32_t flags);
+
+/* Free a plan and its device memory (NULL is accepted).  Synchronises the
+ * device first so that no enqueued call still uses it. */
+int crf_plan_destroy(crf_plan *plan);
+
+/* Sizes and schedule summary of a plan (host only, no HIP call). */
+int crf_plan_info(const crf_plan *plan, crf_plan_stats *out);
+
+/*
+ * crf_inside_fwd -- log partition function (Sec. 2.1, Eq. tree-prob; Sec. 3.1,
+ * Algorithm 1).
+ *   scores  device float32, layout above.
+ *   logZ    device float32[B]: log Z(x_b).
+ */
+int crf_inside_fwd(const crf_plan *plan, const float *scores, float *logZ, void *stream);
+
+/*
+ * crf_inside_bwd -- span marginals as the gradient of log Z (Sec. 3.2,
+ * Eq. partial-derivative).  The inside chart is recomputed on chip.
+ *   grad_logZ  device float32[B] upstream gradient, or NULL for all ones.
+ *   marginals  device float32, layout of scores: grad_logZ[b] * p((i,j)|x_b)
+ *              (labelled: grad_logZ[b] * p((i,j,l)|x_b)) on valid cells only.
+ */
+int crf_inside_bwd(const crf_plan *plan, const float *scores, const float *grad_logZ,
+                   float *marginals, void *stream);
+
+/* crf_inside_fwd_bwd -- both of the above in one pass over the chart.
+ * logZ may be NULL. */
+int crf_inside_fwd_bwd(const crf_plan *plan, const float *scores, const float *grad_logZ,
+                       float *logZ, float *marginals, void *stream);
+
+/*
+ * crf_cky_decode -- 1-best unlabelled tree (Sec. 2.1, Eq. tree-argmax) by CKY
+ * (Sec. 3.3).  The chart is float64: beta(i,i+1) = s(i,i+1),
+ * beta(i,j) = (max_k (beta(i,k) + beta(k,j))) + s(i,j); among equal maxima
+ * the lowest split k is kept.
+ *   spans  device int32[B][2*(N1-1)-1][2]: the 2n_b-1 spans (i,j) of the tree
+ *          in preorder (i ascending, then j descending), then rows of -1.
+ *   best   device float32[B] score of that tree, or NULL.
+ * Unlabelled plans only (CRF_EUNSUPPORTED otherwise).
+ */
+int crf_cky_decode(const crf_plan *plan, const float *scores, int32_t *spans, float *best,
+                   void *stream);
+
+/* Static description of a status code. */
+const char *crf_status_string(int status);
+
+/* Message for the last failing call on this thread ("" if none). */
+const char *crf_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CRF_INSIDE_H */

@@ -61,18 +61,25 @@ def logz(scores, lengths, threads=1):
     return out
 
 
-def marginals(scores, lengths, grad=None, method="adjoint", threads=1):
+def marginals(scores, lengths, grad=None, method="adjoint", threads=1, out=None):
     """(log Z [B], marginals [B,N1,N1]) in float64.
 
     ``method='adjoint'`` differentiates the inside recursion (Sec. 3.2);
     ``method='outside'`` runs the classical log-space outside pass.  The two
-    are independent derivations of Eq. partial-derivative.
+    are independent derivations of Eq. partial-derivative.  ``out`` may supply
+    a float64 [B,N1,N1] buffer for the marginals (its invalid cells are left
+    as they are).
     """
     s, n = _prep(scores, lengths)
     B, ld = s.shape[0], s.shape[1]
     g = None if grad is None else np.ascontiguousarray(grad, dtype=np.float64)
     lz = np.empty(B, np.float64)
-    mu = np.full((B, ld, ld), np.nan, np.float64)
+    if out is None:
+        mu = np.full((B, ld, ld), np.nan, np.float64)
+    else:
+        if out.shape != (B, ld, ld) or out.dtype != np.float64 or not out.flags.c_contiguous:
+            raise ValueError("out must be a C-contiguous float64 [B, N1, N1] array")
+        mu = out
     code = {"adjoint": 0, "outside": 1}[method]
     _check(lib().orc_marginals(B, ld, _ptr(n), _ptr(s), _ptr(g), _ptr(lz), _ptr(mu), code, threads))
     return lz, mu

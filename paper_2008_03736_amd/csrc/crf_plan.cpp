@@ -1,0 +1,294 @@
+// crf_plan.cpp -- host side of the C ABI: argument checks, the per-batch
+// schedule and the plan's device memory.
+//
+// Scheduling.  Sentences are independent (Algorithm 1 parallelises over the
+// batch), and a sentence's cost grows as its number of split points,
+// T(n) = (n+1) n (n-1) / 6, plus a latency term per width step.  Workgroups
+// are dispatched in blockIdx order, so the sentence list is sorted by
+// decreasing length: the longest dependency chains start first and short
+// sentences fill the tail (longest-processing-time-first).
+#include <hip/hip_runtime_api.h>
+
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <new>
+#include <numeric>
+#include <vector>
+
+#include "../../include/crf_inside.h"
+#include "crf_internal.h"
+
+namespace {
+
+thread_local char g_last_error[256] = "";
+
+int fail(int code, const char *fmt, ...) __attribute__((format(printf, 2, 3)));
+int fail(int code, const char *fmt, ...) {
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_last_error, sizeof g_last_error, fmt, ap);
+    va_end(ap);
+    return code;
+}
+
+int ok() {
+    g_last_error[0] = '\0';
+    return CRF_OK;
+}
+
+int hip_fail(hipError_t e, const char *where) {
+    return fail(CRF_EHIP, "%s: %s", where, hipGetErrorString(e));
+}
+
+}  // namespace
+
+struct crf_plan {
+    int device = -1;
+    int32_t B = 0, n1 = 0, L = 1, max_len = 0;
+    uint32_t flags = 0;
+    std::vector<void *> allocations;
+    crf::KernelPlan kp{};
+    int64_t ws_bytes = 0;
+};
+
+namespace {
+
+void release(crf_plan *p) {
+    for (void *a : p->allocations) (void)hipFree(a);
+    p->allocations.clear();
+}
+
+template <typename T>
+hipError_t upload(crf_plan *p, const std::vector<T> &v, const T **dst) {
+    *dst = nullptr;
+    if (v.empty()) return hipSuccess;
+    void *d = nullptr;
+    hipError_t e = hipMalloc(&d, v.size() * sizeof(T));
+    if (e != hipSuccess) return e;
+    p->allocations.push_back(d);
+    e = hipMemcpy(d, v.data(), v.size() * sizeof(T), hipMemcpyHostToDevice);
+    *dst = static_cast<const T *>(d);
+    return e;
+}
+
+// Split the (already ordered) sentence list into LDS and workspace runs for
+// a chart of `bytes(n)` bytes, and lay out the workspace charts.
+struct HostSchedule {
+    std::vector<int32_t> lds, spill;
+    std::vector<int64_t> off;
+    int32_t lds_bytes = 0;
+    int64_t ws_bytes = 0;
+};
+
+template <typename F>
+HostSchedule split(const std::vector<int32_t> &order, const int32_t *len, int64_t lds_cap,
+                   bool force_spill, int64_t ws_base, F bytes) {
+    HostSchedule s;
+    int64_t cursor = ws_base;
+    for (int32_t b : order) {
+        const int64_t need = bytes(len[b]);
+        if (!force_spill && need <= lds_cap && len[b] <= crf::kMaxLenLds) {
+            s.lds.push_back(b);
+            s.lds_bytes = std::max<int32_t>(s.lds_bytes, (int32_t)need);
+        } else {
+            s.spill.push_back(b);
+            s.off.push_back(cursor);
+            cursor += (need + 255) / 256 * 256;
+        }
+    }
+    s.ws_bytes = cursor - ws_base;
+    return s;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *crf_status_string(int status) {
+    switch (status) {
+        case CRF_OK: return "success";
+        case CRF_EINVAL: return "invalid argument";
+        case CRF_ENOMEM: return "out of memory";
+        case CRF_EHIP: return "HIP runtime error";
+        case CRF_EUNSUPPORTED: return "unsupported";
+        default: return "unknown status";
+    }
+}
+
+const char *crf_last_error(void) { return g_last_error; }
+
+int crf_plan_create(crf_plan **out, const int32_t *lengths_host, int32_t batch, int32_t n1,
+                    int32_t num_labels, uint32_t flags) {
+    if (out == nullptr) return fail(CRF_EINVAL, "out is NULL");
+    *out = nullptr;
+    if (lengths_host == nullptr) return fail(CRF_EINVAL, "lengths_host is NULL");
+    if (batch < 1) return fail(CRF_EINVAL, "batch %d < 1", batch);
+    if (n1 < 2 || n1 > CRF_MAX_LEN + 1)
+        return fail(CRF_EINVAL, "n1 %d outside [2, %d]", n1, CRF_MAX_LEN + 1);
+    if (num_labels < 1 || num_labels > CRF_MAX_LABELS)
+        return fail(CRF_EINVAL, "num_labels %d outside [1, %d]", num_labels, CRF_MAX_LABELS);
+    if (flags & ~CRF_FORCE_SPILL) return fail(CRF_EINVAL, "unknown flags 0x%x", flags);
+    int32_t max_len = 0;
+    for (int32_t b = 0; b < batch; ++b) {
+        const int32_t n = lengths_host[b];
+        if (n < 1 || n > n1 - 1)
+            return fail(CRF_EINVAL, "lengths[%d] = %d outside [1, n1-1 = %d]", b, n, n1 - 1);
+        max_len = std::max(max_len, n);
+    }
+
+    // Arguments are valid: from here on HIP calls are made.
+    crf_plan *p = new (std::nothrow) crf_plan();
+    if (p == nullptr) return fail(CRF_ENOMEM, "host allocation of the plan failed");
+    p->B = batch;
+    p->n1 = n1;
+    p->L = num_labels;
+    p->max_len = max_len;
+    p->flags = flags;
+
+    hipError_t e = hipGetDevice(&p->device);
+    if (e != hipSuccess) { delete p; return hip_fail(e, "hipGetDevice"); }
+    int lds_cap = 0;
+    e = hipDeviceGetAttribute(&lds_cap, hipDeviceAttributeMaxSharedMemoryPerBlock, p->device);
+    if (e != hipSuccess) { delete p; return hip_fail(e, "hipDeviceGetAttribute"); }
+    // Static LDS of the kernels (reduction scratch) comes out of the same budget.
+    const int64_t lds_avail = (int64_t)lds_cap - 64;
+
+    // Longest first; ties keep batch order.
+    std::vector<int32_t> order(batch);
+    std::iota(order.begin(), order.end(), 0);
+    std::stable_sort(order.begin(), order.end(),
+                     [&](int32_t a, int32_t b) { return lengths_host[a] > lengths_host[b]; });
+
+    const bool force = (flags & CRF_FORCE_SPILL) != 0;
+    HostSchedule si = split(order, lengths_host, lds_avail, force, 0,
+                            [](int n) { return crf::inside_chart_bytes(n); });
+    HostSchedule sc = split(order, lengths_host, lds_avail, force, si.ws_bytes,
+                            [](int n) { return crf::cky_chart_bytes(n); });
+    p->ws_bytes = si.ws_bytes + sc.ws_bytes;
+
+    std::vector<int32_t> len(lengths_host, lengths_host + batch);
+    crf::KernelPlan &kp = p->kp;
+    kp.B = batch;
+    kp.n1 = n1;
+    kp.L = num_labels;
+    kp.inside.n_lds = (int32_t)si.lds.size();
+    kp.inside.n_spill = (int32_t)si.spill.size();
+    kp.inside.lds_bytes = si.lds_bytes;
+    kp.cky.n_lds = (int32_t)sc.lds.size();
+    kp.cky.n_spill = (int32_t)sc.spill.size();
+    kp.cky.lds_bytes = sc.lds_bytes;
+
+    if ((e = upload(p, len, &kp.len)) != hipSuccess ||
+        (e = upload(p, si.lds, &kp.inside.order_lds)) != hipSuccess ||
+        (e = upload(p, si.spill, &kp.inside.order_spill)) != hipSuccess ||
+        (e = upload(p, si.off, &kp.inside.ws_off)) != hipSuccess ||
+        (e = upload(p, sc.lds, &kp.cky.order_lds)) != hipSuccess ||
+        (e = upload(p, sc.spill, &kp.cky.order_spill)) != hipSuccess ||
+        (e = upload(p, sc.off, &kp.cky.ws_off)) != hipSuccess) {
+        const int code = (e == hipErrorOutOfMemory) ? CRF_ENOMEM : CRF_EHIP;
+        release(p);
+        delete p;
+        return code == CRF_ENOMEM ? fail(code, "device allocation of the schedule failed")
+                                  : hip_fail(e, "schedule upload");
+    }
+    kp.ws = nullptr;
+    if (p->ws_bytes > 0) {
+        void *ws = nullptr;
+        e = hipMalloc(&ws, (size_t)p->ws_bytes);
+        if (e != hipSuccess) {
+            release(p);
+            delete p;
+            return fail(CRF_ENOMEM, "workspace of %lld bytes: %s", (long long)p->ws_bytes,
+                        hipGetErrorString(e));
+        }
+        p->allocations.push_back(ws);
+        kp.ws = static_cast<char *>(ws);
+    }
+    // Best effort: ROCm launches with any dynamic LDS up to the per-block
+    // limit without this attribute; a real shortfall surfaces as a launch error.
+    if (crf::set_kernel_attributes(std::max(si.lds_bytes, sc.lds_bytes)) != hipSuccess)
+        (void)hipGetLastError();
+    *out = p;
+    return ok();
+}
+
+int crf_plan_destroy(crf_plan *plan) {
+    if (plan == nullptr) return ok();
+    int dev = -1;
+    (void)hipGetDevice(&dev);
+    if (dev != plan->device) (void)hipSetDevice(plan->device);
+    hipError_t e = hipDeviceSynchronize();
+    release(plan);
+    if (dev >= 0 && dev != plan->device) (void)hipSetDevice(dev);
+    delete plan;
+    if (e != hipSuccess) return hip_fail(e, "hipDeviceSynchronize");
+    return ok();
+}
+
+int crf_plan_info(const crf_plan *plan, crf_plan_stats *out) {
+    if (plan == nullptr || out == nullptr) return fail(CRF_EINVAL, "NULL argument");
+    out->batch = plan->B;
+    out->n1 = plan->n1;
+    out->num_labels = plan->L;
+    out->max_len = plan->max_len;
+    out->lds_count = plan->kp.inside.n_lds;
+    out->spill_count = plan->kp.inside.n_spill;
+    out->workspace_bytes = plan->ws_bytes;
+    out->lds_bytes_inside = plan->kp.inside.lds_bytes;
+    out->lds_bytes_cky = plan->kp.cky.lds_bytes;
+    return ok();
+}
+
+static int check_device(const crf_plan *plan) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    if (dev != plan->device)
+        return fail(CRF_EINVAL, "plan was created on device %d, current device is %d",
+                    plan->device, dev);
+    return CRF_OK;
+}
+
+int crf_inside_fwd(const crf_plan *plan, const float *scores, float *logZ, void *stream) {
+    if (plan == nullptr) return fail(CRF_EINVAL, "plan is NULL");
+    if (scores == nullptr || logZ == nullptr) return fail(CRF_EINVAL, "scores/logZ is NULL");
+    int rc = check_device(plan);
+    if (rc != CRF_OK) return rc;
+    hipError_t e = crf::launch_inside(plan->kp, scores, nullptr, logZ, nullptr,
+                                      static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? ok() : hip_fail(e, "crf_inside_fwd launch");
+}
+
+int crf_inside_fwd_bwd(const crf_plan *plan, const float *scores, const float *grad_logZ,
+                       float *logZ, float *marginals, void *stream) {
+    if (plan == nullptr) return fail(CRF_EINVAL, "plan is NULL");
+    if (scores == nullptr || marginals == nullptr)
+        return fail(CRF_EINVAL, "scores/marginals is NULL");
+    int rc = check_device(plan);
+    if (rc != CRF_OK) return rc;
+    hipError_t e = crf::launch_inside(plan->kp, scores, grad_logZ, logZ, marginals,
+                                      static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? ok() : hip_fail(e, "crf_inside_fwd_bwd launch");
+}
+
+int crf_inside_bwd(const crf_plan *plan, const float *scores, const float *grad_logZ,
+                   float *marginals, void *stream) {
+    return crf_inside_fwd_bwd(plan, scores, grad_logZ, nullptr, marginals, stream);
+}
+
+int crf_cky_decode(const crf_plan *plan, const float *scores, int32_t *spans, float *best,
+                   void *stream) {
+    if (plan == nullptr) return fail(CRF_EINVAL, "plan is NULL");
+    if (scores == nullptr || spans == nullptr) return fail(CRF_EINVAL, "scores/spans is NULL");
+    if (plan->L != 1)
+        return fail(CRF_EUNSUPPORTED, "CKY decode of labelled scores (L = %d)", plan->L);
+    int rc = check_device(plan);
+    if (rc != CRF_OK) return rc;
+    hipError_t e = crf::launch_cky(plan->kp, scores, spans, best, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? ok() : hip_fail(e, "crf_cky_decode launch");
+}
+
+}  // extern "C"

@@ -1,0 +1,216 @@
+"""GPU parity: the HIP library against the float64 oracle, through the C ABI.
+
+Tolerances (fp32 path vs float64 oracle):
+  log Z      |gpu - oracle| <= 1e-5 * max(1, |oracle|)
+  marginals  |gpu - oracle| <= 1e-4 on every valid cell
+  CKY        spans identical (ties: lowest split), best == float32(oracle best)
+The CKY chart is float64 on both sides with the same association order, so the
+trees and scores must agree bit for bit.
+"""
+import numpy as np
+import pytest
+
+from oracle import oracle as orc
+from paper_2008_03736_amd import binding as B
+from paper_2008_03736_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+LOGZ_RTOL = 1e-5
+MARG_ATOL = 1e-4
+ORACLE_THREADS = 16
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch as _t
+
+    if not _t.cuda.is_available():
+        pytest.fail("GPU tests need a ROCm device")
+    B.load()
+    return _t
+
+
+def gpu_run(torch, batch, flags=0, grad=None, decode=True, marg_fill=0.0):
+    dev = torch.device("cuda", 0)
+    s = torch.from_numpy(batch.scores).to(dev)
+    with B.Plan(batch.lengths, n1=batch.n1, num_labels=batch.num_labels, flags=flags,
+                device=dev) as plan:
+        g = None if grad is None else torch.from_numpy(np.asarray(grad, np.float32)).to(dev)
+        marg = torch.full_like(s, marg_fill)
+        lz, marg = plan.inside_fwd_bwd(s, grad_logZ=g, marginals=marg)
+        lz_only = plan.inside_fwd(s)
+        out = {"logZ": lz, "marg": marg, "logZ_fwd": lz_only, "info": plan.info}
+        if decode and batch.num_labels == 1:
+            spans, best = plan.cky_decode(s)
+            out["spans"], out["best"] = spans, best
+        torch.cuda.synchronize()
+    return {k: (v.cpu().numpy() if hasattr(v, "cpu") else v) for k, v in out.items()}
+
+
+def check_logz(gpu, ref):
+    err = np.abs(gpu.astype(np.float64) - ref)
+    bound = LOGZ_RTOL * np.maximum(1.0, np.abs(ref))
+    bad = np.nonzero(err > bound)[0]
+    assert bad.size == 0, f"logZ mismatch at {bad[:5]}: gpu {gpu[bad[:5]]} ref {ref[bad[:5]]}"
+
+
+def check_marg(gpu, ref, lengths, n1, labeled=False):
+    v = W.valid_mask(np.asarray(lengths), n1)
+    if labeled:
+        v = np.broadcast_to(v[..., None], gpu.shape)
+    err = np.abs(gpu[v].astype(np.float64) - ref[v])
+    worst = float(err.max()) if err.size else 0.0
+    assert worst <= MARG_ATOL, f"max |marginal error| {worst:.3e}"
+    return worst
+
+
+def check_cky(out, batch):
+    spans_ref, best_ref = orc.cky(batch.scores, batch.lengths, threads=ORACLE_THREADS)
+    bad = np.nonzero((out["spans"] != spans_ref).any(axis=(1, 2)))[0]
+    assert bad.size == 0, f"trees differ for sentences {bad[:10]}"
+    assert np.array_equal(out["best"], best_ref.astype(np.float32))
+
+
+def full_check(torch, batch, flags=0, grad=None, decode=True):
+    out = gpu_run(torch, batch, flags=flags, grad=grad, decode=decode)
+    lz, mu = orc.marginals(batch.scores, batch.lengths, grad=grad, threads=ORACLE_THREADS)
+    check_logz(out["logZ"], lz)
+    check_logz(out["logZ_fwd"], lz)
+    worst = check_marg(out["marg"], mu, batch.lengths, batch.n1)
+    if decode:
+        check_cky(out, batch)
+    return out, worst
+
+
+# --------------------------------------------------------------------------
+# Workloads
+
+
+def test_tiny(torch):
+    full_check(torch, W.make("tiny"))
+
+
+def test_mixed_full_batch(torch):
+    # the 5,000-sentence batch in the launch configuration the benchmark times
+    b = W.make("mixed")
+    out, worst = full_check(torch, b)
+    print(f"mixed: max |marginal error| {worst:.2e}, lds {out['info']['lds_count']}")
+
+
+def test_longer_full_batch(torch):
+    b = W.make("longer")
+    full_check(torch, b)
+
+
+def test_stress_full_batch(torch):
+    # n = 256, sd 3, 5% of spans at -1e4: workspace-chart kernels
+    b = W.make("stress")
+    out, worst = full_check(torch, b)
+    assert out["info"]["spill_count"] == b.B
+    print(f"stress: max |marginal error| {worst:.2e}")
+
+
+def test_labeled_sampled(torch):
+    b = W.make("labeled")
+    out = gpu_run(torch, b, decode=False)
+    order = np.argsort(-b.lengths, kind="stable")
+    idx = np.unique(np.concatenate([order[:8], order[-8:], np.arange(0, b.B, 37)]))
+    sub = W.subset(b, idx)
+    lz, mu = orc.labeled(sub.scores, sub.lengths, threads=ORACLE_THREADS)
+    check_logz(out["logZ"][idx], lz)
+    n1 = sub.n1
+    check_marg(out["marg"][idx][:, :n1, :n1], mu, sub.lengths, n1, labeled=True)
+    # label marginals sum to the span marginal, which is 1 on forced spans
+    for k, bi in enumerate(idx[:4]):
+        n = int(b.lengths[bi])
+        assert abs(out["marg"][bi, 0, n].sum() - 1.0) < 1e-5
+
+
+# --------------------------------------------------------------------------
+# Edge cases
+
+
+def test_short_and_padded(torch):
+    # n = 1 and n = 2 (only forced spans), a sentence at full padding, extra
+    # padding beyond the longest sentence
+    b = W.custom([1, 2, 3, 1, 7, 2, 12], seed=3, sd=1.5, n1=16)
+    full_check(torch, b)
+    b = W.custom([15, 1, 15], seed=4, sd=1.0, n1=16)
+    full_check(torch, b)
+
+
+def test_all_zero_scores(torch):
+    # every tree ties: right-branching tree, Catalan-ratio marginals
+    b = W.custom([1, 2, 5, 40, 99], sd=0.0)
+    full_check(torch, b)
+
+
+def test_integer_scores_ties(torch):
+    b = W.custom(list(range(2, 60)) * 2, seed=5, integer=(-2, 2))
+    full_check(torch, b)
+
+
+def test_force_spill_matches(torch):
+    b = W.custom([1, 2, 9, 33, 70, 130], seed=6, sd=2.0)
+    full_check(torch, b, flags=B.CRF_FORCE_SPILL)
+    out_s = gpu_run(torch, b, flags=B.CRF_FORCE_SPILL)
+    out_l = gpu_run(torch, b)
+    assert out_s["info"]["spill_count"] == b.B
+    assert np.array_equal(out_s["spans"], out_l["spans"])
+
+
+def test_upstream_gradient(torch):
+    b = W.custom([4, 17, 30], seed=8, sd=1.0)
+    full_check(torch, b, grad=[2.0, -0.5, 0.0])
+
+
+def test_padding_untouched_and_order(torch):
+    # outputs outside the valid triangle keep the caller's values; sentence
+    # order is preserved whatever the internal schedule
+    rng = np.random.default_rng(10)
+    lengths = rng.permutation(np.array([3, 50, 1, 20, 77, 8, 2, 64]))
+    b = W.custom(lengths, seed=11, sd=2.0)
+    out = gpu_run(torch, b, marg_fill=123.5)
+    v = W.valid_mask(b.lengths, b.n1)
+    assert np.all(out["marg"][~v] == np.float32(123.5))
+    lz, mu = orc.marginals(b.scores, b.lengths)
+    check_logz(out["logZ"], lz)
+    check_marg(out["marg"], mu, b.lengths, b.n1)
+
+
+def test_deterministic(torch):
+    b = W.custom([5, 33, 90, 120], seed=12, sd=2.0)
+    o1 = gpu_run(torch, b)
+    o2 = gpu_run(torch, b)
+    for k in ("logZ", "marg", "spans", "best"):
+        assert np.array_equal(o1[k], o2[k], equal_nan=True), k
+
+
+def test_labeled_small(torch):
+    b = W.custom([1, 2, 6, 13], seed=13, sd=1.0, labels=7)
+    out = gpu_run(torch, b, decode=False)
+    lz, mu = orc.labeled(b.scores, b.lengths)
+    check_logz(out["logZ"], lz)
+    check_marg(out["marg"], mu, b.lengths, b.n1, labeled=True)
+
+
+def test_decode_rejects_labeled_plan(torch):
+    b = W.custom([3], seed=1, labels=2)
+    dev = torch.device("cuda", 0)
+    s = torch.from_numpy(b.scores).to(dev)
+    with B.Plan(b.lengths, num_labels=2, device=dev) as plan:
+        with pytest.raises(B.CrfError) as ei:
+            plan.cky_decode(s)
+        assert ei.value.status == B.CRF_EUNSUPPORTED
+
+
+def test_autograd_function(torch):
+    b = W.custom([6, 11], seed=14, sd=1.0)
+    dev = torch.device("cuda", 0)
+    s = torch.from_numpy(b.scores).to(dev).requires_grad_(True)
+    with B.Plan(b.lengths, device=dev) as plan:
+        lz = B.log_partition(s, plan)
+        (lz * torch.tensor([1.0, 3.0], device=dev)).sum().backward()
+    _, mu = orc.marginals(b.scores, b.lengths, grad=[1.0, 3.0])
+    check_marg(s.grad.cpu().numpy(), mu, b.lengths, b.n1)
