@@ -141,6 +141,16 @@ int crf_inside_fwd_bwd(const crf_plan *plan, const float *scores, const float *g
 int crf_cky_decode(const crf_plan *plan, const float *scores, int32_t *spans, float *best,
                    void *stream);
 
+/*
+ * crf_inside_fwd_bwd_cky -- crf_inside_fwd_bwd and crf_cky_decode in one
+ * launch, their workgroups interleaved so the two run concurrently.  Same
+ * arguments and results as the two calls (logZ and best may be NULL).
+ * Unlabelled plans only (CRF_EUNSUPPORTED otherwise).
+ */
+int crf_inside_fwd_bwd_cky(const crf_plan *plan, const float *scores, const float *grad_logZ,
+                           float *logZ, float *marginals, int32_t *spans, float *best,
+                           void *stream);
+
 /* Static description of a status code. */
 const char *crf_status_string(int status);
 

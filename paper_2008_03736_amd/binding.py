@@ -31,6 +31,7 @@ SIGNATURES = {
     "crf_inside_bwd": (ctypes.c_int, [_P, _P, _P, _P, _P]),
     "crf_inside_fwd_bwd": (ctypes.c_int, [_P, _P, _P, _P, _P, _P]),
     "crf_cky_decode": (ctypes.c_int, [_P, _P, _P, _P, _P]),
+    "crf_inside_fwd_bwd_cky": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _P]),
     "crf_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "crf_last_error": (ctypes.c_char_p, []),
 }
@@ -118,6 +119,11 @@ def crf_inside_fwd_bwd(plan, scores, grad_logZ, logZ, marginals, stream):
 
 def crf_cky_decode(plan, scores, spans, best, stream):
     _check(load().crf_cky_decode(plan, scores, spans, best, stream), "crf_cky_decode")
+
+
+def crf_inside_fwd_bwd_cky(plan, scores, grad_logZ, logZ, marginals, spans, best, stream):
+    _check(load().crf_inside_fwd_bwd_cky(plan, scores, grad_logZ, logZ, marginals, spans, best,
+                                         stream), "crf_inside_fwd_bwd_cky")
 
 
 def crf_status_string(status):
@@ -234,6 +240,29 @@ class Plan:
         crf_inside_bwd(self._handle, sp, self._vec(grad_logZ, "grad_logZ"), marginals.data_ptr(),
                        _stream_ptr(t, self.device))
         return marginals
+
+    def parse(self, scores, grad_logZ=None, logZ=None, marginals=None, spans=None, best=None):
+        """inside_fwd_bwd and cky_decode in one launch:
+        (logZ, marginals, spans, best)."""
+        t = self._torch
+        sp = self._scores(scores)
+        R = 2 * (self.n1 - 1) - 1
+        if logZ is None:
+            logZ = t.empty(self.B, dtype=t.float32, device=self.device)
+        if marginals is None:
+            marginals = t.zeros_like(scores)
+        elif tuple(marginals.shape) != tuple(scores.shape) or not marginals.is_contiguous():
+            raise ValueError("marginals must be a contiguous tensor shaped like scores")
+        if spans is None:
+            spans = t.empty((self.B, R, 2), dtype=t.int32, device=self.device)
+        elif tuple(spans.shape) != (self.B, R, 2) or spans.dtype != t.int32 or not spans.is_contiguous():
+            raise ValueError(f"spans must be contiguous int32 [{self.B}, {R}, 2]")
+        if best is None:
+            best = t.empty(self.B, dtype=t.float32, device=self.device)
+        crf_inside_fwd_bwd_cky(self._handle, sp, self._vec(grad_logZ, "grad_logZ"),
+                               self._vec(logZ, "logZ"), marginals.data_ptr(), spans.data_ptr(),
+                               self._vec(best, "best"), _stream_ptr(t, self.device))
+        return logZ, marginals, spans, best
 
     def cky_decode(self, scores, spans=None, best=None):
         """(spans int32 [B, 2(N1-1)-1, 2] preorder padded with -1, best float32 [B])."""

@@ -6,43 +6,72 @@
 #include <hip/hip_runtime_api.h>
 #include <stdint.h>
 
+#include "../../include/crf_inside.h"
+
 namespace crf {
 
-// Threads per workgroup of every kernel: four 64-wide wavefronts.
-constexpr int kThreads = 256;
+// Workgroup sizes.  Bundled LDS kernels run kThreadsDefault threads, two
+// workgroups per CU when every bundle fits in half the LDS, else one; the
+// workspace ("spill") kernels run kThreadsMax.  Every kernel is built for up
+// to kThreadsMax threads and reads its size from blockDim.
+constexpr int kThreadsDefault = 512;
+constexpr int kThreadsMax = 1024;
 
-// The LDS kernels give a span at most 16 lanes and cache at most 12 split
-// points per lane, so they take sentences of up to 16*12+1 words; longer
-// ones always use the workspace kernels (which allow 64 lanes x 16).
-constexpr int kMaxLenLds = 16 * 12 + 1;
+// Most sentences per bundle (bounds the per-sentence tables in LDS).
+constexpr int kMaxBundle = 256;
 
-// Row stride (in elements) of a sentence's square chart.  One place so the
-// host's LDS sizing and the kernels' indexing cannot disagree.
+// LDS a bundle needs besides its charts: a uint32 table of division magics
+// for span counts 0..n+1.
+__host__ __device__ inline int64_t bundle_extra_bytes(int n) { return 4 * (int64_t)(n + 2); }
+
+// Static LDS the kernels reserve besides the charts.
+constexpr int kStaticLds = 4096;
+
+// Row stride (in elements) of a sentence's square chart.
 __host__ __device__ inline int chart_ld(int n) { return n + 1; }
 
 // Bytes of chart per sentence.
 //   inside: two float32 squares -- alpha (upper triangle + mirrored lower
-//           triangle) and the adjoint accumulators (scores during the
+//           triangle) and the adjoint accumulators (left-child adjoints in
+//           the upper triangle, right-child adjoints in the lower one; the
+//           lower triangle also parks the forced-span scores before the
 //           forward sweep);
-//   cky:    one float64 square (beta, upper + mirror) + a uint16 square of
-//           back-pointers.
+//   cky:    one float64 square (beta, upper + mirror).  The tree walk needs
+//           cky_scratch_ints(n) ints of LDS per wavefront on top.
 __host__ __device__ inline int64_t inside_chart_bytes(int n) {
     const int64_t ld = chart_ld(n);
     return 2 * ld * ld * 4;
 }
 __host__ __device__ inline int64_t cky_chart_bytes(int n) {
     const int64_t ld = chart_ld(n);
-    return ld * ld * 8 + ((ld * ld * 2 + 7) / 8) * 8;
+    return ld * ld * 8;
 }
+__host__ __device__ inline int cky_scratch_ints(int n) { return 3 * n + 3; }
 
-// Which sentences run on the LDS kernel and which on the workspace kernel,
-// for one kind of chart.  Both lists are ordered most expensive first.
+// Longest sentence whose CKY chart can sit in one CU's LDS (160 KiB):
+// 8 (n+1)^2 <= 163840.  The plan sends longer ones to the workspace kernels.
+constexpr int kMaxLenInLds = 142;
+
+// A bundle: `count` sentences of identical length `n`, processed together by
+// one workgroup; their ids are order[first .. first+count).
+struct Bundle {
+    int32_t first;
+    int32_t count;
+    int32_t n;
+    int32_t pad;
+};
+
+// Which sentences run in LDS (in bundles) and which on the workspace kernel,
+// for one kind of chart.  Bundles and spilled sentences are ordered most
+// expensive first.
 struct Schedule {
-    const int32_t *order_lds;    // [n_lds] sentence ids
+    const Bundle *bundles;       // [n_bundles]
+    const int32_t *order;        // sentence ids grouped by bundle
     const int32_t *order_spill;  // [n_spill] sentence ids
     const int64_t *ws_off;       // [n_spill] byte offset of each chart in the workspace
-    int32_t n_lds, n_spill;
-    int32_t lds_bytes;           // dynamic LDS per workgroup of the LDS kernel
+    int32_t n_bundles, n_spill;
+    int32_t lds_bytes;           // dynamic LDS per workgroup (bundle budget)
+    int32_t threads;             // workgroup size of the LDS kernels
 };
 
 // Device-side view of a plan, passed by value to every kernel.
@@ -57,6 +86,8 @@ hipError_t launch_inside(const KernelPlan &p, const float *scores, const float *
                          float *logZ, float *marg, hipStream_t stream);
 hipError_t launch_cky(const KernelPlan &p, const float *scores, int32_t *spans, float *best,
                       hipStream_t stream);
+hipError_t launch_parse(const KernelPlan &p, const float *scores, const float *grad, float *logZ,
+                        float *marg, int32_t *spans, float *best, hipStream_t stream);
 hipError_t set_kernel_attributes(int max_lds_bytes);
 
 }  // namespace crf

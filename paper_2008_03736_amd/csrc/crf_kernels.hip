@@ -8,33 +8,41 @@
 //   labels   s'(i,j) = log sum_l exp s(i,j,l) feeds the inside; per-label
 //            marginals are p((i,j)|x) * softmax_l s(i,j,l) (Sec. 4.2, Eq. tree-label-score)
 //
-// Design (one workgroup of 256 threads per sentence, longest first):
-//   * The sentence's chart stays on chip for the whole call: LDS when it fits
-//     ("lds" kernels), else a plan-owned global workspace that stays mostly
-//     in L2/MALL ("spill" kernels, same code on global pointers).
-//   * Width w is one barrier-separated step.  Each span of the width is
-//     handled by a group of G lanes (G a power of two picked per width), each
-//     lane taking the split points k = i+1+l, i+1+l+G, ...; the split-point
-//     log-sum-exp is a lane-local max / sum-exp followed by a DPP butterfly
-//     across the group.
-//   * alpha is stored twice, at [i][j] and mirrored at [j][i], so both the
-//     row alpha(i,.) and the column alpha(.,j) a span needs are contiguous.
+// Design.
+//   * Bundles.  The host groups sentences of equal length into bundles that
+//     fit one workgroup's LDS; a workgroup runs a whole bundle, all of its
+//     sentences advancing one span width per barrier.  This is the paper's
+//     batching of same-width spans (Sec. 3.1) done inside one CU, where the
+//     chart never leaves LDS.  Sentences too long for LDS run alone on the
+//     same code with the chart in a plan-owned workspace (L2/MALL resident).
+//   * Lanes.  In width w every span has K = w-1 split points and gets G
+//     lanes (a power of two <= 64), chosen so that all spans of the step fill
+//     the workgroup about once; lane l takes splits l, l+G, ... in chunks of
+//     up to 4 whose loads issue together, branch-free.  The split-point
+//     log-sum-exp is a running max / sum-exp per lane finished by a butterfly
+//     over the G lanes (DPP inside a 16-lane row, ds_swizzle across rows,
+//     readlane across the two halves of the wave).
+//   * alpha is stored twice, at [i][j] and mirrored at [j][i], so the row
+//     alpha(i,.) and the column alpha(.,j) of a span are both contiguous.
 //   * The chart holds log2-scaled values (v_exp_f32 / v_log_f32 are base 2).
 //   * Forced spans -- every tree holds the n width-1 spans and the root -- are
 //     factored out of the chart: their scores are summed in float64 and added
-//     to log Z, and their marginal is exactly the upstream gradient.  This
-//     keeps chart magnitudes small (an exact rewrite: Z = exp(forced) * Z').
-//   * The reverse pass walks widths downwards.  For span (i,j) with adjoint
-//     mu, each split gets p_k = exp(x_k - m) / sum exp(x - m) (normalised
-//     with the span's own max), and mu * p_k flows to the left child (i,k)
-//     and right child (k,j).  In one width a child has exactly one parent of
-//     each kind, so left- and right-child adjoints are kept in the upper and
-//     lower triangles of a second square: every write has a single writer
-//     and no atomics are needed.
-//   * CKY runs a float64 chart with the association order
+//     to log Z, and their marginal is exactly the upstream gradient.  This is
+//     exact (Z = exp(forced) Z') and keeps chart magnitudes small.
+//   * Reverse pass.  Widths run downwards.  A span with adjoint mu gives each
+//     split p_k = exp(x_k - m) / sum exp(x - m), normalised with its own max,
+//     and mu p_k flows to the left child (i,k) and the right child (k,j).  In
+//     one width each child has one parent of each kind, so left- and
+//     right-child adjoints live in the upper and lower triangles of a second
+//     square: every write has a single writer, no atomics, deterministic.
+//   * CKY runs a float64 chart in the association order
 //     beta(i,j) = (max_k (beta(i,k) + beta(k,j))) + s(i,j): only IEEE adds
 //     and exact max, so the tree is reproducible bit for bit; ties keep the
-//     lowest split.
+//     lowest split.  The tree is recovered by a breadth-first walk of the
+//     back-pointers (one wavefront per sentence, no barriers) that records
+//     each node's depth; spans starting at position i form a chain of left
+//     children, so a node's preorder slot is the chain's offset plus its
+//     depth below the chain head.
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
@@ -44,14 +52,13 @@
 namespace crf {
 namespace {
 
-constexpr int NT = kThreads;
-constexpr int NWAVES = NT / 64;
 constexpr float LOG2E_F = 1.4426950408889634f;
 constexpr double LN2_D = 0.69314718055994530942;
 
-// Split points cached in registers per lane (LDS kernels / spill kernels).
-constexpr int MAXC_LDS = 12;
-constexpr int MAXC_SPILL = 16;
+template <int G>
+constexpr int ilog2() {
+    return G <= 1 ? 0 : 1 + ilog2<G / 2>();
+}
 
 // ---------------------------------------------------------------------------
 // Cross-lane helpers.  Groups are aligned runs of G lanes; the butterflies
@@ -74,26 +81,26 @@ __device__ __forceinline__ double dpp_d(double v) {
 }
 // xor 16 inside each 32-lane half: ds_swizzle bit-mask mode (and 0x1f, xor 0x10).
 __device__ __forceinline__ int swz16_i(int v) { return __builtin_amdgcn_ds_swizzle(v, 0x401F); }
-// xor 32: cross-half permute.
-__device__ __forceinline__ int x32_i(int v) {
-    const int lane = (int)__lane_id();
-    return __builtin_amdgcn_ds_bpermute((lane ^ 32) << 2, v);
-}
 __device__ __forceinline__ float swz16_f(float v) {
     return __builtin_bit_cast(float, swz16_i(__builtin_bit_cast(int, v)));
-}
-__device__ __forceinline__ float x32_f(float v) {
-    return __builtin_bit_cast(float, x32_i(__builtin_bit_cast(int, v)));
 }
 __device__ __forceinline__ double swz16_d(double v) {
     const uint64_t u = __builtin_bit_cast(uint64_t, v);
     const int lo = swz16_i((int)(uint32_t)u), hi = swz16_i((int)(uint32_t)(u >> 32));
     return __builtin_bit_cast(double, ((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
 }
-__device__ __forceinline__ double x32_d(double v) {
+// The two 32-lane halves' values, for the last level of a 64-lane group.
+__device__ __forceinline__ float half0_f(float v) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 0));
+}
+__device__ __forceinline__ float half1_f(float v) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 32));
+}
+__device__ __forceinline__ double readlane_d(double v, int lane) {
     const uint64_t u = __builtin_bit_cast(uint64_t, v);
-    const int lo = x32_i((int)(uint32_t)u), hi = x32_i((int)(uint32_t)(u >> 32));
-    return __builtin_bit_cast(double, ((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)u, lane);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(u >> 32), lane);
+    return __builtin_bit_cast(double, ((uint64_t)hi << 32) | lo);
 }
 
 // DPP controls: quad_perm [1,0,3,2] (xor 1), quad_perm [2,3,0,1] (xor 2),
@@ -101,14 +108,18 @@ __device__ __forceinline__ double x32_d(double v) {
 // the two halves of each 16-lane row).
 constexpr int DPP_XOR1 = 0xB1, DPP_XOR2 = 0x4E, DPP_HMIRROR = 0x141, DPP_MIRROR = 0x140;
 
+// Plain IEEE max (the library is built with -fno-honor-nans: no NaN reaches
+// the chart, and the DPP moves fold into v_max_f32_dpp).
+__device__ __forceinline__ float fmax_nn(float a, float b) { return __builtin_fmaxf(a, b); }
+
 template <int G>
 __device__ __forceinline__ float grp_max(float v) {
-    if constexpr (G >= 2) v = fmaxf(v, dpp_f<DPP_XOR1>(v));
-    if constexpr (G >= 4) v = fmaxf(v, dpp_f<DPP_XOR2>(v));
-    if constexpr (G >= 8) v = fmaxf(v, dpp_f<DPP_HMIRROR>(v));
-    if constexpr (G >= 16) v = fmaxf(v, dpp_f<DPP_MIRROR>(v));
-    if constexpr (G >= 32) v = fmaxf(v, swz16_f(v));
-    if constexpr (G >= 64) v = fmaxf(v, x32_f(v));
+    if constexpr (G >= 2) v = fmax_nn(v, dpp_f<DPP_XOR1>(v));
+    if constexpr (G >= 4) v = fmax_nn(v, dpp_f<DPP_XOR2>(v));
+    if constexpr (G >= 8) v = fmax_nn(v, dpp_f<DPP_HMIRROR>(v));
+    if constexpr (G >= 16) v = fmax_nn(v, dpp_f<DPP_MIRROR>(v));
+    if constexpr (G >= 32) v = fmax_nn(v, swz16_f(v));
+    if constexpr (G >= 64) v = fmax_nn(half0_f(v), half1_f(v));
     return v;
 }
 template <int G>
@@ -118,7 +129,7 @@ __device__ __forceinline__ float grp_sum(float v) {
     if constexpr (G >= 8) v += dpp_f<DPP_HMIRROR>(v);
     if constexpr (G >= 16) v += dpp_f<DPP_MIRROR>(v);
     if constexpr (G >= 32) v += swz16_f(v);
-    if constexpr (G >= 64) v += x32_f(v);
+    if constexpr (G >= 64) v = half0_f(v) + half1_f(v);
     return v;
 }
 template <int G>
@@ -128,7 +139,7 @@ __device__ __forceinline__ double grp_max_d(double v) {
     if constexpr (G >= 8) v = fmax(v, dpp_d<DPP_HMIRROR>(v));
     if constexpr (G >= 16) v = fmax(v, dpp_d<DPP_MIRROR>(v));
     if constexpr (G >= 32) v = fmax(v, swz16_d(v));
-    if constexpr (G >= 64) v = fmax(v, x32_d(v));
+    if constexpr (G >= 64) v = fmax(readlane_d(v, 0), readlane_d(v, 32));
     return v;
 }
 template <int G>
@@ -138,376 +149,693 @@ __device__ __forceinline__ int grp_min_i(int v) {
     if constexpr (G >= 8) v = min(v, dpp_i<DPP_HMIRROR>(v));
     if constexpr (G >= 16) v = min(v, dpp_i<DPP_MIRROR>(v));
     if constexpr (G >= 32) v = min(v, swz16_i(v));
-    if constexpr (G >= 64) v = min(v, x32_i(v));
+    if constexpr (G >= 64) v = min(__builtin_amdgcn_readlane(v, 0), __builtin_amdgcn_readlane(v, 32));
     return v;
 }
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 __device__ __forceinline__ float fast_log2(float x) { return __builtin_amdgcn_logf(x); }
 
-// Lanes per span for one width: K = w-1 split points, S = n-w+1 spans.
-// Minimises (rounds of spans) x (serial splits per lane + butterfly depth).
-template <int GMAX, int MAXC>
-__device__ __forceinline__ int pick_group(int K, int S) {
-    int best = GMAX, best_cost = 0x7fffffff;
-#pragma unroll
-    for (int g = 1; g <= GMAX; g <<= 1) {
-        const int cnt = (K + g - 1) / g;
-        if (cnt > MAXC) continue;
-        const int groups = NT / g;
-        const int rounds = (S + groups - 1) / groups;
-        const int depth = 31 - __builtin_clz(g);
-        const int cost = rounds * (cnt * 4 + depth * 6 + 10);
-        if (cost < best_cost) { best_cost = cost; best = g; }
-    }
-    return best;
+// a / d for 0 <= a < 2^24, 1 <= d, with inv = 1.0f / d: the float quotient is
+// within one of the truth and is corrected exactly.
+__device__ __forceinline__ int div_small(int a, int d, float inv) {
+    int q = (int)((float)a * inv);
+    q += ((q + 1) * d <= a) ? 1 : 0;
+    q -= (q * d > a) ? 1 : 0;
+    return q;
+}
+
+// Sentinel for "no split": far below any chart value, and finite so that
+// differences of two sentinels stay finite (exp2 of the difference of a
+// sentinel and a real value is 0).
+constexpr float NEG = -1.0e30f;
+
+__device__ __forceinline__ int next_pow2(int x) { return x <= 1 ? 1 : 1 << (32 - __builtin_clz(x - 1)); }
+__device__ __forceinline__ int floor_pow2(int x) { return x <= 1 ? 1 : 1 << (31 - __builtin_clz(x)); }
+
+// Splits per lane: the LDS kernels unroll up to 8; the workspace kernels
+// (long sentences) up to 16.
+constexpr int CMAX_LDS = 8, CMAX_WIDE = 16;
+
+// Lanes per span for one width step: as many as keep the step's spans within
+// one pass over the workgroup, never more than the K split points need, and
+// at least enough that no lane takes more than cmax of them.
+__device__ __forceinline__ int pick_lanes(int K, int spans, int nt, int cmax) {
+    int g = 1;
+    while (g < 64 && spans * (g * 2) <= nt) g <<= 1;
+    g = min(g, next_pow2(K));
+    g = max(g, next_pow2((K + cmax - 1) / cmax));
+    return min(g, 64);
 }
 
 // ---------------------------------------------------------------------------
-// Inside sweep, one width.  al: chart (alpha upper [i][j], mirror [j][i]);
-// before width w runs, al[i][j] of every width-w span holds its log2-scaled
-// score (0 for the root, whose score is factored out).
+// Per-bundle context: nb sentences of length n; sentence sb's chart starts at
+// chart0 + sb * cstride (elements).
 
-template <int G, int MAXC, typename T>
-__device__ __forceinline__ void inside_width(T *al, int ld, int n, int w, int tid) {
-    constexpr int GROUPS = NT / G;
-    const int K = w - 1, S = n - w + 1;
-    const int cnt = (K + G - 1) / G;
-    const int g = tid / G, l = tid % G;
-    for (int s0 = 0; s0 < S; s0 += GROUPS) {
-        const int sp = s0 + g;
-        const bool act = sp < S;
-        const int i = act ? sp : S - 1;
-        const int j = i + w;
-        const T *rp = al + (size_t)i * ld + (i + 1 + l);   // alpha(i, k)
-        const T *cp = al + (size_t)j * ld + (i + 1 + l);   // alpha(k, j), mirrored
-        const float sij = al[(size_t)i * ld + j];
-        float x[MAXC];
-        float m = -INFINITY;
-#pragma unroll
-        for (int c = 0; c < MAXC; ++c) {
-            x[c] = -INFINITY;
-            if (c < cnt && l + c * G < K) x[c] = rp[c * G] + cp[c * G];
-            m = fmaxf(m, x[c]);
-        }
-        m = grp_max<G>(m);
-        float sum = 0.f;
-#pragma unroll
-        for (int c = 0; c < MAXC; ++c)
-            if (c < cnt) sum += fast_exp2(x[c] - m);
-        sum = grp_sum<G>(sum);
-        if (act && l == 0) {
-            const float v = m + fast_log2(sum) + sij;
-            al[(size_t)i * ld + j] = v;
-            al[(size_t)j * ld + i] = v;
-        }
-    }
+template <typename T>
+struct Bundle_ctx {
+    T *chart0;
+    int cstride;   // elements between consecutive sentences' charts
+    int n, ld, nb;
+};
+
+// Where lane `f` of a width-w step works: sentence sb, span start i, lane l
+// of the span's G lanes.  gid / S by multiply-high with magic = 2^32 / S + 1
+// (exact for gid < 2^18, 2 <= S <= 1024); S = 1 (magic would wrap to 0) is
+// the identity.
+struct Lane_at {
+    int sb, i, l;
+};
+__device__ __forceinline__ uint32_t div_magic(int S) { return S > 1 ? 0xFFFFFFFFu / (uint32_t)S + 1u : 0u; }
+template <int G>
+__device__ __forceinline__ Lane_at lane_at(int f, int S, uint32_t magic) {
+    constexpr int LG = ilog2<G>();
+    const int gid = f >> LG;
+    const int sb = S > 1 ? (int)__umulhi((uint32_t)gid, magic) : gid;
+    return Lane_at{sb, gid - (int)__umul24((uint32_t)sb, (uint32_t)S), f & (G - 1)};
 }
 
-// Reverse sweep, one width.  ad: adjoints -- upper [i][k] accumulates what
-// (i,k) receives as a left child, lower [j][k] what (k,j) receives as a
-// right child.  gval is the upstream gradient (the root's adjoint).
-template <int G, int MAXC, typename T>
-__device__ __forceinline__ void reverse_width(const T *al, T *ad, int ld, int n, int w, int tid,
-                                              float gval) {
-    constexpr int GROUPS = NT / G;
+// One width of the inside (REV = false) or reverse (REV = true) sweep for
+// every sentence of the bundle.  Lane l of a span takes split offsets
+// ko = l + c*G, c < C (split k = i+1+ko); C = ceil(K/G), so only the last one
+// can fall past K (or all past the true count when MASK_ALL, used when C is
+// rounded up).  gv: per-sentence upstream gradient (LDS).
+template <int G, int C, bool MASK_ALL, bool REV, typename T>
+__device__ __forceinline__ void span_step(const Bundle_ctx<T> &bx, int w, const float *gv,
+                                          uint32_t magic) {
+    const int tid = threadIdx.x, nt = blockDim.x;
+    const int n = bx.n, ld = bx.ld;
     const int K = w - 1, S = n - w + 1;
-    const int cnt = (K + G - 1) / G;
-    const int g = tid / G, l = tid % G;
-    for (int s0 = 0; s0 < S; s0 += GROUPS) {
-        const int sp = s0 + g;
-        const bool act = sp < S;
-        const int i = act ? sp : S - 1;
-        const int j = i + w;
-        const T *rp = al + (size_t)i * ld + (i + 1 + l);
-        const T *cp = al + (size_t)j * ld + (i + 1 + l);
-        const float mu = (w == n) ? gval : ad[(size_t)i * ld + j] + ad[(size_t)j * ld + i];
-        float x[MAXC];
-        float m = -INFINITY;
+    const int total = bx.nb * S * G;
+    for (int f0 = 0; f0 < total; f0 += nt) {
+        const bool act = f0 + tid < total;
+        const Lane_at at = lane_at<G>(act ? f0 + tid : total - 1, S, magic);
+        const int i = at.i, l = at.l, j = i + w;
+        T *al = bx.chart0 + __umul24((uint32_t)at.sb, (uint32_t)bx.cstride);
+        T *ad = al + __umul24((uint32_t)ld, (uint32_t)ld);
+        const int rowo = (int)__umul24((uint32_t)i, (uint32_t)(ld + 1)) + 1 + l;   // alpha(i, k)
+        const int colo = rowo + (int)__umul24((uint32_t)w, (uint32_t)ld);          // alpha(k, j) mirrored
+        const int dia = (int)__umul24((uint32_t)i, (uint32_t)ld) + j;              // [i][j]
+        const int mir = (int)__umul24((uint32_t)j, (uint32_t)ld) + i;              // [j][i]
+        float x[C], accl[C], accr[C];
 #pragma unroll
-        for (int c = 0; c < MAXC; ++c) {
-            x[c] = -INFINITY;
-            if (c < cnt && l + c * G < K) x[c] = rp[c * G] + cp[c * G];
-            m = fmaxf(m, x[c]);
-        }
-        m = grp_max<G>(m);
-        float sum = 0.f;
+        for (int c = 0; c < C; ++c) x[c] = al[rowo + c * G] + al[colo + c * G];
+        if constexpr (REV) {
 #pragma unroll
-        for (int c = 0; c < MAXC; ++c) {
-            if (c < cnt) {
-                x[c] = fast_exp2(x[c] - m);
-                sum += x[c];
+            for (int c = 0; c < C; ++c) {
+                accl[c] = ad[rowo + c * G];   // current adjoints of the children
+                accr[c] = ad[colo + c * G];
             }
         }
-        sum = grp_sum<G>(sum);
-        const float coef = mu / sum;
-        if (act) {
-            T *lp = ad + (size_t)i * ld + (i + 1 + l);   // left-child slots (i, k)
-            T *rq = ad + (size_t)j * ld + (i + 1 + l);   // right-child slots (k, j)
+        // forward: the span's (log2-scaled) score; reverse: its adjoint
+        const float extra = !REV ? al[dia] : (w == n) ? gv[at.sb] : ad[dia] + ad[mir];
 #pragma unroll
-            for (int c = 0; c < MAXC; ++c) {
-                if (c < cnt && l + c * G < K) {
-                    const float v = coef * x[c];
-                    lp[c * G] += v;
-                    rq[c * G] += v;
-                }
+        for (int c = 0; c < C; ++c)
+            if (MASK_ALL || c == C - 1) x[c] = (l + c * G < K) ? x[c] : NEG;
+        float m = x[0];
+#pragma unroll
+        for (int c = 1; c < C; ++c) m = fmax_nn(m, x[c]);
+        float t[C], s = 0.f;
+#pragma unroll
+        for (int c = 0; c < C; ++c) {
+            t[c] = fast_exp2(x[c] - m);
+            s += t[c];
+        }
+        const float mg = grp_max<G>(m);
+        const float sc = fast_exp2(m - mg);
+        const float sg = grp_sum<G>(s * sc);
+        if constexpr (!REV) {
+            if (act && l == 0) {
+                const float v = mg + fast_log2(sg) + extra;
+                al[dia] = v;
+                al[mir] = v;
+            }
+        } else if (act) {
+            // mu * p_k, p_k = exp2(x_k - mg) / sg, to both children of split k:
+            // the left child (i, k) in the upper triangle, the right child
+            // (k, j) in the lower one.  In one step each of these cells has
+            // this span as its only writer, so a plain read-modify-write is
+            // race-free and deterministic.
+            const float coef = extra * sc * __builtin_amdgcn_rcpf(sg);
+#pragma unroll
+            for (int c = 0; c < C; ++c) {
+                if ((MASK_ALL || c == C - 1) && l + c * G >= K) continue;
+                const float v = coef * t[c];
+                ad[rowo + c * G] = accl[c] + v;
+                ad[colo + c * G] = accr[c] + v;
             }
         }
     }
 }
 
-template <int GMAX, int MAXC, typename T>
-__device__ __forceinline__ void inside_sweep(T *al, int ld, int n, int tid) {
-    for (int w = 2; w <= n; ++w) {
-        const int g = pick_group<GMAX, MAXC>(w - 1, n - w + 1);
-        switch (g) {
-            case 1: inside_width<1, MAXC>(al, ld, n, w, tid); break;
-            case 2: inside_width<2, MAXC>(al, ld, n, w, tid); break;
-            case 4: inside_width<4, MAXC>(al, ld, n, w, tid); break;
-            case 8: inside_width<8, MAXC>(al, ld, n, w, tid); break;
-            case 16: inside_width<16, MAXC>(al, ld, n, w, tid); break;
-            case 32: if constexpr (GMAX >= 32) inside_width<32, MAXC>(al, ld, n, w, tid); break;
-            default: if constexpr (GMAX >= 64) inside_width<64, MAXC>(al, ld, n, w, tid); break;
-        }
+// Lanes per span and splits per lane of a width step.
+struct Step_shape {
+    int G, C;
+};
+template <bool WIDE>
+__device__ __forceinline__ Step_shape step_shape(int n, int nb, int w) {
+    const int K = w - 1;
+    const int G = pick_lanes(K, nb * (n - w + 1), blockDim.x, WIDE ? CMAX_WIDE : CMAX_LDS);
+    return Step_shape{G, (K + G - 1) >> __builtin_ctz(G)};
+}
+
+// A run of widths w0, w0+dir, ... (excluding w1) sharing one step shape:
+// a tight loop with no dispatch.  magic[S] = div_magic(S) (LDS table).
+template <int G, int C, bool MASK_ALL, bool REV, typename T>
+__device__ __forceinline__ void inside_run(const Bundle_ctx<T> &bx, int w0, int w1, int dir,
+                                        const float *gv, const uint32_t *magic) {
+    // magic[S] for the next width is fetched one step ahead (S = n-w+1 stays
+    // in [0, n] even one step past the run).
+    uint32_t mg_cur = magic[bx.n - w0 + 1];
+    for (int w = w0; w != w1; w += dir) {
+        const uint32_t mg_next = magic[bx.n - (w + dir) + 1];
+        span_step<G, C, MASK_ALL, REV>(bx, w, gv, mg_cur);
         __syncthreads();
+        mg_cur = mg_next;
     }
 }
 
-template <int GMAX, int MAXC, typename T>
-__device__ __forceinline__ void reverse_sweep(const T *al, T *ad, int ld, int n, int tid,
-                                              float gval) {
-    for (int w = n; w >= 2; --w) {
-        const int g = pick_group<GMAX, MAXC>(w - 1, n - w + 1);
-        switch (g) {
-            case 1: reverse_width<1, MAXC>(al, ad, ld, n, w, tid, gval); break;
-            case 2: reverse_width<2, MAXC>(al, ad, ld, n, w, tid, gval); break;
-            case 4: reverse_width<4, MAXC>(al, ad, ld, n, w, tid, gval); break;
-            case 8: reverse_width<8, MAXC>(al, ad, ld, n, w, tid, gval); break;
-            case 16: reverse_width<16, MAXC>(al, ad, ld, n, w, tid, gval); break;
-            case 32: if constexpr (GMAX >= 32) reverse_width<32, MAXC>(al, ad, ld, n, w, tid, gval); break;
-            default: if constexpr (GMAX >= 64) reverse_width<64, MAXC>(al, ad, ld, n, w, tid, gval); break;
+// All widths of one sweep: forward 2..n, reverse n..2.
+template <bool REV, bool WIDE, typename T>
+__device__ __forceinline__ void inside_sweep(const Bundle_ctx<T> &bx, const float *gv,
+                                             const uint32_t *magic) {
+    const int n = bx.n, nb = bx.nb;
+    const int dir = REV ? -1 : 1, wend = REV ? 1 : n + 1;
+    int w = REV ? n : 2;
+    while (w != wend) {
+        const Step_shape sh = step_shape<WIDE>(n, nb, w);
+        int w2 = w + dir;
+        while (w2 != wend) {
+            const Step_shape s2 = step_shape<WIDE>(n, nb, w2);
+            if (s2.G != sh.G || s2.C != sh.C) break;
+            w2 += dir;
         }
-        __syncthreads();
+#define CRF_RUN(GG)                                                                             \
+    case GG:                                                                                    \
+        switch (sh.C) {                                                                         \
+            case 1: inside_run<GG, 1, false, REV>(bx, w, w2, dir, gv, magic); break;            \
+            case 2: inside_run<GG, 2, false, REV>(bx, w, w2, dir, gv, magic); break;            \
+            case 3: inside_run<GG, 3, false, REV>(bx, w, w2, dir, gv, magic); break;            \
+            case 4: inside_run<GG, 4, false, REV>(bx, w, w2, dir, gv, magic); break;            \
+            case 5: inside_run<GG, 5, false, REV>(bx, w, w2, dir, gv, magic); break;            \
+            case 6: inside_run<GG, 6, false, REV>(bx, w, w2, dir, gv, magic); break;            \
+            case 7: inside_run<GG, 7, false, REV>(bx, w, w2, dir, gv, magic); break;            \
+            case 8: inside_run<GG, 8, false, REV>(bx, w, w2, dir, gv, magic); break;            \
+            default:                                                                            \
+                if constexpr (WIDE) inside_run<GG, 16, true, REV>(bx, w, w2, dir, gv, magic);   \
+                break;                                                                          \
+        }                                                                                       \
+        break;
+        switch (sh.G) {
+            CRF_RUN(1) CRF_RUN(2) CRF_RUN(4) CRF_RUN(8) CRF_RUN(16) CRF_RUN(32) CRF_RUN(64)
+            default: break;
+        }
+#undef CRF_RUN
+        w = w2;
     }
 }
 
-// Sum of a double over the workgroup (result valid in every thread).
-__device__ __forceinline__ double block_sum_d(double v, double *red) {
+// Visit every valid cell (sb, i, j), 0 <= i < j <= n, of a bundle with one
+// thread per cell of an n x n tile per sentence (row i, column j-1, cells
+// below the diagonal skipped): consecutive threads take consecutive j.
+template <typename F>
+__device__ __forceinline__ void for_cells(int nb, int n, F &&f) {
+    const int NT = blockDim.x;
+    const int nn = n * n;
+    const int total = nb * nn;
+    const float inv_nn = 1.0f / (float)nn, inv_n = 1.0f / (float)n;
+    for (int c = threadIdx.x; c < total; c += NT) {
+        const int sb = div_small(c, nn, inv_nn);
+        const int rem = c - sb * nn;
+        const int i = div_small(rem, n, inv_n);
+        const int j = rem - i * n + 1;
+        if (j > i) f(sb, i, j);
+    }
+}
+
+// Fixed-order float64 sum over a wavefront (same result in every lane).
+__device__ __forceinline__ double wave_sum_d(double v) {
     for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
-    const int tid = threadIdx.x;
-    if ((tid & 63) == 0) red[tid >> 6] = v;
-    __syncthreads();
-    double t = 0.0;
-#pragma unroll
-    for (int q = 0; q < NWAVES; ++q) t += red[q];
-    __syncthreads();
-    return t;
+    return v;
 }
 
-// Log-sum-exp over labels of one span, in log2 units: returns m2 + log2 sum.
+// Log-sum-exp over labels of one span, in log2 units.
 __device__ __forceinline__ float label_lse2(const float *s, int L) {
     float m = -INFINITY;
-    for (int l = 0; l < L; ++l) m = fmaxf(m, s[l] * LOG2E_F);
+    for (int q = 0; q < L; ++q) m = fmax_nn(m, s[q] * LOG2E_F);
     float acc = 0.f;
-    for (int l = 0; l < L; ++l) acc += fast_exp2(s[l] * LOG2E_F - m);
+    for (int q = 0; q < L; ++q) acc += fast_exp2(s[q] * LOG2E_F - m);
     return m + fast_log2(acc);
 }
 
 // ---------------------------------------------------------------------------
-// Inside (+ reverse) for one sentence per workgroup.
-//   REV:  also run the reverse sweep and write marginals.
-//   LAB:  labelled scores [B][N1][N1][L].
-//   SPILL: chart in the plan workspace instead of LDS.
+// Inside (+ reverse).  One workgroup per bundle (or, SPILL, per long
+// sentence with its chart in the workspace).
+//   REV: also run the reverse sweep and write marginals.
+//   LAB: labelled scores [B][N1][N1][L].
+// Dynamic LDS (bundled): nb charts, then nb x {forced (f64), grad (f32), id (i32)}.
 template <bool REV, bool LAB, bool SPILL>
-__global__ __launch_bounds__(NT) void inside_kernel(KernelPlan p, const float *__restrict__ scores,
-                                                    const float *__restrict__ grad,
-                                                    float *__restrict__ logZ,
-                                                    float *__restrict__ marg) {
-    extern __shared__ __align__(16) char smem_raw[];
-    __shared__ double red[NWAVES];
-    const int item = blockIdx.x;
-    const int b = SPILL ? p.inside.order_spill[item] : p.inside.order_lds[item];
-    const int n = p.len[b];
-    const int ld = chart_ld(n);
-    const int tid = threadIdx.x;
-    const int lane = tid & 63, wave = tid >> 6;
+__device__ __forceinline__ void inside_block(const KernelPlan &p, int block, char *smem_raw,
+                                             const float *__restrict__ scores,
+                                             const float *__restrict__ grad,
+                                             float *__restrict__ logZ, float *__restrict__ marg) {
+    __shared__ double spill_forced[1];
+    __shared__ float spill_gv[1];
+    __shared__ int spill_id[1];
+    __shared__ uint32_t spill_magic[SPILL ? CRF_MAX_LEN + 2 : 1];
+    const int NT = blockDim.x, NW = NT >> 6;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int N1 = p.n1, L = p.L;
 
-    float *al;
-    if constexpr (SPILL)
-        al = reinterpret_cast<float *>(p.ws + p.inside.ws_off[item]);
-    else
-        al = reinterpret_cast<float *>(smem_raw);
-    float *ad = al + (size_t)ld * ld;
+    int n, nb;
+    float *chart0;
+    int cstride;
+    double *forced;
+    float *gv;
+    int *sid;
+    uint32_t *magic;
+    if constexpr (SPILL) {
+        const int b = p.inside.order_spill[block];
+        n = p.len[b];
+        nb = 1;
+        chart0 = reinterpret_cast<float *>(p.ws + p.inside.ws_off[block]);
+        cstride = 0;
+        forced = spill_forced;
+        gv = spill_gv;
+        sid = spill_id;
+        magic = spill_magic;
+        if (tid == 0) sid[0] = b;
+    } else {
+        const Bundle bd = p.inside.bundles[block];
+        n = bd.n;
+        nb = bd.count;
+        chart0 = reinterpret_cast<float *>(smem_raw);
+        cstride = (int)(inside_chart_bytes(n) / 4);
+        forced = reinterpret_cast<double *>(smem_raw + (size_t)nb * inside_chart_bytes(n));
+        gv = reinterpret_cast<float *>(forced + nb);
+        sid = reinterpret_cast<int *>(gv + nb);
+        magic = reinterpret_cast<uint32_t *>(sid + nb);
+        for (int t = tid; t < nb; t += NT) sid[t] = p.inside.order[bd.first + t];
+    }
+    for (int S = tid; S <= n; S += NT) magic[S] = div_magic(S);
+    const int ld = chart_ld(n);
+    const Bundle_ctx<float> bx{chart0, cstride, n, ld, nb};
+    __syncthreads();
+    for (int t = tid; t < nb; t += NT) gv[t] = grad ? grad[sid[t]] : 1.0f;
 
     const size_t row_stride = LAB ? (size_t)N1 * L : (size_t)N1;
-    const float *sb = scores + (size_t)b * N1 * row_stride;
+    const size_t sent_stride = (size_t)N1 * row_stride;
 
-    // Prologue: scores of the valid triangle into the chart (log2-scaled),
-    // forced spans (width 1 and the root) summed in float64 and replaced by 0.
-    double forced = 0.0;
-    for (int i = wave; i < n; i += NWAVES) {
-        for (int j = i + 1 + lane; j <= n; j += 64) {
-            float s2;
-            if constexpr (LAB)
-                s2 = label_lse2(sb + (size_t)i * row_stride + (size_t)j * L, L);
-            else
-                s2 = sb[(size_t)i * row_stride + j] * LOG2E_F;
-            const bool root = (i == 0 && j == n);
-            if (j == i + 1) {
-                forced += LAB ? (double)s2 * LN2_D : (double)sb[(size_t)i * row_stride + j];
-                al[(size_t)i * ld + j] = 0.f;
-                al[(size_t)j * ld + i] = 0.f;
-            } else if (root) {
-                forced += LAB ? (double)s2 * LN2_D : (double)sb[(size_t)i * row_stride + j];
-                al[(size_t)i * ld + j] = 0.f;
-            } else {
-                al[(size_t)i * ld + j] = s2;
-            }
+    // Prologue: scores of every valid cell into the charts (log2-scaled);
+    // forced spans get 0 in the chart and park their natural-unit score in
+    // the adjoint square's lower triangle ([i+1][i]; the root at [n][0]).
+    for_cells(nb, n, [&](int sb, int i, int j) {
+        float *al = chart0 + (size_t)sb * cstride;
+        float *ad = al + (size_t)ld * ld;
+        const float *srow = scores + (size_t)sid[sb] * sent_stride + (size_t)i * row_stride;
+        float s;
+        if constexpr (LAB)
+            s = label_lse2(srow + (size_t)j * L, L) * (float)LN2_D;
+        else
+            s = srow[j];
+        if (j == i + 1) {
+            al[i * ld + j] = 0.f;
+            al[j * ld + i] = 0.f;
+            ad[j * ld + i] = s;
+        } else if (i == 0 && j == n) {
+            al[j] = 0.f;
+            ad[n * ld] = s;
+        } else {
+            al[i * ld + j] = s * LOG2E_F;
         }
+    });
+    __syncthreads();
+    // Forced-span sums, one wavefront per sentence, fixed order (deterministic).
+    for (int sb = wave; sb < nb; sb += NW) {
+        const float *ad = chart0 + (size_t)sb * cstride + (size_t)ld * ld;
+        double acc = 0.0;
+        for (int i = lane; i < n; i += 64) acc += (double)ad[(i + 1) * ld + i];
+        if (lane == 0 && n >= 2) acc += (double)ad[n * ld];
+        acc = wave_sum_d(acc);
+        if (lane == 0) forced[sb] = acc;
     }
-    forced = block_sum_d(forced, red);   // contains the barrier that publishes the chart
 
-    inside_sweep<SPILL ? 64 : 16, SPILL ? MAXC_SPILL : MAXC_LDS>(al, ld, n, tid);
-
-    if (logZ != nullptr && tid == 0) logZ[b] = (float)((double)al[n] * LN2_D + forced);
+    inside_sweep<false, SPILL>(bx, gv, magic);
+    if (logZ != nullptr)
+        for (int sb = tid; sb < nb; sb += NT)
+            logZ[sid[sb]] = (float)((double)chart0[(size_t)sb * cstride + n] * LN2_D + forced[sb]);
     if constexpr (!REV) return;
 
-    // Reverse sweep.  Clear both triangles of the adjoint square first.
-    const float gval = grad ? grad[b] : 1.0f;
-    for (int c = tid; c < ld * ld; c += NT) ad[c] = 0.f;
+    // Reverse sweep.  Clear the adjoint squares first.
+    {
+        const int ld2 = ld * ld;
+        const float inv_ld2 = 1.0f / (float)ld2;
+        for (int c = tid; c < nb * ld2; c += NT) {
+            const int sb = div_small(c, ld2, inv_ld2);
+            chart0[(size_t)sb * cstride + ld2 + (c - sb * ld2)] = 0.f;
+        }
+    }
     __syncthreads();
-    reverse_sweep<SPILL ? 64 : 16, SPILL ? MAXC_SPILL : MAXC_LDS>(al, ad, ld, n, tid, gval);
+    inside_sweep<true, SPILL>(bx, gv, magic);
 
-    // Epilogue: marginals of the valid triangle, row by row (coalesced).
-    float *mb = marg + (size_t)b * N1 * row_stride;
-    for (int i = wave; i < n; i += NWAVES) {
-        for (int j = i + 1 + lane; j <= n; j += 64) {
-            const bool forced_span = (j == i + 1) || (i == 0 && j == n);
-            const float mu = forced_span ? gval : ad[(size_t)i * ld + j] + ad[(size_t)j * ld + i];
-            if constexpr (LAB) {
-                const float *s = sb + (size_t)i * row_stride + (size_t)j * L;
-                const float lse2 = label_lse2(s, L);
-                float *o = mb + (size_t)i * row_stride + (size_t)j * L;
-                for (int q = 0; q < L; ++q) o[q] = mu * fast_exp2(s[q] * LOG2E_F - lse2);
-            } else {
-                mb[(size_t)i * row_stride + j] = mu;
-            }
+    // Epilogue: marginals of the valid cells (coalesced stores along rows).
+    for_cells(nb, n, [&](int sb, int i, int j) {
+        const float *ad = chart0 + (size_t)sb * cstride + (size_t)ld * ld;
+        const size_t rowoff = (size_t)sid[sb] * sent_stride + (size_t)i * row_stride;
+        const bool forced_span = (j == i + 1) || (i == 0 && j == n);
+        const float mu = forced_span ? gv[sb] : ad[i * ld + j] + ad[j * ld + i];
+        if constexpr (LAB) {
+            const float *s = scores + rowoff + (size_t)j * L;
+            const float lse2 = label_lse2(s, L);
+            float *o = marg + rowoff + (size_t)j * L;
+            for (int q = 0; q < L; ++q) o[q] = mu * fast_exp2(s[q] * LOG2E_F - lse2);
+        } else {
+            marg[rowoff + j] = mu;
+        }
+    });
+}
+
+// ---------------------------------------------------------------------------
+// CKY.  Each sentence's chart is one float64 square (beta upper + mirror).
+struct Cky_ctx {
+    char *chart0;
+    int cstride;   // bytes between consecutive sentences' charts
+    int n, ld, nb;
+    __device__ double *beta(int sb) const {
+        return reinterpret_cast<double *>(chart0 + (size_t)sb * cstride);
+    }
+};
+
+// One width: float64 max-plus, beta(i,j) = (max_k fl(beta(i,k) + beta(k,j)))
+// + s(i,j).  The split chosen is not stored: the backtrace recomputes it.
+template <int G, int C, bool MASK_ALL>
+__device__ __forceinline__ void cky_step(const Cky_ctx &cx, int w, uint32_t magic) {
+    const int tid = threadIdx.x, nt = blockDim.x;
+    const int n = cx.n, ld = cx.ld;
+    const int K = w - 1, S = n - w + 1;
+    const int total = cx.nb * S * G;
+    for (int f0 = 0; f0 < total; f0 += nt) {
+        const bool act = f0 + tid < total;
+        const Lane_at at = lane_at<G>(act ? f0 + tid : total - 1, S, magic);
+        const int i = at.i, l = at.l, j = i + w;
+        double *be = cx.beta(at.sb);
+        const int rowo = (int)__umul24((uint32_t)i, (uint32_t)(ld + 1)) + 1 + l;
+        const int colo = rowo + (int)__umul24((uint32_t)w, (uint32_t)ld);
+        double x[C];
+#pragma unroll
+        for (int c = 0; c < C; ++c) x[c] = be[rowo + c * G] + be[colo + c * G];
+        const double sij = be[i * ld + j];
+        if (l >= K) x[0] = -INFINITY;   // lane without any split (G > K)
+#pragma unroll
+        for (int c = 1; c < C; ++c)
+            if ((MASK_ALL || c == C - 1) && l + c * G >= K) x[c] = -INFINITY;
+        double m = x[0];
+#pragma unroll
+        for (int c = 1; c < C; ++c) m = fmax(m, x[c]);
+        m = grp_max_d<G>(m);
+        if (act && l == 0) {
+            const double v = m + sij;
+            be[i * ld + j] = v;
+            be[j * ld + i] = v;
         }
     }
 }
 
-// ---------------------------------------------------------------------------
-// CKY, one width: float64 max-plus with the lowest maximising split.
-template <int G, int MAXC, typename DT, typename BT>
-__device__ __forceinline__ void cky_width(DT *be, BT *bp, int ld, int n, int w, int tid) {
-    constexpr int GROUPS = NT / G;
-    const int K = w - 1, S = n - w + 1;
-    const int cnt = (K + G - 1) / G;
-    const int g = tid / G, l = tid % G;
-    for (int s0 = 0; s0 < S; s0 += GROUPS) {
-        const int sp = s0 + g;
-        const bool act = sp < S;
-        const int i = act ? sp : S - 1;
-        const int j = i + w;
-        const DT *rp = be + (size_t)i * ld + (i + 1 + l);
-        const DT *cp = be + (size_t)j * ld + (i + 1 + l);
-        const double sij = be[(size_t)i * ld + j];
-        double lb = -INFINITY;
-        int lk = 0x7fffffff;
-#pragma unroll
-        for (int c = 0; c < MAXC; ++c) {
-            if (c < cnt && l + c * G < K) {
-                const double v = rp[c * G] + cp[c * G];
-                if (lk == 0x7fffffff || v > lb) { lb = v; lk = i + 1 + l + c * G; }
-            }
+template <int G, int C, bool MASK_ALL>
+__device__ __forceinline__ void cky_run(const Cky_ctx &cx, int w0, int w1, const uint32_t *magic) {
+    uint32_t mg_cur = magic[cx.n - w0 + 1];
+    for (int w = w0; w < w1; ++w) {
+        const uint32_t mg_next = magic[cx.n - w];   // S of width w+1 (>= 0)
+        cky_step<G, C, MASK_ALL>(cx, w, mg_cur);
+        __syncthreads();
+        mg_cur = mg_next;
+    }
+}
+
+template <bool WIDE>
+__device__ __forceinline__ void cky_sweep(const Cky_ctx &cx, const uint32_t *magic) {
+    const int n = cx.n, nb = cx.nb;
+    int w = 2;
+    while (w <= n) {
+        const Step_shape sh = step_shape<WIDE>(n, nb, w);
+        int w2 = w + 1;
+        while (w2 <= n) {
+            const Step_shape s2 = step_shape<WIDE>(n, nb, w2);
+            if (s2.G != sh.G || s2.C != sh.C) break;
+            ++w2;
         }
-        const double m = grp_max_d<G>(lb);
-        const int kk = grp_min_i<G>(lb == m ? lk : 0x7fffffff);
-        if (act && l == 0) {
-            const double v = m + sij;
-            be[(size_t)i * ld + j] = v;
-            be[(size_t)j * ld + i] = v;
-            bp[(size_t)i * ld + j] = (BT)kk;
+#define CRF_RUN(GG)                                                            \
+    case GG:                                                                   \
+        switch (sh.C) {                                                        \
+            case 1: cky_run<GG, 1, false>(cx, w, w2, magic); break;            \
+            case 2: cky_run<GG, 2, false>(cx, w, w2, magic); break;            \
+            case 3: cky_run<GG, 3, false>(cx, w, w2, magic); break;            \
+            case 4: cky_run<GG, 4, false>(cx, w, w2, magic); break;            \
+            case 5: cky_run<GG, 5, false>(cx, w, w2, magic); break;            \
+            case 6: cky_run<GG, 6, false>(cx, w, w2, magic); break;            \
+            case 7: cky_run<GG, 7, false>(cx, w, w2, magic); break;            \
+            case 8: cky_run<GG, 8, false>(cx, w, w2, magic); break;            \
+            default:                                                           \
+                if constexpr (WIDE) cky_run<GG, 16, true>(cx, w, w2, magic);   \
+                break;                                                         \
+        }                                                                      \
+        break;
+        switch (sh.G) {
+            CRF_RUN(1) CRF_RUN(2) CRF_RUN(4) CRF_RUN(8) CRF_RUN(16) CRF_RUN(32) CRF_RUN(64)
+            default: break;
+        }
+#undef CRF_RUN
+        w = w2;
+    }
+}
+
+// Order one wavefront's LDS accesses across its lanes.
+__device__ __forceinline__ void wave_sync() { __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront"); }
+
+// Node (i, j, depth) packed in 32 bits (i, j < 1024; depth < 1024).
+__device__ __forceinline__ int pack_node(int i, int j, int d) { return i | (j << 10) | (d << 20); }
+
+// Recover sentence sb's tree and write it in preorder to out (its 2n-1
+// rows of the spans output).  Runs on one wavefront, breadth first, with no
+// barriers: for each internal node of a level a group of 8 lanes recomputes
+// the lowest k maximising fl(beta(i,k) + beta(k,j)) -- exactly the forward's
+// max, so exactly its split.  scr (LDS, cky_scratch_ints(n)) holds the node
+// list, appended level by level so that each level is the frontier for the
+// next, and per start position the depth of its chain head and of its leaf
+// (uint16).  Spans starting at position p form a chain of left children from
+// the head (a right child, or the root) down to the leaf (p, p+1); in
+// preorder the chains follow each other by p, so a node's row is the chain's
+// offset plus its depth below the head.
+template <int PER_LANE>
+__device__ void backtrace(const Cky_ctx &cx, int sb, int32_t *out, int32_t *scr) {
+    const int lane = threadIdx.x & 63, grp = lane >> 3, gl = lane & 7;
+    const int n = cx.n, ld = cx.ld;
+    const double *be = cx.beta(sb);
+    int32_t *nodes = scr;                                   // 2n ints
+    uint16_t *dmin = reinterpret_cast<uint16_t *>(scr + 2 * n);
+    uint16_t *dleaf = dmin + n;                             // n uint16 each
+    if (lane == 0) {
+        nodes[0] = pack_node(0, n, 0);
+        dmin[0] = 0;
+    }
+    wave_sync();
+    int lo = 0, hi = 1;   // the current level is nodes[lo, hi)
+    for (int d = 0; lo < hi && d < n; ++d) {
+        int tail = hi;
+        for (int base = lo; base < hi; base += 8) {   // 8 nodes per pass, 8 lanes each
+            const int idx = base + grp;
+            const bool valid = idx < hi;
+            const int node = valid ? nodes[idx] : 0;
+            const int i = node & 1023, j = (node >> 10) & 1023;
+            const int K = valid ? j - i - 1 : 0;
+            double lb = -INFINITY;
+            int lk = 0x7fffffff;
+            for (int ko = gl; ko < K; ko += 8) {
+                const double v = be[i * ld + i + 1 + ko] + be[j * ld + i + 1 + ko];
+                if (v > lb) {
+                    lb = v;
+                    lk = ko;
+                }
+            }
+            const double m = grp_max_d<8>(lb);
+            const int kb = grp_min_i<8>(lb == m ? lk : 0x7fffffff);
+            const int k = i + 1 + kb;
+            const bool internal = valid && K > 0 && kb < K;
+            if (valid && gl == 0 && K == 0) dleaf[i] = (uint16_t)d;
+            const uint64_t mask = __ballot(internal && gl == 0);
+            const int below = __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
+                                                        __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0));
+            if (internal && gl == 0) {
+                const int o = tail + 2 * below;
+                if (o + 1 < 2 * n) {
+                    nodes[o] = pack_node(i, k, d + 1);
+                    nodes[o + 1] = pack_node(k, j, d + 1);
+                }
+                dmin[k] = (uint16_t)(d + 1);   // a right child heads the chain at k
+            }
+            tail += 2 * __popcll(mask);
+        }
+        wave_sync();
+        lo = hi;
+        hi = tail < 2 * n ? tail : 2 * n;
+    }
+    // Row of chain p's head = exclusive prefix sum of the chain lengths
+    // dleaf - dmin + 1; keep base[p] = row - dmin[p] in registers, then store
+    // it over the depth tables (all of which have been read by then).
+    constexpr int NB = (PER_LANE + 1) / 2;   // ceil(n / 64) with 64 * NB >= n
+    int basev[NB];
+    int carry = 0;
+#pragma unroll
+    for (int q = 0; q < NB; ++q) {
+        const int p = lane + 64 * q;
+        const int dm = p < n ? (int)dmin[p] : 0;
+        const int c = p < n ? (int)dleaf[p] - dm + 1 : 0;
+        int incl = c;
+        for (int sh = 1; sh < 64; sh <<= 1) {
+            const int o = __shfl_up(incl, sh);
+            if (lane >= sh) incl += o;
+        }
+        basev[q] = carry + incl - c - dm;
+        carry += __shfl(incl, 63);
+    }
+    wave_sync();
+    int32_t *basep = scr + 2 * n;   // n ints over the two uint16 tables
+#pragma unroll
+    for (int q = 0; q < NB; ++q) {
+        const int p = lane + 64 * q;
+        if (p < n) basep[p] = basev[q];
+    }
+    wave_sync();
+    const int total = hi < 2 * n - 1 ? hi : 2 * n - 1;
+    for (int t = lane; t < total; t += 64) {
+        const int node = nodes[t];
+        const int i = node & 1023, j = (node >> 10) & 1023, d = node >> 20;
+        const int pos = basep[i] + d;
+        if (pos >= 0 && pos < 2 * n - 1) {
+            out[2 * pos] = i;
+            out[2 * pos + 1] = j;
         }
     }
 }
 
 template <bool SPILL>
-__global__ __launch_bounds__(NT) void cky_kernel(KernelPlan p, const float *__restrict__ scores,
-                                                 int32_t *__restrict__ spans,
-                                                 float *__restrict__ best) {
-    extern __shared__ __align__(16) char smem_raw[];
-    constexpr int GMAX = SPILL ? 64 : 16;
-    constexpr int MAXC = SPILL ? MAXC_SPILL : MAXC_LDS;
-    const int item = blockIdx.x;
-    const int b = SPILL ? p.cky.order_spill[item] : p.cky.order_lds[item];
-    const int n = p.len[b];
-    const int ld = chart_ld(n);
-    const int tid = threadIdx.x;
-    const int lane = tid & 63, wave = tid >> 6;
+__device__ __forceinline__ void cky_block(const KernelPlan &p, int block, char *smem_raw,
+                                          const float *__restrict__ scores,
+                                          int32_t *__restrict__ spans, float *__restrict__ best) {
+    __shared__ int spill_id[1];
+    __shared__ uint32_t spill_magic[SPILL ? CRF_MAX_LEN + 2 : 1];
+    __shared__ int32_t spill_scr[SPILL ? 3 * CRF_MAX_LEN + 3 : 1];
+    const int NT = blockDim.x, NW = NT >> 6;
+    const int tid = threadIdx.x, wave = tid >> 6;
     const int N1 = p.n1;
 
-    char *base = SPILL ? (p.ws + p.cky.ws_off[item]) : smem_raw;
-    double *be = reinterpret_cast<double *>(base);
-    uint16_t *bp = reinterpret_cast<uint16_t *>(base + (size_t)ld * ld * 8);
-
-    const float *sb = scores + (size_t)b * N1 * N1;
-    for (int i = wave; i < n; i += NWAVES) {
-        for (int j = i + 1 + lane; j <= n; j += 64) {
-            const double s = (double)sb[(size_t)i * N1 + j];
-            be[(size_t)i * ld + j] = s;
-            if (j == i + 1) be[(size_t)j * ld + i] = s;
-        }
+    int n, nb, *sid;
+    uint32_t *magic;
+    int32_t *scr;
+    char *chart0;
+    int cstride;
+    if constexpr (SPILL) {
+        const int b = p.cky.order_spill[block];
+        n = p.len[b];
+        nb = 1;
+        chart0 = p.ws + p.cky.ws_off[block];
+        cstride = 0;
+        sid = spill_id;
+        magic = spill_magic;
+        scr = spill_scr;
+        if (tid == 0) sid[0] = b;
+    } else {
+        const Bundle bd = p.cky.bundles[block];
+        n = bd.n;
+        nb = bd.count;
+        chart0 = smem_raw;
+        cstride = (int)cky_chart_bytes(n);
+        sid = reinterpret_cast<int *>(smem_raw + (size_t)nb * cstride);
+        magic = reinterpret_cast<uint32_t *>(sid + nb);
+        scr = reinterpret_cast<int32_t *>(magic + n + 2);
+        for (int t = tid; t < nb; t += NT) sid[t] = p.cky.order[bd.first + t];
     }
+    for (int S = tid; S <= n; S += NT) magic[S] = div_magic(S);
+    const int ld = chart_ld(n);
+    const Cky_ctx cx{chart0, cstride, n, ld, nb};
     __syncthreads();
 
-    for (int w = 2; w <= n; ++w) {
-        const int g = pick_group<GMAX, MAXC>(w - 1, n - w + 1);
-        switch (g) {
-            case 1: cky_width<1, MAXC>(be, bp, ld, n, w, tid); break;
-            case 2: cky_width<2, MAXC>(be, bp, ld, n, w, tid); break;
-            case 4: cky_width<4, MAXC>(be, bp, ld, n, w, tid); break;
-            case 8: cky_width<8, MAXC>(be, bp, ld, n, w, tid); break;
-            case 16: cky_width<16, MAXC>(be, bp, ld, n, w, tid); break;
-            case 32: if constexpr (GMAX >= 32) cky_width<32, MAXC>(be, bp, ld, n, w, tid); break;
-            default: if constexpr (GMAX >= 64) cky_width<64, MAXC>(be, bp, ld, n, w, tid); break;
-        }
-        __syncthreads();
-    }
+    for_cells(nb, n, [&](int sb, int i, int j) {
+        double *be = cx.beta(sb);
+        const double s = (double)scores[((size_t)sid[sb] * N1 + i) * N1 + j];
+        be[i * ld + j] = s;
+        if (j == i + 1) be[j * ld + i] = s;
+    });
+    __syncthreads();
+    cky_sweep<SPILL>(cx, magic);
 
     const int R = 2 * (N1 - 1) - 1;
-    int32_t *out = spans + (size_t)b * R * 2;
-    // Rows past the tree are -1.
-    for (int r = 2 * n - 1 + tid; r < R; r += NT) {
-        out[2 * r] = -1;
-        out[2 * r + 1] = -1;
-    }
-    if (tid == 0) {
-        if (best) best[b] = (float)be[n];
-        // Preorder walk of the back-pointers; the stack reuses the (now dead)
-        // beta square, which holds >= 2(n+1) ints.
-        int32_t *stk = reinterpret_cast<int32_t *>(be);
-        int top = 0, row = 0;
-        stk[top++] = 0;
-        stk[top++] = n;
-        // Bounded: a tree has 2n-1 spans, and a split outside (i, j) ends the walk.
-        while (top > 0 && row < 2 * n - 1) {
-            const int j = stk[--top];
-            const int i = stk[--top];
-            out[2 * row] = i;
-            out[2 * row + 1] = j;
-            ++row;
-            if (j - i > 1) {
-                const int k = bp[(size_t)i * ld + j];
-                if (k <= i || k >= j) break;
-                stk[top++] = k;
-                stk[top++] = j;
-                stk[top++] = i;
-                stk[top++] = k;
-            }
+    const int pad_rows = R - (2 * n - 1);   // rows past the tree are -1
+    if (pad_rows > 0) {
+        const float inv_pad = 1.0f / (float)pad_rows;
+        for (int c = tid; c < nb * pad_rows; c += NT) {
+            const int sbb = div_small(c, pad_rows, inv_pad);
+            const int r = 2 * n - 1 + (c - sbb * pad_rows);
+            int32_t *o = spans + ((size_t)sid[sbb] * R + r) * 2;
+            o[0] = -1;
+            o[1] = -1;
         }
     }
+    if (best != nullptr)
+        for (int sb = tid; sb < nb; sb += NT) best[sid[sb]] = (float)cx.beta(sb)[n];
+    // Wave w walks sentences w, w+NW, ... with its own scratch slot.
+    int32_t *myscr = scr + (size_t)wave * cky_scratch_ints(n);
+    // An LDS chart (8 (n+1)^2 bytes <= 160 KiB) means n <= 142: 5 nodes per lane.
+    constexpr int PER_LANE = SPILL ? (2 * CRF_MAX_LEN + 63) / 64 : (2 * kMaxLenInLds + 63) / 64;
+    for (int sb = wave; sb < nb; sb += NW)
+        backtrace<PER_LANE>(cx, sb, spans + (size_t)sid[sb] * R * 2, myscr);
+}
+
+// Workgroups of 256, 512 or 1024 threads (the plan's choice) share one
+// build of each kernel.
+template <bool REV, bool LAB, bool SPILL>
+__global__ __launch_bounds__(kThreadsMax) void inside_kernel(KernelPlan p, const float *__restrict__ scores,
+                                                             const float *__restrict__ grad,
+                                                             float *__restrict__ logZ,
+                                                             float *__restrict__ marg) {
+    extern __shared__ __align__(16) char smem_raw[];
+    inside_block<REV, LAB, SPILL>(p, blockIdx.x, smem_raw, scores, grad, logZ, marg);
+}
+
+template <bool SPILL>
+__global__ __launch_bounds__(kThreadsMax) void cky_kernel(KernelPlan p, const float *__restrict__ scores,
+                                                          int32_t *__restrict__ spans,
+                                                          float *__restrict__ best) {
+    extern __shared__ __align__(16) char smem_raw[];
+    cky_block<SPILL>(p, blockIdx.x, smem_raw, scores, spans, best);
+}
+
+// The whole pass -- inside, reverse and CKY -- in one launch: inside and CKY
+// bundles alternate in blockIdx order (both lists are most expensive first),
+// so the two halves run side by side instead of one after the other.
+__global__ __launch_bounds__(kThreadsMax) void parse_kernel(KernelPlan p, const float *__restrict__ scores,
+                                                            const float *__restrict__ grad,
+                                                            float *__restrict__ logZ,
+                                                            float *__restrict__ marg,
+                                                            int32_t *__restrict__ spans,
+                                                            float *__restrict__ best) {
+    extern __shared__ __align__(16) char smem_raw[];
+    const int ni = p.inside.n_bundles, nc = p.cky.n_bundles;
+    const int both = 2 * min(ni, nc);
+    const int b = blockIdx.x;
+    bool inside;
+    int idx;
+    if (b < both) {
+        inside = (b & 1) == 0;
+        idx = b >> 1;
+    } else {
+        inside = ni > nc;
+        idx = b - both + min(ni, nc);
+    }
+    if (inside)
+        inside_block<true, false, false>(p, idx, smem_raw, scores, grad, logZ, marg);
+    else
+        cky_block<false>(p, idx, smem_raw, scores, spans, best);
 }
 
 }  // namespace
@@ -519,7 +847,7 @@ hipError_t set_kernel_attributes(int max_lds_bytes) {
     const void *fns[] = {
         (const void *)inside_kernel<false, false, false>, (const void *)inside_kernel<true, false, false>,
         (const void *)inside_kernel<false, true, false>,  (const void *)inside_kernel<true, true, false>,
-        (const void *)cky_kernel<false>,
+        (const void *)cky_kernel<false>,                  (const void *)parse_kernel,
     };
     for (const void *f : fns) {
         hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, max_lds_bytes);
@@ -528,29 +856,28 @@ hipError_t set_kernel_attributes(int max_lds_bytes) {
     return hipSuccess;
 }
 
+template <bool SPILL>
+static void launch_inside_k(const KernelPlan &p, dim3 grid, int threads, size_t lds, hipStream_t s,
+                            const float *scores, const float *grad, float *logZ, float *marg) {
+    const bool rev = marg != nullptr, lab = p.L > 1;
+    const dim3 block(threads);
+    if (rev && lab) hipLaunchKernelGGL((inside_kernel<true, true, SPILL>), grid, block, lds, s, p, scores, grad, logZ, marg);
+    else if (rev) hipLaunchKernelGGL((inside_kernel<true, false, SPILL>), grid, block, lds, s, p, scores, grad, logZ, marg);
+    else if (lab) hipLaunchKernelGGL((inside_kernel<false, true, SPILL>), grid, block, lds, s, p, scores, grad, logZ, marg);
+    else hipLaunchKernelGGL((inside_kernel<false, false, SPILL>), grid, block, lds, s, p, scores, grad, logZ, marg);
+}
+
 hipError_t launch_inside(const KernelPlan &p, const float *scores, const float *grad, float *logZ,
                          float *marg, hipStream_t stream) {
-    const bool rev = marg != nullptr;
-    const bool lab = p.L > 1;
     const Schedule &q = p.inside;
-    if (q.n_lds > 0) {
-        dim3 grid(q.n_lds), block(NT);
-        const size_t lds = (size_t)q.lds_bytes;
-        if (rev && lab) hipLaunchKernelGGL((inside_kernel<true, true, false>), grid, block, lds, stream, p, scores, grad, logZ, marg);
-        else if (rev) hipLaunchKernelGGL((inside_kernel<true, false, false>), grid, block, lds, stream, p, scores, grad, logZ, marg);
-        else if (lab) hipLaunchKernelGGL((inside_kernel<false, true, false>), grid, block, lds, stream, p, scores, grad, logZ, marg);
-        else hipLaunchKernelGGL((inside_kernel<false, false, false>), grid, block, lds, stream, p, scores, grad, logZ, marg);
-        hipError_t e = hipGetLastError();
-        if (e != hipSuccess) return e;
+    hipError_t e;
+    if (q.n_bundles > 0) {
+        launch_inside_k<false>(p, dim3(q.n_bundles), q.threads, q.lds_bytes, stream, scores, grad, logZ, marg);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     if (q.n_spill > 0) {
-        dim3 grid(q.n_spill), block(NT);
-        if (rev && lab) hipLaunchKernelGGL((inside_kernel<true, true, true>), grid, block, 0, stream, p, scores, grad, logZ, marg);
-        else if (rev) hipLaunchKernelGGL((inside_kernel<true, false, true>), grid, block, 0, stream, p, scores, grad, logZ, marg);
-        else if (lab) hipLaunchKernelGGL((inside_kernel<false, true, true>), grid, block, 0, stream, p, scores, grad, logZ, marg);
-        else hipLaunchKernelGGL((inside_kernel<false, false, true>), grid, block, 0, stream, p, scores, grad, logZ, marg);
-        hipError_t e = hipGetLastError();
-        if (e != hipSuccess) return e;
+        launch_inside_k<true>(p, dim3(q.n_spill), kThreadsMax, 0, stream, scores, grad, logZ, marg);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     return hipSuccess;
 }
@@ -558,15 +885,38 @@ hipError_t launch_inside(const KernelPlan &p, const float *scores, const float *
 hipError_t launch_cky(const KernelPlan &p, const float *scores, int32_t *spans, float *best,
                       hipStream_t stream) {
     const Schedule &q = p.cky;
-    if (q.n_lds > 0) {
-        hipLaunchKernelGGL((cky_kernel<false>), dim3(q.n_lds), dim3(NT), (size_t)q.lds_bytes, stream, p, scores, spans, best);
-        hipError_t e = hipGetLastError();
-        if (e != hipSuccess) return e;
+    hipError_t e;
+    if (q.n_bundles > 0) {
+        hipLaunchKernelGGL((cky_kernel<false>), dim3(q.n_bundles), dim3(q.threads), (size_t)q.lds_bytes, stream, p, scores, spans, best);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     if (q.n_spill > 0) {
-        hipLaunchKernelGGL((cky_kernel<true>), dim3(q.n_spill), dim3(NT), 0, stream, p, scores, spans, best);
-        hipError_t e = hipGetLastError();
+        hipLaunchKernelGGL((cky_kernel<true>), dim3(q.n_spill), dim3(kThreadsMax), 0, stream, p, scores, spans, best);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
+hipError_t launch_parse(const KernelPlan &p, const float *scores, const float *grad, float *logZ,
+                        float *marg, int32_t *spans, float *best, hipStream_t stream) {
+    const Schedule &qi = p.inside, &qc = p.cky;
+    if (qi.n_bundles == 0 || qc.n_bundles == 0 || qi.threads != qc.threads || p.L > 1) {
+        hipError_t e = launch_inside(p, scores, grad, logZ, marg, stream);
         if (e != hipSuccess) return e;
+        return launch_cky(p, scores, spans, best, stream);
+    }
+    const size_t lds = (size_t)(qi.lds_bytes > qc.lds_bytes ? qi.lds_bytes : qc.lds_bytes);
+    hipLaunchKernelGGL(parse_kernel, dim3(qi.n_bundles + qc.n_bundles), dim3(qi.threads), lds, stream, p,
+                       scores, grad, logZ, marg, spans, best);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    if (qi.n_spill > 0) {
+        launch_inside_k<true>(p, dim3(qi.n_spill), kThreadsMax, 0, stream, scores, grad, logZ, marg);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    if (qc.n_spill > 0) {
+        hipLaunchKernelGGL((cky_kernel<true>), dim3(qc.n_spill), dim3(kThreadsMax), 0, stream, p, scores, spans, best);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     return hipSuccess;
 }

@@ -74,32 +74,110 @@ hipError_t upload(crf_plan *p, const std::vector<T> &v, const T **dst) {
     return e;
 }
 
-// Split the (already ordered) sentence list into LDS and workspace runs for
-// a chart of `bytes(n)` bytes, and lay out the workspace charts.
+// One kind of chart's schedule on the host: equal-length bundles for the LDS
+// kernel, single sentences for the workspace kernel.
 struct HostSchedule {
-    std::vector<int32_t> lds, spill;
-    std::vector<int64_t> off;
+    std::vector<crf::Bundle> bundles;
+    std::vector<int32_t> order;      // sentence ids grouped by bundle
+    std::vector<int32_t> spill;      // sentence ids on the workspace kernel
+    std::vector<int64_t> off;        // their chart offsets in the workspace
     int32_t lds_bytes = 0;
+    int32_t threads = crf::kThreadsDefault;
     int64_t ws_bytes = 0;
 };
 
+// Cost model of one sentence: split points plus a latency term per width
+// step (two sweeps' worth of barrier-separated steps).
+inline double sentence_cost(int n) {
+    const double T = (double)(n + 1) * n * (n - 1) / 6.0;
+    return T + 200.0 * (n - 1);
+}
+
+// `order` is sorted by decreasing length.  `chart(n)` is the chart size of
+// a sentence; each bundled sentence also needs `per_sentence` bytes of
+// tables, and each wavefront of the workgroup `wave_bytes(n)` of scratch.
 template <typename F>
-HostSchedule split(const std::vector<int32_t> &order, const int32_t *len, int64_t lds_cap,
-                   bool force_spill, int64_t ws_base, F bytes) {
+HostSchedule make_schedule(const std::vector<int32_t> &order, const int32_t *len, int lds_cap,
+                           bool force_spill, int64_t ws_base, int per_sentence, F chart,
+                           F spill_chart, F wave_bytes) {
     HostSchedule s;
+    s.threads = crf::kThreadsDefault;
+    if (const char *ev = getenv("CRF_TUNE_THREADS")) {
+        const int t = atoi(ev);
+        if (t == 256 || t == 512 || t == 1024) s.threads = t;
+    }
+    const int nw = s.threads / 64;
+    // LDS of a bundle of `count` sentences of length n.
+    auto bundle_bytes = [&](int n, int64_t count) {
+        return count * (chart(n) + per_sentence) + crf::bundle_extra_bytes(n) +
+               std::min<int64_t>(count, nw) * wave_bytes(n);
+    };
+    // Workgroup LDS budget: half the CU when every eligible sentence fits in
+    // half (two workgroups per CU), else all of it (one).
+    const int64_t half = lds_cap / 2 - 256, full = lds_cap - 256;
+    int64_t biggest = 0;
+    std::vector<int32_t> eligible;
     int64_t cursor = ws_base;
     for (int32_t b : order) {
-        const int64_t need = bytes(len[b]);
-        if (!force_spill && need <= lds_cap && len[b] <= crf::kMaxLenLds) {
-            s.lds.push_back(b);
-            s.lds_bytes = std::max<int32_t>(s.lds_bytes, (int32_t)need);
+        const int n = len[b];
+        const int64_t need = bundle_bytes(n, 1);
+        if (!force_spill && need <= full && n <= crf::kMaxLenInLds) {
+            eligible.push_back(b);
+            biggest = std::max(biggest, need);
         } else {
             s.spill.push_back(b);
             s.off.push_back(cursor);
-            cursor += (need + 255) / 256 * 256;
+            // The kernels' masked tail loads may read up to 64 elements past
+            // a chart; keep a guard band so they stay inside the workspace.
+            cursor += (spill_chart(n) + 1024 + 255) / 256 * 256;
         }
     }
     s.ws_bytes = cursor - ws_base;
+    const bool small = biggest <= half;
+    const int64_t budget = small ? half : full;
+    const int slots = 256 * (small ? 2 : 1);
+
+    // Target cost per bundle: spread the total over the workgroup slots, but
+    // never split below one sentence.
+    double total = 0.0;
+    for (int32_t b : eligible) total += sentence_cost(len[b]);
+    const double target = std::max(total / slots, 1.0);
+
+    struct Tmp { crf::Bundle bd; double cost; };
+    std::vector<Tmp> tmp;
+    size_t a = 0;
+    while (a < eligible.size()) {
+        const int n = len[eligible[a]];
+        size_t e = a;
+        while (e < eligible.size() && len[eligible[e]] == n) ++e;
+        const int count = (int)(e - a);
+        int by_lds = 1;
+        while (by_lds < crf::kMaxBundle && bundle_bytes(n, by_lds + 1) <= budget) ++by_lds;
+        const int by_cost = std::max(1, (int)(target / sentence_cost(n)));
+        const int per = std::min(by_lds, std::max(1, by_cost));
+        const int nbund = (count + per - 1) / per;
+        for (int q = 0; q < nbund; ++q) {
+            const int lo = (int)((int64_t)count * q / nbund), hi = (int)((int64_t)count * (q + 1) / nbund);
+            Tmp t;
+            t.bd.first = (int32_t)(a + lo);
+            t.bd.count = hi - lo;
+            t.bd.n = n;
+            t.bd.pad = 0;
+            t.cost = (hi - lo) * (sentence_cost(n) - 200.0 * (n - 1)) + 200.0 * (n - 1);
+            tmp.push_back(t);
+            s.lds_bytes = std::max<int32_t>(s.lds_bytes, (int32_t)bundle_bytes(n, hi - lo));
+        }
+        a = e;
+    }
+// Most expensive bundles first: workgroups are dispatched in order.
+    std::stable_sort(tmp.begin(), tmp.end(), [](const Tmp &x, const Tmp &y) { return x.cost > y.cost; });
+    for (const Tmp &t : tmp) {
+        crf::Bundle bd = t.bd;
+        const int first = (int)s.order.size();
+        for (int q = 0; q < bd.count; ++q) s.order.push_back(eligible[bd.first + q]);
+        bd.first = first;
+        s.bundles.push_back(bd);
+    }
     return s;
 }
 
@@ -153,8 +231,6 @@ int crf_plan_create(crf_plan **out, const int32_t *lengths_host, int32_t batch, 
     int lds_cap = 0;
     e = hipDeviceGetAttribute(&lds_cap, hipDeviceAttributeMaxSharedMemoryPerBlock, p->device);
     if (e != hipSuccess) { delete p; return hip_fail(e, "hipDeviceGetAttribute"); }
-    // Static LDS of the kernels (reduction scratch) comes out of the same budget.
-    const int64_t lds_avail = (int64_t)lds_cap - 64;
 
     // Longest first; ties keep batch order.
     std::vector<int32_t> order(batch);
@@ -163,10 +239,15 @@ int crf_plan_create(crf_plan **out, const int32_t *lengths_host, int32_t batch, 
                      [&](int32_t a, int32_t b) { return lengths_host[a] > lengths_host[b]; });
 
     const bool force = (flags & CRF_FORCE_SPILL) != 0;
-    HostSchedule si = split(order, lengths_host, lds_avail, force, 0,
-                            [](int n) { return crf::inside_chart_bytes(n); });
-    HostSchedule sc = split(order, lengths_host, lds_avail, force, si.ws_bytes,
-                            [](int n) { return crf::cky_chart_bytes(n); });
+    auto inside_bytes = [](int n) { return crf::inside_chart_bytes(n); };
+    auto cky_bytes = [](int n) { return crf::cky_chart_bytes(n); };
+    auto no_scratch = [](int) { return (int64_t)0; };
+    auto cky_scratch = [](int n) { return (int64_t)4 * crf::cky_scratch_ints(n); };
+    // inside tables: forced sum (f64), gradient (f32), id (i32); cky: id
+    HostSchedule si = make_schedule(order, lengths_host, lds_cap, force, 0, 16, +inside_bytes,
+                                    +inside_bytes, +no_scratch);
+    HostSchedule sc = make_schedule(order, lengths_host, lds_cap, force, si.ws_bytes, 4, +cky_bytes,
+                                    +cky_bytes, +cky_scratch);
     p->ws_bytes = si.ws_bytes + sc.ws_bytes;
 
     std::vector<int32_t> len(lengths_host, lengths_host + batch);
@@ -174,18 +255,22 @@ int crf_plan_create(crf_plan **out, const int32_t *lengths_host, int32_t batch, 
     kp.B = batch;
     kp.n1 = n1;
     kp.L = num_labels;
-    kp.inside.n_lds = (int32_t)si.lds.size();
-    kp.inside.n_spill = (int32_t)si.spill.size();
-    kp.inside.lds_bytes = si.lds_bytes;
-    kp.cky.n_lds = (int32_t)sc.lds.size();
-    kp.cky.n_spill = (int32_t)sc.spill.size();
-    kp.cky.lds_bytes = sc.lds_bytes;
+    auto fill = [](crf::Schedule &q, const HostSchedule &h) {
+        q.n_bundles = (int32_t)h.bundles.size();
+        q.n_spill = (int32_t)h.spill.size();
+        q.lds_bytes = h.lds_bytes;
+        q.threads = h.threads;
+    };
+    fill(kp.inside, si);
+    fill(kp.cky, sc);
 
     if ((e = upload(p, len, &kp.len)) != hipSuccess ||
-        (e = upload(p, si.lds, &kp.inside.order_lds)) != hipSuccess ||
+        (e = upload(p, si.bundles, &kp.inside.bundles)) != hipSuccess ||
+        (e = upload(p, si.order, &kp.inside.order)) != hipSuccess ||
         (e = upload(p, si.spill, &kp.inside.order_spill)) != hipSuccess ||
         (e = upload(p, si.off, &kp.inside.ws_off)) != hipSuccess ||
-        (e = upload(p, sc.lds, &kp.cky.order_lds)) != hipSuccess ||
+        (e = upload(p, sc.bundles, &kp.cky.bundles)) != hipSuccess ||
+        (e = upload(p, sc.order, &kp.cky.order)) != hipSuccess ||
         (e = upload(p, sc.spill, &kp.cky.order_spill)) != hipSuccess ||
         (e = upload(p, sc.off, &kp.cky.ws_off)) != hipSuccess) {
         const int code = (e == hipErrorOutOfMemory) ? CRF_ENOMEM : CRF_EHIP;
@@ -234,7 +319,7 @@ int crf_plan_info(const crf_plan *plan, crf_plan_stats *out) {
     out->n1 = plan->n1;
     out->num_labels = plan->L;
     out->max_len = plan->max_len;
-    out->lds_count = plan->kp.inside.n_lds;
+    out->lds_count = plan->B - plan->kp.inside.n_spill;
     out->spill_count = plan->kp.inside.n_spill;
     out->workspace_bytes = plan->ws_bytes;
     out->lds_bytes_inside = plan->kp.inside.lds_bytes;
@@ -277,6 +362,21 @@ int crf_inside_fwd_bwd(const crf_plan *plan, const float *scores, const float *g
 int crf_inside_bwd(const crf_plan *plan, const float *scores, const float *grad_logZ,
                    float *marginals, void *stream) {
     return crf_inside_fwd_bwd(plan, scores, grad_logZ, nullptr, marginals, stream);
+}
+
+int crf_inside_fwd_bwd_cky(const crf_plan *plan, const float *scores, const float *grad_logZ,
+                           float *logZ, float *marginals, int32_t *spans, float *best,
+                           void *stream) {
+    if (plan == nullptr) return fail(CRF_EINVAL, "plan is NULL");
+    if (scores == nullptr || marginals == nullptr || spans == nullptr)
+        return fail(CRF_EINVAL, "scores/marginals/spans is NULL");
+    if (plan->L != 1)
+        return fail(CRF_EUNSUPPORTED, "CKY decode of labelled scores (L = %d)", plan->L);
+    int rc = check_device(plan);
+    if (rc != CRF_OK) return rc;
+    hipError_t e = crf::launch_parse(plan->kp, scores, grad_logZ, logZ, marginals, spans, best,
+                                     static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? ok() : hip_fail(e, "crf_inside_fwd_bwd_cky launch");
 }
 
 int crf_cky_decode(const crf_plan *plan, const float *scores, int32_t *spans, float *best,

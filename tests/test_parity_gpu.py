@@ -195,6 +195,21 @@ def test_labeled_small(torch):
     check_marg(out["marg"], mu, b.lengths, b.n1, labeled=True)
 
 
+@pytest.mark.parametrize("name", ["tiny", "mixed"])
+def test_fused_call_matches_separate_calls(torch, name):
+    # one launch for inside + reverse + CKY gives the separate calls' bits
+    b = W.make(name)
+    dev = torch.device("cuda", 0)
+    s = torch.from_numpy(b.scores).to(dev)
+    with B.Plan(b.lengths, device=dev) as plan:
+        lz1, mu1 = plan.inside_fwd_bwd(s)
+        sp1, be1 = plan.cky_decode(s)
+        lz2, mu2, sp2, be2 = plan.parse(s)
+        torch.cuda.synchronize()
+    assert torch.equal(lz1, lz2) and torch.equal(mu1, mu2)
+    assert torch.equal(sp1, sp2) and torch.equal(be1, be2)
+
+
 def test_decode_rejects_labeled_plan(torch):
     b = W.custom([3], seed=1, labels=2)
     dev = torch.device("cuda", 0)
@@ -202,6 +217,9 @@ def test_decode_rejects_labeled_plan(torch):
     with B.Plan(b.lengths, num_labels=2, device=dev) as plan:
         with pytest.raises(B.CrfError) as ei:
             plan.cky_decode(s)
+        assert ei.value.status == B.CRF_EUNSUPPORTED
+        with pytest.raises(B.CrfError) as ei:
+            plan.parse(s)
         assert ei.value.status == B.CRF_EUNSUPPORTED
 
 
