@@ -8,15 +8,19 @@ line.
 
   python bench.py [--steps K] [--warmup W] [--workload mixed] [--no-cpu-baseline]
 
-Roofline: the dominant kernel is the fused inside+reverse kernel; it is bound
-by plain vector-ALU work (log-sum-exp over split points), not HBM and not
-MFMA.  Its algorithmic work per sentence of n words, with T(n) = (n+1)n(n-1)/6
-split points and P(n) = n(n+1)/2 spans:
-  forward  per split 1 exp + 4 VALU, per span 1 log + 2 VALU
-  reverse  per split 1 exp + 4 VALU, per span 2 VALU
-counting a transcendental as 4 issue slots (quarter rate), i.e. 16 slots per
-split and 8 per span.  Peak = 256 CUs x 64 lanes x 2.4 GHz = 39.32 T lane
-slots/s.  CKY: 3 slots per split (add, compare, select) and 1 per span.
+Roofline: the hot path is one launch (parse_kernel: inside, reverse and CKY
+workgroups interleaved).  It is bound by plain vector-ALU work and by the
+dependency chain of width steps, not by HBM and not by MFMA.  Algorithmic work
+per sentence of n words, with T(n) = (n+1)n(n-1)/6 split points and
+P(n) = n(n+1)/2 spans, in VALU issue slots (a transcendental v_exp/v_log/v_rcp
+costs 2 slots, as measured on gfx950):
+  inside   per split: add, max, sub, exp, add          = 6
+           per span:  log, 2 adds                      = 4
+  reverse  per split: sub, exp, mul, 2 adds            = 6
+           per span:  add, rcp                         = 2
+  CKY      per split: add, compare, select             = 3
+           per span:  add                              = 1
+Peak = 256 CUs x 64 lanes x 2.4 GHz = 39.32 T lane-slots/s.
 """
 import argparse
 import ctypes
@@ -32,6 +36,10 @@ sys.path.insert(0, ROOT)
 
 PEAK_SLOTS = 256 * 64 * 2.4e9   # VALU lane-slots per second
 HBM_PEAK = 8.0e12               # bytes per second
+# HBM bytes per launch of the timed kernel from rocprofv3 FETCH_SIZE / WRITE_SIZE,
+# scaled by the same counters on a plain copy of known size, keyed by workload
+# and by the kernel source they were taken on (reported only while it matches).
+MEASURED_TRAFFIC = {"mixed": (67.19e6, "0352a9fa7ec8b914")}
 METRIC = "sentences/sec for inside fwd+bwd and CKY decode; % of binding roofline"
 
 
@@ -39,14 +47,26 @@ def work_model(lengths, labels=1):
     n = lengths.astype(np.int64)
     T = (n + 1) * n * (n - 1) // 6
     P = n * (n + 1) // 2
-    slots_inside = 16 * T.sum() + 8 * P.sum()
+    slots_inside = 12 * T.sum() + 6 * P.sum()
     if labels > 1:   # label log-sum-exp and per-label marginals: (exp + 3) + (exp + 2) per label
-        slots_inside += P.sum() * labels * (4 + 3 + 4 + 2)
+        slots_inside += P.sum() * labels * (2 + 3 + 2 + 2)
     slots_cky = 3 * T.sum() + P.sum()
     bytes_inside = 4 * P.sum() * labels * 2 + 4 * len(n)      # scores in, marginals out, logZ
     bytes_cky = 4 * P.sum() + 8 * (2 * n - 1).sum() + 4 * len(n)
     return dict(T=int(T.sum()), P=int(P.sum()), slots_inside=int(slots_inside),
                 slots_cky=int(slots_cky), bytes_inside=int(bytes_inside), bytes_cky=int(bytes_cky))
+
+
+def measured_traffic(workload):
+    import hashlib
+
+    if workload not in MEASURED_TRAFFIC:
+        return None
+    nbytes, digest = MEASURED_TRAFFIC[workload]
+    src = os.path.join(ROOT, "paper_2008_03736_amd", "csrc", "crf_kernels.hip")
+    with open(src, "rb") as f:
+        now = hashlib.sha256(f.read()).hexdigest()[:16]
+    return nbytes if now == digest else None
 
 
 def cpu_baseline(batch, threads, budget_s=12.0):
@@ -79,6 +99,9 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-threads", type=int, default=min(16, os.cpu_count() or 1))
+    ap.add_argument("--copy-mib", type=int, default=0,
+                    help="after timing, run a plain device copy of this many MiB a few times "
+                         "(a known-size kernel to scale HBM counters by)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); "
@@ -121,10 +144,12 @@ def main():
         if rc:
             raise B.CrfError(rc, "crf_cky_decode")
 
-    def step():
-        fwd_bwd()
-        if decode:
-            cky()
+    def parse():
+        rc = lib.crf_inside_fwd_bwd_cky(h, a_scores, None, a_logz, a_marg, a_spans, a_best, sp)
+        if rc:
+            raise B.CrfError(rc, "crf_inside_fwd_bwd_cky")
+
+    step = parse if decode else fwd_bwd
 
     for _ in range(args.warmup):
         step()
@@ -138,7 +163,7 @@ def main():
     torch.cuda.synchronize()
     ms_per_step = e0.elapsed_time(e1) / args.steps
 
-    # Per-kernel durations, one event pair per launch on the launch stream.
+    # Per-launch durations, one event pair per launch on the launch stream.
     def per_launch_ms(fn, reps):
         evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
                for _ in range(reps)]
@@ -150,25 +175,47 @@ def main():
         return float(np.mean([a.elapsed_time(b) for a, b in evs]))
 
     reps = max(10, args.steps)
+    t_step = per_launch_ms(step, reps)
     t_inside = per_launch_ms(fwd_bwd, reps)
     t_cky = per_launch_ms(cky, reps) if decode else None
 
-    wm = work_model(batch.lengths, labels)
-    ach = wm["slots_inside"] / (t_inside * 1e-3)
-    roof = {"bound": "alu", "kernel": "inside_kernel<rev=1> (fused inside + reverse)",
-            "achieved": round(ach / 1e12, 3), "peak": round(PEAK_SLOTS / 1e12, 3),
-            "unit": "T VALU lane-slots/s", "frac": round(ach / PEAK_SLOTS, 4),
-            "traffic": None, "avg_ms": round(t_inside, 4),
-            "algorithmic_slots": wm["slots_inside"], "algorithmic_bytes": wm["bytes_inside"],
-            "hbm_frac": round(wm["bytes_inside"] / (t_inside * 1e-3) / HBM_PEAK, 4)}
-    extra = {}
+    # The longest sentence alone: the dependency chain no batch can beat.
+    longest = int(np.argmax(batch.lengths))
+    one = W.subset(batch, [longest])
+    s1 = torch.from_numpy(one.scores).to(dev)
+    plan1 = B.Plan(one.lengths, n1=one.n1, num_labels=labels, device=dev)
     if decode:
-        ach_c = wm["slots_cky"] / (t_cky * 1e-3)
-        extra["decode"] = {"bound": "alu", "kernel": "cky_kernel (float64 chart)",
-                           "avg_ms": round(t_cky, 4), "achieved": round(ach_c / 1e12, 3),
-                           "peak": round(PEAK_SLOTS / 1e12, 3), "frac": round(ach_c / PEAK_SLOTS, 4),
-                           "sentences_per_s": round(batch.B / (t_cky * 1e-3), 1)}
-    extra["fwd_bwd_sentences_per_s"] = round(batch.B / (t_inside * 1e-3), 1)
+        t_one = per_launch_ms(lambda: plan1.parse(s1), reps)
+    else:
+        t_one = per_launch_ms(lambda: plan1.inside_fwd_bwd(s1), reps)
+    plan1.close()
+
+    wm = work_model(batch.lengths, labels)
+    slots = wm["slots_inside"] + (wm["slots_cky"] if decode else 0)
+    hbm = wm["bytes_inside"] + (wm["bytes_cky"] if decode else 0)
+    ach = slots / (t_step * 1e-3)
+    roof = {"bound": "alu",
+            "kernel": "parse_kernel (inside + reverse + CKY, one launch)" if decode else "inside_kernel<rev>",
+            "achieved": round(ach / 1e12, 4), "peak": round(PEAK_SLOTS / 1e12, 3),
+            "unit": "T VALU lane-slots/s", "frac": round(ach / PEAK_SLOTS, 5),
+            "traffic": measured_traffic(batch.name) if decode else None, "avg_ms": round(t_step, 4),
+            "algorithmic_slots": int(slots), "algorithmic_bytes": int(hbm),
+            "hbm_frac": round(hbm / (t_step * 1e-3) / HBM_PEAK, 5),
+            "latency_floor_ms": round(t_one, 4),
+            "latency_floor": f"the longest sentence (n={int(one.lengths[0])}) alone"}
+    extra = {"fwd_bwd_ms": round(t_inside, 4),
+             "fwd_bwd_sentences_per_s": round(batch.B / (t_inside * 1e-3), 1)}
+    if decode:
+        extra["decode_ms"] = round(t_cky, 4)
+        extra["decode_sentences_per_s"] = round(batch.B / (t_cky * 1e-3), 1)
+
+    if args.copy_mib > 0:
+        src = torch.empty(args.copy_mib << 18, dtype=torch.float32, device=dev).fill_(1.0)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     cb = None if args.no_cpu_baseline else cpu_baseline(batch, args.cpu_threads)
     info = plan.info
