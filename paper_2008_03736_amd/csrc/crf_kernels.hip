@@ -227,7 +227,9 @@ __device__ __forceinline__ void span_step(const Bundle_ctx<T> &bx, int w, const 
     const int n = bx.n, ld = bx.ld;
     const int K = w - 1, S = n - w + 1;
     const int total = bx.nb * S * G;
+    const int wq0 = __builtin_amdgcn_readfirstlane(tid & ~63);   // this wavefront's first thread
     for (int f0 = 0; f0 < total; f0 += nt) {
+        if (f0 + wq0 >= total) break;   // no span for this wavefront in this pass or later
         const bool act = f0 + tid < total;
         const Lane_at at = lane_at<G>(act ? f0 + tid : total - 1, S, magic);
         const int i = at.i, l = at.l, j = i + w;
@@ -373,6 +375,40 @@ __device__ __forceinline__ void for_cells(int nb, int n, F &&f) {
     }
 }
 
+// The same walk, U cells per thread at a time: their U loads are issued
+// together (one memory latency per U cells instead of one per cell), then
+// `use` consumes them.
+template <int U, typename LD, typename F>
+__device__ __forceinline__ void for_cells_loaded(int nb, int n, LD &&load, F &&use) {
+    const int NT = blockDim.x;
+    const int nn = n * n;
+    const int total = nb * nn;
+    const float inv_nn = 1.0f / (float)nn, inv_n = 1.0f / (float)n;
+    using V = decltype(load(0, 0, 1));
+    for (int c0 = threadIdx.x; c0 < total; c0 += NT * U) {
+        int sbv[U], iv[U], jv[U];
+        bool ok[U];
+        V v[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int c = c0 + u * NT;
+            const int cc = c < total ? c : 0;
+            const int sb = div_small(cc, nn, inv_nn);
+            const int rem = cc - sb * nn;
+            const int i = div_small(rem, n, inv_n);
+            const int j = rem - i * n + 1;
+            sbv[u] = sb;
+            iv[u] = i;
+            jv[u] = j;
+            ok[u] = c < total && j > i;
+            v[u] = ok[u] ? load(sb, i, j) : V(0);
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            if (ok[u]) use(sbv[u], iv[u], jv[u], v[u]);
+    }
+}
+
 // Fixed-order float64 sum over a wavefront (same result in every lane).
 __device__ __forceinline__ double wave_sum_d(double v) {
     for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
@@ -449,15 +485,16 @@ __device__ __forceinline__ void inside_block(const KernelPlan &p, int block, cha
     // Prologue: scores of every valid cell into the charts (log2-scaled);
     // forced spans get 0 in the chart and park their natural-unit score in
     // the adjoint square's lower triangle ([i+1][i]; the root at [n][0]).
-    for_cells(nb, n, [&](int sb, int i, int j) {
+    auto load_score = [&](int sb, int i, int j) -> float {
+        const float *srow = scores + (size_t)sid[sb] * sent_stride + (size_t)i * row_stride;
+        if constexpr (LAB)
+            return label_lse2(srow + (size_t)j * L, L) * (float)LN2_D;
+        else
+            return srow[j];
+    };
+    for_cells_loaded<LAB ? 1 : 8>(nb, n, load_score, [&](int sb, int i, int j, float s) {
         float *al = chart0 + (size_t)sb * cstride;
         float *ad = al + (size_t)ld * ld;
-        const float *srow = scores + (size_t)sid[sb] * sent_stride + (size_t)i * row_stride;
-        float s;
-        if constexpr (LAB)
-            s = label_lse2(srow + (size_t)j * L, L) * (float)LN2_D;
-        else
-            s = srow[j];
         if (j == i + 1) {
             al[i * ld + j] = 0.f;
             al[j * ld + i] = 0.f;
@@ -499,11 +536,13 @@ __device__ __forceinline__ void inside_block(const KernelPlan &p, int block, cha
     inside_sweep<true, SPILL>(bx, gv, magic);
 
     // Epilogue: marginals of the valid cells (coalesced stores along rows).
-    for_cells(nb, n, [&](int sb, int i, int j) {
+    auto load_mu = [&](int sb, int i, int j) -> float {
         const float *ad = chart0 + (size_t)sb * cstride + (size_t)ld * ld;
-        const size_t rowoff = (size_t)sid[sb] * sent_stride + (size_t)i * row_stride;
         const bool forced_span = (j == i + 1) || (i == 0 && j == n);
-        const float mu = forced_span ? gv[sb] : ad[i * ld + j] + ad[j * ld + i];
+        return forced_span ? gv[sb] : ad[i * ld + j] + ad[j * ld + i];
+    };
+    for_cells_loaded<LAB ? 1 : 8>(nb, n, load_mu, [&](int sb, int i, int j, float mu) {
+        const size_t rowoff = (size_t)sid[sb] * sent_stride + (size_t)i * row_stride;
         if constexpr (LAB) {
             const float *s = scores + rowoff + (size_t)j * L;
             const float lse2 = label_lse2(s, L);
@@ -534,7 +573,9 @@ __device__ __forceinline__ void cky_step(const Cky_ctx &cx, int w, uint32_t magi
     const int n = cx.n, ld = cx.ld;
     const int K = w - 1, S = n - w + 1;
     const int total = cx.nb * S * G;
+    const int wq0 = __builtin_amdgcn_readfirstlane(tid & ~63);
     for (int f0 = 0; f0 < total; f0 += nt) {
+        if (f0 + wq0 >= total) break;
         const bool act = f0 + tid < total;
         const Lane_at at = lane_at<G>(act ? f0 + tid : total - 1, S, magic);
         const int i = at.i, l = at.l, j = i + w;
@@ -760,9 +801,12 @@ __device__ __forceinline__ void cky_block(const KernelPlan &p, int block, char *
     const Cky_ctx cx{chart0, cstride, n, ld, nb};
     __syncthreads();
 
-    for_cells(nb, n, [&](int sb, int i, int j) {
+    auto load_score = [&](int sb, int i, int j) -> float {
+        return scores[((size_t)sid[sb] * N1 + i) * N1 + j];
+    };
+    for_cells_loaded<8>(nb, n, load_score, [&](int sb, int i, int j, float sf) {
         double *be = cx.beta(sb);
-        const double s = (double)scores[((size_t)sid[sb] * N1 + i) * N1 + j];
+        const double s = (double)sf;
         be[i * ld + j] = s;
         if (j == i + 1) be[j * ld + i] = s;
     });
