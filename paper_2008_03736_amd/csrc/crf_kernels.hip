@@ -173,21 +173,13 @@ constexpr float NEG = -1.0e30f;
 __device__ __forceinline__ int next_pow2(int x) { return x <= 1 ? 1 : 1 << (32 - __builtin_clz(x - 1)); }
 __device__ __forceinline__ int floor_pow2(int x) { return x <= 1 ? 1 : 1 << (31 - __builtin_clz(x)); }
 
-// Splits per lane: the LDS kernels unroll up to 8; the workspace kernels
-// (long sentences) up to 16.
-constexpr int CMAX_LDS = 8, CMAX_WIDE = 16;
-
-// Lanes per span for one width step: as many as keep the step's spans within
-// one pass over the workgroup, never more than the K split points need, and
-// at least enough that no lane takes more than cmax of them.
-__device__ __forceinline__ int pick_lanes(int K, int spans, int nt, int cmax) {
-    int g = 1;
-    while (g < 64 && spans * (g * 2) <= nt) g <<= 1;
-    g = min(g, next_pow2(K));
-    g = max(g, next_pow2((K + cmax - 1) / cmax));
-    return min(g, 64);
-}
-
+// Step shapes.  Every distinct (lanes per span G, terms per lane C) is its
+// own unrolled body, and entering one a sweep has not run yet refills the
+// instruction cache (thousands of cycles), so sweeps use few shapes: K <= 8
+// splits take G = 1 and C in {1, 2, 4, 8}; wider spans take C = 8 and
+// G = next_pow2(ceil(K / 8)) up to 64, then C = 16 (workspace charts only).
+// C is rounded up: terms c >= C/2 may fall past the K splits and are masked
+// (for K > 8, ceil(K / G) > 4).
 // ---------------------------------------------------------------------------
 // Per-bundle context: nb sentences of length n; sentence sb's chart starts at
 // chart0 + sb * cstride (elements).
@@ -217,10 +209,11 @@ __device__ __forceinline__ Lane_at lane_at(int f, int S, uint32_t magic) {
 
 // One width of the inside (REV = false) or reverse (REV = true) sweep for
 // every sentence of the bundle.  Lane l of a span takes split offsets
-// ko = l + c*G, c < C (split k = i+1+ko); C = ceil(K/G), so only the last one
-// can fall past K (or all past the true count when MASK_ALL, used when C is
-// rounded up).  gv: per-sentence upstream gradient (LDS).
-template <int G, int C, bool MASK_ALL, bool REV, typename T>
+// ko = l + c*G, c < C (split k = i+1+ko); terms c >= MF may fall past K:
+// they count as exp2(-inf) = 0, read cells at most (C - MF)*G columns past
+// the span's last split, and write nothing in the reverse sweep.
+// gv: per-sentence upstream gradient (LDS).
+template <int G, int C, int MF, bool REV, typename T>
 __device__ __forceinline__ void span_step(const Bundle_ctx<T> &bx, int w, const float *gv,
                                           uint32_t magic) {
     const int tid = threadIdx.x, nt = blockDim.x;
@@ -252,8 +245,7 @@ __device__ __forceinline__ void span_step(const Bundle_ctx<T> &bx, int w, const 
         // forward: the span's (log2-scaled) score; reverse: its adjoint
         const float extra = !REV ? al[dia] : (w == n) ? gv[at.sb] : ad[dia] + ad[mir];
 #pragma unroll
-        for (int c = 0; c < C; ++c)
-            if (MASK_ALL || c == C - 1) x[c] = (l + c * G < K) ? x[c] : NEG;
+        for (int c = MF; c < C; ++c) x[c] = (l + c * G < K) ? x[c] : NEG;
         float m = x[0];
 #pragma unroll
         for (int c = 1; c < C; ++c) m = fmax_nn(m, x[c]);
@@ -281,7 +273,7 @@ __device__ __forceinline__ void span_step(const Bundle_ctx<T> &bx, int w, const 
             const float coef = extra * sc * __builtin_amdgcn_rcpf(sg);
 #pragma unroll
             for (int c = 0; c < C; ++c) {
-                if ((MASK_ALL || c == C - 1) && l + c * G >= K) continue;
+                if (c >= MF && l + c * G >= K) continue;
                 const float v = coef * t[c];
                 ad[rowo + c * G] = accl[c] + v;
                 ad[colo + c * G] = accr[c] + v;
@@ -290,20 +282,19 @@ __device__ __forceinline__ void span_step(const Bundle_ctx<T> &bx, int w, const 
     }
 }
 
-// Lanes per span and splits per lane of a width step.
+// Lanes per span and split terms per lane of a width step (K = w - 1).
 struct Step_shape {
     int G, C;
 };
-template <bool WIDE>
-__device__ __forceinline__ Step_shape step_shape(int n, int nb, int w) {
+__device__ __forceinline__ Step_shape step_shape(int w) {
     const int K = w - 1;
-    const int G = pick_lanes(K, nb * (n - w + 1), blockDim.x, WIDE ? CMAX_WIDE : CMAX_LDS);
-    return Step_shape{G, (K + G - 1) >> __builtin_ctz(G)};
+    if (K <= 8) return Step_shape{1, K <= 1 ? 1 : K <= 2 ? 2 : K <= 4 ? 4 : 8};
+    const int g = next_pow2((K + 7) / 8);
+    return g <= 64 ? Step_shape{g, 8} : Step_shape{64, 16};
 }
-
 // A run of widths w0, w0+dir, ... (excluding w1) sharing one step shape:
 // a tight loop with no dispatch.  magic[S] = div_magic(S) (LDS table).
-template <int G, int C, bool MASK_ALL, bool REV, typename T>
+template <int G, int C, int MF, bool REV, typename T>
 __device__ __forceinline__ void inside_run(const Bundle_ctx<T> &bx, int w0, int w1, int dir,
                                         const float *gv, const uint32_t *magic) {
     // magic[S] for the next width is fetched one step ahead (S = n-w+1 stays
@@ -311,48 +302,58 @@ __device__ __forceinline__ void inside_run(const Bundle_ctx<T> &bx, int w0, int 
     uint32_t mg_cur = magic[bx.n - w0 + 1];
     for (int w = w0; w != w1; w += dir) {
         const uint32_t mg_next = magic[bx.n - (w + dir) + 1];
-        span_step<G, C, MASK_ALL, REV>(bx, w, gv, mg_cur);
+        span_step<G, C, MF, REV>(bx, w, gv, mg_cur);
         __syncthreads();
         mg_cur = mg_next;
     }
 }
 
-// All widths of one sweep: forward 2..n, reverse n..2.
+// Calls RUN(G, C, MF) for a step shape (C rounded up to a power of two:
+// terms c >= C/2 may fall past K).
+#define CRF_DISPATCH_SHAPE(SH, RUN)                      \
+    do {                                                 \
+        if ((SH).G == 1) {                               \
+            switch ((SH).C) {                            \
+                case 1: RUN(1, 1, 0); break;             \
+                case 2: RUN(1, 2, 1); break;             \
+                case 4: RUN(1, 4, 2); break;             \
+                default: RUN(1, 8, 4); break;            \
+            }                                            \
+        } else {                                         \
+            switch ((SH).G) {                            \
+                case 2: RUN(2, 8, 4); break;             \
+                case 4: RUN(4, 8, 4); break;             \
+                case 8: RUN(8, 8, 4); break;             \
+                case 16: RUN(16, 8, 4); break;           \
+                case 32: RUN(32, 8, 4); break;           \
+                default:                                 \
+                    if (!WIDE || (SH).C == 8) RUN(64, 8, 4); \
+                    else RUN(64, 16, 8);                 \
+                    break;                               \
+            }                                            \
+        }                                                \
+    } while (0)
+
+// All widths of one sweep: forward 2..n, reverse n..2, one dispatch per run
+// of widths sharing a step shape.
+// WIDE: workspace charts (longer sentences), which may need 16 terms per lane.
 template <bool REV, bool WIDE, typename T>
 __device__ __forceinline__ void inside_sweep(const Bundle_ctx<T> &bx, const float *gv,
                                              const uint32_t *magic) {
-    const int n = bx.n, nb = bx.nb;
+    const int n = bx.n;
     const int dir = REV ? -1 : 1, wend = REV ? 1 : n + 1;
     int w = REV ? n : 2;
     while (w != wend) {
-        const Step_shape sh = step_shape<WIDE>(n, nb, w);
+        const Step_shape sh = step_shape(w);
         int w2 = w + dir;
         while (w2 != wend) {
-            const Step_shape s2 = step_shape<WIDE>(n, nb, w2);
+            const Step_shape s2 = step_shape(w2);
             if (s2.G != sh.G || s2.C != sh.C) break;
             w2 += dir;
         }
-#define CRF_RUN(GG)                                                                             \
-    case GG:                                                                                    \
-        switch (sh.C) {                                                                         \
-            case 1: inside_run<GG, 1, false, REV>(bx, w, w2, dir, gv, magic); break;            \
-            case 2: inside_run<GG, 2, false, REV>(bx, w, w2, dir, gv, magic); break;            \
-            case 3: inside_run<GG, 3, false, REV>(bx, w, w2, dir, gv, magic); break;            \
-            case 4: inside_run<GG, 4, false, REV>(bx, w, w2, dir, gv, magic); break;            \
-            case 5: inside_run<GG, 5, false, REV>(bx, w, w2, dir, gv, magic); break;            \
-            case 6: inside_run<GG, 6, false, REV>(bx, w, w2, dir, gv, magic); break;            \
-            case 7: inside_run<GG, 7, false, REV>(bx, w, w2, dir, gv, magic); break;            \
-            case 8: inside_run<GG, 8, false, REV>(bx, w, w2, dir, gv, magic); break;            \
-            default:                                                                            \
-                if constexpr (WIDE) inside_run<GG, 16, true, REV>(bx, w, w2, dir, gv, magic);   \
-                break;                                                                          \
-        }                                                                                       \
-        break;
-        switch (sh.G) {
-            CRF_RUN(1) CRF_RUN(2) CRF_RUN(4) CRF_RUN(8) CRF_RUN(16) CRF_RUN(32) CRF_RUN(64)
-            default: break;
-        }
-#undef CRF_RUN
+#define CRF_INSIDE_RUN(GG, CC, MM) inside_run<GG, (WIDE || CC <= 8) ? CC : 8, (WIDE || CC <= 8) ? MM : 4, REV>(bx, w, w2, dir, gv, magic)
+        CRF_DISPATCH_SHAPE(sh, CRF_INSIDE_RUN);
+#undef CRF_INSIDE_RUN
         w = w2;
     }
 }
@@ -567,7 +568,7 @@ struct Cky_ctx {
 
 // One width: float64 max-plus, beta(i,j) = (max_k fl(beta(i,k) + beta(k,j)))
 // + s(i,j).  The split chosen is not stored: the backtrace recomputes it.
-template <int G, int C, bool MASK_ALL>
+template <int G, int C, int MF>
 __device__ __forceinline__ void cky_step(const Cky_ctx &cx, int w, uint32_t magic) {
     const int tid = threadIdx.x, nt = blockDim.x;
     const int n = cx.n, ld = cx.ld;
@@ -586,10 +587,9 @@ __device__ __forceinline__ void cky_step(const Cky_ctx &cx, int w, uint32_t magi
 #pragma unroll
         for (int c = 0; c < C; ++c) x[c] = be[rowo + c * G] + be[colo + c * G];
         const double sij = be[i * ld + j];
-        if (l >= K) x[0] = -INFINITY;   // lane without any split (G > K)
 #pragma unroll
-        for (int c = 1; c < C; ++c)
-            if ((MASK_ALL || c == C - 1) && l + c * G >= K) x[c] = -INFINITY;
+        for (int c = MF; c < C; ++c)
+            if (l + c * G >= K) x[c] = -INFINITY;
         double m = x[0];
 #pragma unroll
         for (int c = 1; c < C; ++c) m = fmax(m, x[c]);
@@ -602,12 +602,12 @@ __device__ __forceinline__ void cky_step(const Cky_ctx &cx, int w, uint32_t magi
     }
 }
 
-template <int G, int C, bool MASK_ALL>
+template <int G, int C, int MF>
 __device__ __forceinline__ void cky_run(const Cky_ctx &cx, int w0, int w1, const uint32_t *magic) {
     uint32_t mg_cur = magic[cx.n - w0 + 1];
     for (int w = w0; w < w1; ++w) {
         const uint32_t mg_next = magic[cx.n - w];   // S of width w+1 (>= 0)
-        cky_step<G, C, MASK_ALL>(cx, w, mg_cur);
+        cky_step<G, C, MF>(cx, w, mg_cur);
         __syncthreads();
         mg_cur = mg_next;
     }
@@ -615,37 +615,19 @@ __device__ __forceinline__ void cky_run(const Cky_ctx &cx, int w0, int w1, const
 
 template <bool WIDE>
 __device__ __forceinline__ void cky_sweep(const Cky_ctx &cx, const uint32_t *magic) {
-    const int n = cx.n, nb = cx.nb;
+    const int n = cx.n;
     int w = 2;
     while (w <= n) {
-        const Step_shape sh = step_shape<WIDE>(n, nb, w);
+        const Step_shape sh = step_shape(w);
         int w2 = w + 1;
         while (w2 <= n) {
-            const Step_shape s2 = step_shape<WIDE>(n, nb, w2);
+            const Step_shape s2 = step_shape(w2);
             if (s2.G != sh.G || s2.C != sh.C) break;
             ++w2;
         }
-#define CRF_RUN(GG)                                                            \
-    case GG:                                                                   \
-        switch (sh.C) {                                                        \
-            case 1: cky_run<GG, 1, false>(cx, w, w2, magic); break;            \
-            case 2: cky_run<GG, 2, false>(cx, w, w2, magic); break;            \
-            case 3: cky_run<GG, 3, false>(cx, w, w2, magic); break;            \
-            case 4: cky_run<GG, 4, false>(cx, w, w2, magic); break;            \
-            case 5: cky_run<GG, 5, false>(cx, w, w2, magic); break;            \
-            case 6: cky_run<GG, 6, false>(cx, w, w2, magic); break;            \
-            case 7: cky_run<GG, 7, false>(cx, w, w2, magic); break;            \
-            case 8: cky_run<GG, 8, false>(cx, w, w2, magic); break;            \
-            default:                                                           \
-                if constexpr (WIDE) cky_run<GG, 16, true>(cx, w, w2, magic);   \
-                break;                                                         \
-        }                                                                      \
-        break;
-        switch (sh.G) {
-            CRF_RUN(1) CRF_RUN(2) CRF_RUN(4) CRF_RUN(8) CRF_RUN(16) CRF_RUN(32) CRF_RUN(64)
-            default: break;
-        }
-#undef CRF_RUN
+#define CRF_CKY_RUN(GG, CC, MM) cky_run<GG, (WIDE || CC <= 8) ? CC : 8, (WIDE || CC <= 8) ? MM : 4>(cx, w, w2, magic)
+        CRF_DISPATCH_SHAPE(sh, CRF_CKY_RUN);
+#undef CRF_CKY_RUN
         w = w2;
     }
 }

@@ -127,9 +127,9 @@ HostSchedule make_schedule(const std::vector<int32_t> &order, const int32_t *len
         } else {
             s.spill.push_back(b);
             s.off.push_back(cursor);
-            // The kernels' masked tail loads may read up to 64 elements past
-            // a chart; keep a guard band so they stay inside the workspace.
-            cursor += (spill_chart(n) + 1024 + 255) / 256 * 256;
+            // The kernels' masked tail loads may read up to 511 elements
+            // past a chart; an 8 KiB guard band keeps them inside the workspace.
+            cursor += (spill_chart(n) + 8192 + 255) / 256 * 256;
         }
     }
     s.ws_bytes = cursor - ws_base;
