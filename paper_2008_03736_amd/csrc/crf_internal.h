@@ -77,10 +77,17 @@ struct Schedule {
 };
 
 // Device-side view of a plan, passed by value to every kernel.
+//   mix: the launch order of the fused inside + CKY kernel, one entry per
+//   workgroup: e >= 0 is inside bundle e, e < 0 is CKY bundle ~e.  Entries are
+//   sorted by predicted duration (both kinds merged), so that the hardware's
+//   round-robin of consecutive workgroups over the XCDs hands every XCD the
+//   same mix of long and short, inside and CKY work.
 struct KernelPlan {
     const int32_t *len;          // [B] sentence lengths
     char *ws;                    // workspace base
     Schedule inside, cky;
+    const int32_t *mix;          // [n_mix], or NULL when the fused kernel is not used
+    int32_t n_mix;
     int32_t B, n1, L;
 };
 

@@ -836,9 +836,10 @@ __global__ __launch_bounds__(kThreadsMax) void cky_kernel(KernelPlan p, const fl
     cky_block<SPILL>(p, blockIdx.x, smem_raw, scores, spans, best);
 }
 
-// The whole pass -- inside, reverse and CKY -- in one launch: inside and CKY
-// bundles alternate in blockIdx order (both lists are most expensive first),
-// so the two halves run side by side instead of one after the other.
+// The whole pass -- inside, reverse and CKY -- in one launch.  Workgroup b
+// runs entry b of the plan's merged launch order (inside and CKY bundles by
+// decreasing predicted duration), so the two halves run side by side and
+// every XCD receives the same blend of both.
 __global__ __launch_bounds__(kThreadsMax) void parse_kernel(KernelPlan p, const float *__restrict__ scores,
                                                             const float *__restrict__ grad,
                                                             float *__restrict__ logZ,
@@ -846,18 +847,9 @@ __global__ __launch_bounds__(kThreadsMax) void parse_kernel(KernelPlan p, const 
                                                             int32_t *__restrict__ spans,
                                                             float *__restrict__ best) {
     extern __shared__ __align__(16) char smem_raw[];
-    const int ni = p.inside.n_bundles, nc = p.cky.n_bundles;
-    const int both = 2 * min(ni, nc);
-    const int b = blockIdx.x;
-    bool inside;
-    int idx;
-    if (b < both) {
-        inside = (b & 1) == 0;
-        idx = b >> 1;
-    } else {
-        inside = ni > nc;
-        idx = b - both + min(ni, nc);
-    }
+    const int e = p.mix[blockIdx.x];
+    const bool inside = e >= 0;
+    const int idx = inside ? e : ~e;
     if (inside)
         inside_block<true, false, false>(p, idx, smem_raw, scores, grad, logZ, marg);
     else
@@ -926,13 +918,13 @@ hipError_t launch_cky(const KernelPlan &p, const float *scores, int32_t *spans, 
 hipError_t launch_parse(const KernelPlan &p, const float *scores, const float *grad, float *logZ,
                         float *marg, int32_t *spans, float *best, hipStream_t stream) {
     const Schedule &qi = p.inside, &qc = p.cky;
-    if (qi.n_bundles == 0 || qc.n_bundles == 0 || qi.threads != qc.threads || p.L > 1) {
+    if (p.mix == nullptr || p.n_mix != qi.n_bundles + qc.n_bundles) {
         hipError_t e = launch_inside(p, scores, grad, logZ, marg, stream);
         if (e != hipSuccess) return e;
         return launch_cky(p, scores, spans, best, stream);
     }
     const size_t lds = (size_t)(qi.lds_bytes > qc.lds_bytes ? qi.lds_bytes : qc.lds_bytes);
-    hipLaunchKernelGGL(parse_kernel, dim3(qi.n_bundles + qc.n_bundles), dim3(qi.threads), lds, stream, p,
+    hipLaunchKernelGGL(parse_kernel, dim3(p.n_mix), dim3(qi.threads), lds, stream, p,
                        scores, grad, logZ, marg, spans, best);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;

@@ -93,6 +93,33 @@ inline double sentence_cost(int n) {
     return T + 200.0 * (n - 1);
 }
 
+// Relative duration of a CKY bundle against an inside (forward + reverse)
+// bundle of the same sentences: one max-plus sweep and a tree walk against
+// two log-sum-exp sweeps (measured on single sentences of 30-99 words).
+constexpr double kCkyCostRatio = 0.6;
+
+inline double bundle_cost(const crf::Bundle &b) {
+    const double n = b.n, T = (n + 1) * n * (n - 1) / 6.0;
+    return b.count * T + 200.0 * (n - 1);
+}
+
+// Launch order of the fused kernel: both bundle lists (each already most
+// expensive first) merged by predicted duration.
+std::vector<int32_t> merge_launch_order(const std::vector<crf::Bundle> &in,
+                                        const std::vector<crf::Bundle> &ck) {
+    std::vector<int32_t> mix;
+    mix.reserve(in.size() + ck.size());
+    size_t a = 0, c = 0;
+    while (a < in.size() || c < ck.size()) {
+        const bool take_inside =
+            c >= ck.size() ||
+            (a < in.size() && bundle_cost(in[a]) >= kCkyCostRatio * bundle_cost(ck[c]));
+        if (take_inside) mix.push_back((int32_t)a++);
+        else mix.push_back(~(int32_t)c++);
+    }
+    return mix;
+}
+
 // `order` is sorted by decreasing length.  `chart(n)` is the chart size of
 // a sentence; each bundled sentence also needs `per_sentence` bytes of
 // tables, and each wavefront of the workgroup `wave_bytes(n)` of scratch.
@@ -263,6 +290,10 @@ int crf_plan_create(crf_plan **out, const int32_t *lengths_host, int32_t batch, 
     };
     fill(kp.inside, si);
     fill(kp.cky, sc);
+    std::vector<int32_t> mix;
+    if (num_labels == 1 && !si.bundles.empty() && !sc.bundles.empty() && si.threads == sc.threads)
+        mix = merge_launch_order(si.bundles, sc.bundles);
+    kp.n_mix = (int32_t)mix.size();
 
     if ((e = upload(p, len, &kp.len)) != hipSuccess ||
         (e = upload(p, si.bundles, &kp.inside.bundles)) != hipSuccess ||
@@ -272,7 +303,8 @@ int crf_plan_create(crf_plan **out, const int32_t *lengths_host, int32_t batch, 
         (e = upload(p, sc.bundles, &kp.cky.bundles)) != hipSuccess ||
         (e = upload(p, sc.order, &kp.cky.order)) != hipSuccess ||
         (e = upload(p, sc.spill, &kp.cky.order_spill)) != hipSuccess ||
-        (e = upload(p, sc.off, &kp.cky.ws_off)) != hipSuccess) {
+        (e = upload(p, sc.off, &kp.cky.ws_off)) != hipSuccess ||
+        (e = upload(p, mix, &kp.mix)) != hipSuccess) {
         const int code = (e == hipErrorOutOfMemory) ? CRF_ENOMEM : CRF_EHIP;
         release(p);
         delete p;
