@@ -34,10 +34,9 @@ __host__ __device__ inline int chart_ld(int n) { return n + 1; }
 
 // Bytes of chart per sentence.
 //   inside: two float32 squares -- alpha (upper triangle + mirrored lower
-//           triangle) and the adjoint accumulators (left-child adjoints in
-//           the upper triangle, right-child adjoints in the lower one; the
-//           lower triangle also parks the forced-span scores before the
-//           forward sweep);
+//           triangle) and the outside values (upper + mirrored; before the
+//           outside sweep reaches a span its mirrored cell holds the span's
+//           score, and cells no sweep reads park the forced-span scores);
 //   cky:    one float64 square (beta, upper + mirror).  The tree walk needs
 //           cky_scratch_ints(n) ints of LDS per wavefront on top.
 __host__ __device__ inline int64_t inside_chart_bytes(int n) {

@@ -29,12 +29,16 @@
 //     factored out of the chart: their scores are summed in float64 and added
 //     to log Z, and their marginal is exactly the upstream gradient.  This is
 //     exact (Z = exp(forced) Z') and keeps chart magnitudes small.
-//   * Reverse pass.  Widths run downwards.  A span with adjoint mu gives each
-//     split p_k = exp(x_k - m) / sum exp(x - m), normalised with its own max,
-//     and mu p_k flows to the left child (i,k) and the right child (k,j).  In
-//     one width each child has one parent of each kind, so left- and
-//     right-child adjoints live in the upper and lower triangles of a second
-//     square: every write has a single writer, no atomics, deterministic.
+//   * Marginals.  p((i,j)|x) = exp(alpha(i,j) + O(i,j) - log Z), with O the
+//     log outside score (the derivative of Eq. partial-derivative written as
+//     inside times outside).  The outside of a width-v span needs outside
+//     values of wider spans and alpha of spans no wider than n - v, so the
+//     outside of width n-t runs in the same barrier step as the inside of
+//     width t+1: one joint sweep of n-1 steps instead of an inside sweep
+//     followed by a reverse one.  A per-sentence score shift, estimated a
+//     quarter of the way through the sweep, keeps the chart magnitudes (and
+//     so the float32 rounding of the exponent) small; it moves log Z by a
+//     known amount and leaves every marginal unchanged.
 //   * CKY runs a float64 chart in the association order
 //     beta(i,j) = (max_k (beta(i,k) + beta(k,j))) + s(i,j): only IEEE adds
 //     and exact max, so the tree is reproducible bit for bit; ties keep the
@@ -207,77 +211,168 @@ __device__ __forceinline__ Lane_at lane_at(int f, int S, uint32_t magic) {
     return Lane_at{sb, gid - (int)__umul24((uint32_t)sb, (uint32_t)S), f & (G - 1)};
 }
 
-// One width of the inside (REV = false) or reverse (REV = true) sweep for
-// every sentence of the bundle.  Lane l of a span takes split offsets
-// ko = l + c*G, c < C (split k = i+1+ko); terms c >= MF may fall past K:
-// they count as exp2(-inf) = 0, read cells at most (C - MF)*G columns past
-// the span's last split, and write nothing in the reverse sweep.
-// gv: per-sentence upstream gradient (LDS).
-template <int G, int C, int MF, bool REV, typename T>
-__device__ __forceinline__ void span_step(const Bundle_ctx<T> &bx, int w, const float *gv,
-                                          uint32_t magic) {
+// One span of a width-w inside step (K = w - 1 splits): lane l of the span's
+// G lanes takes split offsets ko = l + c*G, c < C (split k = i+1+ko); terms
+// c >= MF may fall past K: they count as exp2(-inf) = 0 and read cells at most
+// (C - MF)*G columns past the span's last split.  alpha(i,j) = s(i,j) + d +
+// log2 sum_k exp2(alpha(i,k) + alpha(k,j)), written to [i][j] and [j][i];
+// before the sweep [i][j] holds the (log2-scaled) score s(i,j), and d is the
+// sentence's score shift (see rescale_chart).
+template <int G, int C, int MF, typename T>
+__device__ __forceinline__ void inside_span(const Bundle_ctx<T> &bx, int w, int S, int f, bool act,
+                                            uint32_t magic, const float *dsh) {
+    const int ld = bx.ld, K = w - 1;
+    const Lane_at at = lane_at<G>(f, S, magic);
+    const int i = at.i, l = at.l, j = i + w;
+    T *al = bx.chart0 + __umul24((uint32_t)at.sb, (uint32_t)bx.cstride);
+    const int rowo = (int)__umul24((uint32_t)i, (uint32_t)(ld + 1)) + 1 + l;   // alpha(i, k)
+    const int colo = rowo + (int)__umul24((uint32_t)w, (uint32_t)ld);          // alpha(k, j) mirrored
+    const int dia = (int)__umul24((uint32_t)i, (uint32_t)ld) + j;              // [i][j]
+    const int mir = (int)__umul24((uint32_t)j, (uint32_t)ld) + i;              // [j][i]
+    const float own = al[dia] + (w < bx.n ? dsh[at.sb] : 0.f);   // the root is forced: no shift
+    float x[C], xr[C], xc[C];
+#pragma unroll
+    for (int c = 0; c < C; ++c) {
+        xr[c] = al[rowo + c * G];
+        xc[c] = al[colo + c * G];
+    }
+    __builtin_amdgcn_sched_barrier(0);   // every load in flight before the first use
+#pragma unroll
+    for (int c = 0; c < C; ++c) x[c] = xr[c] + xc[c];
+    const int kl = K - l;
+#pragma unroll
+    for (int c = MF; c < C; ++c) x[c] = (c * G < kl) ? x[c] : NEG;
+    float m = x[0];
+#pragma unroll
+    for (int c = 1; c < C; ++c) m = fmax_nn(m, x[c]);
+    float s = 0.f;
+#pragma unroll
+    for (int c = 0; c < C; ++c) s += fast_exp2(x[c] - m);
+    const float mg = grp_max<G>(m);
+    const float sg = grp_sum<G>(s * fast_exp2(m - mg));
+    const float v = mg + fast_log2(sg) + own;
+    // An unconditional use keeps the score load in this block, where it is
+    // issued with the operand loads instead of after the reductions.
+    asm volatile("" ::"v"(v));
+    if (act && l == 0) {
+        al[dia] = v;
+        al[mir] = v;
+    }
+}
+
+// 32-bit LDS address of a generic pointer into LDS, and a load through one.
+typedef __attribute__((address_space(3))) float lds_float;
+__device__ __forceinline__ uint32_t lds_addr(const float *p) {
+    return (uint32_t)(uintptr_t)(const lds_float *)p;
+}
+__device__ __forceinline__ float lds_ld(uint32_t a) { return *(const lds_float *)(uintptr_t)a; }
+
+// One span of a width-v outside step.  With O'(a,b) = O(a,b) + s(a,b) + d
+// (zero at the root) and O the log outside score, a child (i,j) of width v
+// has t = n - v parent terms, indexed q = 0..t-1:
+//   q <  i: parent (q, j),         term O'(q,j) + alpha(q,i)
+//   q >= i: parent (i, k), k = q+v+1, term O'(i,k) + alpha(j,k),
+// every operand a parent of width > v or a sibling of width <= t, so this
+// step runs beside the inside step of width t+1.  Storage: the second square
+// holds O' at [i][j] and mirrored at [j][i]; before the outside reaches
+// (i,j), [j][i] holds its score.  Left terms read rows j (O' mirror) and i
+// (alpha mirror), right terms rows i (O') and j (alpha), all contiguous in q.
+template <int G, int C, int MF, bool WIDE, typename T>
+__device__ __forceinline__ void outside_span(const Bundle_ctx<T> &bx, int v, int S, int f, bool act,
+                                             uint32_t magic, const float *dsh) {
+    const int ld = bx.ld, K = bx.n - v;
+    const Lane_at at = lane_at<G>(f, S, magic);
+    const int i = at.i, l = at.l, j = i + v;
+    T *al = bx.chart0 + __umul24((uint32_t)at.sb, (uint32_t)bx.cstride);
+    T *ou = al + __umul24((uint32_t)ld, (uint32_t)ld);
+    const int ri = (int)__umul24((uint32_t)i, (uint32_t)ld);
+    const int rj = (int)__umul24((uint32_t)j, (uint32_t)ld);
+    const T *oL = ou + rj + l, *aL = al + ri + l;                    // q < i
+    const T *oR = ou + ri + v + 1 + l, *aR = al + rj + v + 1 + l;    // q >= i
+    const int il = i - l, kl = K - l;   // term c is left iff c*G < il, valid iff c*G < kl
+    const float own = ou[rj + i] + dsh[at.sb];
+    float x[C];
+    if constexpr (!WIDE) {
+        // LDS chart: pick each term's row by selecting between two 32-bit LDS
+        // addresses, the split offset folded into the load's immediate.  The
+        // empty asm keeps the compiler from pulling the common lane offset out
+        // of the selects (which costs two adds per term).
+        uint32_t oLa = lds_addr(oL), aLa = lds_addr(aL), oRa = lds_addr(oR), aRa = lds_addr(aR);
+        asm volatile("" : "+v"(oLa), "+v"(aLa), "+v"(oRa), "+v"(aRa));
+        float xo[C], xa[C];
+#pragma unroll
+        for (int c = 0; c < C; ++c) {
+            const bool left = c * G < il;
+            xo[c] = lds_ld((left ? oLa : oRa) + 4 * c * G);
+            xa[c] = lds_ld((left ? aLa : aRa) + 4 * c * G);
+        }
+        // all loads in flight before the first use: one LDS round trip
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int c = 0; c < C; ++c) x[c] = xo[c] + xa[c];
+    } else {
+#pragma unroll
+        for (int c = 0; c < C; ++c) {
+            const bool left = c * G < il;
+            x[c] = (left ? oL : oR)[c * G] + (left ? aL : aR)[c * G];
+        }
+    }
+#pragma unroll
+    for (int c = MF; c < C; ++c) x[c] = (c * G < kl) ? x[c] : NEG;
+    float m = x[0];
+#pragma unroll
+    for (int c = 1; c < C; ++c) m = fmax_nn(m, x[c]);
+    float s = 0.f;
+#pragma unroll
+    for (int c = 0; c < C; ++c) s += fast_exp2(x[c] - m);
+    const float mg = grp_max<G>(m);
+    const float sg = grp_sum<G>(s * fast_exp2(m - mg));
+    const float o = mg + fast_log2(sg) + own;
+    asm volatile("" ::"v"(o));
+    if (act && l == 0) {
+        ou[ri + j] = o;
+        ou[rj + i] = o;
+    }
+}
+
+// Forward-only width step: every span of width w of every sentence.
+template <int G, int C, int MF, typename T>
+__device__ __forceinline__ void fwd_step(const Bundle_ctx<T> &bx, int w, uint32_t magic, const float *dsh) {
     const int tid = threadIdx.x, nt = blockDim.x;
-    const int n = bx.n, ld = bx.ld;
-    const int K = w - 1, S = n - w + 1;
+    const int S = bx.n - w + 1;
     const int total = bx.nb * S * G;
     const int wq0 = __builtin_amdgcn_readfirstlane(tid & ~63);   // this wavefront's first thread
     for (int f0 = 0; f0 < total; f0 += nt) {
         if (f0 + wq0 >= total) break;   // no span for this wavefront in this pass or later
         const bool act = f0 + tid < total;
-        const Lane_at at = lane_at<G>(act ? f0 + tid : total - 1, S, magic);
-        const int i = at.i, l = at.l, j = i + w;
-        T *al = bx.chart0 + __umul24((uint32_t)at.sb, (uint32_t)bx.cstride);
-        T *ad = al + __umul24((uint32_t)ld, (uint32_t)ld);
-        const int rowo = (int)__umul24((uint32_t)i, (uint32_t)(ld + 1)) + 1 + l;   // alpha(i, k)
-        const int colo = rowo + (int)__umul24((uint32_t)w, (uint32_t)ld);          // alpha(k, j) mirrored
-        const int dia = (int)__umul24((uint32_t)i, (uint32_t)ld) + j;              // [i][j]
-        const int mir = (int)__umul24((uint32_t)j, (uint32_t)ld) + i;              // [j][i]
-        float x[C], accl[C], accr[C];
-#pragma unroll
-        for (int c = 0; c < C; ++c) x[c] = al[rowo + c * G] + al[colo + c * G];
-        if constexpr (REV) {
-#pragma unroll
-            for (int c = 0; c < C; ++c) {
-                accl[c] = ad[rowo + c * G];   // current adjoints of the children
-                accr[c] = ad[colo + c * G];
-            }
-        }
-        // forward: the span's (log2-scaled) score; reverse: its adjoint
-        const float extra = !REV ? al[dia] : (w == n) ? gv[at.sb] : ad[dia] + ad[mir];
-#pragma unroll
-        for (int c = MF; c < C; ++c) x[c] = (l + c * G < K) ? x[c] : NEG;
-        float m = x[0];
-#pragma unroll
-        for (int c = 1; c < C; ++c) m = fmax_nn(m, x[c]);
-        float t[C], s = 0.f;
-#pragma unroll
-        for (int c = 0; c < C; ++c) {
-            t[c] = fast_exp2(x[c] - m);
-            s += t[c];
-        }
-        const float mg = grp_max<G>(m);
-        const float sc = fast_exp2(m - mg);
-        const float sg = grp_sum<G>(s * sc);
-        if constexpr (!REV) {
-            if (act && l == 0) {
-                const float v = mg + fast_log2(sg) + extra;
-                al[dia] = v;
-                al[mir] = v;
-            }
-        } else if (act) {
-            // mu * p_k, p_k = exp2(x_k - mg) / sg, to both children of split k:
-            // the left child (i, k) in the upper triangle, the right child
-            // (k, j) in the lower one.  In one step each of these cells has
-            // this span as its only writer, so a plain read-modify-write is
-            // race-free and deterministic.
-            const float coef = extra * sc * __builtin_amdgcn_rcpf(sg);
-#pragma unroll
-            for (int c = 0; c < C; ++c) {
-                if (c >= MF && l + c * G >= K) continue;
-                const float v = coef * t[c];
-                ad[rowo + c * G] = accl[c] + v;
-                ad[colo + c * G] = accr[c] + v;
-            }
+        inside_span<G, C, MF>(bx, w, S, act ? f0 + tid : total - 1, act, magic, dsh);
+    }
+}
+
+// Step t of the joint sweep: inside width t+1 and outside width n-t (when
+// >= 2), both with K = t terms per span, so one step shape serves both.
+// Inside spans take the first threads, outside spans start at the next
+// wavefront boundary, so every wavefront runs one kind.
+template <int G, int C, int MF, bool WIDE, typename T>
+__device__ __forceinline__ void io_step(const Bundle_ctx<T> &bx, int t, uint32_t mg_in, uint32_t mg_out,
+                                        const float *dsh) {
+    const int tid = threadIdx.x, nt = blockDim.x;
+    const int n = bx.n, w = t + 1, v = n - t;
+    const int s_in = n - t, s_out = v >= 2 ? t + 1 : 0;
+    const int tin = bx.nb * s_in * G, tout = bx.nb * s_out * G;
+    const int obase = (tin + 63) & ~63;
+    const int total = obase + tout;
+    const int wq0 = __builtin_amdgcn_readfirstlane(tid & ~63);
+    for (int f0 = 0; f0 < total; f0 += nt) {
+        const int fw = f0 + wq0;
+        if (fw >= total) break;
+        if (fw < obase) {
+            const bool act = f0 + tid < tin;
+            inside_span<G, C, MF>(bx, w, s_in, act ? f0 + tid : tin - 1, act, mg_in, dsh);
+        } else {
+            const int fo = f0 + tid - obase;
+            const bool act = fo < tout;
+            outside_span<G, C, MF, WIDE>(bx, v, s_out, act ? fo : tout - 1, act, mg_out, dsh);
         }
     }
 }
@@ -292,19 +387,33 @@ __device__ __forceinline__ Step_shape step_shape(int w) {
     const int g = next_pow2((K + 7) / 8);
     return g <= 64 ? Step_shape{g, 8} : Step_shape{64, 16};
 }
-// A run of widths w0, w0+dir, ... (excluding w1) sharing one step shape:
-// a tight loop with no dispatch.  magic[S] = div_magic(S) (LDS table).
-template <int G, int C, int MF, bool REV, typename T>
-__device__ __forceinline__ void inside_run(const Bundle_ctx<T> &bx, int w0, int w1, int dir,
-                                        const float *gv, const uint32_t *magic) {
-    // magic[S] for the next width is fetched one step ahead (S = n-w+1 stays
-    // in [0, n] even one step past the run).
+// A run of forward widths [w0, w1) sharing one step shape: a tight loop with
+// no dispatch.  magic[S] = div_magic(S) (LDS table), fetched one step ahead
+// (S = n-w+1 stays in [0, n] even one step past the run).
+template <int G, int C, int MF, typename T>
+__device__ __forceinline__ void fwd_run(const Bundle_ctx<T> &bx, int w0, int w1, const uint32_t *magic,
+                                        const float *dsh) {
     uint32_t mg_cur = magic[bx.n - w0 + 1];
-    for (int w = w0; w != w1; w += dir) {
-        const uint32_t mg_next = magic[bx.n - (w + dir) + 1];
-        span_step<G, C, MF, REV>(bx, w, gv, mg_cur);
+    for (int w = w0; w < w1; ++w) {
+        const uint32_t mg_next = magic[bx.n - w];
+        fwd_step<G, C, MF>(bx, w, mg_cur, dsh);
         __syncthreads();
         mg_cur = mg_next;
+    }
+}
+
+// A run of joint steps [t0, t1) sharing one step shape.  Span counts are
+// n - t (inside) and t + 1 (outside), both in [1, n+1].
+template <int G, int C, int MF, bool WIDE, typename T>
+__device__ __forceinline__ void io_run(const Bundle_ctx<T> &bx, int t0, int t1, const uint32_t *magic,
+                                       const float *dsh) {
+    uint32_t mi = magic[bx.n - t0], mo = magic[t0 + 1];
+    for (int t = t0; t < t1; ++t) {
+        const uint32_t mi_next = magic[bx.n - t - 1], mo_next = magic[t + 2];
+        io_step<G, C, MF, WIDE>(bx, t, mi, mo, dsh);
+        __syncthreads();
+        mi = mi_next;
+        mo = mo_next;
     }
 }
 
@@ -334,27 +443,125 @@ __device__ __forceinline__ void inside_run(const Bundle_ctx<T> &bx, int w0, int 
         }                                                \
     } while (0)
 
-// All widths of one sweep: forward 2..n, reverse n..2, one dispatch per run
-// of widths sharing a step shape.
+// The forward sweep alone: widths 2..n, one dispatch per run of widths
+// sharing a step shape.
 // WIDE: workspace charts (longer sentences), which may need 16 terms per lane.
-template <bool REV, bool WIDE, typename T>
-__device__ __forceinline__ void inside_sweep(const Bundle_ctx<T> &bx, const float *gv,
-                                             const uint32_t *magic) {
+template <bool WIDE, typename T>
+__device__ __forceinline__ void fwd_sweep(const Bundle_ctx<T> &bx, const uint32_t *magic, const float *dsh) {
     const int n = bx.n;
-    const int dir = REV ? -1 : 1, wend = REV ? 1 : n + 1;
-    int w = REV ? n : 2;
-    while (w != wend) {
+    int w = 2;
+    while (w <= n) {
         const Step_shape sh = step_shape(w);
-        int w2 = w + dir;
-        while (w2 != wend) {
+        int w2 = w + 1;
+        while (w2 <= n) {
             const Step_shape s2 = step_shape(w2);
             if (s2.G != sh.G || s2.C != sh.C) break;
-            w2 += dir;
+            ++w2;
         }
-#define CRF_INSIDE_RUN(GG, CC, MM) inside_run<GG, (WIDE || CC <= 8) ? CC : 8, (WIDE || CC <= 8) ? MM : 4, REV>(bx, w, w2, dir, gv, magic)
-        CRF_DISPATCH_SHAPE(sh, CRF_INSIDE_RUN);
-#undef CRF_INSIDE_RUN
+#define CRF_FWD_RUN(GG, CC, MM) fwd_run<GG, (WIDE || CC <= 8) ? CC : 8, (WIDE || CC <= 8) ? MM : 4>(bx, w, w2, magic, dsh)
+        CRF_DISPATCH_SHAPE(sh, CRF_FWD_RUN);
+#undef CRF_FWD_RUN
         w = w2;
+    }
+}
+
+// Fixed-order reductions over a wavefront (same result in every lane).
+__device__ __forceinline__ double wave_sum_d(double v) {
+    for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
+    return v;
+}
+__device__ __forceinline__ float wave_max_f(float v) {
+    for (int off = 32; off >= 1; off >>= 1) v = fmax_nn(v, __shfl_xor(v, off));
+    return v;
+}
+__device__ __forceinline__ float wave_sum_f(float v) {
+    for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
+    return v;
+}
+
+// Spans below a sentence's largest alpha of the probe width by more than this
+// many log2 units per internal node are left out of its growth estimate (they
+// hold near-forbidden scores, not the typical growth).
+constexpr float kShiftBand = 30.0f;
+
+// Score shift.  Adding one constant d to every non-forced score adds d times
+// their number, n - 2, to the log score of every tree: log Z moves by
+// (n-2) d and no marginal changes.  Chart values grow about linearly with the
+// span width, and float32 rounding of alpha + O - log Z, the exponent of a
+// marginal, grows with them; d = minus the typical growth per internal node
+// keeps both near zero.  After joint step t0 (inside widths <= t0+1 done,
+// outside widths >= n-t0 done) the growth is estimated from alpha at width
+// w0 = t0+1, and the stored values are moved to the shifted problem:
+//   alpha(i,j) += d (w-1)   (w-1 non-forced nodes below and at (i,j))
+//   O'(i,j)    += d (n-w)   (n-1-w above it, plus its own score)
+// Later steps add d to each score as they read it; the root's O' stays 0.
+template <typename T>
+__device__ void rescale_chart(const Bundle_ctx<T> &bx, int t0, float *dsh) {
+    const int n = bx.n, ld = bx.ld, nb = bx.nb, w0 = t0 + 1, S = n - t0;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, NW = blockDim.x >> 6;
+    for (int sb = wave; sb < nb; sb += NW) {
+        const T *al = bx.chart0 + (size_t)sb * bx.cstride;
+        float m = NEG;
+        for (int i = lane; i < S; i += 64) m = fmax_nn(m, al[i * (ld + 1) + w0]);
+        m = wave_max_f(m);
+        const float floor_v = m - kShiftBand * (float)(w0 - 1);
+        float acc = 0.f, cnt = 0.f;
+        for (int i = lane; i < S; i += 64) {
+            const float a = al[i * (ld + 1) + w0];
+            if (a >= floor_v) {
+                acc += a;
+                cnt += 1.f;
+            }
+        }
+        acc = wave_sum_f(acc);
+        cnt = wave_sum_f(cnt);
+        if (lane == 0) dsh[sb] = -acc / (cnt * (float)(w0 - 1));
+    }
+    __syncthreads();
+    const int nn = n * n, total = nb * nn;
+    const float inv_nn = 1.0f / (float)nn, inv_n = 1.0f / (float)n;
+    for (int c = tid; c < total; c += blockDim.x) {
+        const int sb = div_small(c, nn, inv_nn);
+        const int rem = c - sb * nn;
+        const int i = div_small(rem, n, inv_n);
+        const int j = rem - i * n + 1, w = j - i;
+        T *al = bx.chart0 + (size_t)sb * bx.cstride;
+        T *ou = al + (size_t)ld * ld;
+        const float d = dsh[sb];
+        if (w >= 2 && w <= w0) {
+            const float a = al[i * ld + j] + d * (float)(w - 1);
+            al[i * ld + j] = a;
+            al[j * ld + i] = a;
+        }
+        if (w >= n - t0 && w <= n - 1 && w >= 2) {
+            const float o = ou[i * ld + j] + d * (float)(n - w);
+            ou[i * ld + j] = o;
+            ou[j * ld + i] = o;
+        }
+    }
+    __syncthreads();
+}
+
+// The joint sweep: steps t = 1..n-1 (inside widths 2..n, outside widths
+// n-1..2), one dispatch per run of steps sharing a step shape; the runs are
+// cut after step t0 for the rescale (t0 = 0: none).
+template <bool WIDE, typename T>
+__device__ __forceinline__ void io_sweep(const Bundle_ctx<T> &bx, const uint32_t *magic, float *dsh, int t0) {
+    const int n = bx.n;
+    int t = 1;
+    while (t <= n - 1) {
+        const Step_shape sh = step_shape(t + 1);
+        int t2 = t + 1;
+        while (t2 <= n - 1 && t2 - 1 != t0) {
+            const Step_shape s2 = step_shape(t2 + 1);
+            if (s2.G != sh.G || s2.C != sh.C) break;
+            ++t2;
+        }
+#define CRF_IO_RUN(GG, CC, MM) io_run<GG, (WIDE || CC <= 8) ? CC : 8, (WIDE || CC <= 8) ? MM : 4, WIDE>(bx, t, t2, magic, dsh)
+        CRF_DISPATCH_SHAPE(sh, CRF_IO_RUN);
+#undef CRF_IO_RUN
+        if (t2 - 1 == t0) rescale_chart(bx, t0, dsh);
+        t = t2;
     }
 }
 
@@ -410,12 +617,6 @@ __device__ __forceinline__ void for_cells_loaded(int nb, int n, LD &&load, F &&u
     }
 }
 
-// Fixed-order float64 sum over a wavefront (same result in every lane).
-__device__ __forceinline__ double wave_sum_d(double v) {
-    for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
-    return v;
-}
-
 // Log-sum-exp over labels of one span, in log2 units.
 __device__ __forceinline__ float label_lse2(const float *s, int L) {
     float m = -INFINITY;
@@ -426,11 +627,16 @@ __device__ __forceinline__ float label_lse2(const float *s, int L) {
 }
 
 // ---------------------------------------------------------------------------
-// Inside (+ reverse).  One workgroup per bundle (or, SPILL, per long
+// Inside (+ marginals).  One workgroup per bundle (or, SPILL, per long
 // sentence with its chart in the workspace).
-//   REV: also run the reverse sweep and write marginals.
+//   REV: also compute the marginals (joint inside/outside sweep) and write them.
 //   LAB: labelled scores [B][N1][N1][L].
-// Dynamic LDS (bundled): nb charts, then nb x {forced (f64), grad (f32), id (i32)}.
+// Dynamic LDS (bundled): nb charts, then nb x {forced (f64), grad (f32),
+// id (i32), shift (f32)}, then the magic table.
+// Chart of a sentence: two squares of ld x ld floats.  The first holds alpha
+// (upper triangle and mirrored).  The second holds the outside values O'
+// (REV, upper and mirrored) and parks the forced spans' scores where nothing
+// else reads: width-1 spans at [i+1][i], the root at [0][0].
 template <bool REV, bool LAB, bool SPILL>
 __device__ __forceinline__ void inside_block(const KernelPlan &p, int block, char *smem_raw,
                                              const float *__restrict__ scores,
@@ -439,6 +645,7 @@ __device__ __forceinline__ void inside_block(const KernelPlan &p, int block, cha
     __shared__ double spill_forced[1];
     __shared__ float spill_gv[1];
     __shared__ int spill_id[1];
+    __shared__ float spill_dsh[1];
     __shared__ uint32_t spill_magic[SPILL ? CRF_MAX_LEN + 2 : 1];
     const int NT = blockDim.x, NW = NT >> 6;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -448,7 +655,7 @@ __device__ __forceinline__ void inside_block(const KernelPlan &p, int block, cha
     float *chart0;
     int cstride;
     double *forced;
-    float *gv;
+    float *gv, *dsh;
     int *sid;
     uint32_t *magic;
     if constexpr (SPILL) {
@@ -460,6 +667,7 @@ __device__ __forceinline__ void inside_block(const KernelPlan &p, int block, cha
         forced = spill_forced;
         gv = spill_gv;
         sid = spill_id;
+        dsh = spill_dsh;
         magic = spill_magic;
         if (tid == 0) sid[0] = b;
     } else {
@@ -471,21 +679,25 @@ __device__ __forceinline__ void inside_block(const KernelPlan &p, int block, cha
         forced = reinterpret_cast<double *>(smem_raw + (size_t)nb * inside_chart_bytes(n));
         gv = reinterpret_cast<float *>(forced + nb);
         sid = reinterpret_cast<int *>(gv + nb);
-        magic = reinterpret_cast<uint32_t *>(sid + nb);
+        dsh = reinterpret_cast<float *>(sid + nb);
+        magic = reinterpret_cast<uint32_t *>(dsh + nb);
         for (int t = tid; t < nb; t += NT) sid[t] = p.inside.order[bd.first + t];
     }
-    for (int S = tid; S <= n; S += NT) magic[S] = div_magic(S);
+    for (int S = tid; S <= n + 1; S += NT) magic[S] = div_magic(S);
     const int ld = chart_ld(n);
     const Bundle_ctx<float> bx{chart0, cstride, n, ld, nb};
     __syncthreads();
-    for (int t = tid; t < nb; t += NT) gv[t] = grad ? grad[sid[t]] : 1.0f;
+    for (int t = tid; t < nb; t += NT) {
+        gv[t] = grad ? grad[sid[t]] : 1.0f;
+        dsh[t] = 0.f;
+    }
 
     const size_t row_stride = LAB ? (size_t)N1 * L : (size_t)N1;
     const size_t sent_stride = (size_t)N1 * row_stride;
 
-    // Prologue: scores of every valid cell into the charts (log2-scaled);
-    // forced spans get 0 in the chart and park their natural-unit score in
-    // the adjoint square's lower triangle ([i+1][i]; the root at [n][0]).
+    // Prologue: scores of every valid cell into the charts (log2-scaled; the
+    // outside reads its own copy at the mirrored cell of the second square);
+    // forced spans get 0 in alpha and park their natural-unit score.
     auto load_score = [&](int sb, int i, int j) -> float {
         const float *srow = scores + (size_t)sid[sb] * sent_stride + (size_t)i * row_stride;
         if constexpr (LAB)
@@ -495,60 +707,68 @@ __device__ __forceinline__ void inside_block(const KernelPlan &p, int block, cha
     };
     for_cells_loaded<LAB ? 1 : 8>(nb, n, load_score, [&](int sb, int i, int j, float s) {
         float *al = chart0 + (size_t)sb * cstride;
-        float *ad = al + (size_t)ld * ld;
+        float *ou = al + (size_t)ld * ld;
         if (j == i + 1) {
             al[i * ld + j] = 0.f;
             al[j * ld + i] = 0.f;
-            ad[j * ld + i] = s;
+            ou[j * ld + i] = s;
         } else if (i == 0 && j == n) {
             al[j] = 0.f;
-            ad[n * ld] = s;
+            ou[0] = s;
+            if constexpr (REV) {
+                ou[j] = 0.f;        // O'(0,n) = 0
+                ou[n * ld] = 0.f;
+            }
         } else {
-            al[i * ld + j] = s * LOG2E_F;
+            const float s2 = s * LOG2E_F;
+            al[i * ld + j] = s2;
+            if constexpr (REV) ou[j * ld + i] = s2;
         }
     });
     __syncthreads();
     // Forced-span sums, one wavefront per sentence, fixed order (deterministic).
     for (int sb = wave; sb < nb; sb += NW) {
-        const float *ad = chart0 + (size_t)sb * cstride + (size_t)ld * ld;
+        const float *ou = chart0 + (size_t)sb * cstride + (size_t)ld * ld;
         double acc = 0.0;
-        for (int i = lane; i < n; i += 64) acc += (double)ad[(i + 1) * ld + i];
-        if (lane == 0 && n >= 2) acc += (double)ad[n * ld];
+        for (int i = lane; i < n; i += 64) acc += (double)ou[(i + 1) * ld + i];
+        if (lane == 0 && n >= 2) acc += (double)ou[0];
         acc = wave_sum_d(acc);
         if (lane == 0) forced[sb] = acc;
     }
 
-    inside_sweep<false, SPILL>(bx, gv, magic);
+    if constexpr (!REV) {
+        fwd_sweep<SPILL>(bx, magic, dsh);
+    } else {
+        // The rescale needs a few widths of alpha to estimate the growth;
+        // short sentences keep small magnitudes and skip it.
+        io_sweep<SPILL>(bx, magic, dsh, n >= 8 ? n / 4 : 0);
+    }
+    // log Z = (alpha~(0,n) - (n-2) d) ln 2 + forced sum.
     if (logZ != nullptr)
-        for (int sb = tid; sb < nb; sb += NT)
-            logZ[sid[sb]] = (float)((double)chart0[(size_t)sb * cstride + n] * LN2_D + forced[sb]);
+        for (int sb = tid; sb < nb; sb += NT) {
+            const double z2 = (double)chart0[(size_t)sb * cstride + n] - (double)dsh[sb] * (n >= 2 ? n - 2 : 0);
+            logZ[sid[sb]] = (float)(z2 * LN2_D + forced[sb]);
+        }
     if constexpr (!REV) return;
 
-    // Reverse sweep.  Clear the adjoint squares first.
-    {
-        const int ld2 = ld * ld;
-        const float inv_ld2 = 1.0f / (float)ld2;
-        for (int c = tid; c < nb * ld2; c += NT) {
-            const int sb = div_small(c, ld2, inv_ld2);
-            chart0[(size_t)sb * cstride + ld2 + (c - sb * ld2)] = 0.f;
-        }
-    }
-    __syncthreads();
-    inside_sweep<true, SPILL>(bx, gv, magic);
-
-    // Epilogue: marginals of the valid cells (coalesced stores along rows).
-    auto load_mu = [&](int sb, int i, int j) -> float {
-        const float *ad = chart0 + (size_t)sb * cstride + (size_t)ld * ld;
-        const bool forced_span = (j == i + 1) || (i == 0 && j == n);
-        return forced_span ? gv[sb] : ad[i * ld + j] + ad[j * ld + i];
-    };
-    for_cells_loaded<LAB ? 1 : 8>(nb, n, load_mu, [&](int sb, int i, int j, float mu) {
+    // Epilogue: marginals of the valid cells (coalesced stores along rows),
+    //   mu(i,j) = g exp2(alpha~(i,j) + O'(i,j) - (s(i,j) + d) - alpha~(0,n)),
+    // and exactly g on forced spans.
+    for_cells_loaded<LAB ? 1 : 8>(nb, n, load_score, [&](int sb, int i, int j, float s) {
         const size_t rowoff = (size_t)sid[sb] * sent_stride + (size_t)i * row_stride;
+        const float *al = chart0 + (size_t)sb * cstride;
+        const float *ou = al + (size_t)ld * ld;
+        const bool forced_span = (j == i + 1) || (i == 0 && j == n);
+        float mu = gv[sb];
+        if (!forced_span) {
+            const float own = s * LOG2E_F + dsh[sb];
+            mu *= fast_exp2(((al[i * ld + j] - al[n]) + ou[i * ld + j]) - own);
+        }
         if constexpr (LAB) {
-            const float *s = scores + rowoff + (size_t)j * L;
-            const float lse2 = label_lse2(s, L);
+            const float *sl = scores + rowoff + (size_t)j * L;
+            const float lse2 = label_lse2(sl, L);
             float *o = marg + rowoff + (size_t)j * L;
-            for (int q = 0; q < L; ++q) o[q] = mu * fast_exp2(s[q] * LOG2E_F - lse2);
+            for (int q = 0; q < L; ++q) o[q] = mu * fast_exp2(sl[q] * LOG2E_F - lse2);
         } else {
             marg[rowoff + j] = mu;
         }

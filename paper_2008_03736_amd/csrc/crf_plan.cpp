@@ -270,8 +270,8 @@ int crf_plan_create(crf_plan **out, const int32_t *lengths_host, int32_t batch, 
     auto cky_bytes = [](int n) { return crf::cky_chart_bytes(n); };
     auto no_scratch = [](int) { return (int64_t)0; };
     auto cky_scratch = [](int n) { return (int64_t)4 * crf::cky_scratch_ints(n); };
-    // inside tables: forced sum (f64), gradient (f32), id (i32); cky: id
-    HostSchedule si = make_schedule(order, lengths_host, lds_cap, force, 0, 16, +inside_bytes,
+    // inside tables: forced sum (f64), gradient (f32), id (i32), score shift (f32); cky: id
+    HostSchedule si = make_schedule(order, lengths_host, lds_cap, force, 0, 20, +inside_bytes,
                                     +inside_bytes, +no_scratch);
     HostSchedule sc = make_schedule(order, lengths_host, lds_cap, force, si.ws_bytes, 4, +cky_bytes,
                                     +cky_bytes, +cky_scratch);
