@@ -21,9 +21,9 @@ constexpr int kThreadsMax = 1024;
 constexpr int kMaxBundle = 256;
 
 // LDS a bundle needs besides its charts: a uint32 table of division magics
-// for span counts 0..n+1.  (The masked tail loads of the last chart reach at
-// most 4G-1 <= n/2 + 3 elements past it, into the tables that follow the
-// charts.)
+// for span counts 0..n+1.  (Masked tail loads stay inside a sentence's inside
+// chart; the CKY chart's reach at most n + 13 float64 past the last chart,
+// into this table and the tree-walk scratch that follow it.)
 __host__ __device__ inline int64_t bundle_extra_bytes(int n) { return 4 * (int64_t)(n + 2); }
 
 // Static LDS the kernels reserve besides the charts.

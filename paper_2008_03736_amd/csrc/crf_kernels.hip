@@ -180,10 +180,12 @@ __device__ __forceinline__ int floor_pow2(int x) { return x <= 1 ? 1 : 1 << (31 
 // Step shapes.  Every distinct (lanes per span G, terms per lane C) is its
 // own unrolled body, and entering one a sweep has not run yet refills the
 // instruction cache (thousands of cycles), so sweeps use few shapes: K <= 8
-// splits take G = 1 and C in {1, 2, 4, 8}; wider spans take C = 8 and
-// G = next_pow2(ceil(K / 8)) up to 64, then C = 16 (workspace charts only).
-// C is rounded up: terms c >= C/2 may fall past the K splits and are masked
-// (for K > 8, ceil(K / G) > 4).
+// splits take G = 1 and C in {1, 2, 4, 8}; K <= 64 take C = 8 and
+// G = next_pow2(ceil(K / 8)); longer spans take C = 16 and
+// G = next_pow2(ceil(K / 16)) (at most 64).  C is rounded up: terms
+// c >= C/2 may fall past the K splits and are masked (for K > 8,
+// ceil(K / G) > C/2), so a lane reads at most (C/2) G - 1 <= K + 14 cells
+// past its span's last split.
 // ---------------------------------------------------------------------------
 // Per-bundle context: nb sentences of length n; sentence sb's chart starts at
 // chart0 + sb * cstride (elements).
@@ -384,8 +386,8 @@ struct Step_shape {
 __device__ __forceinline__ Step_shape step_shape(int w) {
     const int K = w - 1;
     if (K <= 8) return Step_shape{1, K <= 1 ? 1 : K <= 2 ? 2 : K <= 4 ? 4 : 8};
-    const int g = next_pow2((K + 7) / 8);
-    return g <= 64 ? Step_shape{g, 8} : Step_shape{64, 16};
+    if (K <= 64) return Step_shape{next_pow2((K + 7) / 8), 8};
+    return Step_shape{min(64, next_pow2((K + 15) / 16)), 16};
 }
 // A run of forward widths [w0, w1) sharing one step shape: a tight loop with
 // no dispatch.  magic[S] = div_magic(S) (LDS table), fetched one step ahead
@@ -418,29 +420,33 @@ __device__ __forceinline__ void io_run(const Bundle_ctx<T> &bx, int t0, int t1, 
 }
 
 // Calls RUN(G, C, MF) for a step shape (C rounded up to a power of two:
-// terms c >= C/2 may fall past K).
-#define CRF_DISPATCH_SHAPE(SH, RUN)                      \
-    do {                                                 \
-        if ((SH).G == 1) {                               \
-            switch ((SH).C) {                            \
-                case 1: RUN(1, 1, 0); break;             \
-                case 2: RUN(1, 2, 1); break;             \
-                case 4: RUN(1, 4, 2); break;             \
-                default: RUN(1, 8, 4); break;            \
-            }                                            \
-        } else {                                         \
-            switch ((SH).G) {                            \
-                case 2: RUN(2, 8, 4); break;             \
-                case 4: RUN(4, 8, 4); break;             \
-                case 8: RUN(8, 8, 4); break;             \
-                case 16: RUN(16, 8, 4); break;           \
-                case 32: RUN(32, 8, 4); break;           \
-                default:                                 \
-                    if (!WIDE || (SH).C == 8) RUN(64, 8, 4); \
-                    else RUN(64, 16, 8);                 \
-                    break;                               \
-            }                                            \
-        }                                                \
+// terms c >= C/2 may fall past K).  Charts in LDS hold at most 142 words, so
+// their sweeps never need G >= 32; only the workspace (WIDE) kernels build it.
+#define CRF_DISPATCH_SHAPE(SH, RUN)                          \
+    do {                                                     \
+        switch ((SH).G) {                                    \
+            case 1:                                          \
+                switch ((SH).C) {                            \
+                    case 1: RUN(1, 1, 0); break;             \
+                    case 2: RUN(1, 2, 1); break;             \
+                    case 4: RUN(1, 4, 2); break;             \
+                    default: RUN(1, 8, 4); break;            \
+                }                                            \
+                break;                                       \
+            case 2: RUN(2, 8, 4); break;                     \
+            case 4: RUN(4, 8, 4); break;                     \
+            case 8:                                          \
+                if ((SH).C == 8) RUN(8, 8, 4);               \
+                else RUN(8, 16, 8);                          \
+                break;                                       \
+            case 16: RUN(16, 16, 8); break;                  \
+            default:                                         \
+                if constexpr (WIDE) {                        \
+                    if ((SH).G == 32) RUN(32, 16, 8);        \
+                    else RUN(64, 16, 8);                     \
+                }                                            \
+                break;                                       \
+        }                                                    \
     } while (0)
 
 // The forward sweep alone: widths 2..n, one dispatch per run of widths
@@ -458,7 +464,7 @@ __device__ __forceinline__ void fwd_sweep(const Bundle_ctx<T> &bx, const uint32_
             if (s2.G != sh.G || s2.C != sh.C) break;
             ++w2;
         }
-#define CRF_FWD_RUN(GG, CC, MM) fwd_run<GG, (WIDE || CC <= 8) ? CC : 8, (WIDE || CC <= 8) ? MM : 4>(bx, w, w2, magic, dsh)
+#define CRF_FWD_RUN(GG, CC, MM) fwd_run<GG, CC, MM>(bx, w, w2, magic, dsh)
         CRF_DISPATCH_SHAPE(sh, CRF_FWD_RUN);
 #undef CRF_FWD_RUN
         w = w2;
@@ -518,25 +524,38 @@ __device__ void rescale_chart(const Bundle_ctx<T> &bx, int t0, float *dsh) {
         if (lane == 0) dsh[sb] = -acc / (cnt * (float)(w0 - 1));
     }
     __syncthreads();
-    const int nn = n * n, total = nb * nn;
-    const float inv_nn = 1.0f / (float)nn, inv_n = 1.0f / (float)n;
-    for (int c = tid; c < total; c += blockDim.x) {
-        const int sb = div_small(c, nn, inv_nn);
-        const int rem = c - sb * nn;
-        const int i = div_small(rem, n, inv_n);
-        const int j = rem - i * n + 1, w = j - i;
-        T *al = bx.chart0 + (size_t)sb * bx.cstride;
-        T *ou = al + (size_t)ld * ld;
-        const float d = dsh[sb];
-        if (w >= 2 && w <= w0) {
-            const float a = al[i * ld + j] + d * (float)(w - 1);
-            al[i * ld + j] = a;
-            al[j * ld + i] = a;
+    // alpha of widths 2..w0: per sentence n rows x (w0-1) widths
+    {
+        const int A = w0 - 1, per = n * A, total = nb * per;
+        const float inv_per = 1.0f / (float)per, inv_a = 1.0f / (float)A;
+        for (int f = tid; f < total; f += blockDim.x) {
+            const int sb = div_small(f, per, inv_per);
+            const int r = f - sb * per;
+            const int i = div_small(r, A, inv_a);
+            const int w = 2 + r - i * A, j = i + w;
+            if (j <= n) {
+                T *al = bx.chart0 + (size_t)sb * bx.cstride;
+                const float a = al[i * ld + j] + dsh[sb] * (float)(w - 1);
+                al[i * ld + j] = a;
+                al[j * ld + i] = a;
+            }
         }
-        if (w >= n - t0 && w <= n - 1 && w >= 2) {
-            const float o = ou[i * ld + j] + d * (float)(n - w);
-            ou[i * ld + j] = o;
-            ou[j * ld + i] = o;
+    }
+    // O' of widths n-t0..n-1: spans (i, i+v) with i + (v - (n-t0)) <= t0
+    {
+        const int per = (t0 + 1) * t0, total = nb * per;
+        const float inv_per = 1.0f / (float)per, inv_t = 1.0f / (float)t0;
+        for (int f = tid; f < total; f += blockDim.x) {
+            const int sb = div_small(f, per, inv_per);
+            const int r = f - sb * per;
+            const int i = div_small(r, t0, inv_t);
+            const int e = r - i * t0, v = n - t0 + e, j = i + v;
+            if (i + e <= t0) {
+                T *ou = bx.chart0 + (size_t)sb * bx.cstride + (size_t)ld * ld;
+                const float o = ou[i * ld + j] + dsh[sb] * (float)(n - v);
+                ou[i * ld + j] = o;
+                ou[j * ld + i] = o;
+            }
         }
     }
     __syncthreads();
@@ -557,7 +576,7 @@ __device__ __forceinline__ void io_sweep(const Bundle_ctx<T> &bx, const uint32_t
             if (s2.G != sh.G || s2.C != sh.C) break;
             ++t2;
         }
-#define CRF_IO_RUN(GG, CC, MM) io_run<GG, (WIDE || CC <= 8) ? CC : 8, (WIDE || CC <= 8) ? MM : 4, WIDE>(bx, t, t2, magic, dsh)
+#define CRF_IO_RUN(GG, CC, MM) io_run<GG, CC, MM, WIDE>(bx, t, t2, magic, dsh)
         CRF_DISPATCH_SHAPE(sh, CRF_IO_RUN);
 #undef CRF_IO_RUN
         if (t2 - 1 == t0) rescale_chart(bx, t0, dsh);
@@ -845,7 +864,7 @@ __device__ __forceinline__ void cky_sweep(const Cky_ctx &cx, const uint32_t *mag
             if (s2.G != sh.G || s2.C != sh.C) break;
             ++w2;
         }
-#define CRF_CKY_RUN(GG, CC, MM) cky_run<GG, (WIDE || CC <= 8) ? CC : 8, (WIDE || CC <= 8) ? MM : 4>(cx, w, w2, magic)
+#define CRF_CKY_RUN(GG, CC, MM) cky_run<GG, CC, MM>(cx, w, w2, magic)
         CRF_DISPATCH_SHAPE(sh, CRF_CKY_RUN);
 #undef CRF_CKY_RUN
         w = w2;
