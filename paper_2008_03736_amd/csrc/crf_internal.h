@@ -22,8 +22,8 @@ constexpr int kMaxBundle = 256;
 
 // LDS a bundle needs besides its charts: a uint32 table of division magics
 // for span counts 0..n+1.  (Masked tail loads stay inside a sentence's inside
-// chart; the CKY chart's reach at most n + 13 float64 past the last chart,
-// into this table and the tree-walk scratch that follow it.)
+// chart; those of the last CKY chart reach up to masked_reach(n) float64 past
+// it, into the tables that follow it, which the plan pads to that size.)
 __host__ __device__ inline int64_t bundle_extra_bytes(int n) { return 4 * (int64_t)(n + 2); }
 
 // Static LDS the kernels reserve besides the charts.
@@ -37,8 +37,8 @@ __host__ __device__ inline int chart_ld(int n) { return n + 1; }
 //           triangle) and the outside values (upper + mirrored; before the
 //           outside sweep reaches a span its mirrored cell holds the span's
 //           score, and cells no sweep reads park the forced-span scores);
-//   cky:    one float64 square (beta, upper + mirror).  The tree walk needs
-//           cky_scratch_ints(n) ints of LDS per wavefront on top.
+//   cky:    one float64 square (beta, upper + mirror); the tree walk needs
+//           cky_walk_bytes of LDS on top.
 __host__ __device__ inline int64_t inside_chart_bytes(int n) {
     const int64_t ld = chart_ld(n);
     return 2 * ld * ld * 4;
@@ -47,7 +47,31 @@ __host__ __device__ inline int64_t cky_chart_bytes(int n) {
     const int64_t ld = chart_ld(n);
     return ld * ld * 8;
 }
+// The CKY tree walk: bundles of fewer than kDfsMinBundle sentences walk
+// breadth first, one wavefront per sentence, with cky_scratch_ints(n) ints
+// per wavefront; larger bundles walk depth first, one lane group per
+// sentence, with a stack of n ints per sentence.
+constexpr int kDfsMinBundle = 16;
 __host__ __device__ inline int cky_scratch_ints(int n) { return 3 * n + 3; }
+__host__ __device__ inline int64_t cky_walk_bytes(int n, int64_t count, int waves) {
+    return count < kDfsMinBundle ? 4 * (int64_t)(count < waves ? count : waves) * cky_scratch_ints(n)
+                                 : 4 * count * n;
+}
+
+// Cells past its span's last split that a masked split read may reach at the
+// widest step of a sentence of n words: (C/2) G for that step's shape (lanes
+// per span G, splits per lane C; the kernels' step-shape rule).
+__host__ __device__ inline int masked_reach(int n) {
+    const int K = n - 1;
+    if (K <= 8) return K <= 1 ? 0 : K <= 2 ? 1 : K <= 4 ? 2 : 4;
+    int g = 1;
+    if (K <= 64) {
+        while (g < (K + 7) / 8) g <<= 1;
+        return 4 * g;
+    }
+    while (g < (K + 15) / 16 && g < 64) g <<= 1;
+    return 8 * g;
+}
 
 // Longest sentence whose CKY chart can sit in one CU's LDS (160 KiB):
 // 8 (n+1)^2 <= 163840.  The plan sends longer ones to the workspace kernels.

@@ -980,6 +980,74 @@ __device__ void backtrace(const Cky_ctx &cx, int sb, int32_t *out, int32_t *scr)
     }
 }
 
+// Recover the 1-best trees of a bundle and write them in preorder.  A group
+// of L lanes walks one sentence depth first, so all sentences of the bundle
+// walk at once: a node's row is the number of rows written before it, and
+// the right children still to visit wait on the sentence's stack in LDS (at
+// most n - 1 deep).  Each internal node's split is recomputed with the
+// group's lanes as the lowest k maximising fl(beta(i,k) + beta(k,j)) --
+// exactly the sweep's max, so exactly its split.  A left child that is a
+// single word is written at once and the walk goes right without a push.
+template <int L>
+__device__ void walk_trees(const Cky_ctx &cx, const int *sid, int32_t *spans, int R, int32_t *stacks) {
+    const int tid = threadIdx.x, gl = tid & (L - 1);
+    const int groups = blockDim.x / L;
+    const int n = cx.n, ld = cx.ld;
+    for (int sb0 = 0; sb0 < cx.nb; sb0 += groups) {
+        const int sb = sb0 + tid / L;
+        bool active = sb < cx.nb;
+        const double *be = cx.beta(active ? sb : 0);
+        int32_t *out = spans + (size_t)sid[active ? sb : 0] * R * 2;
+        int32_t *stack = stacks + (size_t)(active ? sb : 0) * n;
+        int i = 0, j = n, row = 0, sp = 0;
+        for (int it = 0; it < 2 * n; ++it) {   // every step writes a row: at most 2n-1
+            if (__ballot(active) == 0) break;
+            if (active && gl == 0) {
+                out[2 * row] = i;
+                out[2 * row + 1] = j;
+            }
+            const int K = j - i - 1;
+            double lb = -INFINITY;
+            int lk = 0x7fffffff;
+            for (int ko = gl; ko < (active ? K : 0); ko += L) {
+                const double v = be[i * ld + i + 1 + ko] + be[j * ld + i + 1 + ko];
+                if (v > lb) {
+                    lb = v;
+                    lk = ko;
+                }
+            }
+            const double m = grp_max_d<L>(lb);
+            // (clamped so that even a chart without a finite maximum walks a tree)
+            const int kb = min(grp_min_i<L>(lb == m ? lk : 0x7fffffff), K - 1);
+            if (!active) continue;
+            ++row;
+            if (K == 0) {   // a word: resume at the last pending right child
+                if (sp == 0) {
+                    active = false;
+                } else {
+                    const int node = stack[--sp];
+                    i = node & 0xffff;
+                    j = node >> 16;
+                }
+            } else {
+                const int k = i + 1 + kb;
+                if (k == i + 1) {   // left child is a word
+                    if (gl == 0) {
+                        out[2 * row] = i;
+                        out[2 * row + 1] = k;
+                    }
+                    ++row;
+                    i = k;
+                } else {
+                    if (gl == 0) stack[sp] = k | (j << 16);
+                    ++sp;
+                    j = k;
+                }
+            }
+        }
+    }
+}
+
 template <bool SPILL>
 __device__ __forceinline__ void cky_block(const KernelPlan &p, int block, char *smem_raw,
                                           const float *__restrict__ scores,
@@ -987,13 +1055,13 @@ __device__ __forceinline__ void cky_block(const KernelPlan &p, int block, char *
     __shared__ int spill_id[1];
     __shared__ uint32_t spill_magic[SPILL ? CRF_MAX_LEN + 2 : 1];
     __shared__ int32_t spill_scr[SPILL ? 3 * CRF_MAX_LEN + 3 : 1];
-    const int NT = blockDim.x, NW = NT >> 6;
-    const int tid = threadIdx.x, wave = tid >> 6;
+    const int NT = blockDim.x;
+    const int tid = threadIdx.x;
     const int N1 = p.n1;
 
     int n, nb, *sid;
     uint32_t *magic;
-    int32_t *scr;
+    int32_t *scratch;   // tree-walk scratch (cky_walk_bytes)
     char *chart0;
     int cstride;
     if constexpr (SPILL) {
@@ -1004,7 +1072,7 @@ __device__ __forceinline__ void cky_block(const KernelPlan &p, int block, char *
         cstride = 0;
         sid = spill_id;
         magic = spill_magic;
-        scr = spill_scr;
+        scratch = spill_scr;
         if (tid == 0) sid[0] = b;
     } else {
         const Bundle bd = p.cky.bundles[block];
@@ -1014,7 +1082,7 @@ __device__ __forceinline__ void cky_block(const KernelPlan &p, int block, char *
         cstride = (int)cky_chart_bytes(n);
         sid = reinterpret_cast<int *>(smem_raw + (size_t)nb * cstride);
         magic = reinterpret_cast<uint32_t *>(sid + nb);
-        scr = reinterpret_cast<int32_t *>(magic + n + 2);
+        scratch = reinterpret_cast<int32_t *>(magic + n + 2);
         for (int t = tid; t < nb; t += NT) sid[t] = p.cky.order[bd.first + t];
     }
     for (int S = tid; S <= n; S += NT) magic[S] = div_magic(S);
@@ -1048,12 +1116,20 @@ __device__ __forceinline__ void cky_block(const KernelPlan &p, int block, char *
     }
     if (best != nullptr)
         for (int sb = tid; sb < nb; sb += NT) best[sid[sb]] = (float)cx.beta(sb)[n];
-    // Wave w walks sentences w, w+NW, ... with its own scratch slot.
-    int32_t *myscr = scr + (size_t)wave * cky_scratch_ints(n);
-    // An LDS chart (8 (n+1)^2 bytes <= 160 KiB) means n <= 142: 5 nodes per lane.
-    constexpr int PER_LANE = SPILL ? (2 * CRF_MAX_LEN + 63) / 64 : (2 * kMaxLenInLds + 63) / 64;
-    for (int sb = wave; sb < nb; sb += NW)
-        backtrace<PER_LANE>(cx, sb, spans + (size_t)sid[sb] * R * 2, myscr);
+    // Tree walks.  A few (long) sentences: one wavefront each, breadth first,
+    // up to 8 nodes of a level at a time.  Many (short) sentences: one group
+    // of lanes each, depth first, all at once.
+    if (nb < kDfsMinBundle) {
+        constexpr int PER_LANE = SPILL ? (2 * CRF_MAX_LEN + 63) / 64 : (2 * kMaxLenInLds + 63) / 64;
+        const int wave = tid >> 6;
+        for (int sb = wave; sb < nb; sb += NT >> 6)
+            backtrace<PER_LANE>(cx, sb, spans + (size_t)sid[sb] * R * 2,
+                                scratch + (size_t)wave * cky_scratch_ints(n));
+    } else if (nb <= NT / 16) {
+        walk_trees<16>(cx, sid, spans, R, scratch);
+    } else {
+        walk_trees<8>(cx, sid, spans, R, scratch);
+    }
 }
 
 // Workgroups of 256, 512 or 1024 threads (the plan's choice) share one

@@ -93,51 +93,46 @@ inline double sentence_cost(int n) {
     return T + 200.0 * (n - 1);
 }
 
-// Relative duration of a CKY bundle against an inside (forward + reverse)
-// bundle of the same sentences: one max-plus sweep and a tree walk against
-// two log-sum-exp sweeps (measured on single sentences of 30-99 words).
-constexpr double kCkyCostRatio = 0.6;
-
-inline double bundle_cost(const crf::Bundle &b) {
-    const double n = b.n, T = (n + 1) * n * (n - 1) / 6.0;
-    return b.count * T + 200.0 * (n - 1);
+// Predicted duration (microseconds on MI355X, two workgroups per CU) of a
+// bundle of `count` sentences of n words, fitted to per-workgroup timings of
+// the fused launch: a latency per width step, a per-cell term for the global
+// loads and stores around the sweep (inside) or the tree walk (CKY), and the
+// split points themselves.
+inline double split_points(int n) { return (double)(n + 1) * n * (n - 1) / 6.0; }
+inline double predict_inside(int n, int count) {
+    return 0.86 * (n - 1) + 0.0037 * count * (double)n * n + 1.0e-4 * count * split_points(n) + 3.6;
+}
+inline double predict_cky(int n, int count) {
+    return 0.94 * (n - 1) + 0.045 * count * (double)n + 7.0e-5 * count * split_points(n) + 4.7;
 }
 
-// Launch order of the fused kernel: both bundle lists (each already most
-// expensive first) merged by predicted duration.
+// Launch order of the fused kernel: both bundle lists merged by predicted
+// duration, longest first.
 std::vector<int32_t> merge_launch_order(const std::vector<crf::Bundle> &in,
                                         const std::vector<crf::Bundle> &ck) {
+    std::vector<std::pair<double, int32_t>> all;
+    all.reserve(in.size() + ck.size());
+    for (size_t a = 0; a < in.size(); ++a) all.push_back({predict_inside(in[a].n, in[a].count), (int32_t)a});
+    for (size_t c = 0; c < ck.size(); ++c) all.push_back({predict_cky(ck[c].n, ck[c].count), ~(int32_t)c});
+    std::stable_sort(all.begin(), all.end(), [](const auto &x, const auto &y) { return x.first > y.first; });
     std::vector<int32_t> mix;
-    mix.reserve(in.size() + ck.size());
-    size_t a = 0, c = 0;
-    while (a < in.size() || c < ck.size()) {
-        const bool take_inside =
-            c >= ck.size() ||
-            (a < in.size() && bundle_cost(in[a]) >= kCkyCostRatio * bundle_cost(ck[c]));
-        if (take_inside) mix.push_back((int32_t)a++);
-        else mix.push_back(~(int32_t)c++);
-    }
+    mix.reserve(all.size());
+    for (const auto &e : all) mix.push_back(e.second);
     return mix;
 }
 
-// `order` is sorted by decreasing length.  `chart(n)` is the chart size of
-// a sentence; each bundled sentence also needs `per_sentence` bytes of
-// tables, and each wavefront of the workgroup `wave_bytes(n)` of scratch.
-template <typename F>
+// `order` is sorted by decreasing length.  `chart(n)` is the LDS a bundled
+// sentence needs besides `per_sentence` bytes of tables, `spill_chart(n)` its
+// workspace chart, and `tail(n, count)` the bytes a bundle adds at its end.
+template <typename F, typename TF>
 HostSchedule make_schedule(const std::vector<int32_t> &order, const int32_t *len, int lds_cap,
                            bool force_spill, int64_t ws_base, int per_sentence, F chart,
-                           F spill_chart, F wave_bytes) {
+                           F spill_chart, TF tail, const char *target_env) {
     HostSchedule s;
     s.threads = crf::kThreadsDefault;
-    if (const char *ev = getenv("CRF_TUNE_THREADS")) {
-        const int t = atoi(ev);
-        if (t == 256 || t == 512 || t == 1024) s.threads = t;
-    }
-    const int nw = s.threads / 64;
     // LDS of a bundle of `count` sentences of length n.
     auto bundle_bytes = [&](int n, int64_t count) {
-        return count * (chart(n) + per_sentence) + crf::bundle_extra_bytes(n) +
-               std::min<int64_t>(count, nw) * wave_bytes(n);
+        return count * (chart(n) + per_sentence) + crf::bundle_extra_bytes(n) + tail(n, count);
     };
     // Workgroup LDS budget: half the CU when every eligible sentence fits in
     // half (two workgroups per CU), else all of it (one).
@@ -168,7 +163,12 @@ HostSchedule make_schedule(const std::vector<int32_t> &order, const int32_t *len
     // never split below one sentence.
     double total = 0.0;
     for (int32_t b : eligible) total += sentence_cost(len[b]);
-    const double target = std::max(total / slots, 1.0);
+    double scale = 1.0;
+    if (const char *ev = getenv(target_env)) {
+        const double v = atof(ev);
+        if (v > 0.0 && v < 100.0) scale = v;
+    }
+    const double target = std::max(total / slots, 1.0) * scale;
 
     struct Tmp { crf::Bundle bd; double cost; };
     std::vector<Tmp> tmp;
@@ -268,13 +268,21 @@ int crf_plan_create(crf_plan **out, const int32_t *lengths_host, int32_t batch, 
     const bool force = (flags & CRF_FORCE_SPILL) != 0;
     auto inside_bytes = [](int n) { return crf::inside_chart_bytes(n); };
     auto cky_bytes = [](int n) { return crf::cky_chart_bytes(n); };
-    auto no_scratch = [](int) { return (int64_t)0; };
-    auto cky_scratch = [](int n) { return (int64_t)4 * crf::cky_scratch_ints(n); };
+    // The CKY bundle's tail: the tree-walk scratch, padded so that the last
+    // chart's masked reads (into the id, magic and scratch tables behind it)
+    // stay inside the bundle.
+    constexpr int nwaves = crf::kThreadsDefault / 64;
+    auto no_tail = [](int, int64_t) { return (int64_t)0; };
+    auto cky_tail = [](int n, int64_t count) {
+        const int64_t walk = crf::cky_walk_bytes(n, count, nwaves);
+        const int64_t tables = 4 * count + crf::bundle_extra_bytes(n) + walk;
+        return walk + std::max<int64_t>(0, 8 * (int64_t)crf::masked_reach(n) - tables);
+    };
     // inside tables: forced sum (f64), gradient (f32), id (i32), score shift (f32); cky: id
     HostSchedule si = make_schedule(order, lengths_host, lds_cap, force, 0, 20, +inside_bytes,
-                                    +inside_bytes, +no_scratch);
+                                    +inside_bytes, +no_tail, "CRF_TUNE_TARGET_INSIDE");
     HostSchedule sc = make_schedule(order, lengths_host, lds_cap, force, si.ws_bytes, 4, +cky_bytes,
-                                    +cky_bytes, +cky_scratch);
+                                    +cky_bytes, cky_tail, "CRF_TUNE_TARGET_CKY");
     p->ws_bytes = si.ws_bytes + sc.ws_bytes;
 
     std::vector<int32_t> len(lengths_host, lengths_host + batch);
