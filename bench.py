@@ -1,19 +1,20 @@
 #!/usr/bin/env python3
 """Throughput of the batched tree-CRF hot path on one MI355X.
 
-One step = one pass of the whole path over the batch: inside forward (log Z)
-+ reverse pass (span marginals) in one fused call, then CKY decode (1-best
-trees).  Inputs are resident in HBM before timing starts.  Prints one JSON
+One step = one pass of the whole path over the batch: inside (log Z), span
+marginals (the derivative of log Z, as inside x outside) and CKY decode
+(1-best trees), in one fused launch.  Inputs are resident in HBM before timing starts.  Prints one JSON
 line.
 
   python bench.py [--steps K] [--warmup W] [--workload mixed] [--no-cpu-baseline]
 
-Roofline: the hot path is one launch (parse_kernel: inside, reverse and CKY
-workgroups interleaved).  It is bound by plain vector-ALU work and by the
+Roofline: the hot path is one launch (parse_kernel: inside + marginal and CKY
+workgroups side by side).  It is bound by plain vector-ALU work and by the
 dependency chain of width steps, not by HBM and not by MFMA.  Algorithmic work
 per sentence of n words, with T(n) = (n+1)n(n-1)/6 split points and
 P(n) = n(n+1)/2 spans, in VALU issue slots (a transcendental v_exp/v_log/v_rcp
-costs 2 slots, as measured on gfx950):
+costs 2 slots, as measured on gfx950), counting the marginals as a reverse-mode
+pass (the cheaper formulation; the kernel's outside pass does more):
   inside   per split: add, max, sub, exp, add          = 6
            per span:  log, 2 adds                      = 4
   reverse  per split: sub, exp, mul, 2 adds            = 6
@@ -39,7 +40,7 @@ HBM_PEAK = 8.0e12               # bytes per second
 # HBM bytes per launch of the timed kernel from rocprofv3 FETCH_SIZE / WRITE_SIZE,
 # scaled by the same counters on a plain copy of known size, keyed by workload
 # and by the kernel source they were taken on (reported only while it matches).
-MEASURED_TRAFFIC = {"mixed": (66.64e6, "8834349c9ca1f352")}
+MEASURED_TRAFFIC = {"mixed": (75.29e6, "1c9ded82d7ec5133")}
 METRIC = "sentences/sec for inside fwd+bwd and CKY decode; % of binding roofline"
 
 
@@ -195,7 +196,7 @@ def main():
     hbm = wm["bytes_inside"] + (wm["bytes_cky"] if decode else 0)
     ach = slots / (t_step * 1e-3)
     roof = {"bound": "alu",
-            "kernel": "parse_kernel (inside + reverse + CKY, one launch)" if decode else "inside_kernel<rev>",
+            "kernel": "parse_kernel (inside + marginals + CKY, one launch)" if decode else "inside_kernel (inside + marginals)",
             "achieved": round(ach / 1e12, 4), "peak": round(PEAK_SLOTS / 1e12, 3),
             "unit": "T VALU lane-slots/s", "frac": round(ach / PEAK_SLOTS, 5),
             "traffic": measured_traffic(batch.name) if decode else None, "avg_ms": round(t_step, 4),

@@ -8,7 +8,8 @@
  *     (Sec. 2.1, Eq. tree-prob), by the inside recursion of Sec. 3.1
  *     (Algorithm 1);
  *   - the span marginals p((i,j)|x) = d log Z / d s(i,j) (Sec. 3.2,
- *     Eq. partial-derivative) by differentiating that recursion in reverse;
+ *     Eq. partial-derivative), evaluated as exp(inside + outside - log Z)
+ *     with the outside recursion run beside the inside one;
  *   - the 1-best tree argmax_y s(x,y) (Sec. 2.1, Eq. tree-argmax) by CKY,
  *     the same recursion with max in place of sum (Sec. 3.3);
  *   - for the one-stage labelled CRF (Sec. 4.2, Eq. tree-label-score),

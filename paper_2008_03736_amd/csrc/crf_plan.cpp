@@ -121,13 +121,20 @@ std::vector<int32_t> merge_launch_order(const std::vector<crf::Bundle> &in,
     return mix;
 }
 
+// Bundle sizing.  A bundle's split points are aimed at target_scale times the
+// batch's share per workgroup slot.  Inside bundles aim at twice the share:
+// their width steps are latency bound, so more sentences per step cost
+// little, and fewer, fuller bundles measured 3-5% faster on the 5,000-sentence
+// mixed batch than an even share; CKY bundles take the share.
+constexpr double kInsideTargetScale = 2.0, kCkyTargetScale = 1.0;
+
 // `order` is sorted by decreasing length.  `chart(n)` is the LDS a bundled
 // sentence needs besides `per_sentence` bytes of tables, `spill_chart(n)` its
 // workspace chart, and `tail(n, count)` the bytes a bundle adds at its end.
 template <typename F, typename TF>
 HostSchedule make_schedule(const std::vector<int32_t> &order, const int32_t *len, int lds_cap,
                            bool force_spill, int64_t ws_base, int per_sentence, F chart,
-                           F spill_chart, TF tail, const char *target_env) {
+                           F spill_chart, TF tail, double target_scale) {
     HostSchedule s;
     s.threads = crf::kThreadsDefault;
     // LDS of a bundle of `count` sentences of length n.
@@ -163,12 +170,7 @@ HostSchedule make_schedule(const std::vector<int32_t> &order, const int32_t *len
     // never split below one sentence.
     double total = 0.0;
     for (int32_t b : eligible) total += sentence_cost(len[b]);
-    double scale = 1.0;
-    if (const char *ev = getenv(target_env)) {
-        const double v = atof(ev);
-        if (v > 0.0 && v < 100.0) scale = v;
-    }
-    const double target = std::max(total / slots, 1.0) * scale;
+    const double target = std::max(total / slots, 1.0) * target_scale;
 
     struct Tmp { crf::Bundle bd; double cost; };
     std::vector<Tmp> tmp;
@@ -280,9 +282,9 @@ int crf_plan_create(crf_plan **out, const int32_t *lengths_host, int32_t batch, 
     };
     // inside tables: forced sum (f64), gradient (f32), id (i32), score shift (f32); cky: id
     HostSchedule si = make_schedule(order, lengths_host, lds_cap, force, 0, 20, +inside_bytes,
-                                    +inside_bytes, +no_tail, "CRF_TUNE_TARGET_INSIDE");
+                                    +inside_bytes, +no_tail, kInsideTargetScale);
     HostSchedule sc = make_schedule(order, lengths_host, lds_cap, force, si.ws_bytes, 4, +cky_bytes,
-                                    +cky_bytes, cky_tail, "CRF_TUNE_TARGET_CKY");
+                                    +cky_bytes, cky_tail, kCkyTargetScale);
     p->ws_bytes = si.ws_bytes + sc.ws_bytes;
 
     std::vector<int32_t> len(lengths_host, lengths_host + batch);
