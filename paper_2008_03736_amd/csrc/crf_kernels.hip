@@ -584,55 +584,63 @@ __device__ __forceinline__ void io_sweep(const Bundle_ctx<T> &bx, const uint32_t
     }
 }
 
-// Visit every valid cell (sb, i, j), 0 <= i < j <= n, of a bundle with one
-// thread per cell of an n x n tile per sentence (row i, column j-1, cells
-// below the diagonal skipped): consecutive threads take consecutive j.
-template <typename F>
-__device__ __forceinline__ void for_cells(int nb, int n, F &&f) {
-    const int NT = blockDim.x;
-    const int nn = n * n;
-    const int total = nb * nn;
-    const float inv_nn = 1.0f / (float)nn, inv_n = 1.0f / (float)n;
-    for (int c = threadIdx.x; c < total; c += NT) {
-        const int sb = div_small(c, nn, inv_nn);
-        const int rem = c - sb * nn;
-        const int i = div_small(rem, n, inv_n);
-        const int j = rem - i * n + 1;
-        if (j > i) f(sb, i, j);
+// Visit every valid cell (sb, i, j), 0 <= i < j <= n, of a bundle.  Rows r
+// and n-1-r of the upper triangle (n-r and r+1 cells) share one folded row
+// of n+1 slots: slot q < n-r is (r, r+1+q), slot q >= n-r is (n-1-r, q).
+// So a walk touches (n+1) ceil(n/2) slots per sentence instead of n^2, and
+// consecutive threads take consecutive j of one row.
+struct Cell {
+    int sb, i, j;
+    bool ok;
+};
+struct Cell_walk {
+    int n, W, per, total;
+    float inv_per, inv_w;
+    __device__ Cell_walk(int nb, int n_) : n(n_), W(n_ + 1) {
+        per = ((n + 1) / 2) * W;
+        total = nb * per;
+        inv_per = 1.0f / (float)per;
+        inv_w = 1.0f / (float)W;
     }
-}
+    __device__ __forceinline__ Cell at(int c) const {
+        Cell e;
+        const int cc = c < total ? c : 0;
+        e.sb = div_small(cc, per, inv_per);
+        const int rem = cc - e.sb * per;
+        const int r = div_small(rem, W, inv_w);
+        const int q = rem - r * W;
+        if (q < n - r) {
+            e.i = r;
+            e.j = r + 1 + q;
+            e.ok = c < total;
+        } else {
+            e.i = n - 1 - r;
+            e.j = q;
+            e.ok = c < total && e.i > r;   // odd n: the middle row is not folded twice
+        }
+        return e;
+    }
+};
 
-// The same walk, U cells per thread at a time: their U loads are issued
-// together (one memory latency per U cells instead of one per cell), then
-// `use` consumes them.
+// The walk, U cells per thread at a time: their U loads are issued together
+// (one memory latency per U cells), then `use` consumes them.
 template <int U, typename LD, typename F>
 __device__ __forceinline__ void for_cells_loaded(int nb, int n, LD &&load, F &&use) {
     const int NT = blockDim.x;
-    const int nn = n * n;
-    const int total = nb * nn;
-    const float inv_nn = 1.0f / (float)nn, inv_n = 1.0f / (float)n;
+    const Cell_walk cw(nb, n);
     using V = decltype(load(0, 0, 1));
-    for (int c0 = threadIdx.x; c0 < total; c0 += NT * U) {
-        int sbv[U], iv[U], jv[U];
-        bool ok[U];
+    for (int c0 = threadIdx.x; c0 < cw.total; c0 += NT * U) {
         V v[U];
+        int cell[U];   // sb << 20 | i << 10 | j (sb < 256, i, j < 1024), or -1
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            const int c = c0 + u * NT;
-            const int cc = c < total ? c : 0;
-            const int sb = div_small(cc, nn, inv_nn);
-            const int rem = cc - sb * nn;
-            const int i = div_small(rem, n, inv_n);
-            const int j = rem - i * n + 1;
-            sbv[u] = sb;
-            iv[u] = i;
-            jv[u] = j;
-            ok[u] = c < total && j > i;
-            v[u] = ok[u] ? load(sb, i, j) : V(0);
+            const Cell e = cw.at(c0 + u * NT);
+            cell[u] = e.ok ? (e.sb << 20) | (e.i << 10) | e.j : -1;
+            v[u] = e.ok ? load(e.sb, e.i, e.j) : V(0);
         }
 #pragma unroll
         for (int u = 0; u < U; ++u)
-            if (ok[u]) use(sbv[u], iv[u], jv[u], v[u]);
+            if (cell[u] >= 0) use(cell[u] >> 20, (cell[u] >> 10) & 1023, cell[u] & 1023, v[u]);
     }
 }
 
