@@ -58,19 +58,33 @@ __host__ __device__ inline int64_t cky_walk_bytes(int n, int64_t count, int wave
                                  : 4 * count * n;
 }
 
-// Cells past its span's last split that a masked split read may reach at the
-// widest step of a sentence of n words: (C/2) G for that step's shape (lanes
-// per span G, splits per lane C; the kernels' step-shape rule).
+// Shape of a width step with K split points per span: G lanes per span (a
+// power of two <= 64), C splits per lane (lane l takes splits l, l+G, ...),
+// of which the first MF are in range for every lane (MF G <= K) and the rest
+// are masked.  Every distinct shape is its own unrolled body, and entering
+// one that a sweep has not run yet refills the instruction cache, so sweeps
+// use few shapes; past 32 splits G doubles every 32 G splits and C is 12 or
+// 16, which keeps the masked share of a step under a quarter.
+struct StepShape {
+    int G, C, MF;
+};
+__host__ __device__ inline StepShape step_shape_k(int K) {
+    if (K <= 1) return StepShape{1, 1, 0};
+    if (K <= 2) return StepShape{1, 2, 1};
+    if (K <= 4) return StepShape{1, 4, 2};
+    if (K <= 8) return StepShape{1, 8, 4};
+    if (K <= 16) return StepShape{2, 8, 4};
+    if (K <= 32) return StepShape{4, 8, 4};
+    int g = 4;
+    while (16 * g < K && g < 64) g <<= 1;
+    return 12 * g >= K ? StepShape{g, 12, 8} : StepShape{g, 16, 12};
+}
+
+// Cells past its span's last split that a masked split read may reach, at
+// the widest step of a sentence of n words: (C - MF) G.
 __host__ __device__ inline int masked_reach(int n) {
-    const int K = n - 1;
-    if (K <= 8) return K <= 1 ? 0 : K <= 2 ? 1 : K <= 4 ? 2 : 4;
-    int g = 1;
-    if (K <= 64) {
-        while (g < (K + 7) / 8) g <<= 1;
-        return 4 * g;
-    }
-    while (g < (K + 15) / 16 && g < 64) g <<= 1;
-    return 8 * g;
+    const StepShape sh = step_shape_k(n - 1 > 0 ? n - 1 : 0);
+    return (sh.C - sh.MF) * sh.G;
 }
 
 // Longest sentence whose CKY chart can sit in one CU's LDS (160 KiB):

@@ -177,15 +177,6 @@ constexpr float NEG = -1.0e30f;
 __device__ __forceinline__ int next_pow2(int x) { return x <= 1 ? 1 : 1 << (32 - __builtin_clz(x - 1)); }
 __device__ __forceinline__ int floor_pow2(int x) { return x <= 1 ? 1 : 1 << (31 - __builtin_clz(x)); }
 
-// Step shapes.  Every distinct (lanes per span G, terms per lane C) is its
-// own unrolled body, and entering one a sweep has not run yet refills the
-// instruction cache (thousands of cycles), so sweeps use few shapes: K <= 8
-// splits take G = 1 and C in {1, 2, 4, 8}; K <= 64 take C = 8 and
-// G = next_pow2(ceil(K / 8)); longer spans take C = 16 and
-// G = next_pow2(ceil(K / 16)) (at most 64).  C is rounded up: terms
-// c >= C/2 may fall past the K splits and are masked (for K > 8,
-// ceil(K / G) > C/2), so a lane reads at most (C/2) G - 1 <= K + 14 cells
-// past its span's last split.
 // ---------------------------------------------------------------------------
 // Per-bundle context: nb sentences of length n; sentence sb's chart starts at
 // chart0 + sb * cstride (elements).
@@ -379,16 +370,6 @@ __device__ __forceinline__ void io_step(const Bundle_ctx<T> &bx, int t, uint32_t
     }
 }
 
-// Lanes per span and split terms per lane of a width step (K = w - 1).
-struct Step_shape {
-    int G, C;
-};
-__device__ __forceinline__ Step_shape step_shape(int w) {
-    const int K = w - 1;
-    if (K <= 8) return Step_shape{1, K <= 1 ? 1 : K <= 2 ? 2 : K <= 4 ? 4 : 8};
-    if (K <= 64) return Step_shape{next_pow2((K + 7) / 8), 8};
-    return Step_shape{min(64, next_pow2((K + 15) / 16)), 16};
-}
 // A run of forward widths [w0, w1) sharing one step shape: a tight loop with
 // no dispatch.  magic[S] = div_magic(S) (LDS table), fetched one step ahead
 // (S = n-w+1 stays in [0, n] even one step past the run).
@@ -419,9 +400,9 @@ __device__ __forceinline__ void io_run(const Bundle_ctx<T> &bx, int t0, int t1, 
     }
 }
 
-// Calls RUN(G, C, MF) for a step shape (C rounded up to a power of two:
-// terms c >= C/2 may fall past K).  Charts in LDS hold at most 142 words, so
-// their sweeps never need G >= 32; only the workspace (WIDE) kernels build it.
+// Calls RUN(G, C, MF) for a step shape.  Charts in LDS hold at most 142
+// words, so their sweeps never need G >= 32; only the workspace (WIDE)
+// kernels build those shapes.
 #define CRF_DISPATCH_SHAPE(SH, RUN)                          \
     do {                                                     \
         switch ((SH).G) {                                    \
@@ -434,16 +415,28 @@ __device__ __forceinline__ void io_run(const Bundle_ctx<T> &bx, int t0, int t1, 
                 }                                            \
                 break;                                       \
             case 2: RUN(2, 8, 4); break;                     \
-            case 4: RUN(4, 8, 4); break;                     \
-            case 8:                                          \
-                if ((SH).C == 8) RUN(8, 8, 4);               \
-                else RUN(8, 16, 8);                          \
+            case 4:                                          \
+                if ((SH).C == 8) RUN(4, 8, 4);               \
+                else if ((SH).C == 12) RUN(4, 12, 8);        \
+                else RUN(4, 16, 12);                         \
                 break;                                       \
-            case 16: RUN(16, 16, 8); break;                  \
+            case 8:                                          \
+                if ((SH).C == 12) RUN(8, 12, 8);             \
+                else RUN(8, 16, 12);                         \
+                break;                                       \
+            case 16:                                         \
+                if ((SH).C == 12) RUN(16, 12, 8);            \
+                else RUN(16, 16, 12);                        \
+                break;                                       \
             default:                                         \
                 if constexpr (WIDE) {                        \
-                    if ((SH).G == 32) RUN(32, 16, 8);        \
-                    else RUN(64, 16, 8);                     \
+                    if ((SH).G == 32) {                      \
+                        if ((SH).C == 12) RUN(32, 12, 8);    \
+                        else RUN(32, 16, 12);                \
+                    } else {                                 \
+                        if ((SH).C == 12) RUN(64, 12, 8);    \
+                        else RUN(64, 16, 12);                \
+                    }                                        \
                 }                                            \
                 break;                                       \
         }                                                    \
@@ -457,10 +450,10 @@ __device__ __forceinline__ void fwd_sweep(const Bundle_ctx<T> &bx, const uint32_
     const int n = bx.n;
     int w = 2;
     while (w <= n) {
-        const Step_shape sh = step_shape(w);
+        const StepShape sh = step_shape_k(w - 1);
         int w2 = w + 1;
         while (w2 <= n) {
-            const Step_shape s2 = step_shape(w2);
+            const StepShape s2 = step_shape_k(w2 - 1);
             if (s2.G != sh.G || s2.C != sh.C) break;
             ++w2;
         }
@@ -569,10 +562,10 @@ __device__ __forceinline__ void io_sweep(const Bundle_ctx<T> &bx, const uint32_t
     const int n = bx.n;
     int t = 1;
     while (t <= n - 1) {
-        const Step_shape sh = step_shape(t + 1);
+        const StepShape sh = step_shape_k(t);
         int t2 = t + 1;
         while (t2 <= n - 1 && t2 - 1 != t0) {
-            const Step_shape s2 = step_shape(t2 + 1);
+            const StepShape s2 = step_shape_k(t2);
             if (s2.G != sh.G || s2.C != sh.C) break;
             ++t2;
         }
@@ -865,10 +858,10 @@ __device__ __forceinline__ void cky_sweep(const Cky_ctx &cx, const uint32_t *mag
     const int n = cx.n;
     int w = 2;
     while (w <= n) {
-        const Step_shape sh = step_shape(w);
+        const StepShape sh = step_shape_k(w - 1);
         int w2 = w + 1;
         while (w2 <= n) {
-            const Step_shape s2 = step_shape(w2);
+            const StepShape s2 = step_shape_k(w2 - 1);
             if (s2.G != sh.G || s2.C != sh.C) break;
             ++w2;
         }
