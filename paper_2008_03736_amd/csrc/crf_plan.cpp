@@ -106,19 +106,95 @@ inline double predict_cky(int n, int count) {
     return 0.94 * (n - 1) + 0.045 * count * (double)n + 7.0e-5 * count * split_points(n) + 4.7;
 }
 
-// Launch order of the fused kernel: both bundle lists merged by predicted
-// duration, longest first.
-std::vector<int32_t> merge_launch_order(const std::vector<crf::Bundle> &in,
-                                        const std::vector<crf::Bundle> &ck) {
-    std::vector<std::pair<double, int32_t>> all;
-    all.reserve(in.size() + ck.size());
-    for (size_t a = 0; a < in.size(); ++a) all.push_back({predict_inside(in[a].n, in[a].count), (int32_t)a});
-    for (size_t c = 0; c < ck.size(); ++c) all.push_back({predict_cky(ck[c].n, ck[c].count), ~(int32_t)c});
-    std::stable_sort(all.begin(), all.end(), [](const auto &x, const auto &y) { return x.first > y.first; });
-    std::vector<int32_t> mix;
-    mix.reserve(all.size());
-    for (const auto &e : all) mix.push_back(e.second);
-    return mix;
+// Predicted end of a launch whose workgroups (durations `dur`, in launch
+// order) are dealt round-robin to n_part partitions (XCDs) of `slots`
+// workgroup slots each, a workgroup starting when a slot of its partition
+// frees up.  ends[b] receives each workgroup's predicted end.
+double simulate_launch(const std::vector<double> &dur, int n_part, int slots, std::vector<double> &ends,
+                       std::vector<double> &heap) {
+    heap.assign((size_t)n_part * slots, 0.0);
+    ends.resize(dur.size());
+    double end = 0.0;
+    auto later = [](double a, double b) { return a > b; };   // min-heap
+    for (size_t b = 0; b < dur.size(); ++b) {
+        double *h = heap.data() + (b % n_part) * (size_t)slots;
+        std::pop_heap(h, h + slots, later);
+        const double e = h[slots - 1] + dur[b];
+        h[slots - 1] = e;
+        std::push_heap(h, h + slots, later);
+        ends[b] = e;
+        end = std::max(end, e);
+    }
+    return end;
+}
+
+// Launch order of the fused kernel (mix: e >= 0 inside bundle e, e < 0 CKY
+// bundle ~e), longest predicted first.  Then the tail: while it helps the
+// predicted makespan, the multi-sentence bundle that ends last is split in
+// two (the halves keep their sentences' slots of the order array), which
+// trades a little more total work for a shorter end of the launch.  Both
+// bundle lists come back in launch order.
+void plan_fused_launch(std::vector<crf::Bundle> &in, std::vector<crf::Bundle> &ck, int n_part, int slots,
+                       std::vector<int32_t> &mix) {
+    struct Item {
+        double d;
+        bool inside;
+        crf::Bundle bd;
+    };
+    auto predict = [](const Item &x) {
+        return x.inside ? predict_inside(x.bd.n, x.bd.count) : predict_cky(x.bd.n, x.bd.count);
+    };
+    std::vector<Item> items;
+    items.reserve(2 * (in.size() + ck.size()));
+    for (const crf::Bundle &b : in) items.push_back({0.0, true, b});
+    for (const crf::Bundle &b : ck) items.push_back({0.0, false, b});
+    for (Item &x : items) x.d = predict(x);
+    auto longer = [](const Item &a, const Item &b) { return a.d > b.d; };
+    std::stable_sort(items.begin(), items.end(), longer);
+
+    std::vector<double> dur, ends, heap;
+    auto simulate = [&]() {
+        dur.resize(items.size());
+        for (size_t i = 0; i < items.size(); ++i) dur[i] = items[i].d;
+        return simulate_launch(dur, n_part, slots, ends, heap);
+    };
+    double best = simulate();
+    std::vector<Item> best_items = items;
+    const int max_iter = (int)items.size() / 2;
+    for (int it = 0, stale = 0; it < max_iter && stale < 64; ++it) {
+        int j = -1;
+        for (int i = 0; i < (int)items.size(); ++i)
+            if (items[i].bd.count >= 2 && (j < 0 || ends[i] > ends[j])) j = i;
+        if (j < 0) break;
+        Item a = items[j], b = items[j];
+        a.bd.count = items[j].bd.count / 2;
+        b.bd.first += a.bd.count;
+        b.bd.count -= a.bd.count;
+        a.d = predict(a);
+        b.d = predict(b);
+        items.erase(items.begin() + j);
+        for (const Item &x : {a, b}) items.insert(std::upper_bound(items.begin(), items.end(), x, longer), x);
+        const double m = simulate();
+        if (m < best - 1e-6) {
+            best = m;
+            best_items = items;
+            stale = 0;
+        } else {
+            ++stale;
+        }
+    }
+    in.clear();
+    ck.clear();
+    mix.clear();
+    for (const Item &x : best_items) {
+        if (x.inside) {
+            mix.push_back((int32_t)in.size());
+            in.push_back(x.bd);
+        } else {
+            mix.push_back(~(int32_t)ck.size());
+            ck.push_back(x.bd);
+        }
+    }
 }
 
 // Bundle sizing.  A bundle's split points are aimed at target_scale times the
@@ -292,6 +368,18 @@ int crf_plan_create(crf_plan **out, const int32_t *lengths_host, int32_t batch, 
     kp.B = batch;
     kp.n1 = n1;
     kp.L = num_labels;
+    std::vector<int32_t> mix;
+    if (num_labels == 1 && !si.bundles.empty() && !sc.bundles.empty() && si.threads == sc.threads) {
+        // One workgroup slot per CU per half of the LDS; the hardware deals
+        // consecutive workgroups to the XCDs (32 CUs each on gfx950) in turn.
+        int cus = 0;
+        if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, p->device) != hipSuccess || cus < 1)
+            cus = 256;
+        const int n_part = std::max(1, cus / 32);
+        const int per_cu = std::min(4, std::max(1, (int)(lds_cap / std::max(si.lds_bytes, sc.lds_bytes))));
+        plan_fused_launch(si.bundles, sc.bundles, n_part, std::max(1, cus / n_part) * per_cu, mix);
+    }
+    kp.n_mix = (int32_t)mix.size();
     auto fill = [](crf::Schedule &q, const HostSchedule &h) {
         q.n_bundles = (int32_t)h.bundles.size();
         q.n_spill = (int32_t)h.spill.size();
@@ -300,10 +388,6 @@ int crf_plan_create(crf_plan **out, const int32_t *lengths_host, int32_t batch, 
     };
     fill(kp.inside, si);
     fill(kp.cky, sc);
-    std::vector<int32_t> mix;
-    if (num_labels == 1 && !si.bundles.empty() && !sc.bundles.empty() && si.threads == sc.threads)
-        mix = merge_launch_order(si.bundles, sc.bundles);
-    kp.n_mix = (int32_t)mix.size();
 
     if ((e = upload(p, len, &kp.len)) != hipSuccess ||
         (e = upload(p, si.bundles, &kp.inside.bundles)) != hipSuccess ||
