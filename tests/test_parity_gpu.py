@@ -232,3 +232,28 @@ def test_autograd_function(torch):
         (lz * torch.tensor([1.0, 3.0], device=dev)).sum().backward()
     _, mu = orc.marginals(b.scores, b.lengths, grad=[1.0, 3.0])
     check_marg(s.grad.cpu().numpy(), mu, b.lengths, b.n1)
+
+
+def test_step_shape_boundaries(torch):
+    # lengths on both sides of every change of step shape (split counts 1, 2,
+    # 3, 5, 9, 17, 33, 49, 65, 97, 129), the last length whose CKY chart fits
+    # in LDS (142) and the first that does not (143)
+    lengths = [2, 3, 4, 5, 6, 9, 10, 17, 18, 33, 34, 49, 50, 65, 66, 97, 98, 129, 130, 142, 143]
+    b = W.custom(lengths, seed=21, sd=2.0)
+    out, worst = full_check(torch, b)
+    assert out["info"]["spill_count"] >= 1
+    print(f"shape boundaries: max |marginal error| {worst:.2e}")
+
+
+def test_many_short_sentences(torch):
+    # large bundles of short sentences: the depth-first tree walk
+    b = W.custom([12] * 700 + [7] * 300 + [3] * 50, seed=22, sd=2.0)
+    full_check(torch, b)
+
+
+def test_longest_sentence(torch):
+    # the longest sentence the library accepts, on the workspace kernels
+    b = W.custom([1023], seed=23, sd=1.0)
+    out, worst = full_check(torch, b)
+    assert out["info"]["spill_count"] == 1
+    print(f"n = 1023: max |marginal error| {worst:.2e}")
