@@ -63,8 +63,8 @@ __host__ __device__ inline int64_t cky_walk_bytes(int n, int64_t count, int wave
 // of which the first MF are in range for every lane (MF G <= K) and the rest
 // are masked.  Every distinct shape is its own unrolled body, and entering
 // one that a sweep has not run yet refills the instruction cache, so sweeps
-// use few shapes; past 32 splits G doubles every 32 G splits and C is 12 or
-// 16, which keeps the masked share of a step under a quarter.
+// use few shapes; C grows in steps of a quarter or a third, which keeps the
+// masked share of a step under a quarter.
 struct StepShape {
     int G, C, MF;
 };
@@ -75,7 +75,13 @@ __host__ __device__ inline StepShape step_shape_k(int K) {
     if (K <= 8) return StepShape{1, 8, 4};
     if (K <= 16) return StepShape{2, 8, 4};
     if (K <= 32) return StepShape{4, 8, 4};
-    int g = 4;
+    // 33..128 splits: 4 lanes per span, so that a lone sentence of up to 127
+    // words takes one pass of a 512-thread workgroup per joint step
+    if (K <= 48) return StepShape{4, 12, 8};
+    if (K <= 64) return StepShape{4, 16, 12};
+    if (K <= 96) return StepShape{4, 24, 16};
+    if (K <= 128) return StepShape{4, 32, 24};
+    int g = 8;
     while (16 * g < K && g < 64) g <<= 1;
     return 12 * g >= K ? StepShape{g, 12, 8} : StepShape{g, 16, 12};
 }

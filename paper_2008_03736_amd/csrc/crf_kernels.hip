@@ -400,9 +400,10 @@ __device__ __forceinline__ void io_run(const Bundle_ctx<T> &bx, int t0, int t1, 
     }
 }
 
-// Calls RUN(G, C, MF) for a step shape.  Charts in LDS hold at most 142
-// words, so their sweeps never need G >= 32; only the workspace (WIDE)
-// kernels build those shapes.
+// Calls RUN(G, C, MF) for a step shape (step_shape_k never gives G = 8).
+// Charts in LDS hold at most 142 words (K <= 141), so their sweeps need
+// neither G >= 32 nor (16, 16); only the workspace (WIDE) kernels build
+// those shapes.
 #define CRF_DISPATCH_SHAPE(SH, RUN)                          \
     do {                                                     \
         switch ((SH).G) {                                    \
@@ -418,14 +419,12 @@ __device__ __forceinline__ void io_run(const Bundle_ctx<T> &bx, int t0, int t1, 
             case 4:                                          \
                 if ((SH).C == 8) RUN(4, 8, 4);               \
                 else if ((SH).C == 12) RUN(4, 12, 8);        \
-                else RUN(4, 16, 12);                         \
-                break;                                       \
-            case 8:                                          \
-                if ((SH).C == 12) RUN(8, 12, 8);             \
-                else RUN(8, 16, 12);                         \
+                else if ((SH).C == 16) RUN(4, 16, 12);       \
+                else if ((SH).C == 24) RUN(4, 24, 16);       \
+                else RUN(4, 32, 24);                         \
                 break;                                       \
             case 16:                                         \
-                if ((SH).C == 12) RUN(16, 12, 8);            \
+                if (!WIDE || (SH).C == 12) RUN(16, 12, 8);   \
                 else RUN(16, 16, 12);                        \
                 break;                                       \
             default:                                         \
