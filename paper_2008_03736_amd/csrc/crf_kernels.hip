@@ -822,19 +822,29 @@ __device__ __forceinline__ void cky_step(const Cky_ctx &cx, int w, uint32_t magi
         double *be = cx.beta(at.sb);
         const int rowo = (int)__umul24((uint32_t)i, (uint32_t)(ld + 1)) + 1 + l;
         const int colo = rowo + (int)__umul24((uint32_t)w, (uint32_t)ld);
-        double x[C];
-#pragma unroll
-        for (int c = 0; c < C; ++c) x[c] = be[rowo + c * G] + be[colo + c * G];
         const double sij = be[i * ld + j];
+        double x[C], xr[C], xc[C];
+#pragma unroll
+        for (int c = 0; c < C; ++c) {
+            xr[c] = be[rowo + c * G];
+            xc[c] = be[colo + c * G];
+        }
+        // every load in flight before the first use (float64 operands of
+        // up to 16 splits fit in registers; longer lanes interleave)
+        if constexpr (C <= 16) __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int c = 0; c < C; ++c) x[c] = xr[c] + xc[c];
+        const int kl = K - l;
 #pragma unroll
         for (int c = MF; c < C; ++c)
-            if (l + c * G >= K) x[c] = -INFINITY;
+            if (c * G >= kl) x[c] = -INFINITY;
         double m = x[0];
 #pragma unroll
         for (int c = 1; c < C; ++c) m = fmax(m, x[c]);
         m = grp_max_d<G>(m);
+        const double v = m + sij;
+        asm volatile("" ::"v"(v));   // keeps the score load with the operand loads
         if (act && l == 0) {
-            const double v = m + sij;
             be[i * ld + j] = v;
             be[j * ld + i] = v;
         }
