@@ -3,7 +3,7 @@
 // Method (Zhang, Zhou & Li, IJCAI 2020):
 //   inside   alpha(i,j) = s(i,j) + log sum_{i<k<j} exp(alpha(i,k) + alpha(k,j)),
 //            log Z = alpha(0,n)                           (Sec. 3.1, Algorithm 1)
-//   reverse  p((i,j)|x) = d log Z / d s(i,j)              (Sec. 3.2, Eq. partial-derivative)
+//   marginal p((i,j)|x) = d log Z / d s(i,j)              (Sec. 3.2, Eq. partial-derivative)
 //   CKY      the same recursion under max, 1-best tree    (Sec. 3.3, Eq. tree-argmax)
 //   labels   s'(i,j) = log sum_l exp s(i,j,l) feeds the inside; per-label
 //            marginals are p((i,j)|x) * softmax_l s(i,j,l) (Sec. 4.2, Eq. tree-label-score)
@@ -16,12 +16,11 @@
 //     chart never leaves LDS.  Sentences too long for LDS run alone on the
 //     same code with the chart in a plan-owned workspace (L2/MALL resident).
 //   * Lanes.  In width w every span has K = w-1 split points and gets G
-//     lanes (a power of two <= 64), chosen so that all spans of the step fill
-//     the workgroup about once; lane l takes splits l, l+G, ... in chunks of
-//     up to 4 whose loads issue together, branch-free.  The split-point
-//     log-sum-exp is a running max / sum-exp per lane finished by a butterfly
-//     over the G lanes (DPP inside a 16-lane row, ds_swizzle across rows,
-//     readlane across the two halves of the wave).
+//     lanes (a power of two <= 64) of C splits each, by the step-shape rule
+//     step_shape_k; lane l takes splits l, l+G, ..., all loads issued before
+//     the first use.  The split-point log-sum-exp is a max / sum-exp per lane
+//     finished by a butterfly over the G lanes (DPP inside a 16-lane row,
+//     ds_swizzle across rows, readlane across the two halves of the wave).
 //   * alpha is stored twice, at [i][j] and mirrored at [j][i], so the row
 //     alpha(i,.) and the column alpha(.,j) of a span are both contiguous.
 //   * The chart holds log2-scaled values (v_exp_f32 / v_log_f32 are base 2).
@@ -42,11 +41,13 @@
 //   * CKY runs a float64 chart in the association order
 //     beta(i,j) = (max_k (beta(i,k) + beta(k,j))) + s(i,j): only IEEE adds
 //     and exact max, so the tree is reproducible bit for bit; ties keep the
-//     lowest split.  The tree is recovered by a breadth-first walk of the
-//     back-pointers (one wavefront per sentence, no barriers) that records
-//     each node's depth; spans starting at position i form a chain of left
-//     children, so a node's preorder slot is the chain's offset plus its
-//     depth below the chain head.
+//     lowest split.  No back-pointers are stored: the tree walk recomputes
+//     each visited node's split from the chart.  Bundles of few (long)
+//     sentences walk breadth first, one wavefront per sentence, recording
+//     depths (spans starting at position i form a chain of left children, so
+//     a node's preorder slot is the chain's offset plus its depth below the
+//     chain head); bundles of many (short) sentences walk depth first, one
+//     lane group per sentence, the preorder slot being a running count.
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
@@ -1161,7 +1162,7 @@ __global__ __launch_bounds__(kThreadsMax) void cky_kernel(KernelPlan p, const fl
     cky_block<SPILL>(p, blockIdx.x, smem_raw, scores, spans, best);
 }
 
-// The whole pass -- inside, reverse and CKY -- in one launch.  Workgroup b
+// The whole pass -- inside, marginals and CKY -- in one launch.  Workgroup b
 // runs entry b of the plan's merged launch order (inside and CKY bundles by
 // decreasing predicted duration), so the two halves run side by side and
 // every XCD receives the same blend of both.

@@ -4,9 +4,10 @@
 // Scheduling.  Sentences are independent (Algorithm 1 parallelises over the
 // batch), and a sentence's cost grows as its number of split points,
 // T(n) = (n+1) n (n-1) / 6, plus a latency term per width step.  Workgroups
-// are dispatched in blockIdx order, so the sentence list is sorted by
-// decreasing length: the longest dependency chains start first and short
-// sentences fill the tail (longest-processing-time-first).
+// are dispatched in blockIdx order, so bundles are launched longest first:
+// the longest dependency chains start first and short bundles fill the tail
+// (longest-processing-time-first); the fused launch's order and the split of
+// its last bundles come from a replay of the dispatch (plan_fused_launch).
 #include <hip/hip_runtime_api.h>
 
 #include <algorithm>
@@ -86,8 +87,8 @@ struct HostSchedule {
     int64_t ws_bytes = 0;
 };
 
-// Cost model of one sentence: split points plus a latency term per width
-// step (two sweeps' worth of barrier-separated steps).
+// Cost model of one sentence for sizing bundles: split points plus a latency
+// term per width step.
 inline double sentence_cost(int n) {
     const double T = (double)(n + 1) * n * (n - 1) / 6.0;
     return T + 200.0 * (n - 1);
