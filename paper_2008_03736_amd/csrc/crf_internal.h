@@ -37,25 +37,33 @@ __host__ __device__ inline int chart_ld(int n) { return n + 1; }
 //           triangle) and the outside values (upper + mirrored; before the
 //           outside sweep reaches a span its mirrored cell holds the span's
 //           score, and cells no sweep reads park the forced-span scores);
-//   cky:    one float64 square (beta, upper + mirror); the tree walk needs
-//           cky_walk_bytes of LDS on top.
+//   cky:    one float64 square (beta, upper + mirror), followed by the
+//           split table (cky_split_index) when split_bytes > 0: the best
+//           split k of every span (i, j) of two or more words, stored as
+//           k - i - 1 in split_bytes bytes (1 for n <= kMaxLenInLds, 2 in
+//           the workspace).  A bundle whose tables do not fit in LDS beside
+//           its charts keeps them in the workspace (Bundle::split_ws).
 __host__ __device__ inline int64_t inside_chart_bytes(int n) {
     const int64_t ld = chart_ld(n);
     return 2 * ld * ld * 4;
 }
-__host__ __device__ inline int64_t cky_chart_bytes(int n) {
-    const int64_t ld = chart_ld(n);
-    return ld * ld * 8;
+__host__ __device__ inline int64_t cky_split_count(int n) { return (int64_t)n * (n - 1) / 2; }
+// Entry of span (i, i + w), w >= 2, in the split table: all spans of width 2,
+// then of width 3, and so on.
+__host__ __device__ inline int cky_split_index(int n, int w, int i) {
+    return (w - 2) * (n + 1) - ((w - 1) * w / 2 - 1) + i;
 }
-// The CKY tree walk: bundles of fewer than kDfsMinBundle sentences walk
-// breadth first, one wavefront per sentence, with cky_scratch_ints(n) ints
-// per wavefront; larger bundles walk depth first, one lane group per
-// sentence, with a stack of n ints per sentence.
+__host__ __device__ inline int64_t cky_chart_bytes(int n, int split_bytes) {
+    const int64_t ld = chart_ld(n);
+    return ld * ld * 8 + (cky_split_count(n) * split_bytes + 7) / 8 * 8;
+}
+// The CKY tree walk follows the split table.  Bundles of fewer than
+// kDfsMinBundle sentences walk breadth first, one wavefront per sentence,
+// with a list of at most n - 1 internal nodes per wavefront; larger bundles
+// walk depth first, one lane per sentence, with a stack of n ints each.
 constexpr int kDfsMinBundle = 16;
-__host__ __device__ inline int cky_scratch_ints(int n) { return 3 * n + 3; }
 __host__ __device__ inline int64_t cky_walk_bytes(int n, int64_t count, int waves) {
-    return count < kDfsMinBundle ? 4 * (int64_t)(count < waves ? count : waves) * cky_scratch_ints(n)
-                                 : 4 * count * n;
+    return count < kDfsMinBundle ? 4 * (int64_t)(count < waves ? count : waves) * n : 4 * count * n;
 }
 
 // Shape of a width step with K split points per span: G lanes per span (a
@@ -93,8 +101,9 @@ __host__ __device__ inline int masked_reach(int n) {
     return (sh.C - sh.MF) * sh.G;
 }
 
-// Longest sentence whose CKY chart can sit in one CU's LDS (160 KiB):
-// 8 (n+1)^2 <= 163840.  The plan sends longer ones to the workspace kernels.
+// Longest sentence whose CKY chart could sit in one CU's LDS (160 KiB):
+// 8 (n+1)^2 <= 163840 (with its split table and tables the plan finds
+// somewhat less).  The plan sends longer ones to the workspace kernels.
 constexpr int kMaxLenInLds = 142;
 
 // A bundle: `count` sentences of identical length `n`, processed together by
@@ -103,7 +112,10 @@ struct Bundle {
     int32_t first;
     int32_t count;
     int32_t n;
-    int32_t pad;
+    // CKY: where the bundle's split tables live -- -1: in LDS after each
+    // chart; else at workspace byte 256 * split_ws, count tables of
+    // cky_split_count(n) bytes back to back.  Unused for inside bundles.
+    int32_t split_ws;
 };
 
 // Which sentences run in LDS (in bundles) and which on the workspace kernel,

@@ -52,6 +52,8 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "crf_internal.h"
 
 namespace crf {
@@ -796,20 +798,63 @@ __device__ __forceinline__ void inside_block(const KernelPlan &p, int block, cha
 }
 
 // ---------------------------------------------------------------------------
-// CKY.  Each sentence's chart is one float64 square (beta upper + mirror).
+// CKY.  Each sentence's chart is one float64 square (beta upper + mirror);
+// its split table (entries SP: uint8_t for bundles, uint16_t on the
+// workspace kernel) follows the chart or sits in the workspace.
+template <typename SP>
 struct Cky_ctx {
     char *chart0;
     int cstride;   // bytes between consecutive sentences' charts
+    char *split0;
+    int sstride;   // bytes between consecutive sentences' split tables
     int n, ld, nb;
+    bool split_lds;   // split tables in LDS (else in global memory)
     __device__ double *beta(int sb) const {
         return reinterpret_cast<double *>(chart0 + (size_t)sb * cstride);
     }
+    // Split table entry e of sentence sb, through an LDS or a global pointer
+    // (not a generic one: flat accesses cost more, and a flat store to LDS
+    // holds up the next barrier).
+    __device__ void put_split(int sb, int e, int v) const {
+        SP *q = reinterpret_cast<SP *>(split0 + (size_t)sb * sstride) + e;
+        if (split_lds)
+            *(__attribute__((address_space(3))) SP *)q = (SP)v;
+        else
+            *(__attribute__((address_space(1))) SP *)q = (SP)v;
+    }
+    __device__ int get_split(int sb, int e) const {
+        const SP *q = reinterpret_cast<const SP *>(split0 + (size_t)sb * sstride) + e;
+        return split_lds ? (int)*(const __attribute__((address_space(3))) SP *)q
+                         : (int)*(const __attribute__((address_space(1))) SP *)q;
+    }
 };
 
+// Max of x[LO .. LO+N) and the first index attaining it (as (c0 + c) * G),
+// paired as a balanced tree.  Indices are template constants, so no select
+// ever picks between array slots (the compiler would then index the array
+// dynamically).
+struct Arg_max {
+    double v;
+    int k;
+};
+template <int LO, int N>
+__device__ __forceinline__ Arg_max tree_arg_max(const double *x, int c0, int G) {
+    if constexpr (N == 1) {
+        return Arg_max{x[LO], (c0 + LO) * G};
+    } else {
+        constexpr int H = (N + 1) / 2;
+        const Arg_max a = tree_arg_max<LO, H>(x, c0, G), b = tree_arg_max<LO + H, N - H>(x, c0, G);
+        return Arg_max{fmax(a.v, b.v), b.v > a.v ? b.k : a.k};
+    }
+}
+
 // One width: float64 max-plus, beta(i,j) = (max_k fl(beta(i,k) + beta(k,j)))
-// + s(i,j).  The split chosen is not stored: the backtrace recomputes it.
-template <int G, int C, int MF>
-__device__ __forceinline__ void cky_step(const Cky_ctx &cx, int w, uint32_t magic) {
+// + s(i,j), and the lowest k attaining the max into the split table (entry
+// sp0 + i).  Each lane keeps its running max and the first of its terms to
+// reach it; the group then takes the lowest split among its lanes at the
+// group's max.
+template <int G, int C, int MF, typename SP>
+__device__ __forceinline__ void cky_step(const Cky_ctx<SP> &cx, int w, uint32_t magic, int sp0) {
     const int tid = threadIdx.x, nt = blockDim.x;
     const int n = cx.n, ld = cx.ld;
     const int K = w - 1, S = n - w + 1;
@@ -824,47 +869,63 @@ __device__ __forceinline__ void cky_step(const Cky_ctx &cx, int w, uint32_t magi
         const int rowo = (int)__umul24((uint32_t)i, (uint32_t)(ld + 1)) + 1 + l;
         const int colo = rowo + (int)__umul24((uint32_t)w, (uint32_t)ld);
         const double sij = be[i * ld + j];
-        double x[C], xr[C], xc[C];
-#pragma unroll
-        for (int c = 0; c < C; ++c) {
-            xr[c] = be[rowo + c * G];
-            xc[c] = be[colo + c * G];
-        }
-        // every load in flight before the first use (float64 operands of
-        // up to 16 splits fit in registers; longer lanes interleave)
-        if constexpr (C <= 16) __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-        for (int c = 0; c < C; ++c) x[c] = xr[c] + xc[c];
         const int kl = K - l;
+        // Terms in chunks of up to 16.  Up to 16 splits per lane (one chunk),
+        // every float64 operand is loaded before the first is used; longer
+        // lanes interleave loads and arithmetic.  A chunk's max and its
+        // lowest term at the max pair up as a tree; chunks merge in order.
+        constexpr int CH = C < 16 ? C : 16;
+        double m = -INFINITY;
+        int kc = 0;   // this lane's first term at its max, as c * G
 #pragma unroll
-        for (int c = MF; c < C; ++c)
-            if (c * G >= kl) x[c] = -INFINITY;
-        double m = x[0];
+        for (int c0 = 0; c0 < C; c0 += CH) {
+            double xr[CH], xc[CH];
 #pragma unroll
-        for (int c = 1; c < C; ++c) m = fmax(m, x[c]);
-        m = grp_max_d<G>(m);
-        const double v = m + sij;
+            for (int c = 0; c < CH; ++c) {
+                xr[c] = be[rowo + (c0 + c) * G];
+                xc[c] = be[colo + (c0 + c) * G];
+            }
+            if constexpr (C <= 16) __builtin_amdgcn_sched_barrier(0);
+            double x[CH];
+#pragma unroll
+            for (int c = 0; c < CH; ++c) {
+                x[c] = xr[c] + xc[c];
+                if (c0 + c >= MF && (c0 + c) * G >= kl) x[c] = -INFINITY;
+            }
+            const Arg_max a = tree_arg_max<0, CH>(x, c0, G);
+            if (c0 == 0) {
+                m = a.v;
+                kc = a.k;
+            } else {
+                kc = a.v > m ? a.k : kc;
+                m = fmax(m, a.v);
+            }
+        }
+        const double mg = grp_max_d<G>(m);
+        const int kb = min(grp_min_i<G>(m == mg ? kc + l : 0x7fffffff), K - 1);
+        const double v = mg + sij;
         asm volatile("" ::"v"(v));   // keeps the score load with the operand loads
         if (act && l == 0) {
             be[i * ld + j] = v;
             be[j * ld + i] = v;
+            cx.put_split(at.sb, sp0 + i, kb);
         }
     }
 }
 
-template <int G, int C, int MF>
-__device__ __forceinline__ void cky_run(const Cky_ctx &cx, int w0, int w1, const uint32_t *magic) {
+template <int G, int C, int MF, typename SP>
+__device__ __forceinline__ void cky_run(const Cky_ctx<SP> &cx, int w0, int w1, const uint32_t *magic) {
     uint32_t mg_cur = magic[cx.n - w0 + 1];
     for (int w = w0; w < w1; ++w) {
         const uint32_t mg_next = magic[cx.n - w];   // S of width w+1 (>= 0)
-        cky_step<G, C, MF>(cx, w, mg_cur);
+        cky_step<G, C, MF>(cx, w, mg_cur, cky_split_index(cx.n, w, 0));
         __syncthreads();
         mg_cur = mg_next;
     }
 }
 
-template <bool WIDE>
-__device__ __forceinline__ void cky_sweep(const Cky_ctx &cx, const uint32_t *magic) {
+template <bool WIDE, typename SP>
+__device__ __forceinline__ void cky_sweep(const Cky_ctx<SP> &cx, const uint32_t *magic) {
     const int n = cx.n;
     int w = 2;
     while (w <= n) {
@@ -885,175 +946,96 @@ __device__ __forceinline__ void cky_sweep(const Cky_ctx &cx, const uint32_t *mag
 // Order one wavefront's LDS accesses across its lanes.
 __device__ __forceinline__ void wave_sync() { __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront"); }
 
-// Node (i, j, depth) packed in 32 bits (i, j < 1024; depth < 1024).
-__device__ __forceinline__ int pack_node(int i, int j, int d) { return i | (j << 10) | (d << 20); }
+// Tree nodes are spans (i, j) with their preorder row: once a node's split k
+// is known, its left child (i, k) takes the next row and its right child
+// (k, j) the row after the left subtree's 2(k-i)-1 rows.  A node (i, j, row)
+// packs into 31 bits (i, j < 1024, row < 2048).
+__device__ __forceinline__ uint32_t pack_node(int i, int j, int row) {
+    return (uint32_t)i | ((uint32_t)j << 10) | ((uint32_t)row << 20);
+}
+template <typename SP>
+__device__ __forceinline__ int split_of(const Cky_ctx<SP> &cx, int sb, int i, int j) {
+    return i + 1 + cx.get_split(sb, cky_split_index(cx.n, j - i, i));
+}
+__device__ __forceinline__ void put_row(int32_t *out, int row, int i, int j) {
+    out[2 * row] = i;
+    out[2 * row + 1] = j;
+}
 
-// Recover sentence sb's tree and write it in preorder to out (its 2n-1
-// rows of the spans output).  Runs on one wavefront, breadth first, with no
-// barriers: for each internal node of a level a group of 8 lanes recomputes
-// the lowest k maximising fl(beta(i,k) + beta(k,j)) -- exactly the forward's
-// max, so exactly its split.  scr (LDS, cky_scratch_ints(n)) holds the node
-// list, appended level by level so that each level is the frontier for the
-// next, and per start position the depth of its chain head and of its leaf
-// (uint16).  Spans starting at position p form a chain of left children from
-// the head (a right child, or the root) down to the leaf (p, p+1); in
-// preorder the chains follow each other by p, so a node's row is the chain's
-// offset plus its depth below the head.
-template <int PER_LANE>
-__device__ void backtrace(const Cky_ctx &cx, int sb, int32_t *out, int32_t *scr) {
-    const int lane = threadIdx.x & 63, grp = lane >> 3, gl = lane & 7;
-    const int n = cx.n, ld = cx.ld;
-    const double *be = cx.beta(sb);
-    int32_t *nodes = scr;                                   // 2n ints
-    uint16_t *dmin = reinterpret_cast<uint16_t *>(scr + 2 * n);
-    uint16_t *dleaf = dmin + n;                             // n uint16 each
+// Write sentence sb's tree in preorder to out (its 2n-1 rows of the spans
+// output) on one wavefront, breadth first: each level's internal nodes,
+// one lane each, look up their splits, write both children and append the
+// children that are not single words to the node list `nodes` (LDS, at
+// most n - 1 ints), which thereby holds level after level.
+template <typename SP>
+__device__ void walk_bfs(const Cky_ctx<SP> &cx, int sb, int32_t *out, uint32_t *nodes) {
+    const int lane = threadIdx.x & 63, n = cx.n;
     if (lane == 0) {
+        put_row(out, 0, 0, n);
         nodes[0] = pack_node(0, n, 0);
-        dmin[0] = 0;
     }
     wave_sync();
-    int lo = 0, hi = 1;   // the current level is nodes[lo, hi)
-    for (int d = 0; lo < hi && d < n; ++d) {
+    int lo = 0, hi = n >= 2 ? 1 : 0;   // the current level is nodes[lo, hi)
+    while (lo < hi) {
         int tail = hi;
-        for (int base = lo; base < hi; base += 8) {   // 8 nodes per pass, 8 lanes each
-            const int idx = base + grp;
+        for (int base = lo; base < hi; base += 64) {
+            const int idx = base + lane;
             const bool valid = idx < hi;
-            const int node = valid ? nodes[idx] : 0;
-            const int i = node & 1023, j = (node >> 10) & 1023;
-            const int K = valid ? j - i - 1 : 0;
-            double lb = -INFINITY;
-            int lk = 0x7fffffff;
-            for (int ko = gl; ko < K; ko += 8) {
-                const double v = be[i * ld + i + 1 + ko] + be[j * ld + i + 1 + ko];
-                if (v > lb) {
-                    lb = v;
-                    lk = ko;
-                }
+            const uint32_t node = nodes[valid ? idx : lo];
+            const int i = node & 1023, j = (node >> 10) & 1023, row = node >> 20;
+            const int k = split_of(cx, sb, i, j);
+            const int rl = row + 1, rr = row + 2 * (k - i);
+            if (valid) {
+                put_row(out, rl, i, k);
+                put_row(out, rr, k, j);
             }
-            const double m = grp_max_d<8>(lb);
-            const int kb = grp_min_i<8>(lb == m ? lk : 0x7fffffff);
-            const int k = i + 1 + kb;
-            const bool internal = valid && K > 0 && kb < K;
-            if (valid && gl == 0 && K == 0) dleaf[i] = (uint16_t)d;
-            const uint64_t mask = __ballot(internal && gl == 0);
-            const int below = __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
-                                                        __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0));
-            if (internal && gl == 0) {
-                const int o = tail + 2 * below;
-                if (o + 1 < 2 * n) {
-                    nodes[o] = pack_node(i, k, d + 1);
-                    nodes[o + 1] = pack_node(k, j, d + 1);
-                }
-                dmin[k] = (uint16_t)(d + 1);   // a right child heads the chain at k
-            }
-            tail += 2 * __popcll(mask);
+            const bool li = valid && k - i >= 2, ri = valid && j - k >= 2;
+            const uint64_t ml = __ballot(li), mr = __ballot(ri);
+            const int nl = __popcll(ml);
+            if (li)
+                nodes[tail + __builtin_amdgcn_mbcnt_hi((uint32_t)(ml >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)ml, 0))] =
+                    pack_node(i, k, rl);
+            if (ri)
+                nodes[tail + nl + __builtin_amdgcn_mbcnt_hi((uint32_t)(mr >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mr, 0))] =
+                    pack_node(k, j, rr);
+            tail += nl + __popcll(mr);
         }
         wave_sync();
         lo = hi;
-        hi = tail < 2 * n ? tail : 2 * n;
-    }
-    // Row of chain p's head = exclusive prefix sum of the chain lengths
-    // dleaf - dmin + 1; keep base[p] = row - dmin[p] in registers, then store
-    // it over the depth tables (all of which have been read by then).
-    constexpr int NB = (PER_LANE + 1) / 2;   // ceil(n / 64) with 64 * NB >= n
-    int basev[NB];
-    int carry = 0;
-#pragma unroll
-    for (int q = 0; q < NB; ++q) {
-        const int p = lane + 64 * q;
-        const int dm = p < n ? (int)dmin[p] : 0;
-        const int c = p < n ? (int)dleaf[p] - dm + 1 : 0;
-        int incl = c;
-        for (int sh = 1; sh < 64; sh <<= 1) {
-            const int o = __shfl_up(incl, sh);
-            if (lane >= sh) incl += o;
-        }
-        basev[q] = carry + incl - c - dm;
-        carry += __shfl(incl, 63);
-    }
-    wave_sync();
-    int32_t *basep = scr + 2 * n;   // n ints over the two uint16 tables
-#pragma unroll
-    for (int q = 0; q < NB; ++q) {
-        const int p = lane + 64 * q;
-        if (p < n) basep[p] = basev[q];
-    }
-    wave_sync();
-    const int total = hi < 2 * n - 1 ? hi : 2 * n - 1;
-    for (int t = lane; t < total; t += 64) {
-        const int node = nodes[t];
-        const int i = node & 1023, j = (node >> 10) & 1023, d = node >> 20;
-        const int pos = basep[i] + d;
-        if (pos >= 0 && pos < 2 * n - 1) {
-            out[2 * pos] = i;
-            out[2 * pos + 1] = j;
-        }
+        hi = tail;
     }
 }
 
-// Recover the 1-best trees of a bundle and write them in preorder.  A group
-// of L lanes walks one sentence depth first, so all sentences of the bundle
-// walk at once: a node's row is the number of rows written before it, and
-// the right children still to visit wait on the sentence's stack in LDS (at
-// most n - 1 deep).  Each internal node's split is recomputed with the
-// group's lanes as the lowest k maximising fl(beta(i,k) + beta(k,j)) --
-// exactly the sweep's max, so exactly its split.  A left child that is a
-// single word is written at once and the walk goes right without a push.
-template <int L>
-__device__ void walk_trees(const Cky_ctx &cx, const int *sid, int32_t *spans, int R, int32_t *stacks) {
-    const int tid = threadIdx.x, gl = tid & (L - 1);
-    const int groups = blockDim.x / L;
-    const int n = cx.n, ld = cx.ld;
-    for (int sb0 = 0; sb0 < cx.nb; sb0 += groups) {
-        const int sb = sb0 + tid / L;
-        bool active = sb < cx.nb;
-        const double *be = cx.beta(active ? sb : 0);
-        int32_t *out = spans + (size_t)sid[active ? sb : 0] * R * 2;
-        int32_t *stack = stacks + (size_t)(active ? sb : 0) * n;
-        int i = 0, j = n, row = 0, sp = 0;
-        for (int it = 0; it < 2 * n; ++it) {   // every step writes a row: at most 2n-1
-            if (__ballot(active) == 0) break;
-            if (active && gl == 0) {
-                out[2 * row] = i;
-                out[2 * row + 1] = j;
-            }
-            const int K = j - i - 1;
-            double lb = -INFINITY;
-            int lk = 0x7fffffff;
-            for (int ko = gl; ko < (active ? K : 0); ko += L) {
-                const double v = be[i * ld + i + 1 + ko] + be[j * ld + i + 1 + ko];
-                if (v > lb) {
-                    lb = v;
-                    lk = ko;
-                }
-            }
-            const double m = grp_max_d<L>(lb);
-            // (clamped so that even a chart without a finite maximum walks a tree)
-            const int kb = min(grp_min_i<L>(lb == m ? lk : 0x7fffffff), K - 1);
-            if (!active) continue;
-            ++row;
-            if (K == 0) {   // a word: resume at the last pending right child
-                if (sp == 0) {
-                    active = false;
-                } else {
-                    const int node = stack[--sp];
-                    i = node & 0xffff;
-                    j = node >> 16;
-                }
-            } else {
-                const int k = i + 1 + kb;
-                if (k == i + 1) {   // left child is a word
-                    if (gl == 0) {
-                        out[2 * row] = i;
-                        out[2 * row + 1] = k;
-                    }
-                    ++row;
+// Write the trees of all the bundle's sentences in preorder, one lane per
+// sentence, depth first: the walk goes left, with the right children still
+// to visit on the sentence's stack (LDS, at most n - 1 deep), and a left
+// child that is a single word is written at once and the walk goes right.
+template <typename SP>
+__device__ void walk_dfs(const Cky_ctx<SP> &cx, const int *sid, int32_t *spans, int R, uint32_t *stacks) {
+    const int n = cx.n;
+    for (int sb = threadIdx.x; sb < cx.nb; sb += blockDim.x) {
+        int32_t *out = spans + (size_t)sid[sb] * R * 2;
+        uint32_t *stack = stacks + (size_t)sb * n;
+        int i = 0, j = n, row = 0, top = 0;
+        for (int it = 0; it < 2 * n; ++it) {   // one row per pass: 2n-1 in all
+            put_row(out, row, i, j);
+            if (j - i >= 2) {
+                const int k = split_of(cx, sb, i, j);
+                if (k - i == 1) {   // left child is a word
+                    put_row(out, row + 1, i, k);
+                    row += 2;
                     i = k;
                 } else {
-                    if (gl == 0) stack[sp] = k | (j << 16);
-                    ++sp;
+                    stack[top++] = pack_node(k, j, row + 2 * (k - i));
+                    ++row;
                     j = k;
                 }
+            } else {
+                if (top == 0) break;
+                const uint32_t node = stack[--top];
+                i = node & 1023;
+                j = (node >> 10) & 1023;
+                row = node >> 20;
             }
         }
     }
@@ -1065,22 +1047,25 @@ __device__ __forceinline__ void cky_block(const KernelPlan &p, int block, char *
                                           int32_t *__restrict__ spans, float *__restrict__ best) {
     __shared__ int spill_id[1];
     __shared__ uint32_t spill_magic[SPILL ? CRF_MAX_LEN + 2 : 1];
-    __shared__ int32_t spill_scr[SPILL ? 3 * CRF_MAX_LEN + 3 : 1];
+    __shared__ uint32_t spill_scr[SPILL ? CRF_MAX_LEN : 1];
     const int NT = blockDim.x;
     const int tid = threadIdx.x;
     const int N1 = p.n1;
 
     int n, nb, *sid;
     uint32_t *magic;
-    int32_t *scratch;   // tree-walk scratch (cky_walk_bytes)
-    char *chart0;
-    int cstride;
+    uint32_t *scratch;   // tree-walk scratch (cky_walk_bytes)
+    char *chart0, *split0;
+    int cstride, sstride;
+    bool split_lds = false;
     if constexpr (SPILL) {
         const int b = p.cky.order_spill[block];
         n = p.len[b];
         nb = 1;
         chart0 = p.ws + p.cky.ws_off[block];
         cstride = 0;
+        split0 = chart0 + (size_t)8 * chart_ld(n) * chart_ld(n);
+        sstride = 0;
         sid = spill_id;
         magic = spill_magic;
         scratch = spill_scr;
@@ -1090,15 +1075,19 @@ __device__ __forceinline__ void cky_block(const KernelPlan &p, int block, char *
         n = bd.n;
         nb = bd.count;
         chart0 = smem_raw;
-        cstride = (int)cky_chart_bytes(n);
+        split_lds = bd.split_ws < 0;
+        cstride = (int)cky_chart_bytes(n, split_lds ? 1 : 0);
+        split0 = split_lds ? chart0 + (size_t)8 * chart_ld(n) * chart_ld(n) : p.ws + (size_t)bd.split_ws * 256;
+        sstride = split_lds ? cstride : (int)cky_split_count(n);
         sid = reinterpret_cast<int *>(smem_raw + (size_t)nb * cstride);
         magic = reinterpret_cast<uint32_t *>(sid + nb);
-        scratch = reinterpret_cast<int32_t *>(magic + n + 2);
+        scratch = magic + n + 2;
         for (int t = tid; t < nb; t += NT) sid[t] = p.cky.order[bd.first + t];
     }
     for (int S = tid; S <= n; S += NT) magic[S] = div_magic(S);
     const int ld = chart_ld(n);
-    const Cky_ctx cx{chart0, cstride, n, ld, nb};
+    typedef typename std::conditional<SPILL, uint16_t, uint8_t>::type SP;
+    const Cky_ctx<SP> cx{chart0, cstride, split0, sstride, n, ld, nb, !SPILL && split_lds};
     __syncthreads();
 
     auto load_score = [&](int sb, int i, int j) -> float {
@@ -1127,19 +1116,14 @@ __device__ __forceinline__ void cky_block(const KernelPlan &p, int block, char *
     }
     if (best != nullptr)
         for (int sb = tid; sb < nb; sb += NT) best[sid[sb]] = (float)cx.beta(sb)[n];
-    // Tree walks.  A few (long) sentences: one wavefront each, breadth first,
-    // up to 8 nodes of a level at a time.  Many (short) sentences: one group
-    // of lanes each, depth first, all at once.
+    // Tree walks.  A few (long) sentences: one wavefront each, breadth first.
+    // Many (short) sentences: one lane each, depth first, all at once.
     if (nb < kDfsMinBundle) {
-        constexpr int PER_LANE = SPILL ? (2 * CRF_MAX_LEN + 63) / 64 : (2 * kMaxLenInLds + 63) / 64;
         const int wave = tid >> 6;
         for (int sb = wave; sb < nb; sb += NT >> 6)
-            backtrace<PER_LANE>(cx, sb, spans + (size_t)sid[sb] * R * 2,
-                                scratch + (size_t)wave * cky_scratch_ints(n));
-    } else if (nb <= NT / 16) {
-        walk_trees<16>(cx, sid, spans, R, scratch);
+            walk_bfs(cx, sb, spans + (size_t)sid[sb] * R * 2, scratch + (size_t)wave * n);
     } else {
-        walk_trees<8>(cx, sid, spans, R, scratch);
+        walk_dfs(cx, sid, spans, R, scratch);
     }
 }
 

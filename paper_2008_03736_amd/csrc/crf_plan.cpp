@@ -208,10 +208,10 @@ constexpr double kInsideTargetScale = 2.0, kCkyTargetScale = 1.0;
 // `order` is sorted by decreasing length.  `chart(n)` is the LDS a bundled
 // sentence needs besides `per_sentence` bytes of tables, `spill_chart(n)` its
 // workspace chart, and `tail(n, count)` the bytes a bundle adds at its end.
-template <typename F, typename TF>
+template <typename F, typename FS, typename TF>
 HostSchedule make_schedule(const std::vector<int32_t> &order, const int32_t *len, int lds_cap,
                            bool force_spill, int64_t ws_base, int per_sentence, F chart,
-                           F spill_chart, TF tail, double target_scale) {
+                           FS spill_chart, TF tail, double target_scale) {
     HostSchedule s;
     s.threads = crf::kThreadsDefault;
     // LDS of a bundle of `count` sentences of length n.
@@ -268,7 +268,7 @@ HostSchedule make_schedule(const std::vector<int32_t> &order, const int32_t *len
             t.bd.first = (int32_t)(a + lo);
             t.bd.count = hi - lo;
             t.bd.n = n;
-            t.bd.pad = 0;
+            t.bd.split_ws = -1;
             t.cost = (hi - lo) * (sentence_cost(n) - 200.0 * (n - 1)) + 200.0 * (n - 1);
             tmp.push_back(t);
             s.lds_bytes = std::max<int32_t>(s.lds_bytes, (int32_t)bundle_bytes(n, hi - lo));
@@ -346,7 +346,7 @@ int crf_plan_create(crf_plan **out, const int32_t *lengths_host, int32_t batch, 
 
     const bool force = (flags & CRF_FORCE_SPILL) != 0;
     auto inside_bytes = [](int n) { return crf::inside_chart_bytes(n); };
-    auto cky_bytes = [](int n) { return crf::cky_chart_bytes(n); };
+    auto cky_spill_bytes = [](int n) { return crf::cky_chart_bytes(n, 2); };
     // The CKY bundle's tail: the tree-walk scratch, padded so that the last
     // chart's masked reads (into the id, magic and scratch tables behind it)
     // stay inside the bundle.
@@ -357,11 +357,26 @@ int crf_plan_create(crf_plan **out, const int32_t *lengths_host, int32_t batch, 
         const int64_t tables = 4 * count + crf::bundle_extra_bytes(n) + walk;
         return walk + std::max<int64_t>(0, 8 * (int64_t)crf::masked_reach(n) - tables);
     };
+    // A sentence's split table sits in LDS after its chart when a bundle of
+    // one such sentence still fits in half the CU; longer sentences keep it
+    // in the workspace.
+    const int64_t half_cu = lds_cap / 2 - 256;
+    auto split_in_lds = [=](int n) {
+        return crf::cky_chart_bytes(n, 1) + 4 + crf::bundle_extra_bytes(n) + cky_tail(n, 1) <= half_cu;
+    };
+    auto cky_bytes = [=](int n) { return crf::cky_chart_bytes(n, split_in_lds(n) ? 1 : 0); };
     // inside tables: forced sum (f64), gradient (f32), id (i32), score shift (f32); cky: id
     HostSchedule si = make_schedule(order, lengths_host, lds_cap, force, 0, 20, +inside_bytes,
                                     +inside_bytes, +no_tail, kInsideTargetScale);
-    HostSchedule sc = make_schedule(order, lengths_host, lds_cap, force, si.ws_bytes, 4, +cky_bytes,
-                                    +cky_bytes, cky_tail, kCkyTargetScale);
+    HostSchedule sc = make_schedule(order, lengths_host, lds_cap, force, si.ws_bytes, 4, cky_bytes,
+                                    +cky_spill_bytes, cky_tail, kCkyTargetScale);
+    int64_t split_cursor = si.ws_bytes + sc.ws_bytes;
+    for (crf::Bundle &bd : sc.bundles) {
+        if (split_in_lds(bd.n)) continue;
+        bd.split_ws = (int32_t)(split_cursor / 256);
+        split_cursor += (bd.count * crf::cky_split_count(bd.n) + 255) / 256 * 256;
+    }
+    sc.ws_bytes = split_cursor - si.ws_bytes;
     p->ws_bytes = si.ws_bytes + sc.ws_bytes;
 
     std::vector<int32_t> len(lengths_host, lengths_host + batch);

@@ -257,3 +257,11 @@ def test_longest_sentence(torch):
     out, worst = full_check(torch, b)
     assert out["info"]["spill_count"] == 1
     print(f"n = 1023: max |marginal error| {worst:.2e}")
+
+
+def test_split_tables_in_workspace(torch):
+    # sentences whose CKY chart leaves no room in half a CU for the split
+    # table keep it in global memory; a longer one moves every bundle to a
+    # whole CU
+    b = W.custom([97, 97, 98, 99, 99, 120, 3, 40], seed=24, sd=2.0)
+    full_check(torch, b)
