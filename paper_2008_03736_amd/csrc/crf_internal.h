@@ -17,8 +17,10 @@ namespace crf {
 constexpr int kThreadsDefault = 512;
 constexpr int kThreadsMax = 1024;
 
-// Most sentences per bundle (bounds the per-sentence tables in LDS).
+// Most sentences per bundle (bounds the per-sentence tables in LDS; each
+// thread of a bundle's workgroup fetches at most one sentence id).
 constexpr int kMaxBundle = 256;
+static_assert(kMaxBundle <= kThreadsDefault, "one sentence id per thread");
 
 // LDS a bundle needs besides its charts: a uint32 table of division magics
 // for span counts 0..n+1.  (Masked tail loads stay inside a sentence's inside
@@ -118,12 +120,17 @@ struct Bundle {
     int32_t split_ws;
 };
 
+// What a bundle's workgroup reads first: one record of rec_stride ints --
+// n, count, split_ws (CKY; -1 for inside), kind (1 inside, 0 CKY), then the
+// count sentence ids -- so that its sentence ids arrive with its shape, one
+// memory round trip before its scores.
+constexpr int kRecHeader = 4;
+
 // Which sentences run in LDS (in bundles) and which on the workspace kernel,
 // for one kind of chart.  Bundles and spilled sentences are ordered most
 // expensive first.
 struct Schedule {
-    const Bundle *bundles;       // [n_bundles]
-    const int32_t *order;        // sentence ids grouped by bundle
+    const int32_t *recs;         // [n_bundles] records, rec_stride ints each
     const int32_t *order_spill;  // [n_spill] sentence ids
     const int64_t *ws_off;       // [n_spill] byte offset of each chart in the workspace
     int32_t n_bundles, n_spill;
@@ -132,17 +139,17 @@ struct Schedule {
 };
 
 // Device-side view of a plan, passed by value to every kernel.
-//   mix: the launch order of the fused inside + CKY kernel, one entry per
-//   workgroup: e >= 0 is inside bundle e, e < 0 is CKY bundle ~e.  Entries are
-//   sorted by predicted duration (both kinds merged), so that the hardware's
-//   round-robin of consecutive workgroups over the XCDs hands every XCD the
-//   same mix of long and short, inside and CKY work.
+//   mix: the records of the fused inside + CKY kernel in launch order, one
+//   per workgroup, sorted by predicted duration (both kinds merged), so that
+//   the hardware's round-robin of consecutive workgroups over the XCDs hands
+//   every XCD the same mix of long and short, inside and CKY work.
 struct KernelPlan {
     const int32_t *len;          // [B] sentence lengths
     char *ws;                    // workspace base
     Schedule inside, cky;
-    const int32_t *mix;          // [n_mix], or NULL when the fused kernel is not used
+    const int32_t *mix;          // [n_mix] records, or NULL when the fused kernel is not used
     int32_t n_mix;
+    int32_t rec_stride;          // ints per record: kRecHeader + the largest bundle
     int32_t B, n1, L;
 };
 

@@ -597,6 +597,7 @@ struct Cell_walk {
         inv_per = 1.0f / (float)per;
         inv_w = 1.0f / (float)W;
     }
+    // Cell c of the walk; past the end (ok = false) still a valid cell.
     __device__ __forceinline__ Cell at(int c) const {
         Cell e;
         const int cc = c < total ? c : 0;
@@ -618,7 +619,10 @@ struct Cell_walk {
 };
 
 // The walk, U cells per thread at a time: their U loads are issued together
-// (one memory latency per U cells), then `use` consumes them.
+// (one memory latency per U cells), then `use` consumes them.  The loads are
+// unconditional -- at() names a cell of the bundle even past the end -- so
+// that no branch separates them (a load inside a branch is waited for
+// before the branch joins).
 template <int U, typename LD, typename F>
 __device__ __forceinline__ void for_cells_loaded(int nb, int n, LD &&load, F &&use) {
     const int NT = blockDim.x;
@@ -631,7 +635,7 @@ __device__ __forceinline__ void for_cells_loaded(int nb, int n, LD &&load, F &&u
         for (int u = 0; u < U; ++u) {
             const Cell e = cw.at(c0 + u * NT);
             cell[u] = e.ok ? (e.sb << 20) | (e.i << 10) | e.j : -1;
-            v[u] = e.ok ? load(e.sb, e.i, e.j) : V(0);
+            v[u] = load(e.sb, e.i, e.j);
         }
 #pragma unroll
         for (int u = 0; u < U; ++u)
@@ -660,7 +664,7 @@ __device__ __forceinline__ float label_lse2(const float *s, int L) {
 // (REV, upper and mirrored) and parks the forced spans' scores where nothing
 // else reads: width-1 spans at [i+1][i], the root at [0][0].
 template <bool REV, bool LAB, bool SPILL>
-__device__ __forceinline__ void inside_block(const KernelPlan &p, int block, char *smem_raw,
+__device__ __forceinline__ void inside_block(const KernelPlan &p, int block, const int32_t *rec, char *smem_raw,
                                              const float *__restrict__ scores,
                                              const float *__restrict__ grad,
                                              float *__restrict__ logZ, float *__restrict__ marg) {
@@ -693,9 +697,11 @@ __device__ __forceinline__ void inside_block(const KernelPlan &p, int block, cha
         magic = spill_magic;
         if (tid == 0) sid[0] = b;
     } else {
-        const Bundle bd = p.inside.bundles[block];
-        n = bd.n;
-        nb = bd.count;
+        // the record's ids are fetched with its header (a bundle holds at
+        // most kMaxBundle <= blockDim.x sentences)
+        const int id0 = tid < p.rec_stride - kRecHeader ? rec[kRecHeader + tid] : 0;
+        n = rec[0];
+        nb = rec[1];
         chart0 = reinterpret_cast<float *>(smem_raw);
         cstride = (int)(inside_chart_bytes(n) / 4);
         forced = reinterpret_cast<double *>(smem_raw + (size_t)nb * inside_chart_bytes(n));
@@ -703,7 +709,7 @@ __device__ __forceinline__ void inside_block(const KernelPlan &p, int block, cha
         sid = reinterpret_cast<int *>(gv + nb);
         dsh = reinterpret_cast<float *>(sid + nb);
         magic = reinterpret_cast<uint32_t *>(dsh + nb);
-        for (int t = tid; t < nb; t += NT) sid[t] = p.inside.order[bd.first + t];
+        if (tid < nb) sid[tid] = id0;
     }
     for (int S = tid; S <= n + 1; S += NT) magic[S] = div_magic(S);
     const int ld = chart_ld(n);
@@ -1042,7 +1048,7 @@ __device__ void walk_dfs(const Cky_ctx<SP> &cx, const int *sid, int32_t *spans, 
 }
 
 template <bool SPILL>
-__device__ __forceinline__ void cky_block(const KernelPlan &p, int block, char *smem_raw,
+__device__ __forceinline__ void cky_block(const KernelPlan &p, int block, const int32_t *rec, char *smem_raw,
                                           const float *__restrict__ scores,
                                           int32_t *__restrict__ spans, float *__restrict__ best) {
     __shared__ int spill_id[1];
@@ -1071,18 +1077,19 @@ __device__ __forceinline__ void cky_block(const KernelPlan &p, int block, char *
         scratch = spill_scr;
         if (tid == 0) sid[0] = b;
     } else {
-        const Bundle bd = p.cky.bundles[block];
-        n = bd.n;
-        nb = bd.count;
+        const int id0 = tid < p.rec_stride - kRecHeader ? rec[kRecHeader + tid] : 0;
+        n = rec[0];
+        nb = rec[1];
+        const int split_ws = rec[2];
         chart0 = smem_raw;
-        split_lds = bd.split_ws < 0;
+        split_lds = split_ws < 0;
         cstride = (int)cky_chart_bytes(n, split_lds ? 1 : 0);
-        split0 = split_lds ? chart0 + (size_t)8 * chart_ld(n) * chart_ld(n) : p.ws + (size_t)bd.split_ws * 256;
+        split0 = split_lds ? chart0 + (size_t)8 * chart_ld(n) * chart_ld(n) : p.ws + (size_t)split_ws * 256;
         sstride = split_lds ? cstride : (int)cky_split_count(n);
         sid = reinterpret_cast<int *>(smem_raw + (size_t)nb * cstride);
         magic = reinterpret_cast<uint32_t *>(sid + nb);
         scratch = magic + n + 2;
-        for (int t = tid; t < nb; t += NT) sid[t] = p.cky.order[bd.first + t];
+        if (tid < nb) sid[tid] = id0;
     }
     for (int S = tid; S <= n; S += NT) magic[S] = div_magic(S);
     const int ld = chart_ld(n);
@@ -1135,7 +1142,8 @@ __global__ __launch_bounds__(kThreadsMax) void inside_kernel(KernelPlan p, const
                                                              float *__restrict__ logZ,
                                                              float *__restrict__ marg) {
     extern __shared__ __align__(16) char smem_raw[];
-    inside_block<REV, LAB, SPILL>(p, blockIdx.x, smem_raw, scores, grad, logZ, marg);
+    inside_block<REV, LAB, SPILL>(p, blockIdx.x, SPILL ? nullptr : p.inside.recs + (size_t)blockIdx.x * p.rec_stride,
+                                  smem_raw, scores, grad, logZ, marg);
 }
 
 template <bool SPILL>
@@ -1143,11 +1151,12 @@ __global__ __launch_bounds__(kThreadsMax) void cky_kernel(KernelPlan p, const fl
                                                           int32_t *__restrict__ spans,
                                                           float *__restrict__ best) {
     extern __shared__ __align__(16) char smem_raw[];
-    cky_block<SPILL>(p, blockIdx.x, smem_raw, scores, spans, best);
+    cky_block<SPILL>(p, blockIdx.x, SPILL ? nullptr : p.cky.recs + (size_t)blockIdx.x * p.rec_stride, smem_raw,
+                     scores, spans, best);
 }
 
 // The whole pass -- inside, marginals and CKY -- in one launch.  Workgroup b
-// runs entry b of the plan's merged launch order (inside and CKY bundles by
+// runs record b of the plan's merged launch order (inside and CKY bundles by
 // decreasing predicted duration), so the two halves run side by side and
 // every XCD receives the same blend of both.
 __global__ __launch_bounds__(kThreadsMax) void parse_kernel(KernelPlan p, const float *__restrict__ scores,
@@ -1157,13 +1166,11 @@ __global__ __launch_bounds__(kThreadsMax) void parse_kernel(KernelPlan p, const 
                                                             int32_t *__restrict__ spans,
                                                             float *__restrict__ best) {
     extern __shared__ __align__(16) char smem_raw[];
-    const int e = p.mix[blockIdx.x];
-    const bool inside = e >= 0;
-    const int idx = inside ? e : ~e;
-    if (inside)
-        inside_block<true, false, false>(p, idx, smem_raw, scores, grad, logZ, marg);
+    const int32_t *rec = p.mix + (size_t)blockIdx.x * p.rec_stride;
+    if (rec[3])
+        inside_block<true, false, false>(p, 0, rec, smem_raw, scores, grad, logZ, marg);
     else
-        cky_block<false>(p, idx, smem_raw, scores, spans, best);
+        cky_block<false>(p, 0, rec, smem_raw, scores, spans, best);
 }
 
 }  // namespace

@@ -396,6 +396,32 @@ int crf_plan_create(crf_plan **out, const int32_t *lengths_host, int32_t batch, 
         plan_fused_launch(si.bundles, sc.bundles, n_part, std::max(1, cus / n_part) * per_cu, mix);
     }
     kp.n_mix = (int32_t)mix.size();
+    // Workgroup records: the bundle's shape and its sentence ids.
+    int max_count = 1;
+    for (const crf::Bundle &bd : si.bundles) max_count = std::max(max_count, (int)bd.count);
+    for (const crf::Bundle &bd : sc.bundles) max_count = std::max(max_count, (int)bd.count);
+    const int stride = crf::kRecHeader + max_count;
+    kp.rec_stride = stride;
+    auto records = [&](const HostSchedule &h, bool inside) {
+        std::vector<int32_t> r((size_t)h.bundles.size() * stride, 0);
+        for (size_t b = 0; b < h.bundles.size(); ++b) {
+            const crf::Bundle &bd = h.bundles[b];
+            int32_t *q = r.data() + b * stride;
+            q[0] = bd.n;
+            q[1] = bd.count;
+            q[2] = inside ? -1 : bd.split_ws;
+            q[3] = inside ? 1 : 0;
+            for (int t = 0; t < bd.count; ++t) q[crf::kRecHeader + t] = h.order[bd.first + t];
+        }
+        return r;
+    };
+    const std::vector<int32_t> rec_in = records(si, true), rec_ck = records(sc, false);
+    std::vector<int32_t> rec_mix;
+    rec_mix.reserve(mix.size() * stride);
+    for (int32_t e : mix) {
+        const int32_t *q = e >= 0 ? rec_in.data() + (size_t)e * stride : rec_ck.data() + (size_t)(~e) * stride;
+        rec_mix.insert(rec_mix.end(), q, q + stride);
+    }
     auto fill = [](crf::Schedule &q, const HostSchedule &h) {
         q.n_bundles = (int32_t)h.bundles.size();
         q.n_spill = (int32_t)h.spill.size();
@@ -406,15 +432,13 @@ int crf_plan_create(crf_plan **out, const int32_t *lengths_host, int32_t batch, 
     fill(kp.cky, sc);
 
     if ((e = upload(p, len, &kp.len)) != hipSuccess ||
-        (e = upload(p, si.bundles, &kp.inside.bundles)) != hipSuccess ||
-        (e = upload(p, si.order, &kp.inside.order)) != hipSuccess ||
+        (e = upload(p, rec_in, &kp.inside.recs)) != hipSuccess ||
         (e = upload(p, si.spill, &kp.inside.order_spill)) != hipSuccess ||
         (e = upload(p, si.off, &kp.inside.ws_off)) != hipSuccess ||
-        (e = upload(p, sc.bundles, &kp.cky.bundles)) != hipSuccess ||
-        (e = upload(p, sc.order, &kp.cky.order)) != hipSuccess ||
+        (e = upload(p, rec_ck, &kp.cky.recs)) != hipSuccess ||
         (e = upload(p, sc.spill, &kp.cky.order_spill)) != hipSuccess ||
         (e = upload(p, sc.off, &kp.cky.ws_off)) != hipSuccess ||
-        (e = upload(p, mix, &kp.mix)) != hipSuccess) {
+        (e = upload(p, rec_mix, &kp.mix)) != hipSuccess) {
         const int code = (e == hipErrorOutOfMemory) ? CRF_ENOMEM : CRF_EHIP;
         release(p);
         delete p;
