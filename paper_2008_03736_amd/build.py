@@ -17,6 +17,9 @@ FLAGS = [
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     # no NaN ever reaches the charts; lets max fold into v_max_f32_dpp / v_max3
     "-fno-honor-nans",
+    # keep single-lane atomics plain: the wave-aggregating rewrite waits for
+    # the result at once, which would stall the fused kernel's early claims
+    "-mllvm", "-amdgpu-atomic-optimizer-strategy=None",
     "-Wall", "-Wno-unused-function",
     "-I" + os.path.join(ROOT, "include"),
 ]

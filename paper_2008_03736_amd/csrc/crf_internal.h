@@ -28,8 +28,9 @@ static_assert(kMaxBundle <= kThreadsDefault, "one sentence id per thread");
 // it, into the tables that follow it, which the plan pads to that size.)
 __host__ __device__ inline int64_t bundle_extra_bytes(int n) { return 4 * (int64_t)(n + 2); }
 
-// Static LDS the kernels reserve besides the charts.
-constexpr int kStaticLds = 4096;
+// LDS a workgroup holds besides its bundle (the fused kernel's claim slot)
+// and slack.  Bundle budgets leave it free.
+constexpr int kReservedLds = 256;
 
 // Row stride (in elements) of a sentence's square chart.
 __host__ __device__ inline int chart_ld(int n) { return n + 1; }
@@ -139,16 +140,17 @@ struct Schedule {
 };
 
 // Device-side view of a plan, passed by value to every kernel.
-//   mix: the records of the fused inside + CKY kernel in launch order, one
-//   per workgroup, sorted by predicted duration (both kinds merged), so that
-//   the hardware's round-robin of consecutive workgroups over the XCDs hands
-//   every XCD the same mix of long and short, inside and CKY work.
+//   mix: the records of the fused inside + CKY kernel, sorted by predicted
+//   duration (both kinds merged); its fused_grid workgroups take them in
+//   this order (see parse_kernel).
 struct KernelPlan {
     const int32_t *len;          // [B] sentence lengths
     char *ws;                    // workspace base
     Schedule inside, cky;
     const int32_t *mix;          // [n_mix] records, or NULL when the fused kernel is not used
     int32_t n_mix;
+    int32_t fused_grid;          // workgroups of the fused kernel (<= n_mix)
+    int32_t *counter;            // the fused kernel's bundle claims; zero between launches
     int32_t rec_stride;          // ints per record: kRecHeader + the largest bundle
     int32_t B, n1, L;
 };

@@ -618,25 +618,31 @@ struct Cell_walk {
     }
 };
 
-// The walk, U cells per thread at a time: their U loads are issued together
-// (one memory latency per U cells), then `use` consumes them.  The loads are
+// The walk, U cells per thread at a time: the U addresses first (`addr`,
+// which may read LDS tables), then the U loads together (`load`: one memory
+// latency per U cells), then `use` consumes them.  The loads are
 // unconditional -- at() names a cell of the bundle even past the end -- so
 // that no branch separates them (a load inside a branch is waited for
 // before the branch joins).
-template <int U, typename LD, typename F>
-__device__ __forceinline__ void for_cells_loaded(int nb, int n, LD &&load, F &&use) {
+template <int U, typename AD, typename LD, typename F>
+__device__ __forceinline__ void for_cells_loaded(int nb, int n, AD &&addr, LD &&load, F &&use) {
     const int NT = blockDim.x;
     const Cell_walk cw(nb, n);
-    using V = decltype(load(0, 0, 1));
+    using A = decltype(addr(0, 0, 1));
+    using V = decltype(load(addr(0, 0, 1)));
     for (int c0 = threadIdx.x; c0 < cw.total; c0 += NT * U) {
+        A a[U];
         V v[U];
         int cell[U];   // sb << 20 | i << 10 | j (sb < 256, i, j < 1024), or -1
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const Cell e = cw.at(c0 + u * NT);
             cell[u] = e.ok ? (e.sb << 20) | (e.i << 10) | e.j : -1;
-            v[u] = load(e.sb, e.i, e.j);
+            a[u] = addr(e.sb, e.i, e.j);
         }
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int u = 0; u < U; ++u) v[u] = load(a[u]);
 #pragma unroll
         for (int u = 0; u < U; ++u)
             if (cell[u] >= 0) use(cell[u] >> 20, (cell[u] >> 10) & 1023, cell[u] & 1023, v[u]);
@@ -726,14 +732,16 @@ __device__ __forceinline__ void inside_block(const KernelPlan &p, int block, con
     // Prologue: scores of every valid cell into the charts (log2-scaled; the
     // outside reads its own copy at the mirrored cell of the second square);
     // forced spans get 0 in alpha and park their natural-unit score.
-    auto load_score = [&](int sb, int i, int j) -> float {
-        const float *srow = scores + (size_t)sid[sb] * sent_stride + (size_t)i * row_stride;
-        if constexpr (LAB)
-            return label_lse2(srow + (size_t)j * L, L) * (float)LN2_D;
-        else
-            return srow[j];
+    auto score_at = [&](int sb, int i, int j) -> const float * {
+        return scores + (size_t)sid[sb] * sent_stride + (size_t)i * row_stride + (size_t)j * (LAB ? L : 1);
     };
-    for_cells_loaded<LAB ? 1 : 8>(nb, n, load_score, [&](int sb, int i, int j, float s) {
+    auto load_score = [&](const float *q) -> float {
+        if constexpr (LAB)
+            return label_lse2(q, L) * (float)LN2_D;
+        else
+            return *q;
+    };
+    auto put_score = [&](int sb, int i, int j, float s) {
         float *al = chart0 + (size_t)sb * cstride;
         float *ou = al + (size_t)ld * ld;
         if (j == i + 1) {
@@ -752,7 +760,8 @@ __device__ __forceinline__ void inside_block(const KernelPlan &p, int block, con
             al[i * ld + j] = s2;
             if constexpr (REV) ou[j * ld + i] = s2;
         }
-    });
+    };
+    for_cells_loaded<LAB ? 1 : 8>(nb, n, score_at, load_score, put_score);
     __syncthreads();
     // Forced-span sums, one wavefront per sentence, fixed order (deterministic).
     for (int sb = wave; sb < nb; sb += NW) {
@@ -782,7 +791,7 @@ __device__ __forceinline__ void inside_block(const KernelPlan &p, int block, con
     // Epilogue: marginals of the valid cells (coalesced stores along rows),
     //   mu(i,j) = g exp2(alpha~(i,j) + O'(i,j) - (s(i,j) + d) - alpha~(0,n)),
     // and exactly g on forced spans.
-    for_cells_loaded<LAB ? 1 : 8>(nb, n, load_score, [&](int sb, int i, int j, float s) {
+    for_cells_loaded<LAB ? 1 : 8>(nb, n, score_at, load_score, [&](int sb, int i, int j, float s) {
         const size_t rowoff = (size_t)sid[sb] * sent_stride + (size_t)i * row_stride;
         const float *al = chart0 + (size_t)sb * cstride;
         const float *ou = al + (size_t)ld * ld;
@@ -1097,15 +1106,17 @@ __device__ __forceinline__ void cky_block(const KernelPlan &p, int block, const 
     const Cky_ctx<SP> cx{chart0, cstride, split0, sstride, n, ld, nb, !SPILL && split_lds};
     __syncthreads();
 
-    auto load_score = [&](int sb, int i, int j) -> float {
-        return scores[((size_t)sid[sb] * N1 + i) * N1 + j];
+    auto score_at = [&](int sb, int i, int j) -> const float * {
+        return scores + ((size_t)sid[sb] * N1 + i) * N1 + j;
     };
-    for_cells_loaded<8>(nb, n, load_score, [&](int sb, int i, int j, float sf) {
+    auto load_score = [](const float *q) -> float { return *q; };
+    auto put_score = [&](int sb, int i, int j, float sf) {
         double *be = cx.beta(sb);
         const double s = (double)sf;
         be[i * ld + j] = s;
         if (j == i + 1) be[j * ld + i] = s;
-    });
+    };
+    for_cells_loaded<8>(nb, n, score_at, load_score, put_score);
     __syncthreads();
     cky_sweep<SPILL>(cx, magic);
 
@@ -1155,10 +1166,17 @@ __global__ __launch_bounds__(kThreadsMax) void cky_kernel(KernelPlan p, const fl
                      scores, spans, best);
 }
 
-// The whole pass -- inside, marginals and CKY -- in one launch.  Workgroup b
-// runs record b of the plan's merged launch order (inside and CKY bundles by
-// decreasing predicted duration), so the two halves run side by side and
-// every XCD receives the same blend of both.
+// The whole pass -- inside, marginals and CKY -- in one launch of at most
+// one workgroup per workgroup slot, each running a chain of bundles from the
+// plan's merged list (inside and CKY bundles by decreasing predicted
+// duration): workgroup b starts with bundle b and, as each bundle ends,
+// claims the next from a counter (ticket t is bundle grid + t), so that
+// workgroups take the next bundles in the order they free up, whatever their
+// XCD.  (Claiming any earlier -- at the end of the sweep, to fetch ahead --
+// measured slower: the order then strays from the order of freeing.)  Every
+// processed bundle claims once, so the n_mix claims end on ticket n_mix - 1,
+// whose holder zeroes the counter for the next launch; with as many
+// workgroups as bundles nobody claims.
 __global__ __launch_bounds__(kThreadsMax) void parse_kernel(KernelPlan p, const float *__restrict__ scores,
                                                             const float *__restrict__ grad,
                                                             float *__restrict__ logZ,
@@ -1166,11 +1184,25 @@ __global__ __launch_bounds__(kThreadsMax) void parse_kernel(KernelPlan p, const 
                                                             int32_t *__restrict__ spans,
                                                             float *__restrict__ best) {
     extern __shared__ __align__(16) char smem_raw[];
-    const int32_t *rec = p.mix + (size_t)blockIdx.x * p.rec_stride;
-    if (rec[3])
-        inside_block<true, false, false>(p, 0, rec, smem_raw, scores, grad, logZ, marg);
-    else
-        cky_block<false>(p, 0, rec, smem_raw, scores, spans, best);
+    __shared__ int slot;
+    int cur = blockIdx.x;
+    for (;;) {
+        const int32_t *rec = p.mix + (size_t)cur * p.rec_stride;
+        if (rec[3])
+            inside_block<true, false, false>(p, 0, rec, smem_raw, scores, grad, logZ, marg);
+        else
+            cky_block<false>(p, 0, rec, smem_raw, scores, spans, best);
+        if ((int)gridDim.x >= p.n_mix) break;   // one bundle per workgroup: no claims at all
+        if (threadIdx.x == 0) {
+            const int ticket = atomicAdd(p.counter, 1);
+            if (ticket == p.n_mix - 1) atomicExch(p.counter, 0);
+            slot = (int)gridDim.x + ticket;
+        }
+        __syncthreads();   // the claim is published and the bundle's LDS is free
+        cur = slot;
+        __syncthreads();   // every thread has read the slot
+        if (cur >= p.n_mix) break;
+    }
 }
 
 }  // namespace
@@ -1235,13 +1267,13 @@ hipError_t launch_cky(const KernelPlan &p, const float *scores, int32_t *spans, 
 hipError_t launch_parse(const KernelPlan &p, const float *scores, const float *grad, float *logZ,
                         float *marg, int32_t *spans, float *best, hipStream_t stream) {
     const Schedule &qi = p.inside, &qc = p.cky;
-    if (p.mix == nullptr || p.n_mix != qi.n_bundles + qc.n_bundles) {
+    if (p.mix == nullptr || p.counter == nullptr || p.fused_grid < 1 || p.n_mix != qi.n_bundles + qc.n_bundles) {
         hipError_t e = launch_inside(p, scores, grad, logZ, marg, stream);
         if (e != hipSuccess) return e;
         return launch_cky(p, scores, spans, best, stream);
     }
     const size_t lds = (size_t)(qi.lds_bytes > qc.lds_bytes ? qi.lds_bytes : qc.lds_bytes);
-    hipLaunchKernelGGL(parse_kernel, dim3(p.n_mix), dim3(qi.threads), lds, stream, p,
+    hipLaunchKernelGGL(parse_kernel, dim3(p.fused_grid), dim3(qi.threads), lds, stream, p,
                        scores, grad, logZ, marg, spans, best);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;

@@ -220,7 +220,7 @@ HostSchedule make_schedule(const std::vector<int32_t> &order, const int32_t *len
     };
     // Workgroup LDS budget: half the CU when every eligible sentence fits in
     // half (two workgroups per CU), else all of it (one).
-    const int64_t half = lds_cap / 2 - 256, full = lds_cap - 256;
+    const int64_t half = lds_cap / 2 - crf::kReservedLds, full = lds_cap - crf::kReservedLds;
     int64_t biggest = 0;
     std::vector<int32_t> eligible;
     int64_t cursor = ws_base;
@@ -360,7 +360,7 @@ int crf_plan_create(crf_plan **out, const int32_t *lengths_host, int32_t batch, 
     // A sentence's split table sits in LDS after its chart when a bundle of
     // one such sentence still fits in half the CU; longer sentences keep it
     // in the workspace.
-    const int64_t half_cu = lds_cap / 2 - 256;
+    const int64_t half_cu = lds_cap / 2 - crf::kReservedLds;
     auto split_in_lds = [=](int n) {
         return crf::cky_chart_bytes(n, 1) + 4 + crf::bundle_extra_bytes(n) + cky_tail(n, 1) <= half_cu;
     };
@@ -385,17 +385,20 @@ int crf_plan_create(crf_plan **out, const int32_t *lengths_host, int32_t batch, 
     kp.n1 = n1;
     kp.L = num_labels;
     std::vector<int32_t> mix;
+    int32_t fused_slots = 0;
     if (num_labels == 1 && !si.bundles.empty() && !sc.bundles.empty() && si.threads == sc.threads) {
-        // One workgroup slot per CU per half of the LDS; the hardware deals
-        // consecutive workgroups to the XCDs (32 CUs each on gfx950) in turn.
+        // One workgroup slot per CU per half of the LDS; the fused kernel's
+        // workgroups fill every slot and take bundles from one queue, in the
+        // order they free up.
         int cus = 0;
         if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, p->device) != hipSuccess || cus < 1)
             cus = 256;
-        const int n_part = std::max(1, cus / 32);
         const int per_cu = std::min(4, std::max(1, (int)(lds_cap / std::max(si.lds_bytes, sc.lds_bytes))));
-        plan_fused_launch(si.bundles, sc.bundles, n_part, std::max(1, cus / n_part) * per_cu, mix);
+        fused_slots = cus * per_cu;
+        plan_fused_launch(si.bundles, sc.bundles, 1, fused_slots, mix);
     }
     kp.n_mix = (int32_t)mix.size();
+    kp.fused_grid = std::min<int32_t>(kp.n_mix, fused_slots);
     // Workgroup records: the bundle's shape and its sentence ids.
     int max_count = 1;
     for (const crf::Bundle &bd : si.bundles) max_count = std::max(max_count, (int)bd.count);
@@ -444,6 +447,17 @@ int crf_plan_create(crf_plan **out, const int32_t *lengths_host, int32_t batch, 
         delete p;
         return code == CRF_ENOMEM ? fail(code, "device allocation of the schedule failed")
                                   : hip_fail(e, "schedule upload");
+    }
+    kp.counter = nullptr;
+    if (kp.fused_grid > 0) {
+        void *c = nullptr;
+        if ((e = hipMalloc(&c, 256)) != hipSuccess || (p->allocations.push_back(c), false) ||
+            (e = hipMemset(c, 0, 256)) != hipSuccess) {
+            release(p);
+            delete p;
+            return hip_fail(e, "claim counter");
+        }
+        kp.counter = static_cast<int32_t *>(c);
     }
     kp.ws = nullptr;
     if (p->ws_bytes > 0) {

@@ -265,3 +265,20 @@ def test_split_tables_in_workspace(torch):
     # whole CU
     b = W.custom([97, 97, 98, 99, 99, 120, 3, 40], seed=24, sd=2.0)
     full_check(torch, b)
+
+
+@pytest.mark.parametrize("name", ["tiny", "mixed"])
+def test_fused_repeat_launches(torch, name):
+    # the fused kernel's workgroups pull bundles from a counter that the last
+    # claim resets: back-to-back launches on one plan give the same bits
+    b = W.make(name)
+    dev = torch.device("cuda", 0)
+    s = torch.from_numpy(b.scores).to(dev)
+    with B.Plan(b.lengths, device=dev) as plan:
+        lz0, mu0 = plan.inside_fwd_bwd(s)
+        sp0, be0 = plan.cky_decode(s)
+        outs = [plan.parse(s) for _ in range(4)]
+        torch.cuda.synchronize()
+    for lz, mu, sp, be in outs:
+        assert torch.equal(lz, lz0) and torch.equal(mu, mu0)
+        assert torch.equal(sp, sp0) and torch.equal(be, be0)
