@@ -41,13 +41,13 @@
 //   * CKY runs a float64 chart in the association order
 //     beta(i,j) = (max_k (beta(i,k) + beta(k,j))) + s(i,j): only IEEE adds
 //     and exact max, so the tree is reproducible bit for bit; ties keep the
-//     lowest split.  No back-pointers are stored: the tree walk recomputes
-//     each visited node's split from the chart.  Bundles of few (long)
-//     sentences walk breadth first, one wavefront per sentence, recording
-//     depths (spans starting at position i form a chain of left children, so
-//     a node's preorder slot is the chain's offset plus its depth below the
-//     chain head); bundles of many (short) sentences walk depth first, one
-//     lane group per sentence, the preorder slot being a running count.
+//     lowest split, which the sweep records per span in a split table.  The
+//     tree walk only looks splits up: a node (i,j) written at preorder row r
+//     with split k puts (i,k) at row r+1 and (k,j) at row r+2(k-i).  Bundles
+//     of few (long) sentences walk breadth first, one wavefront per sentence;
+//     bundles of many (short) sentences depth first, one lane per sentence.
+//   * The fused launch is persistent: one workgroup per slot runs a chain of
+//     bundles, claiming each next one from a device counter as it frees up.
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdint.h>
