@@ -221,10 +221,13 @@ __device__ __forceinline__ void inside_span(const Bundle_ctx<T> &bx, int w, int 
     const Lane_at at = lane_at<G>(f, S, magic);
     const int i = at.i, l = at.l, j = i + w;
     T *al = bx.chart0 + __umul24((uint32_t)at.sb, (uint32_t)bx.cstride);
-    const int rowo = (int)__umul24((uint32_t)i, (uint32_t)(ld + 1)) + 1 + l;   // alpha(i, k)
-    const int colo = rowo + (int)__umul24((uint32_t)w, (uint32_t)ld);          // alpha(k, j) mirrored
-    const int dia = (int)__umul24((uint32_t)i, (uint32_t)ld) + j;              // [i][j]
-    const int mir = (int)__umul24((uint32_t)j, (uint32_t)ld) + i;              // [j][i]
+    // every index from the diagonal cell [i][i] and the uniform w * ld
+    const int rb = (int)__umul24((uint32_t)i, (uint32_t)(ld + 1));   // [i][i]
+    const int cb = rb + (int)__umul24((uint32_t)w, (uint32_t)ld);    // [j][i]
+    const int rowo = rb + 1 + l;   // alpha(i, k)
+    const int colo = cb + 1 + l;   // alpha(k, j) mirrored
+    const int dia = rb + w;        // [i][j]
+    const int mir = cb;            // [j][i]
     const float own = al[dia] + (w < bx.n ? dsh[at.sb] : 0.f);   // the root is forced: no shift
     float x[C], xr[C], xc[C];
 #pragma unroll
@@ -241,9 +244,9 @@ __device__ __forceinline__ void inside_span(const Bundle_ctx<T> &bx, int w, int 
     float m = x[0];
 #pragma unroll
     for (int c = 1; c < C; ++c) m = fmax_nn(m, x[c]);
-    float s = 0.f;
+    float s = fast_exp2(x[0] - m);
 #pragma unroll
-    for (int c = 0; c < C; ++c) s += fast_exp2(x[c] - m);
+    for (int c = 1; c < C; ++c) s += fast_exp2(x[c] - m);
     const float mg = grp_max<G>(m);
     const float sg = grp_sum<G>(s * fast_exp2(m - mg));
     const float v = mg + fast_log2(sg) + own;
@@ -282,7 +285,7 @@ __device__ __forceinline__ void outside_span(const Bundle_ctx<T> &bx, int v, int
     T *al = bx.chart0 + __umul24((uint32_t)at.sb, (uint32_t)bx.cstride);
     T *ou = al + __umul24((uint32_t)ld, (uint32_t)ld);
     const int ri = (int)__umul24((uint32_t)i, (uint32_t)ld);
-    const int rj = (int)__umul24((uint32_t)j, (uint32_t)ld);
+    const int rj = ri + (int)__umul24((uint32_t)v, (uint32_t)ld);   // (the second term is uniform)
     const T *oL = ou + rj + l, *aL = al + ri + l;                    // q < i
     const T *oR = ou + ri + v + 1 + l, *aR = al + rj + v + 1 + l;    // q >= i
     const int il = i - l, kl = K - l;   // term c is left iff c*G < il, valid iff c*G < kl
@@ -318,9 +321,9 @@ __device__ __forceinline__ void outside_span(const Bundle_ctx<T> &bx, int v, int
     float m = x[0];
 #pragma unroll
     for (int c = 1; c < C; ++c) m = fmax_nn(m, x[c]);
-    float s = 0.f;
+    float s = fast_exp2(x[0] - m);
 #pragma unroll
-    for (int c = 0; c < C; ++c) s += fast_exp2(x[c] - m);
+    for (int c = 1; c < C; ++c) s += fast_exp2(x[c] - m);
     const float mg = grp_max<G>(m);
     const float sg = grp_sum<G>(s * fast_exp2(m - mg));
     const float o = mg + fast_log2(sg) + own;
@@ -879,11 +882,13 @@ __device__ __forceinline__ void cky_step(const Cky_ctx<SP> &cx, int w, uint32_t 
         if (f0 + wq0 >= total) break;
         const bool act = f0 + tid < total;
         const Lane_at at = lane_at<G>(act ? f0 + tid : total - 1, S, magic);
-        const int i = at.i, l = at.l, j = i + w;
+        const int i = at.i, l = at.l;
         double *be = cx.beta(at.sb);
-        const int rowo = (int)__umul24((uint32_t)i, (uint32_t)(ld + 1)) + 1 + l;
-        const int colo = rowo + (int)__umul24((uint32_t)w, (uint32_t)ld);
-        const double sij = be[i * ld + j];
+        // every index from the diagonal cell [i][i] and the uniform w * ld
+        const int rb = (int)__umul24((uint32_t)i, (uint32_t)(ld + 1));   // [i][i]
+        const int cb = rb + (int)__umul24((uint32_t)w, (uint32_t)ld);    // [j][i]
+        const int rowo = rb + 1 + l, colo = cb + 1 + l;
+        const double sij = be[rb + w];
         const int kl = K - l;
         // Terms in chunks of up to 16.  Up to 16 splits per lane (one chunk),
         // every float64 operand is loaded before the first is used; longer
@@ -921,8 +926,8 @@ __device__ __forceinline__ void cky_step(const Cky_ctx<SP> &cx, int w, uint32_t 
         const double v = mg + sij;
         asm volatile("" ::"v"(v));   // keeps the score load with the operand loads
         if (act && l == 0) {
-            be[i * ld + j] = v;
-            be[j * ld + i] = v;
+            be[rb + w] = v;
+            be[cb] = v;
             cx.put_split(at.sb, sp0 + i, kb);
         }
     }
