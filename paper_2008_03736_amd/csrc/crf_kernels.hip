@@ -834,16 +834,23 @@ struct Cky_ctx {
     // (not a generic one: flat accesses cost more, and a flat store to LDS
     // holds up the next barrier).
     __device__ void put_split(int sb, int e, int v) const {
-        SP *q = reinterpret_cast<SP *>(split0 + (size_t)sb * sstride) + e;
-        if (split_lds)
-            *(__attribute__((address_space(3))) SP *)q = (SP)v;
-        else
+        if (split_lds) {   // 32-bit LDS address arithmetic
+            const uint32_t a = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char *)split0 +
+                               __umul24((uint32_t)sb, (uint32_t)sstride) + (uint32_t)e * sizeof(SP);
+            *(__attribute__((address_space(3))) SP *)(uintptr_t)a = (SP)v;
+        } else {
+            SP *q = reinterpret_cast<SP *>(split0 + (size_t)sb * sstride) + e;
             *(__attribute__((address_space(1))) SP *)q = (SP)v;
+        }
     }
     __device__ int get_split(int sb, int e) const {
+        if (split_lds) {
+            const uint32_t a = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char *)split0 +
+                               __umul24((uint32_t)sb, (uint32_t)sstride) + (uint32_t)e * sizeof(SP);
+            return (int)*(const __attribute__((address_space(3))) SP *)(uintptr_t)a;
+        }
         const SP *q = reinterpret_cast<const SP *>(split0 + (size_t)sb * sstride) + e;
-        return split_lds ? (int)*(const __attribute__((address_space(3))) SP *)q
-                         : (int)*(const __attribute__((address_space(1))) SP *)q;
+        return (int)*(const __attribute__((address_space(1))) SP *)q;
     }
 };
 
@@ -910,7 +917,13 @@ __device__ __forceinline__ void cky_step(const Cky_ctx<SP> &cx, int w, uint32_t 
 #pragma unroll
             for (int c = 0; c < CH; ++c) {
                 x[c] = xr[c] + xc[c];
-                if (c0 + c >= MF && (c0 + c) * G >= kl) x[c] = -INFINITY;
+                // a split past the span's last: the high word alone makes it
+                // about -1.8e308, below any chart value (one select, not two)
+                if (c0 + c >= MF) {
+                    const uint64_t u = __builtin_bit_cast(uint64_t, x[c]);
+                    const uint32_t hi = (c0 + c) * G >= kl ? 0xFFEFFFFFu : (uint32_t)(u >> 32);
+                    x[c] = __builtin_bit_cast(double, ((uint64_t)hi << 32) | (uint32_t)u);
+                }
             }
             const Arg_max a = tree_arg_max<0, CH>(x, c0, G);
             if (c0 == 0) {
