@@ -32,8 +32,23 @@ __host__ __device__ inline int64_t bundle_extra_bytes(int n) { return 4 * (int64
 // and slack.  Bundle budgets leave it free.
 constexpr int kReservedLds = 256;
 
-// Row stride (in elements) of a sentence's square chart.
-__host__ __device__ inline int chart_ld(int n) { return n + 1; }
+// Row stride (in elements) of a sentence's square charts, at least n + 1.
+// Spans of one width sit ld + 1 elements apart along the diagonal (the
+// inside and CKY split operands) and ld apart down a column (the outside
+// operands); LDS has 32 four-byte banks, so a stride with a factor 2^k
+// makes 2^k lanes collide on a bank.  The inside chart takes ld = 1 or 2
+// (mod 4) -- one stride odd, the other twice odd, at worst 2-way; the
+// float64 CKY chart takes ld even, which makes ld + 1 odd and its
+// 8-byte diagonal accesses conflict-free.  (Sentences of 98 and 99 words
+// keep ld = n + 1 for the inside: padded, their two float32 squares would
+// no longer fit in half a CU, and one bundle that needs a whole CU moves
+// every bundle of the launch to one workgroup per CU.)
+__host__ __device__ inline int inside_ld(int n) {
+    int ld = n + 1;
+    while ((ld & 3) == 0 || (ld & 3) == 3) ++ld;
+    return (ld > 100 && n + 1 <= 100) ? n + 1 : ld;
+}
+__host__ __device__ inline int cky_ld(int n) { return (n + 1) + ((n + 1) & 1); }
 
 // Bytes of chart per sentence.
 //   inside: two float32 squares -- alpha (upper triangle + mirrored lower
@@ -47,7 +62,7 @@ __host__ __device__ inline int chart_ld(int n) { return n + 1; }
 //           the workspace).  A bundle whose tables do not fit in LDS beside
 //           its charts keeps them in the workspace (Bundle::split_ws).
 __host__ __device__ inline int64_t inside_chart_bytes(int n) {
-    const int64_t ld = chart_ld(n);
+    const int64_t ld = inside_ld(n);
     return 2 * ld * ld * 4;
 }
 __host__ __device__ inline int64_t cky_split_count(int n) { return (int64_t)n * (n - 1) / 2; }
@@ -57,7 +72,7 @@ __host__ __device__ inline int cky_split_index(int n, int w, int i) {
     return (w - 2) * (n + 1) - ((w - 1) * w / 2 - 1) + i;
 }
 __host__ __device__ inline int64_t cky_chart_bytes(int n, int split_bytes) {
-    const int64_t ld = chart_ld(n);
+    const int64_t ld = cky_ld(n);
     return ld * ld * 8 + (cky_split_count(n) * split_bytes + 7) / 8 * 8;
 }
 // The CKY tree walk follows the split table.  Bundles of fewer than
@@ -105,8 +120,9 @@ __host__ __device__ inline int masked_reach(int n) {
 }
 
 // Longest sentence whose CKY chart could sit in one CU's LDS (160 KiB):
-// 8 (n+1)^2 <= 163840 (with its split table and tables the plan finds
-// somewhat less).  The plan sends longer ones to the workspace kernels.
+// 8 (n+1)^2 <= 163840 (with row padding, its split table and tables the
+// plan finds somewhat less).  The plan sends longer ones to the workspace
+// kernels.
 constexpr int kMaxLenInLds = 142;
 
 // A bundle: `count` sentences of identical length `n`, processed together by

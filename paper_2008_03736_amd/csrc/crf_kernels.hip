@@ -721,7 +721,7 @@ __device__ __forceinline__ void inside_block(const KernelPlan &p, int block, con
         if (tid < nb) sid[tid] = id0;
     }
     for (int S = tid; S <= n + 1; S += NT) magic[S] = div_magic(S);
-    const int ld = chart_ld(n);
+    const int ld = inside_ld(n);
     const Bundle_ctx<float> bx{chart0, cstride, n, ld, nb};
     __syncthreads();
     for (int t = tid; t < nb; t += NT) {
@@ -1097,7 +1097,7 @@ __device__ __forceinline__ void cky_block(const KernelPlan &p, int block, const 
         nb = 1;
         chart0 = p.ws + p.cky.ws_off[block];
         cstride = 0;
-        split0 = chart0 + (size_t)8 * chart_ld(n) * chart_ld(n);
+        split0 = chart0 + (size_t)8 * cky_ld(n) * cky_ld(n);
         sstride = 0;
         sid = spill_id;
         magic = spill_magic;
@@ -1111,7 +1111,7 @@ __device__ __forceinline__ void cky_block(const KernelPlan &p, int block, const 
         chart0 = smem_raw;
         split_lds = split_ws < 0;
         cstride = (int)cky_chart_bytes(n, split_lds ? 1 : 0);
-        split0 = split_lds ? chart0 + (size_t)8 * chart_ld(n) * chart_ld(n) : p.ws + (size_t)split_ws * 256;
+        split0 = split_lds ? chart0 + (size_t)8 * cky_ld(n) * cky_ld(n) : p.ws + (size_t)split_ws * 256;
         sstride = split_lds ? cstride : (int)cky_split_count(n);
         sid = reinterpret_cast<int *>(smem_raw + (size_t)nb * cstride);
         magic = reinterpret_cast<uint32_t *>(sid + nb);
@@ -1119,7 +1119,7 @@ __device__ __forceinline__ void cky_block(const KernelPlan &p, int block, const 
         if (tid < nb) sid[tid] = id0;
     }
     for (int S = tid; S <= n; S += NT) magic[S] = div_magic(S);
-    const int ld = chart_ld(n);
+    const int ld = cky_ld(n);
     typedef typename std::conditional<SPILL, uint16_t, uint8_t>::type SP;
     const Cky_ctx<SP> cx{chart0, cstride, split0, sstride, n, ld, nb, !SPILL && split_lds};
     __syncthreads();
