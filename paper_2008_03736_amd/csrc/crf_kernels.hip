@@ -21,8 +21,10 @@
 //     the first use.  The split-point log-sum-exp is a max / sum-exp per lane
 //     finished by a butterfly over the G lanes (DPP inside a 16-lane row,
 //     ds_swizzle across rows, readlane across the two halves of the wave).
-//   * alpha is stored twice, at [i][j] and mirrored at [j][i], so the row
-//     alpha(i,.) and the column alpha(.,j) of a span are both contiguous.
+//   * alpha and the outside values are each stored twice, in two squares
+//     whose rows are stored rotated, so that every split operand of the
+//     inside and of the outside is a contiguous run (see the inside chart
+//     layout below).
 //   * The chart holds log2-scaled values (v_exp_f32 / v_log_f32 are base 2).
 //   * Forced spans -- every tree holds the n width-1 spans and the root -- are
 //     factored out of the chart: their scores are summed in float64 and added
@@ -207,38 +209,44 @@ __device__ __forceinline__ Lane_at lane_at(int f, int S, uint32_t magic) {
     return Lane_at{sb, gid - (int)__umul24((uint32_t)sb, (uint32_t)S), f & (G - 1)};
 }
 
-// One span of a width-w inside step (K = w - 1 splits): lane l of the span's
-// G lanes takes split offsets ko = l + c*G, c < C (split k = i+1+ko); terms
-// c >= MF may fall past K: they count as exp2(-inf) = 0 and read cells at most
-// (C - MF)*G columns past the span's last split.  alpha(i,j) = s(i,j) + d +
-// log2 sum_k exp2(alpha(i,k) + alpha(k,j)), written to [i][j] and [j][i];
-// before the sweep [i][j] holds the (log2-scaled) score s(i,j), and d is the
-// sentence's score shift (see rescale_chart).
+// Inside chart layout.  Two ld x ld float32 squares per sentence, P and Q,
+// with P upper = alpha, P lower = O' mirrored, and Q = P transposed (Q upper
+// = O', Q lower = alpha mirrored), where O'(a,b) = O(a,b) + s(a,b) + d is the
+// outside score plus the span's own (shifted) score, zero at the root.  Row r
+// of P is stored rotated left by r+1 and row r of Q by r (position p of row r
+// holds column (p + r + 1) mod (n+1), resp. (p + r) mod (n+1)).  Then both
+// recursions read two contiguous runs at offsets uniform over a step:
+//   inside  (i,j), w = j-i:  alpha(i,k) + alpha(k,j) = P[i][p] + Q[j][p + n+2-w],
+//                            p = k-i-1 in [0, w-1);
+//   outside (i,j), v = j-i:  the parents' O' plus the siblings' alpha, over
+//                            t in [0,i) u (j,n], = P[j][p] + Q[i][p + v+1],
+//                            p in [0, n-v)
+// (rows and positions in the rotated squares).  A span (a,b) of width w
+// keeps alpha at P[a][w-1] and Q[b][n+1-w], O' at Q[a][w] and P[b][n-w];
+// before the sweeps reach it those cells hold its (log2-scaled) score, which
+// the steps read as the span's own term.  Cells no sweep reads park the
+// natural-unit scores of the forced spans: width 1 at P[i+1][n-1], the root
+// at P[0][n].
+__host__ __device__ constexpr int rot_alpha_p(int w) { return w - 1; }
+template <typename T>
+__device__ __forceinline__ T *sq_p(const Bundle_ctx<T> &bx, int sb) { return bx.chart0 + (size_t)sb * bx.cstride; }
+
+// One span's log-sum-exp over the K split terms of a step: lane l of the
+// span's G lanes takes positions p = l + c*G, c < C, of the two runs a and b
+// (terms c >= MF may fall past K: they count as exp2(-inf) = 0 and read at
+// most (C - MF)*G cells past the run); the group's result plus `own` is
+// returned to every lane of the group.
 template <int G, int C, int MF, typename T>
-__device__ __forceinline__ void inside_span(const Bundle_ctx<T> &bx, int w, int S, int f, bool act,
-                                            uint32_t magic, const float *dsh) {
-    const int ld = bx.ld, K = w - 1;
-    const Lane_at at = lane_at<G>(f, S, magic);
-    const int i = at.i, l = at.l, j = i + w;
-    T *al = bx.chart0 + __umul24((uint32_t)at.sb, (uint32_t)bx.cstride);
-    // every index from the diagonal cell [i][i] and the uniform w * ld
-    const int rb = (int)__umul24((uint32_t)i, (uint32_t)(ld + 1));   // [i][i]
-    const int cb = rb + (int)__umul24((uint32_t)w, (uint32_t)ld);    // [j][i]
-    const int rowo = rb + 1 + l;   // alpha(i, k)
-    const int colo = cb + 1 + l;   // alpha(k, j) mirrored
-    const int dia = rb + w;        // [i][j]
-    const int mir = cb;            // [j][i]
-    const float own = al[dia] + (w < bx.n ? dsh[at.sb] : 0.f);   // the root is forced: no shift
-    float x[C], xr[C], xc[C];
+__device__ __forceinline__ float span_lse(const T *a, const T *b, int kl, float own) {
+    float x[C], xa[C], xb[C];
 #pragma unroll
     for (int c = 0; c < C; ++c) {
-        xr[c] = al[rowo + c * G];
-        xc[c] = al[colo + c * G];
+        xa[c] = a[c * G];
+        xb[c] = b[c * G];
     }
     __builtin_amdgcn_sched_barrier(0);   // every load in flight before the first use
 #pragma unroll
-    for (int c = 0; c < C; ++c) x[c] = xr[c] + xc[c];
-    const int kl = K - l;
+    for (int c = 0; c < C; ++c) x[c] = xa[c] + xb[c];
 #pragma unroll
     for (int c = MF; c < C; ++c) x[c] = (c * G < kl) ? x[c] : NEG;
     float m = x[0];
@@ -249,88 +257,54 @@ __device__ __forceinline__ void inside_span(const Bundle_ctx<T> &bx, int w, int 
     for (int c = 1; c < C; ++c) s += fast_exp2(x[c] - m);
     const float mg = grp_max<G>(m);
     const float sg = grp_sum<G>(s * fast_exp2(m - mg));
-    const float v = mg + fast_log2(sg) + own;
-    // An unconditional use keeps the score load in this block, where it is
-    // issued with the operand loads instead of after the reductions.
+    return mg + fast_log2(sg) + own;
+}
+
+// One span of a width-w inside step (K = w - 1 splits):
+// alpha(i,j) = s(i,j) + d + log2 sum_k exp2(alpha(i,k) + alpha(k,j)), d the
+// sentence's score shift (see rescale_chart); the root's own term is not
+// shifted.
+template <int G, int C, int MF, typename T>
+__device__ __forceinline__ void inside_span(const Bundle_ctx<T> &bx, int w, int S, int f, bool act,
+                                            uint32_t magic, const float *dsh) {
+    const int ld = bx.ld, n = bx.n, K = w - 1;
+    const Lane_at at = lane_at<G>(f, S, magic);
+    const int i = at.i, l = at.l;
+    T *pq = sq_p(bx, at.sb);
+    const int rp = (int)__umul24((uint32_t)i, (uint32_t)ld);                   // P row i
+    const int rq = rp + (int)__umul24((uint32_t)(ld + w), (uint32_t)ld);        // Q row j (uniform offset)
+    const int pa = rp + rot_alpha_p(w), qa = rq + n + 1 - w;                   // alpha(i,j) cells
+    const float own = pq[pa] + (w < n ? dsh[at.sb] : 0.f);
+    const float v = span_lse<G, C, MF>(pq + rp + l, pq + rq + (n + 2 - w) + l, K - l, own);
+    // An unconditional use keeps the score load in the load block, where it
+    // is issued with the operand loads instead of after the reductions.
     asm volatile("" ::"v"(v));
     if (act && l == 0) {
-        al[dia] = v;
-        al[mir] = v;
+        pq[pa] = v;
+        pq[qa] = v;
     }
 }
 
-// 32-bit LDS address of a generic pointer into LDS, and a load through one.
-typedef __attribute__((address_space(3))) float lds_float;
-__device__ __forceinline__ uint32_t lds_addr(const float *p) {
-    return (uint32_t)(uintptr_t)(const lds_float *)p;
-}
-__device__ __forceinline__ float lds_ld(uint32_t a) { return *(const lds_float *)(uintptr_t)a; }
-
-// One span of a width-v outside step.  With O'(a,b) = O(a,b) + s(a,b) + d
-// (zero at the root) and O the log outside score, a child (i,j) of width v
-// has t = n - v parent terms, indexed q = 0..t-1:
-//   q <  i: parent (q, j),         term O'(q,j) + alpha(q,i)
-//   q >= i: parent (i, k), k = q+v+1, term O'(i,k) + alpha(j,k),
-// every operand a parent of width > v or a sibling of width <= t, so this
-// step runs beside the inside step of width t+1.  Storage: the second square
-// holds O' at [i][j] and mirrored at [j][i]; before the outside reaches
-// (i,j), [j][i] holds its score.  Left terms read rows j (O' mirror) and i
-// (alpha mirror), right terms rows i (O') and j (alpha), all contiguous in q.
+// One span (i,j) of a width-v outside step: K = n - v parent terms, every
+// operand a parent of width > v or a sibling of width <= n - v, so this step
+// runs beside the inside step of width n - v + 1.
 template <int G, int C, int MF, bool WIDE, typename T>
 __device__ __forceinline__ void outside_span(const Bundle_ctx<T> &bx, int v, int S, int f, bool act,
                                              uint32_t magic, const float *dsh) {
-    const int ld = bx.ld, K = bx.n - v;
+    const int ld = bx.ld, n = bx.n, K = n - v;
     const Lane_at at = lane_at<G>(f, S, magic);
-    const int i = at.i, l = at.l, j = i + v;
-    T *al = bx.chart0 + __umul24((uint32_t)at.sb, (uint32_t)bx.cstride);
-    T *ou = al + __umul24((uint32_t)ld, (uint32_t)ld);
+    const int i = at.i, l = at.l;
+    T *pq = sq_p(bx, at.sb);
     const int ri = (int)__umul24((uint32_t)i, (uint32_t)ld);
-    const int rj = ri + (int)__umul24((uint32_t)v, (uint32_t)ld);   // (the second term is uniform)
-    const T *oL = ou + rj + l, *aL = al + ri + l;                    // q < i
-    const T *oR = ou + ri + v + 1 + l, *aR = al + rj + v + 1 + l;    // q >= i
-    const int il = i - l, kl = K - l;   // term c is left iff c*G < il, valid iff c*G < kl
-    const float own = ou[rj + i] + dsh[at.sb];
-    float x[C];
-    if constexpr (!WIDE) {
-        // LDS chart: pick each term's row by selecting between two 32-bit LDS
-        // addresses, the split offset folded into the load's immediate.  The
-        // empty asm keeps the compiler from pulling the common lane offset out
-        // of the selects (which costs two adds per term).
-        uint32_t oLa = lds_addr(oL), aLa = lds_addr(aL), oRa = lds_addr(oR), aRa = lds_addr(aR);
-        asm volatile("" : "+v"(oLa), "+v"(aLa), "+v"(oRa), "+v"(aRa));
-        float xo[C], xa[C];
-#pragma unroll
-        for (int c = 0; c < C; ++c) {
-            const bool left = c * G < il;
-            xo[c] = lds_ld((left ? oLa : oRa) + 4 * c * G);
-            xa[c] = lds_ld((left ? aLa : aRa) + 4 * c * G);
-        }
-        // all loads in flight before the first use: one LDS round trip
-        __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-        for (int c = 0; c < C; ++c) x[c] = xo[c] + xa[c];
-    } else {
-#pragma unroll
-        for (int c = 0; c < C; ++c) {
-            const bool left = c * G < il;
-            x[c] = (left ? oL : oR)[c * G] + (left ? aL : aR)[c * G];
-        }
-    }
-#pragma unroll
-    for (int c = MF; c < C; ++c) x[c] = (c * G < kl) ? x[c] : NEG;
-    float m = x[0];
-#pragma unroll
-    for (int c = 1; c < C; ++c) m = fmax_nn(m, x[c]);
-    float s = fast_exp2(x[0] - m);
-#pragma unroll
-    for (int c = 1; c < C; ++c) s += fast_exp2(x[c] - m);
-    const float mg = grp_max<G>(m);
-    const float sg = grp_sum<G>(s * fast_exp2(m - mg));
-    const float o = mg + fast_log2(sg) + own;
+    const int rp = ri + (int)__umul24((uint32_t)v, (uint32_t)ld);   // P row j (uniform offset)
+    const int rq = ri + (int)__umul24((uint32_t)ld, (uint32_t)ld);  // Q row i
+    const int po = rp + n - v, qo = rq + v;                          // O'(i,j) cells
+    const float own = pq[po] + dsh[at.sb];
+    const float o = span_lse<G, C, MF>(pq + rp + l, pq + rq + v + 1 + l, K - l, own);
     asm volatile("" ::"v"(o));
     if (act && l == 0) {
-        ou[ri + j] = o;
-        ou[rj + i] = o;
+        pq[qo] = o;
+        pq[po] = o;
     }
 }
 
@@ -504,14 +478,14 @@ __device__ void rescale_chart(const Bundle_ctx<T> &bx, int t0, float *dsh) {
     const int n = bx.n, ld = bx.ld, nb = bx.nb, w0 = t0 + 1, S = n - t0;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, NW = blockDim.x >> 6;
     for (int sb = wave; sb < nb; sb += NW) {
-        const T *al = bx.chart0 + (size_t)sb * bx.cstride;
+        const T *P = bx.chart0 + (size_t)sb * bx.cstride;
         float m = NEG;
-        for (int i = lane; i < S; i += 64) m = fmax_nn(m, al[i * (ld + 1) + w0]);
+        for (int i = lane; i < S; i += 64) m = fmax_nn(m, P[i * ld + w0 - 1]);
         m = wave_max_f(m);
         const float floor_v = m - kShiftBand * (float)(w0 - 1);
         float acc = 0.f, cnt = 0.f;
         for (int i = lane; i < S; i += 64) {
-            const float a = al[i * (ld + 1) + w0];
+            const float a = P[i * ld + w0 - 1];
             if (a >= floor_v) {
                 acc += a;
                 cnt += 1.f;
@@ -532,10 +506,10 @@ __device__ void rescale_chart(const Bundle_ctx<T> &bx, int t0, float *dsh) {
             const int i = div_small(r, A, inv_a);
             const int w = 2 + r - i * A, j = i + w;
             if (j <= n) {
-                T *al = bx.chart0 + (size_t)sb * bx.cstride;
-                const float a = al[i * ld + j] + dsh[sb] * (float)(w - 1);
-                al[i * ld + j] = a;
-                al[j * ld + i] = a;
+                T *P = bx.chart0 + (size_t)sb * bx.cstride, *Q = P + (size_t)ld * ld;
+                const float a = P[i * ld + w - 1] + dsh[sb] * (float)(w - 1);
+                P[i * ld + w - 1] = a;
+                Q[j * ld + n + 1 - w] = a;
             }
         }
     }
@@ -549,10 +523,10 @@ __device__ void rescale_chart(const Bundle_ctx<T> &bx, int t0, float *dsh) {
             const int i = div_small(r, t0, inv_t);
             const int e = r - i * t0, v = n - t0 + e, j = i + v;
             if (i + e <= t0) {
-                T *ou = bx.chart0 + (size_t)sb * bx.cstride + (size_t)ld * ld;
-                const float o = ou[i * ld + j] + dsh[sb] * (float)(n - v);
-                ou[i * ld + j] = o;
-                ou[j * ld + i] = o;
+                T *P = bx.chart0 + (size_t)sb * bx.cstride, *Q = P + (size_t)ld * ld;
+                const float o = Q[i * ld + v] + dsh[sb] * (float)(n - v);
+                Q[i * ld + v] = o;
+                P[j * ld + n - v] = o;
             }
         }
     }
@@ -668,10 +642,8 @@ __device__ __forceinline__ float label_lse2(const float *s, int L) {
 //   LAB: labelled scores [B][N1][N1][L].
 // Dynamic LDS (bundled): nb charts, then nb x {forced (f64), grad (f32),
 // id (i32), shift (f32)}, then the magic table.
-// Chart of a sentence: two squares of ld x ld floats.  The first holds alpha
-// (upper triangle and mirrored).  The second holds the outside values O'
-// (REV, upper and mirrored) and parks the forced spans' scores where nothing
-// else reads: width-1 spans at [i+1][i], the root at [0][0].
+// Chart of a sentence: the rotated squares P and Q of the inside chart
+// layout (ld x ld floats each).
 template <bool REV, bool LAB, bool SPILL>
 __device__ __forceinline__ void inside_block(const KernelPlan &p, int block, const int32_t *rec, char *smem_raw,
                                              const float *__restrict__ scores,
@@ -732,9 +704,9 @@ __device__ __forceinline__ void inside_block(const KernelPlan &p, int block, con
     const size_t row_stride = LAB ? (size_t)N1 * L : (size_t)N1;
     const size_t sent_stride = (size_t)N1 * row_stride;
 
-    // Prologue: scores of every valid cell into the charts (log2-scaled; the
-    // outside reads its own copy at the mirrored cell of the second square);
-    // forced spans get 0 in alpha and park their natural-unit score.
+    // Prologue: scores of every valid cell into the charts (log2-scaled, in
+    // the cells of alpha and, for the outside, of O'); forced spans get 0 in
+    // alpha and park their natural-unit score.
     auto score_at = [&](int sb, int i, int j) -> const float * {
         return scores + (size_t)sid[sb] * sent_stride + (size_t)i * row_stride + (size_t)j * (LAB ? L : 1);
     };
@@ -744,34 +716,35 @@ __device__ __forceinline__ void inside_block(const KernelPlan &p, int block, con
         else
             return *q;
     };
+    // (cells of the rotated P / Q squares, see the inside chart layout)
     auto put_score = [&](int sb, int i, int j, float s) {
-        float *al = chart0 + (size_t)sb * cstride;
-        float *ou = al + (size_t)ld * ld;
-        if (j == i + 1) {
-            al[i * ld + j] = 0.f;
-            al[j * ld + i] = 0.f;
-            ou[j * ld + i] = s;
-        } else if (i == 0 && j == n) {
-            al[j] = 0.f;
-            ou[0] = s;
+        float *P = chart0 + (size_t)sb * cstride, *Q = P + (size_t)ld * ld;
+        const int w = j - i;
+        if (w == 1) {   // forced: alpha 0, score parked in the O' cell no sweep uses
+            P[i * ld] = 0.f;
+            Q[j * ld + n] = 0.f;
+            P[j * ld + n - 1] = s;
+        } else if (i == 0 && j == n) {   // the root: own term 0, O' 0, score parked
+            P[n - 1] = 0.f;
+            P[n] = s;
             if constexpr (REV) {
-                ou[j] = 0.f;        // O'(0,n) = 0
-                ou[n * ld] = 0.f;
+                Q[n] = 0.f;
+                P[n * ld] = 0.f;
             }
         } else {
             const float s2 = s * LOG2E_F;
-            al[i * ld + j] = s2;
-            if constexpr (REV) ou[j * ld + i] = s2;
+            P[i * ld + w - 1] = s2;
+            if constexpr (REV) P[j * ld + n - w] = s2;
         }
     };
     for_cells_loaded<LAB ? 1 : 8>(nb, n, score_at, load_score, put_score);
     __syncthreads();
     // Forced-span sums, one wavefront per sentence, fixed order (deterministic).
     for (int sb = wave; sb < nb; sb += NW) {
-        const float *ou = chart0 + (size_t)sb * cstride + (size_t)ld * ld;
+        const float *P = chart0 + (size_t)sb * cstride;
         double acc = 0.0;
-        for (int i = lane; i < n; i += 64) acc += (double)ou[(i + 1) * ld + i];
-        if (lane == 0 && n >= 2) acc += (double)ou[0];
+        for (int i = lane; i < n; i += 64) acc += (double)P[(i + 1) * ld + n - 1];
+        if (lane == 0 && n >= 2) acc += (double)P[n];
         acc = wave_sum_d(acc);
         if (lane == 0) forced[sb] = acc;
     }
@@ -786,7 +759,7 @@ __device__ __forceinline__ void inside_block(const KernelPlan &p, int block, con
     // log Z = (alpha~(0,n) - (n-2) d) ln 2 + forced sum.
     if (logZ != nullptr)
         for (int sb = tid; sb < nb; sb += NT) {
-            const double z2 = (double)chart0[(size_t)sb * cstride + n] - (double)dsh[sb] * (n >= 2 ? n - 2 : 0);
+            const double z2 = (double)chart0[(size_t)sb * cstride + n - 1] - (double)dsh[sb] * (n >= 2 ? n - 2 : 0);
             logZ[sid[sb]] = (float)(z2 * LN2_D + forced[sb]);
         }
     if constexpr (!REV) return;
@@ -796,13 +769,13 @@ __device__ __forceinline__ void inside_block(const KernelPlan &p, int block, con
     // and exactly g on forced spans.
     for_cells_loaded<LAB ? 1 : 8>(nb, n, score_at, load_score, [&](int sb, int i, int j, float s) {
         const size_t rowoff = (size_t)sid[sb] * sent_stride + (size_t)i * row_stride;
-        const float *al = chart0 + (size_t)sb * cstride;
-        const float *ou = al + (size_t)ld * ld;
+        const float *P = chart0 + (size_t)sb * cstride, *Q = P + (size_t)ld * ld;
         const bool forced_span = (j == i + 1) || (i == 0 && j == n);
         float mu = gv[sb];
         if (!forced_span) {
             const float own = s * LOG2E_F + dsh[sb];
-            mu *= fast_exp2(((al[i * ld + j] - al[n]) + ou[i * ld + j]) - own);
+            const int w = j - i;
+            mu *= fast_exp2(((P[i * ld + w - 1] - P[n - 1]) + Q[i * ld + w]) - own);
         }
         if constexpr (LAB) {
             const float *sl = scores + rowoff + (size_t)j * L;
