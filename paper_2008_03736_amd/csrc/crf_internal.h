@@ -22,36 +22,100 @@ constexpr int kThreadsMax = 1024;
 constexpr int kMaxBundle = 256;
 static_assert(kMaxBundle <= kThreadsDefault, "one sentence id per thread");
 
-// LDS a bundle needs besides its charts: a uint32 table of division magics
-// for span counts 0..n+1.  (Masked tail loads stay inside a sentence's inside
-// chart; those of the last CKY chart reach up to masked_reach(n) float64 past
-// it, into the tables that follow it, which the plan pads to that size.)
+// LDS a bundle needs besides its charts and per-sentence tables: for CKY a
+// uint32 table of division magics for span counts 0..n+1; the inside keeps
+// the same room unused.  Masked tail loads of the last chart of a bundle
+// reach past it, into the tables that follow it: up to masked_reach(n)
+// float32 (inside, whose tables and this room always cover that) or float64
+// (CKY, whose tail the plan pads to that size).
 __host__ __device__ inline int64_t bundle_extra_bytes(int n) { return 4 * (int64_t)(n + 2); }
 
 // LDS a workgroup holds besides its bundle (the fused kernel's claim slot)
 // and slack.  Bundle budgets leave it free.
 constexpr int kReservedLds = 256;
 
-// Row stride (in elements) of a sentence's square charts, at least n + 1.
-// Spans of one width sit ld + 1 elements apart along the diagonal (the
-// inside and CKY split operands) and ld apart down a column (the outside
-// operands); LDS has 32 four-byte banks, so a stride with a factor 2^k
-// makes 2^k lanes collide on a bank.  The inside chart takes ld = 1 or 2
-// (mod 4) -- one stride odd, the other twice odd, at worst 2-way; the
-// float64 CKY chart takes ld even, which makes ld + 1 odd and its
-// 8-byte diagonal accesses conflict-free.  (Sentences of 98 and 99 words
-// keep ld = n + 1 for the inside: padded, their two float32 squares would
-// no longer fit in half a CU, and one bundle that needs a whole CU moves
-// every bundle of the launch to one workgroup per CU.)
-__host__ __device__ inline int inside_ld(int n) {
-    int ld = n + 1;
-    while ((ld & 3) == 0 || (ld & 3) == 3) ++ld;
-    return (ld > 100 && n + 1 <= 100) ? n + 1 : ld;
+// LDS has 32 four-byte banks, and each 32-lane half of a wavefront is served
+// on its own: lanes of one half that hit one bank with different addresses
+// are served one after another.
+//
+// Inside chart geometry of a bundle of nb sentences of n words: row stride
+// ld >= n + 1 and chart stride cs >= 2 ld^2 (elements) of the two squares.
+// A width step numbers its spans sentence-minor, g = i nb + sb (span start i,
+// sentence sb), and every operand run of span g starts at sb cs + i ld plus
+// an offset uniform over the step.  With cs = sigma and ld = nb sigma
+// (mod 32) that start is sigma g (mod 32) for every g, whatever the step:
+// lanes that take g, g + q, g + 2q, ... with their G split lanes side by side
+// then cover 32 distinct banks when sigma q = G times an odd number (the
+// sweeps pick q = G >> e, where 2^e is the power of two in sigma).
+// The strict layout: sigma odd (e = 0) and ld with the same power of two as
+// nb, both the smallest that fit, except
+//  - bundles of 32 or more sentences whose count has a factor 4: ld odd and
+//    sigma = 1 (the start then jumps only where i changes, every nb spans);
+//  - sentences of 98 and 99 words keep ld = n + 1: padded, their two float32
+//    squares would no longer fit in half a CU, and one bundle that needs a
+//    whole CU moves every bundle of the launch to one workgroup per CU.  A
+//    single sentence then takes sigma = ld (e = 2 at n = 99: the sweeps then
+//    lay spans side by side, and its 4-lane steps, most of its work, stay
+//    conflict-free).
+// Of the sigma that satisfy these, the one that needs the least padding.
+// A count with a factor 2^b widens the strict ld by up to 2^(b+1) words;
+// where the strict layout would not fit in half a CU, the plan takes the
+// loose one instead: the smallest ld = 1 or 2 (mod 4) and sigma odd with one
+// word of padding, spans side by side (e = 5; about 2-way conflicts on the
+// steps of 2 and 4 lanes, where interleaving them does worse).
+struct InsideLayout {
+    int ld, cs, e;
+};
+__host__ __device__ inline int pow2_mod32(int x) {   // the power of two in x mod 32 (5 for 0)
+    x &= 31;
+    if (x == 0) return 5;
+    int b = 0;
+    while ((x & 1) == 0) {
+        x >>= 1;
+        ++b;
+    }
+    return b;
 }
+__host__ __device__ inline int inverse_mod32(int m) {   // m odd: m x = 1 (mod 32)
+    int x = m;
+    for (int k = 0; k < 4; ++k) x *= 2 - m * x;   // Newton: each step doubles the correct low bits
+    return x & 31;
+}
+constexpr int kInsideLdCap = 100;
+__host__ __device__ inline InsideLayout inside_layout(int n, int nb, bool strict) {
+    const int bn = pow2_mod32(nb);
+    if (!strict || (nb >= 32 && bn >= 2)) {
+        // loose: the smallest ld = 1 or 2 (mod 4), one word of padding (2 ld^2
+        // is even, so sigma = 2 ld^2 + 1 is odd), spans side by side (e = 5)
+        int ld = n + 1;
+        while ((ld & 3) == 0 || (ld & 3) == 3) ++ld;
+        if (ld > kInsideLdCap && n + 1 <= kInsideLdCap) ld = n + 1;
+        return InsideLayout{ld, 2 * ld * ld + 1, 5};
+    }
+    int ld = n + 1;
+    while (pow2_mod32(ld) != bn) ++ld;
+    if (ld > kInsideLdCap && n + 1 <= kInsideLdCap) ld = n + 1;
+    const int sq2 = 2 * ld * ld;
+    int e = 0, pad = (1 - sq2) & 31;   // sigma = 1 where no sigma solves it
+    const int bl = pow2_mod32(ld);
+    if (bl >= bn && bn < 5) {
+        // nb sigma = ld (mod 32): (nb >> b) sigma = ld >> b (mod 2^(5-b)),
+        // 2^b solutions mod 32; the one needing the least padding
+        const int step = 32 >> bn;
+        const int s0 = ((ld >> bn) * inverse_mod32(nb >> bn)) & (step - 1);
+        pad = 32;
+        for (int s = s0; s < 32; s += step) pad = ((s - sq2) & 31) < pad ? (s - sq2) & 31 : pad;
+        e = bl - bn;
+    }
+    return InsideLayout{ld, sq2 + pad, e};
+}
+// Row stride of the float64 CKY chart: even, which makes the diagonal stride
+// ld + 1 odd and its 8-byte accesses conflict-free.
 __host__ __device__ inline int cky_ld(int n) { return (n + 1) + ((n + 1) & 1); }
 
 // Bytes of chart per sentence.
-//   inside: two float32 squares -- alpha (upper triangle + mirrored lower
+//   inside: two float32 squares, padded to the chart stride of its bundle
+//           (inside_layout) -- alpha (upper triangle + mirrored lower
 //           triangle) and the outside values (upper + mirrored; before the
 //           outside sweep reaches a span its mirrored cell holds the span's
 //           score, and cells no sweep reads park the forced-span scores);
@@ -61,9 +125,14 @@ __host__ __device__ inline int cky_ld(int n) { return (n + 1) + ((n + 1) & 1); }
 //           k - i - 1 in split_bytes bytes (1 for n <= kMaxLenInLds, 2 in
 //           the workspace).  A bundle whose tables do not fit in LDS beside
 //           its charts keeps them in the workspace (Bundle::split_ws).
-__host__ __device__ inline int64_t inside_chart_bytes(int n) {
-    const int64_t ld = inside_ld(n);
-    return 2 * ld * ld * 4;
+// Byte offset of an inside bundle's per-sentence tables (the first holds
+// float64): its charts, rounded up to 8 bytes (the chart stride may be odd).
+__host__ __device__ inline int64_t inside_tables_offset(int nb, int cs) { return ((int64_t)nb * cs * 4 + 7) & ~(int64_t)7; }
+// LDS of an inside bundle: the charts, then per sentence the forced sum
+// (f64), gradient (f32), id (i32) and score shift (f32), then the room of
+// bundle_extra_bytes.
+__host__ __device__ inline int64_t inside_bundle_bytes(int n, int nb, bool strict) {
+    return inside_tables_offset(nb, inside_layout(n, nb, strict).cs) + 20 * (int64_t)nb + bundle_extra_bytes(n);
 }
 __host__ __device__ inline int64_t cky_split_count(int n) { return (int64_t)n * (n - 1) / 2; }
 // Entry of span (i, i + w), w >= 2, in the split table: all spans of width 2,
@@ -138,7 +207,8 @@ struct Bundle {
 };
 
 // What a bundle's workgroup reads first: one record of rec_stride ints --
-// n, count, split_ws (CKY; -1 for inside), kind (1 inside, 0 CKY), then the
+// n, count, split_ws (CKY) or the strict flag of inside_layout (inside),
+// kind (1 inside, 0 CKY), then the
 // count sentence ids -- so that its sentence ids arrive with its shape, one
 // memory round trip before its scores.
 constexpr int kRecHeader = 4;

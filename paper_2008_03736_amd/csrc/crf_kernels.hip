@@ -191,22 +191,77 @@ struct Bundle_ctx {
     T *chart0;
     int cstride;   // elements between consecutive sentences' charts
     int n, ld, nb;
+    uint32_t mnb;   // div_magic(nb)
+    int e;          // the inside layout's bank exponent (inside_layout); 5 on the workspace
 };
 
-// Where lane `f` of a width-w step works: sentence sb, span start i, lane l
-// of the span's G lanes.  gid / S by multiply-high with magic = 2^32 / S + 1
-// (exact for gid < 2^18, 2 <= S <= 1024); S = 1 (magic would wrap to 0) is
-// the identity.
+__device__ __forceinline__ uint32_t div_magic(int S) { return S > 1 ? 0xFFFFFFFFu / (uint32_t)S + 1u : 0u; }
+
+// Where lane f of a step's region works.  The region's nsp spans are numbered
+// sentence-minor, g = i nb + sb (sentence sb, span start i; g / nb by
+// multiply-high with mnb = 2^32 / nb + 1, exact for g < 2^18, nb <= 1024).
+// Interleaved (IL, for layouts with e = 0), lanes come in blocks of G
+// half-wavefronts holding 32 spans: half h of a block takes spans h, h + G,
+// h + 2G, ..., each span's G lanes side by side, lane l of them taking split
+// positions l, l + G, ...  With the inside layout's chart strides span g's
+// operand runs start sigma g (mod 32) banks apart, so for sigma odd the 32
+// lanes of a half hit 32 distinct banks.  Otherwise (e >= 2, or spans of 32
+// or more lanes) spans lie side by side in lane order.  A lane past the
+// region's spans (act = false) copies span and lane of an active lane of its
+// half, or in a half with none the last span: its loads repeat addresses the
+// half already reads, which costs no bank cycle.
 struct Lane_at {
     int sb, i, l;
+    bool act;
 };
-__device__ __forceinline__ uint32_t div_magic(int S) { return S > 1 ? 0xFFFFFFFFu / (uint32_t)S + 1u : 0u; }
-template <int G>
-__device__ __forceinline__ Lane_at lane_at(int f, int S, uint32_t magic) {
+template <int G, bool IL>
+__device__ __forceinline__ Lane_at lane_at(int f, int nsp, int nb, uint32_t mnb) {
     constexpr int LG = ilog2<G>();
-    const int gid = f >> LG;
-    const int sb = S > 1 ? (int)__umulhi((uint32_t)gid, magic) : gid;
-    return Lane_at{sb, gid - (int)__umul24((uint32_t)sb, (uint32_t)S), f & (G - 1)};
+    constexpr int lq = (IL && G < 32) ? LG : 0;
+    const int l = f & (G - 1);
+    int g;
+    bool act;
+    if constexpr (G >= 32) {   // a span fills one or two halves on its own
+        g = f >> LG;
+        act = g < nsp;
+        if (!act) g = nsp - 1;
+    } else {
+        const int h = (f >> 5) & ((1 << lq) - 1);
+        const int b0 = (f >> (5 + lq)) << (5 + lq - LG);
+        g = b0 + h + (((f & 31) >> LG) << lq);
+        act = g < nsp;
+        if (!act) {
+            const int rem = nsp - b0;
+            g = h < rem ? b0 + h + (((rem - 1 - h) >> lq) << lq) : nsp - 1;
+        }
+    }
+    const int i = nb > 1 ? (int)__umulhi((uint32_t)g, mnb) : g;
+    return Lane_at{g - (int)__umul24((uint32_t)i, (uint32_t)nb), i, l, act};
+}
+// Whether the wavefront whose first lane is f of a region (f a multiple of
+// 64) holds any of its nsp spans.
+template <int G, bool IL>
+__device__ __forceinline__ bool wave_has_span(int f, int nsp) {
+    constexpr int LG = ilog2<G>();
+    constexpr int lq = (IL && G < 32) ? LG : 0;
+    if constexpr (G >= 32) return (f >> LG) < nsp;
+    else return ((f >> (5 + lq)) << (5 + lq - LG)) + ((f >> 5) & ((1 << lq) - 1)) < nsp;
+}
+// The CKY steps number spans sentence-major, g = sb S + i (S spans per
+// sentence, magic = div_magic(S)), G lanes per span side by side.
+template <int G>
+__device__ __forceinline__ Lane_at lane_at_major(int f, int S, uint32_t magic) {
+    constexpr int LG = ilog2<G>();
+    const int g = f >> LG;
+    const int sb = S > 1 ? (int)__umulhi((uint32_t)g, magic) : g;
+    return Lane_at{sb, g - (int)__umul24((uint32_t)sb, (uint32_t)S), f & (G - 1), true};
+}
+// Lanes of a region of nsp spans: whole blocks (32 G lanes interleaved,
+// else 32).
+template <int G, bool IL>
+__device__ __forceinline__ int region_lanes(int nsp) {
+    constexpr int unit = 32 << ((IL && G < 32) ? ilog2<G>() : 0);
+    return (nsp * G + unit - 1) & ~(unit - 1);
 }
 
 // Inside chart layout.  Two ld x ld float32 squares per sentence, P and Q,
@@ -264,11 +319,10 @@ __device__ __forceinline__ float span_lse(const T *a, const T *b, int kl, float 
 // alpha(i,j) = s(i,j) + d + log2 sum_k exp2(alpha(i,k) + alpha(k,j)), d the
 // sentence's score shift (see rescale_chart); the root's own term is not
 // shifted.
-template <int G, int C, int MF, typename T>
-__device__ __forceinline__ void inside_span(const Bundle_ctx<T> &bx, int w, int S, int f, bool act,
-                                            uint32_t magic, const float *dsh) {
+template <int G, int C, int MF, bool IL, typename T>
+__device__ __forceinline__ void inside_span(const Bundle_ctx<T> &bx, int w, int nsp, int f, const float *dsh) {
     const int ld = bx.ld, n = bx.n, K = w - 1;
-    const Lane_at at = lane_at<G>(f, S, magic);
+    const Lane_at at = lane_at<G, IL>(f, nsp, bx.nb, bx.mnb);
     const int i = at.i, l = at.l;
     T *pq = sq_p(bx, at.sb);
     const int rp = (int)__umul24((uint32_t)i, (uint32_t)ld);                   // P row i
@@ -279,7 +333,7 @@ __device__ __forceinline__ void inside_span(const Bundle_ctx<T> &bx, int w, int 
     // An unconditional use keeps the score load in the load block, where it
     // is issued with the operand loads instead of after the reductions.
     asm volatile("" ::"v"(v));
-    if (act && l == 0) {
+    if (at.act && l == 0) {
         pq[pa] = v;
         pq[qa] = v;
     }
@@ -288,11 +342,10 @@ __device__ __forceinline__ void inside_span(const Bundle_ctx<T> &bx, int w, int 
 // One span (i,j) of a width-v outside step: K = n - v parent terms, every
 // operand a parent of width > v or a sibling of width <= n - v, so this step
 // runs beside the inside step of width n - v + 1.
-template <int G, int C, int MF, bool WIDE, typename T>
-__device__ __forceinline__ void outside_span(const Bundle_ctx<T> &bx, int v, int S, int f, bool act,
-                                             uint32_t magic, const float *dsh) {
+template <int G, int C, int MF, bool IL, typename T>
+__device__ __forceinline__ void outside_span(const Bundle_ctx<T> &bx, int v, int nsp, int f, const float *dsh) {
     const int ld = bx.ld, n = bx.n, K = n - v;
-    const Lane_at at = lane_at<G>(f, S, magic);
+    const Lane_at at = lane_at<G, IL>(f, nsp, bx.nb, bx.mnb);
     const int i = at.i, l = at.l;
     T *pq = sq_p(bx, at.sb);
     const int ri = (int)__umul24((uint32_t)i, (uint32_t)ld);
@@ -302,23 +355,23 @@ __device__ __forceinline__ void outside_span(const Bundle_ctx<T> &bx, int v, int
     const float own = pq[po] + dsh[at.sb];
     const float o = span_lse<G, C, MF>(pq + rp + l, pq + rq + v + 1 + l, K - l, own);
     asm volatile("" ::"v"(o));
-    if (act && l == 0) {
+    if (at.act && l == 0) {
         pq[qo] = o;
         pq[po] = o;
     }
 }
 
 // Forward-only width step: every span of width w of every sentence.
-template <int G, int C, int MF, typename T>
-__device__ __forceinline__ void fwd_step(const Bundle_ctx<T> &bx, int w, uint32_t magic, const float *dsh) {
+template <int G, int C, int MF, bool IL, typename T>
+__device__ __forceinline__ void fwd_step(const Bundle_ctx<T> &bx, int w, const float *dsh) {
     const int tid = threadIdx.x, nt = blockDim.x;
-    const int S = bx.n - w + 1;
-    const int total = bx.nb * S * G;
+    const int nsp = bx.nb * (bx.n - w + 1);
+    const int total = region_lanes<G, IL>(nsp);
     const int wq0 = __builtin_amdgcn_readfirstlane(tid & ~63);   // this wavefront's first thread
     for (int f0 = 0; f0 < total; f0 += nt) {
-        if (f0 + wq0 >= total) break;   // no span for this wavefront in this pass or later
-        const bool act = f0 + tid < total;
-        inside_span<G, C, MF>(bx, w, S, act ? f0 + tid : total - 1, act, magic, dsh);
+        const int fw = f0 + wq0;
+        if (fw >= total) break;   // no span for this wavefront in this pass or later
+        if (wave_has_span<G, IL>(fw, nsp)) inside_span<G, C, MF, IL>(bx, w, nsp, f0 + tid, dsh);
     }
 }
 
@@ -326,57 +379,43 @@ __device__ __forceinline__ void fwd_step(const Bundle_ctx<T> &bx, int w, uint32_
 // >= 2), both with K = t terms per span, so one step shape serves both.
 // Inside spans take the first threads, outside spans start at the next
 // wavefront boundary, so every wavefront runs one kind.
-template <int G, int C, int MF, bool WIDE, typename T>
-__device__ __forceinline__ void io_step(const Bundle_ctx<T> &bx, int t, uint32_t mg_in, uint32_t mg_out,
-                                        const float *dsh) {
+template <int G, int C, int MF, bool IL, typename T>
+__device__ __forceinline__ void io_step(const Bundle_ctx<T> &bx, int t, const float *dsh) {
     const int tid = threadIdx.x, nt = blockDim.x;
     const int n = bx.n, w = t + 1, v = n - t;
-    const int s_in = n - t, s_out = v >= 2 ? t + 1 : 0;
-    const int tin = bx.nb * s_in * G, tout = bx.nb * s_out * G;
-    const int obase = (tin + 63) & ~63;
-    const int total = obase + tout;
+    const int nin = bx.nb * (n - t), nout = v >= 2 ? bx.nb * (t + 1) : 0;
+    const int obase = (region_lanes<G, IL>(nin) + 63) & ~63;
+    const int total = obase + region_lanes<G, IL>(nout);
     const int wq0 = __builtin_amdgcn_readfirstlane(tid & ~63);
     for (int f0 = 0; f0 < total; f0 += nt) {
         const int fw = f0 + wq0;
         if (fw >= total) break;
         if (fw < obase) {
-            const bool act = f0 + tid < tin;
-            inside_span<G, C, MF>(bx, w, s_in, act ? f0 + tid : tin - 1, act, mg_in, dsh);
+            if (wave_has_span<G, IL>(fw, nin)) inside_span<G, C, MF, IL>(bx, w, nin, f0 + tid, dsh);
         } else {
-            const int fo = f0 + tid - obase;
-            const bool act = fo < tout;
-            outside_span<G, C, MF, WIDE>(bx, v, s_out, act ? fo : tout - 1, act, mg_out, dsh);
+            if (wave_has_span<G, IL>(fw - obase, nout))
+                outside_span<G, C, MF, IL>(bx, v, nout, f0 + tid - obase, dsh);
         }
     }
 }
 
 // A run of forward widths [w0, w1) sharing one step shape: a tight loop with
-// no dispatch.  magic[S] = div_magic(S) (LDS table), fetched one step ahead
-// (S = n-w+1 stays in [0, n] even one step past the run).
-template <int G, int C, int MF, typename T>
-__device__ __forceinline__ void fwd_run(const Bundle_ctx<T> &bx, int w0, int w1, const uint32_t *magic,
-                                        const float *dsh) {
-    uint32_t mg_cur = magic[bx.n - w0 + 1];
+// no dispatch.
+template <int G, int C, int MF, bool IL, typename T>
+__device__ __forceinline__ void fwd_run(const Bundle_ctx<T> &bx, int w0, int w1, const float *dsh) {
     for (int w = w0; w < w1; ++w) {
-        const uint32_t mg_next = magic[bx.n - w];
-        fwd_step<G, C, MF>(bx, w, mg_cur, dsh);
+        fwd_step<G, C, MF, IL>(bx, w, dsh);
         __syncthreads();
-        mg_cur = mg_next;
     }
 }
 
 // A run of joint steps [t0, t1) sharing one step shape.  Span counts are
 // n - t (inside) and t + 1 (outside), both in [1, n+1].
-template <int G, int C, int MF, bool WIDE, typename T>
-__device__ __forceinline__ void io_run(const Bundle_ctx<T> &bx, int t0, int t1, const uint32_t *magic,
-                                       const float *dsh) {
-    uint32_t mi = magic[bx.n - t0], mo = magic[t0 + 1];
+template <int G, int C, int MF, bool IL, typename T>
+__device__ __forceinline__ void io_run(const Bundle_ctx<T> &bx, int t0, int t1, const float *dsh) {
     for (int t = t0; t < t1; ++t) {
-        const uint32_t mi_next = magic[bx.n - t - 1], mo_next = magic[t + 2];
-        io_step<G, C, MF, WIDE>(bx, t, mi, mo, dsh);
+        io_step<G, C, MF, IL>(bx, t, dsh);
         __syncthreads();
-        mi = mi_next;
-        mo = mo_next;
     }
 }
 
@@ -424,8 +463,9 @@ __device__ __forceinline__ void io_run(const Bundle_ctx<T> &bx, int t0, int t1, 
 // The forward sweep alone: widths 2..n, one dispatch per run of widths
 // sharing a step shape.
 // WIDE: workspace charts (longer sentences), which may need 16 terms per lane.
-template <bool WIDE, typename T>
-__device__ __forceinline__ void fwd_sweep(const Bundle_ctx<T> &bx, const uint32_t *magic, const float *dsh) {
+// IL: interleaved span numbering (lane_at).
+template <bool WIDE, bool IL, typename T>
+__device__ __forceinline__ void fwd_sweep(const Bundle_ctx<T> &bx, const float *dsh) {
     const int n = bx.n;
     int w = 2;
     while (w <= n) {
@@ -436,7 +476,7 @@ __device__ __forceinline__ void fwd_sweep(const Bundle_ctx<T> &bx, const uint32_
             if (s2.G != sh.G || s2.C != sh.C) break;
             ++w2;
         }
-#define CRF_FWD_RUN(GG, CC, MM) fwd_run<GG, CC, MM>(bx, w, w2, magic, dsh)
+#define CRF_FWD_RUN(GG, CC, MM) fwd_run<GG, CC, MM, IL>(bx, w, w2, dsh)
         CRF_DISPATCH_SHAPE(sh, CRF_FWD_RUN);
 #undef CRF_FWD_RUN
         w = w2;
@@ -536,8 +576,8 @@ __device__ void rescale_chart(const Bundle_ctx<T> &bx, int t0, float *dsh) {
 // The joint sweep: steps t = 1..n-1 (inside widths 2..n, outside widths
 // n-1..2), one dispatch per run of steps sharing a step shape; the runs are
 // cut after step t0 for the rescale (t0 = 0: none).
-template <bool WIDE, typename T>
-__device__ __forceinline__ void io_sweep(const Bundle_ctx<T> &bx, const uint32_t *magic, float *dsh, int t0) {
+template <bool WIDE, bool IL, typename T>
+__device__ __forceinline__ void io_sweep(const Bundle_ctx<T> &bx, float *dsh, int t0) {
     const int n = bx.n;
     int t = 1;
     while (t <= n - 1) {
@@ -548,7 +588,7 @@ __device__ __forceinline__ void io_sweep(const Bundle_ctx<T> &bx, const uint32_t
             if (s2.G != sh.G || s2.C != sh.C) break;
             ++t2;
         }
-#define CRF_IO_RUN(GG, CC, MM) io_run<GG, CC, MM, WIDE>(bx, t, t2, magic, dsh)
+#define CRF_IO_RUN(GG, CC, MM) io_run<GG, CC, MM, IL>(bx, t, t2, dsh)
         CRF_DISPATCH_SHAPE(sh, CRF_IO_RUN);
 #undef CRF_IO_RUN
         if (t2 - 1 == t0) rescale_chart(bx, t0, dsh);
@@ -640,8 +680,9 @@ __device__ __forceinline__ float label_lse2(const float *s, int L) {
 // sentence with its chart in the workspace).
 //   REV: also compute the marginals (joint inside/outside sweep) and write them.
 //   LAB: labelled scores [B][N1][N1][L].
-// Dynamic LDS (bundled): nb charts, then nb x {forced (f64), grad (f32),
-// id (i32), shift (f32)}, then the magic table.
+// Dynamic LDS (bundled): nb charts (chart stride from inside_layout), then
+// nb x {forced (f64), grad (f32), id (i32), shift (f32)}, then the room
+// bundle_extra_bytes gives every bundle.
 // Chart of a sentence: the rotated squares P and Q of the inside chart
 // layout (ld x ld floats each).
 template <bool REV, bool LAB, bool SPILL>
@@ -653,7 +694,6 @@ __device__ __forceinline__ void inside_block(const KernelPlan &p, int block, con
     __shared__ float spill_gv[1];
     __shared__ int spill_id[1];
     __shared__ float spill_dsh[1];
-    __shared__ uint32_t spill_magic[SPILL ? CRF_MAX_LEN + 2 : 1];
     const int NT = blockDim.x, NW = NT >> 6;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int N1 = p.n1, L = p.L;
@@ -664,18 +704,19 @@ __device__ __forceinline__ void inside_block(const KernelPlan &p, int block, con
     double *forced;
     float *gv, *dsh;
     int *sid;
-    uint32_t *magic;
+    InsideLayout lay;
     if constexpr (SPILL) {
         const int b = p.inside.order_spill[block];
         n = p.len[b];
         nb = 1;
         chart0 = reinterpret_cast<float *>(p.ws + p.inside.ws_off[block]);
+        lay = inside_layout(n, 1, true);
+        lay.e = 5;   // a workspace chart: no banks, spans side by side
         cstride = 0;
         forced = spill_forced;
         gv = spill_gv;
         sid = spill_id;
         dsh = spill_dsh;
-        magic = spill_magic;
         if (tid == 0) sid[0] = b;
     } else {
         // the record's ids are fetched with its header (a bundle holds at
@@ -683,18 +724,17 @@ __device__ __forceinline__ void inside_block(const KernelPlan &p, int block, con
         const int id0 = tid < p.rec_stride - kRecHeader ? rec[kRecHeader + tid] : 0;
         n = rec[0];
         nb = rec[1];
+        lay = inside_layout(n, nb, rec[2] != 0);
         chart0 = reinterpret_cast<float *>(smem_raw);
-        cstride = (int)(inside_chart_bytes(n) / 4);
-        forced = reinterpret_cast<double *>(smem_raw + (size_t)nb * inside_chart_bytes(n));
+        cstride = lay.cs;
+        forced = reinterpret_cast<double *>(smem_raw + inside_tables_offset(nb, lay.cs));
         gv = reinterpret_cast<float *>(forced + nb);
         sid = reinterpret_cast<int *>(gv + nb);
         dsh = reinterpret_cast<float *>(sid + nb);
-        magic = reinterpret_cast<uint32_t *>(dsh + nb);
         if (tid < nb) sid[tid] = id0;
     }
-    for (int S = tid; S <= n + 1; S += NT) magic[S] = div_magic(S);
-    const int ld = inside_ld(n);
-    const Bundle_ctx<float> bx{chart0, cstride, n, ld, nb};
+    const int ld = lay.ld;
+    const Bundle_ctx<float> bx{chart0, cstride, n, ld, nb, div_magic(nb), lay.e};
     __syncthreads();
     for (int t = tid; t < nb; t += NT) {
         gv[t] = grad ? grad[sid[t]] : 1.0f;
@@ -749,12 +789,19 @@ __device__ __forceinline__ void inside_block(const KernelPlan &p, int block, con
         if (lane == 0) forced[sb] = acc;
     }
 
+    // Workspace charts lay spans side by side; LDS charts interleave them
+    // when their layout allows (e = 0).
     if constexpr (!REV) {
-        fwd_sweep<SPILL>(bx, magic, dsh);
+        if constexpr (SPILL) fwd_sweep<true, false>(bx, dsh);
+        else if (lay.e == 0) fwd_sweep<false, true>(bx, dsh);
+        else fwd_sweep<false, false>(bx, dsh);
     } else {
         // The rescale needs a few widths of alpha to estimate the growth;
         // short sentences keep small magnitudes and skip it.
-        io_sweep<SPILL>(bx, magic, dsh, n >= 8 ? n / 4 : 0);
+        const int t0 = n >= 8 ? n / 4 : 0;
+        if constexpr (SPILL) io_sweep<true, false>(bx, dsh, t0);
+        else if (lay.e == 0) io_sweep<false, true>(bx, dsh, t0);
+        else io_sweep<false, false>(bx, dsh, t0);
     }
     // log Z = (alpha~(0,n) - (n-2) d) ln 2 + forced sum.
     if (logZ != nullptr)
@@ -861,7 +908,7 @@ __device__ __forceinline__ void cky_step(const Cky_ctx<SP> &cx, int w, uint32_t 
     for (int f0 = 0; f0 < total; f0 += nt) {
         if (f0 + wq0 >= total) break;
         const bool act = f0 + tid < total;
-        const Lane_at at = lane_at<G>(act ? f0 + tid : total - 1, S, magic);
+        const Lane_at at = lane_at_major<G>(act ? f0 + tid : total - 1, S, magic);
         const int i = at.i, l = at.l;
         double *be = cx.beta(at.sb);
         // every index from the diagonal cell [i][i] and the uniform w * ld

@@ -134,12 +134,17 @@ double simulate_launch(const std::vector<double> &dur, int n_part, int slots, st
 // predicted makespan, the multi-sentence bundle that ends last is split in
 // two (the halves keep their sentences' slots of the order array), which
 // trades a little more total work for a shorter end of the launch.  Both
-// bundle lists come back in launch order.
+// bundle lists come back in launch order.  fits(inside, n, count) says
+// whether a bundle of that shape fits the launch's LDS; a split takes the
+// count nearest to half whose two parts both fit, and a bundle with no such
+// count stays whole.
+template <typename FIT>
 void plan_fused_launch(std::vector<crf::Bundle> &in, std::vector<crf::Bundle> &ck, int n_part, int slots,
-                       std::vector<int32_t> &mix) {
+                       std::vector<int32_t> &mix, FIT &&fits) {
     struct Item {
         double d;
         bool inside;
+        bool whole;   // no split of it fits
         crf::Bundle bd;
     };
     auto predict = [](const Item &x) {
@@ -147,8 +152,8 @@ void plan_fused_launch(std::vector<crf::Bundle> &in, std::vector<crf::Bundle> &c
     };
     std::vector<Item> items;
     items.reserve(2 * (in.size() + ck.size()));
-    for (const crf::Bundle &b : in) items.push_back({0.0, true, b});
-    for (const crf::Bundle &b : ck) items.push_back({0.0, false, b});
+    for (const crf::Bundle &b : in) items.push_back({0.0, true, false, b});
+    for (const crf::Bundle &b : ck) items.push_back({0.0, false, false, b});
     for (Item &x : items) x.d = predict(x);
     auto longer = [](const Item &a, const Item &b) { return a.d > b.d; };
     std::stable_sort(items.begin(), items.end(), longer);
@@ -165,10 +170,20 @@ void plan_fused_launch(std::vector<crf::Bundle> &in, std::vector<crf::Bundle> &c
     for (int it = 0, stale = 0; it < max_iter && stale < 64; ++it) {
         int j = -1;
         for (int i = 0; i < (int)items.size(); ++i)
-            if (items[i].bd.count >= 2 && (j < 0 || ends[i] > ends[j])) j = i;
+            if (items[i].bd.count >= 2 && !items[i].whole && (j < 0 || ends[i] > ends[j])) j = i;
         if (j < 0) break;
+        const int c = items[j].bd.count, n = items[j].bd.n;
+        const bool kind = items[j].inside;
+        int half = 0;
+        for (int d = 0; d <= 3 && half == 0; ++d)
+            for (int h : {c / 2 - d, c / 2 + d})
+                if (half == 0 && h >= 1 && h < c && fits(kind, n, h) && fits(kind, n, c - h)) half = h;
+        if (half == 0) {
+            items[j].whole = true;
+            continue;
+        }
         Item a = items[j], b = items[j];
-        a.bd.count = items[j].bd.count / 2;
+        a.bd.count = half;
         b.bd.first += a.bd.count;
         b.bd.count -= a.bd.count;
         a.d = predict(a);
@@ -205,19 +220,18 @@ void plan_fused_launch(std::vector<crf::Bundle> &in, std::vector<crf::Bundle> &c
 // mixed batch than an even share; CKY bundles take the share.
 constexpr double kInsideTargetScale = 2.0, kCkyTargetScale = 1.0;
 
-// `order` is sorted by decreasing length.  `chart(n)` is the LDS a bundled
-// sentence needs besides `per_sentence` bytes of tables, `spill_chart(n)` its
-// workspace chart, and `tail(n, count)` the bytes a bundle adds at its end.
-template <typename F, typename FS, typename TF>
+// `order` is sorted by decreasing length.  `bundle_bytes(n, count)` is the
+// LDS of a bundle of `count` sentences of n words, `spill_chart(n)` a
+// sentence's workspace chart.  A bundle's LDS need not grow with its count
+// (the inside chart stride depends on the count's factors of two), so a
+// length's bundles hold at most the largest count below which every count
+// fits.
+template <typename BB, typename FS>
 HostSchedule make_schedule(const std::vector<int32_t> &order, const int32_t *len, int lds_cap,
-                           bool force_spill, int64_t ws_base, int per_sentence, F chart,
-                           FS spill_chart, TF tail, double target_scale) {
+                           bool force_spill, int64_t ws_base, BB &&bundle_bytes, FS &&spill_chart,
+                           double target_scale) {
     HostSchedule s;
     s.threads = crf::kThreadsDefault;
-    // LDS of a bundle of `count` sentences of length n.
-    auto bundle_bytes = [&](int n, int64_t count) {
-        return count * (chart(n) + per_sentence) + crf::bundle_extra_bytes(n) + tail(n, count);
-    };
     // Workgroup LDS budget: half the CU when every eligible sentence fits in
     // half (two workgroups per CU), else all of it (one).
     const int64_t half = lds_cap / 2 - crf::kReservedLds, full = lds_cap - crf::kReservedLds;
@@ -345,13 +359,21 @@ int crf_plan_create(crf_plan **out, const int32_t *lengths_host, int32_t batch, 
                      [&](int32_t a, int32_t b) { return lengths_host[a] > lengths_host[b]; });
 
     const bool force = (flags & CRF_FORCE_SPILL) != 0;
-    auto inside_bytes = [](int n) { return crf::inside_chart_bytes(n); };
+    // Inside bundles take the strict chart layout when it fits in half a CU,
+    // else the loose one (inside_layout).
+    const int64_t half_cu = lds_cap / 2 - crf::kReservedLds;
+    auto inside_strict = [=](int n, int64_t count) {
+        return crf::inside_bundle_bytes(n, (int)count, true) <= half_cu;
+    };
+    auto inside_bundle_bytes = [=](int n, int64_t count) {
+        return crf::inside_bundle_bytes(n, (int)count, inside_strict(n, count));
+    };
+    auto inside_spill_bytes = [](int n) { return 4 * (int64_t)crf::inside_layout(n, 1, true).cs; };
     auto cky_spill_bytes = [](int n) { return crf::cky_chart_bytes(n, 2); };
     // The CKY bundle's tail: the tree-walk scratch, padded so that the last
     // chart's masked reads (into the id, magic and scratch tables behind it)
     // stay inside the bundle.
     constexpr int nwaves = crf::kThreadsDefault / 64;
-    auto no_tail = [](int, int64_t) { return (int64_t)0; };
     auto cky_tail = [](int n, int64_t count) {
         const int64_t walk = crf::cky_walk_bytes(n, count, nwaves);
         const int64_t tables = 4 * count + crf::bundle_extra_bytes(n) + walk;
@@ -360,16 +382,19 @@ int crf_plan_create(crf_plan **out, const int32_t *lengths_host, int32_t batch, 
     // A sentence's split table sits in LDS after its chart when a bundle of
     // one such sentence still fits in half the CU; longer sentences keep it
     // in the workspace.
-    const int64_t half_cu = lds_cap / 2 - crf::kReservedLds;
     auto split_in_lds = [=](int n) {
         return crf::cky_chart_bytes(n, 1) + 4 + crf::bundle_extra_bytes(n) + cky_tail(n, 1) <= half_cu;
     };
-    auto cky_bytes = [=](int n) { return crf::cky_chart_bytes(n, split_in_lds(n) ? 1 : 0); };
-    // inside tables: forced sum (f64), gradient (f32), id (i32), score shift (f32); cky: id
-    HostSchedule si = make_schedule(order, lengths_host, lds_cap, force, 0, 20, +inside_bytes,
-                                    +inside_bytes, +no_tail, kInsideTargetScale);
-    HostSchedule sc = make_schedule(order, lengths_host, lds_cap, force, si.ws_bytes, 4, cky_bytes,
-                                    +cky_spill_bytes, cky_tail, kCkyTargetScale);
+    // CKY bundle: the charts (with their split tables when they fit), the
+    // ids (i32), the magic table, the tail.
+    auto cky_bundle_bytes = [=](int n, int64_t count) {
+        return count * (crf::cky_chart_bytes(n, split_in_lds(n) ? 1 : 0) + 4) + crf::bundle_extra_bytes(n) +
+               cky_tail(n, count);
+    };
+    HostSchedule si = make_schedule(order, lengths_host, lds_cap, force, 0, inside_bundle_bytes,
+                                    inside_spill_bytes, kInsideTargetScale);
+    HostSchedule sc = make_schedule(order, lengths_host, lds_cap, force, si.ws_bytes, cky_bundle_bytes,
+                                    cky_spill_bytes, kCkyTargetScale);
     int64_t split_cursor = si.ws_bytes + sc.ws_bytes;
     for (crf::Bundle &bd : sc.bundles) {
         if (split_in_lds(bd.n)) continue;
@@ -395,7 +420,10 @@ int crf_plan_create(crf_plan **out, const int32_t *lengths_host, int32_t batch, 
             cus = 256;
         const int per_cu = std::min(4, std::max(1, (int)(lds_cap / std::max(si.lds_bytes, sc.lds_bytes))));
         fused_slots = cus * per_cu;
-        plan_fused_launch(si.bundles, sc.bundles, 1, fused_slots, mix);
+        auto fits = [&](bool inside, int n, int count) {
+            return inside ? inside_bundle_bytes(n, count) <= si.lds_bytes : cky_bundle_bytes(n, count) <= sc.lds_bytes;
+        };
+        plan_fused_launch(si.bundles, sc.bundles, 1, fused_slots, mix, fits);
     }
     kp.n_mix = (int32_t)mix.size();
     kp.fused_grid = std::min<int32_t>(kp.n_mix, fused_slots);
@@ -412,7 +440,7 @@ int crf_plan_create(crf_plan **out, const int32_t *lengths_host, int32_t batch, 
             int32_t *q = r.data() + b * stride;
             q[0] = bd.n;
             q[1] = bd.count;
-            q[2] = inside ? -1 : bd.split_ws;
+            q[2] = inside ? (inside_strict(bd.n, bd.count) ? 1 : 0) : bd.split_ws;
             q[3] = inside ? 1 : 0;
             for (int t = 0; t < bd.count; ++t) q[crf::kRecHeader + t] = h.order[bd.first + t];
         }

@@ -251,6 +251,18 @@ def test_many_short_sentences(torch):
     full_check(torch, b)
 
 
+@pytest.mark.parametrize("n,count", [(9, 4), (12, 33), (14, 16), (14, 40), (17, 32), (20, 20), (22, 8),
+                                     (30, 8), (45, 4), (56, 3), (98, 1)])
+def test_bundle_counts_and_chart_strides(torch, n, count):
+    # `count` sentences of n words, which the plan puts in one bundle when the
+    # batch's total work is large (the 99-word sentences make it so), with
+    # counts of various factors of two: the inside chart strides depend on
+    # both (strict and loose layouts, spans interleaved across half-wavefronts
+    # or side by side, rows changing inside a half).
+    b = W.custom([n] * count + [99] * 200, seed=100 + n + count, sd=2.0)
+    full_check(torch, b)
+
+
 def test_longest_sentence(torch):
     # the longest sentence the library accepts, on the workspace kernels
     b = W.custom([1023], seed=23, sd=1.0)
