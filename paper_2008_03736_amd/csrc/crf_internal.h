@@ -22,12 +22,11 @@ constexpr int kThreadsMax = 1024;
 constexpr int kMaxBundle = 256;
 static_assert(kMaxBundle <= kThreadsDefault, "one sentence id per thread");
 
-// LDS a bundle needs besides its charts and per-sentence tables: for CKY a
-// uint32 table of division magics for span counts 0..n+1; the inside keeps
-// the same room unused.  Masked tail loads of the last chart of a bundle
-// reach past it, into the tables that follow it: up to masked_reach(n)
-// float32 (inside, whose tables and this room always cover that) or float64
-// (CKY, whose tail the plan pads to that size).
+// LDS a bundle keeps besides its charts and per-sentence tables: n + 2
+// words of room.  Masked tail loads of the last chart of a bundle reach
+// past it, into the tables that follow it: up to masked_reach(n) float32
+// (inside, whose tables and this room always cover that) or float64 (CKY,
+// whose tail the plan pads to that size).
 __host__ __device__ inline int64_t bundle_extra_bytes(int n) { return 4 * (int64_t)(n + 2); }
 
 // LDS a workgroup holds besides its bundle (the fused kernel's claim slot)
@@ -109,8 +108,8 @@ __host__ __device__ inline InsideLayout inside_layout(int n, int nb, bool strict
     }
     return InsideLayout{ld, sq2 + pad, e};
 }
-// Row stride of the float64 CKY chart: even, which makes the diagonal stride
-// ld + 1 odd and its 8-byte accesses conflict-free.
+// Row stride of a float64 CKY chart on the workspace, and of a loose one
+// in LDS: even, which makes the diagonal stride ld + 1 odd.
 __host__ __device__ inline int cky_ld(int n) { return (n + 1) + ((n + 1) & 1); }
 
 // Bytes of chart per sentence.
@@ -125,6 +124,50 @@ __host__ __device__ inline int cky_ld(int n) { return (n + 1) + ((n + 1) & 1); }
 //           k - i - 1 in split_bytes bytes (1 for n <= kMaxLenInLds, 2 in
 //           the workspace).  A bundle whose tables do not fit in LDS beside
 //           its charts keeps them in the workspace (Bundle::split_ws).
+__host__ __device__ inline int64_t cky_split_bytes_of(int n, int split_bytes) {
+    return ((int64_t)n * (n - 1) / 2 * split_bytes + 7) / 8 * 8;
+}
+// CKY chart geometry of a bundle in LDS: row stride ld, chart stride cs
+// (bytes, the chart and its split table, if in LDS, padded), and e as for
+// the inside.  8-byte reads are served 16 lanes at a time over 16 bank
+// pairs.  A step's spans are numbered sentence-minor, g = i nb + sb, and
+// span g's two operand runs start at sb cs/8 + i (ld + 1) doubles (plus an
+// offset uniform over the step): with cs/8 = sigma and ld + 1 = nb sigma
+// (mod 16) that is sigma g (mod 16), and sigma odd with the spans
+// interleaved over the G 16-lane groups of a block keeps every group on 16
+// distinct bank pairs.  Strict: the smallest ld whose ld + 1 has nb's power
+// of two, the odd sigma needing the least padding.  Loose (where the strict
+// layout does not fit in half a CU, and bundles of 16 or more sentences
+// whose count has a factor 4): ld even, sigma odd, spans still interleaved
+// (a bank model of such bundles: 1.7x the conflict-free read cycles, 1.8x
+// side by side).
+struct CkyLayout {
+    int ld, cs, e;
+};
+__host__ __device__ inline int pow2_mod16(int x) { return pow2_mod32(x & 15) >= 4 ? 4 : pow2_mod32(x & 15); }
+__host__ __device__ inline CkyLayout cky_layout(int n, int nb, int split_bytes, bool strict) {
+    const int bn = pow2_mod16(nb);
+    const int64_t split = cky_split_bytes_of(n, split_bytes);
+    if (!strict || (nb >= 16 && bn >= 2)) {
+        const int ld = cky_ld(n);
+        const int64_t u = ((int64_t)ld * ld * 8 + split) / 8;
+        return CkyLayout{ld, (int)(8 * (u + ((u & 1) ^ 1))), 0};
+    }
+    int ld = n + 1;
+    while (pow2_mod16(ld + 1) != bn) ++ld;
+    const int64_t u = ((int64_t)ld * ld * 8 + split) / 8;
+    int pad = (int)((1 - u) & 15), e = 0;
+    const int bl = pow2_mod16(ld + 1);
+    if (bn < 4) {
+        // nb sigma = ld + 1 (mod 16): 2^b solutions; the least padding
+        const int step = 16 >> bn;
+        const int s0 = (((ld + 1) >> bn) * inverse_mod32(nb >> bn)) & (step - 1);
+        pad = 16;
+        for (int sg = s0; sg < 16; sg += step) pad = (int)((sg - u) & 15) < pad ? (int)((sg - u) & 15) : pad;
+        e = bl - bn;
+    }
+    return CkyLayout{ld, (int)(8 * (u + pad)), e};
+}
 // Byte offset of an inside bundle's per-sentence tables (the first holds
 // float64): its charts, rounded up to 8 bytes (the chart stride may be odd).
 __host__ __device__ inline int64_t inside_tables_offset(int nb, int cs) { return ((int64_t)nb * cs * 4 + 7) & ~(int64_t)7; }
@@ -142,7 +185,7 @@ __host__ __device__ inline int cky_split_index(int n, int w, int i) {
 }
 __host__ __device__ inline int64_t cky_chart_bytes(int n, int split_bytes) {
     const int64_t ld = cky_ld(n);
-    return ld * ld * 8 + (cky_split_count(n) * split_bytes + 7) / 8 * 8;
+    return ld * ld * 8 + cky_split_bytes_of(n, split_bytes);
 }
 // The CKY tree walk follows the split table.  Bundles of fewer than
 // kDfsMinBundle sentences walk breadth first, one wavefront per sentence,
@@ -207,11 +250,11 @@ struct Bundle {
 };
 
 // What a bundle's workgroup reads first: one record of rec_stride ints --
-// n, count, split_ws (CKY) or the strict flag of inside_layout (inside),
-// kind (1 inside, 0 CKY), then the
+// n, count, split_ws (CKY; -1 for inside), kind (1 inside, 0 CKY), the
+// strict flag of its chart layout (inside_layout, cky_layout), then the
 // count sentence ids -- so that its sentence ids arrive with its shape, one
 // memory round trip before its scores.
-constexpr int kRecHeader = 4;
+constexpr int kRecHeader = 5;
 
 // Which sentences run in LDS (in bundles) and which on the workspace kernel,
 // for one kind of chart.  Bundles and spilled sentences are ordered most

@@ -200,35 +200,43 @@ __device__ __forceinline__ uint32_t div_magic(int S) { return S > 1 ? 0xFFFFFFFF
 // Where lane f of a step's region works.  The region's nsp spans are numbered
 // sentence-minor, g = i nb + sb (sentence sb, span start i; g / nb by
 // multiply-high with mnb = 2^32 / nb + 1, exact for g < 2^18, nb <= 1024).
-// Interleaved (IL, for layouts with e = 0), lanes come in blocks of G
-// half-wavefronts holding 32 spans: half h of a block takes spans h, h + G,
-// h + 2G, ..., each span's G lanes side by side, lane l of them taking split
-// positions l, l + G, ...  With the inside layout's chart strides span g's
-// operand runs start sigma g (mod 32) banks apart, so for sigma odd the 32
-// lanes of a half hit 32 distinct banks.  Otherwise (e >= 2, or spans of 32
-// or more lanes) spans lie side by side in lane order.  A lane past the
-// region's spans (act = false) copies span and lane of an active lane of its
-// half, or in a half with none the last span: its loads repeat addresses the
-// half already reads, which costs no bank cycle.
+// LDS serves a wavefront's accesses in groups of HW lanes (32 for 4-byte
+// words, 16 for 8-byte ones), each over 32 banks.  Interleaved (IL, for
+// layouts with e = 0), lanes come in blocks of G groups holding HW spans:
+// group h of a block takes spans h, h + G, h + 2G, ..., each span's G lanes
+// side by side, lane l of them taking split positions l, l + G, ...  With
+// the chart layouts' strides span g's operand runs start sigma g banks (or
+// bank pairs) apart, modulo the group's bank count, so for sigma odd the
+// HW lanes of a group hit distinct banks.  Otherwise (e > 0, or spans of a
+// whole group or more) spans lie side by side in lane order.  A lane past
+// the region's spans (act = false) copies span and lane of an active lane
+// of its group, or in a group with none the last span: its loads repeat
+// addresses the group already reads, which costs no bank cycle.
 struct Lane_at {
     int sb, i, l;
     bool act;
 };
-template <int G, bool IL>
+template <int G, bool IL, int HW>
+struct Lane_map {
+    static constexpr int LG = ilog2<G>(), LH = ilog2<HW>();
+    static constexpr int lq = (IL && G < HW) ? LG : 0;   // log2 of the groups per block
+    static constexpr int unit = HW << lq;                // lanes per block
+};
+template <int G, bool IL, int HW = 32>
 __device__ __forceinline__ Lane_at lane_at(int f, int nsp, int nb, uint32_t mnb) {
-    constexpr int LG = ilog2<G>();
-    constexpr int lq = (IL && G < 32) ? LG : 0;
+    using M = Lane_map<G, IL, HW>;
+    constexpr int LG = M::LG, LH = M::LH, lq = M::lq;
     const int l = f & (G - 1);
     int g;
     bool act;
-    if constexpr (G >= 32) {   // a span fills one or two halves on its own
+    if constexpr (G >= HW) {   // a span fills one or more groups on its own
         g = f >> LG;
         act = g < nsp;
         if (!act) g = nsp - 1;
     } else {
-        const int h = (f >> 5) & ((1 << lq) - 1);
-        const int b0 = (f >> (5 + lq)) << (5 + lq - LG);
-        g = b0 + h + (((f & 31) >> LG) << lq);
+        const int h = (f >> LH) & ((1 << lq) - 1);
+        const int b0 = (f >> (LH + lq)) << (LH + lq - LG);
+        g = b0 + h + (((f & (HW - 1)) >> LG) << lq);
         act = g < nsp;
         if (!act) {
             const int rem = nsp - b0;
@@ -239,28 +247,18 @@ __device__ __forceinline__ Lane_at lane_at(int f, int nsp, int nb, uint32_t mnb)
     return Lane_at{g - (int)__umul24((uint32_t)i, (uint32_t)nb), i, l, act};
 }
 // Whether the wavefront whose first lane is f of a region (f a multiple of
-// 64) holds any of its nsp spans.
-template <int G, bool IL>
+// 64) holds any of its nsp spans (its first group's first span).
+template <int G, bool IL, int HW = 32>
 __device__ __forceinline__ bool wave_has_span(int f, int nsp) {
-    constexpr int LG = ilog2<G>();
-    constexpr int lq = (IL && G < 32) ? LG : 0;
-    if constexpr (G >= 32) return (f >> LG) < nsp;
-    else return ((f >> (5 + lq)) << (5 + lq - LG)) + ((f >> 5) & ((1 << lq) - 1)) < nsp;
+    using M = Lane_map<G, IL, HW>;
+    constexpr int LG = M::LG, LH = M::LH, lq = M::lq;
+    if constexpr (G >= HW) return (f >> LG) < nsp;
+    else return ((f >> (LH + lq)) << (LH + lq - LG)) + ((f >> LH) & ((1 << lq) - 1)) < nsp;
 }
-// The CKY steps number spans sentence-major, g = sb S + i (S spans per
-// sentence, magic = div_magic(S)), G lanes per span side by side.
-template <int G>
-__device__ __forceinline__ Lane_at lane_at_major(int f, int S, uint32_t magic) {
-    constexpr int LG = ilog2<G>();
-    const int g = f >> LG;
-    const int sb = S > 1 ? (int)__umulhi((uint32_t)g, magic) : g;
-    return Lane_at{sb, g - (int)__umul24((uint32_t)sb, (uint32_t)S), f & (G - 1), true};
-}
-// Lanes of a region of nsp spans: whole blocks (32 G lanes interleaved,
-// else 32).
-template <int G, bool IL>
+// Lanes of a region of nsp spans: whole blocks.
+template <int G, bool IL, int HW = 32>
 __device__ __forceinline__ int region_lanes(int nsp) {
-    constexpr int unit = 32 << ((IL && G < 32) ? ilog2<G>() : 0);
+    constexpr int unit = Lane_map<G, IL, HW>::unit;
     return (nsp * G + unit - 1) & ~(unit - 1);
 }
 
@@ -724,7 +722,7 @@ __device__ __forceinline__ void inside_block(const KernelPlan &p, int block, con
         const int id0 = tid < p.rec_stride - kRecHeader ? rec[kRecHeader + tid] : 0;
         n = rec[0];
         nb = rec[1];
-        lay = inside_layout(n, nb, rec[2] != 0);
+        lay = inside_layout(n, nb, rec[4] != 0);
         chart0 = reinterpret_cast<float *>(smem_raw);
         cstride = lay.cs;
         forced = reinterpret_cast<double *>(smem_raw + inside_tables_offset(nb, lay.cs));
@@ -846,6 +844,7 @@ struct Cky_ctx {
     char *split0;
     int sstride;   // bytes between consecutive sentences' split tables
     int n, ld, nb;
+    uint32_t mnb;     // div_magic(nb)
     bool split_lds;   // split tables in LDS (else in global memory)
     __device__ double *beta(int sb) const {
         return reinterpret_cast<double *>(chart0 + (size_t)sb * cstride);
@@ -898,17 +897,17 @@ __device__ __forceinline__ Arg_max tree_arg_max(const double *x, int c0, int G) 
 // sp0 + i).  Each lane keeps its running max and the first of its terms to
 // reach it; the group then takes the lowest split among its lanes at the
 // group's max.
-template <int G, int C, int MF, typename SP>
-__device__ __forceinline__ void cky_step(const Cky_ctx<SP> &cx, int w, uint32_t magic, int sp0) {
+template <int G, int C, int MF, bool IL, typename SP>
+__device__ __forceinline__ void cky_step(const Cky_ctx<SP> &cx, int w, int sp0) {
     const int tid = threadIdx.x, nt = blockDim.x;
     const int n = cx.n, ld = cx.ld;
-    const int K = w - 1, S = n - w + 1;
-    const int total = cx.nb * S * G;
+    const int K = w - 1, nsp = cx.nb * (n - w + 1);
+    const int total = region_lanes<G, IL, 16>(nsp);
     const int wq0 = __builtin_amdgcn_readfirstlane(tid & ~63);
     for (int f0 = 0; f0 < total; f0 += nt) {
         if (f0 + wq0 >= total) break;
-        const bool act = f0 + tid < total;
-        const Lane_at at = lane_at_major<G>(act ? f0 + tid : total - 1, S, magic);
+        if (!wave_has_span<G, IL, 16>(f0 + wq0, nsp)) continue;
+        const Lane_at at = lane_at<G, IL, 16>(f0 + tid, nsp, cx.nb, cx.mnb);
         const int i = at.i, l = at.l;
         double *be = cx.beta(at.sb);
         // every index from the diagonal cell [i][i] and the uniform w * ld
@@ -958,7 +957,7 @@ __device__ __forceinline__ void cky_step(const Cky_ctx<SP> &cx, int w, uint32_t 
         const int kb = min(grp_min_i<G>(m == mg ? kc + l : 0x7fffffff), K - 1);
         const double v = mg + sij;
         asm volatile("" ::"v"(v));   // keeps the score load with the operand loads
-        if (act && l == 0) {
+        if (at.act && l == 0) {
             be[rb + w] = v;
             be[cb] = v;
             cx.put_split(at.sb, sp0 + i, kb);
@@ -966,19 +965,16 @@ __device__ __forceinline__ void cky_step(const Cky_ctx<SP> &cx, int w, uint32_t 
     }
 }
 
-template <int G, int C, int MF, typename SP>
-__device__ __forceinline__ void cky_run(const Cky_ctx<SP> &cx, int w0, int w1, const uint32_t *magic) {
-    uint32_t mg_cur = magic[cx.n - w0 + 1];
+template <int G, int C, int MF, bool IL, typename SP>
+__device__ __forceinline__ void cky_run(const Cky_ctx<SP> &cx, int w0, int w1) {
     for (int w = w0; w < w1; ++w) {
-        const uint32_t mg_next = magic[cx.n - w];   // S of width w+1 (>= 0)
-        cky_step<G, C, MF>(cx, w, mg_cur, cky_split_index(cx.n, w, 0));
+        cky_step<G, C, MF, IL>(cx, w, cky_split_index(cx.n, w, 0));
         __syncthreads();
-        mg_cur = mg_next;
     }
 }
 
-template <bool WIDE, typename SP>
-__device__ __forceinline__ void cky_sweep(const Cky_ctx<SP> &cx, const uint32_t *magic) {
+template <bool WIDE, bool IL, typename SP>
+__device__ __forceinline__ void cky_sweep(const Cky_ctx<SP> &cx) {
     const int n = cx.n;
     int w = 2;
     while (w <= n) {
@@ -989,7 +985,7 @@ __device__ __forceinline__ void cky_sweep(const Cky_ctx<SP> &cx, const uint32_t 
             if (s2.G != sh.G || s2.C != sh.C) break;
             ++w2;
         }
-#define CRF_CKY_RUN(GG, CC, MM) cky_run<GG, CC, MM>(cx, w, w2, magic)
+#define CRF_CKY_RUN(GG, CC, MM) cky_run<GG, CC, MM, IL>(cx, w, w2)
         CRF_DISPATCH_SHAPE(sh, CRF_CKY_RUN);
 #undef CRF_CKY_RUN
         w = w2;
@@ -1099,28 +1095,27 @@ __device__ __forceinline__ void cky_block(const KernelPlan &p, int block, const 
                                           const float *__restrict__ scores,
                                           int32_t *__restrict__ spans, float *__restrict__ best) {
     __shared__ int spill_id[1];
-    __shared__ uint32_t spill_magic[SPILL ? CRF_MAX_LEN + 2 : 1];
     __shared__ uint32_t spill_scr[SPILL ? CRF_MAX_LEN : 1];
     const int NT = blockDim.x;
     const int tid = threadIdx.x;
     const int N1 = p.n1;
 
     int n, nb, *sid;
-    uint32_t *magic;
     uint32_t *scratch;   // tree-walk scratch (cky_walk_bytes)
     char *chart0, *split0;
     int cstride, sstride;
     bool split_lds = false;
+    CkyLayout lay;
     if constexpr (SPILL) {
         const int b = p.cky.order_spill[block];
         n = p.len[b];
         nb = 1;
+        lay = CkyLayout{cky_ld(n), 0, 5};   // a workspace chart: no banks, spans side by side
         chart0 = p.ws + p.cky.ws_off[block];
         cstride = 0;
-        split0 = chart0 + (size_t)8 * cky_ld(n) * cky_ld(n);
+        split0 = chart0 + (size_t)8 * lay.ld * lay.ld;
         sstride = 0;
         sid = spill_id;
-        magic = spill_magic;
         scratch = spill_scr;
         if (tid == 0) sid[0] = b;
     } else {
@@ -1128,20 +1123,20 @@ __device__ __forceinline__ void cky_block(const KernelPlan &p, int block, const 
         n = rec[0];
         nb = rec[1];
         const int split_ws = rec[2];
-        chart0 = smem_raw;
         split_lds = split_ws < 0;
-        cstride = (int)cky_chart_bytes(n, split_lds ? 1 : 0);
-        split0 = split_lds ? chart0 + (size_t)8 * cky_ld(n) * cky_ld(n) : p.ws + (size_t)split_ws * 256;
+        lay = cky_layout(n, nb, split_lds ? 1 : 0, rec[4] != 0);
+        chart0 = smem_raw;
+        cstride = lay.cs;
+        split0 = split_lds ? chart0 + (size_t)8 * lay.ld * lay.ld : p.ws + (size_t)split_ws * 256;
         sstride = split_lds ? cstride : (int)cky_split_count(n);
         sid = reinterpret_cast<int *>(smem_raw + (size_t)nb * cstride);
-        magic = reinterpret_cast<uint32_t *>(sid + nb);
-        scratch = magic + n + 2;
+        // (then the room of bundle_extra_bytes, then the walk scratch)
+        scratch = reinterpret_cast<uint32_t *>(sid + nb) + n + 2;
         if (tid < nb) sid[tid] = id0;
     }
-    for (int S = tid; S <= n; S += NT) magic[S] = div_magic(S);
-    const int ld = cky_ld(n);
+    const int ld = lay.ld;
     typedef typename std::conditional<SPILL, uint16_t, uint8_t>::type SP;
-    const Cky_ctx<SP> cx{chart0, cstride, split0, sstride, n, ld, nb, !SPILL && split_lds};
+    const Cky_ctx<SP> cx{chart0, cstride, split0, sstride, n, ld, nb, div_magic(nb), !SPILL && split_lds};
     __syncthreads();
 
     auto score_at = [&](int sb, int i, int j) -> const float * {
@@ -1156,7 +1151,11 @@ __device__ __forceinline__ void cky_block(const KernelPlan &p, int block, const 
     };
     for_cells_loaded<8>(nb, n, score_at, load_score, put_score);
     __syncthreads();
-    cky_sweep<SPILL>(cx, magic);
+    // Workspace charts lay spans side by side; LDS charts interleave them
+    // when their layout allows (e = 0).
+    if constexpr (SPILL) cky_sweep<true, false>(cx);
+    else if (lay.e == 0) cky_sweep<false, true>(cx);
+    else cky_sweep<false, false>(cx);
 
     const int R = 2 * (N1 - 1) - 1;
     const int pad_rows = R - (2 * n - 1);   // rows past the tree are -1

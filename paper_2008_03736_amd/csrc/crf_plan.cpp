@@ -371,8 +371,8 @@ int crf_plan_create(crf_plan **out, const int32_t *lengths_host, int32_t batch, 
     auto inside_spill_bytes = [](int n) { return 4 * (int64_t)crf::inside_layout(n, 1, true).cs; };
     auto cky_spill_bytes = [](int n) { return crf::cky_chart_bytes(n, 2); };
     // The CKY bundle's tail: the tree-walk scratch, padded so that the last
-    // chart's masked reads (into the id, magic and scratch tables behind it)
-    // stay inside the bundle.
+    // chart's masked reads (into the ids, room and scratch behind it) stay
+    // inside the bundle.
     constexpr int nwaves = crf::kThreadsDefault / 64;
     auto cky_tail = [](int n, int64_t count) {
         const int64_t walk = crf::cky_walk_bytes(n, count, nwaves);
@@ -386,11 +386,14 @@ int crf_plan_create(crf_plan **out, const int32_t *lengths_host, int32_t batch, 
         return crf::cky_chart_bytes(n, 1) + 4 + crf::bundle_extra_bytes(n) + cky_tail(n, 1) <= half_cu;
     };
     // CKY bundle: the charts (with their split tables when they fit), the
-    // ids (i32), the magic table, the tail.
-    auto cky_bundle_bytes = [=](int n, int64_t count) {
-        return count * (crf::cky_chart_bytes(n, split_in_lds(n) ? 1 : 0) + 4) + crf::bundle_extra_bytes(n) +
-               cky_tail(n, count);
+    // ids (i32), the room of bundle_extra_bytes, the tail; the strict chart layout when it
+    // fits in half a CU, else the loose one (cky_layout).
+    auto cky_bytes_with = [=](int n, int64_t count, bool strict) {
+        const int cs = crf::cky_layout(n, (int)count, split_in_lds(n) ? 1 : 0, strict).cs;
+        return count * (cs + 4) + crf::bundle_extra_bytes(n) + cky_tail(n, count);
     };
+    auto cky_strict = [=](int n, int64_t count) { return cky_bytes_with(n, count, true) <= half_cu; };
+    auto cky_bundle_bytes = [=](int n, int64_t count) { return cky_bytes_with(n, count, cky_strict(n, count)); };
     HostSchedule si = make_schedule(order, lengths_host, lds_cap, force, 0, inside_bundle_bytes,
                                     inside_spill_bytes, kInsideTargetScale);
     HostSchedule sc = make_schedule(order, lengths_host, lds_cap, force, si.ws_bytes, cky_bundle_bytes,
@@ -440,8 +443,9 @@ int crf_plan_create(crf_plan **out, const int32_t *lengths_host, int32_t batch, 
             int32_t *q = r.data() + b * stride;
             q[0] = bd.n;
             q[1] = bd.count;
-            q[2] = inside ? (inside_strict(bd.n, bd.count) ? 1 : 0) : bd.split_ws;
+            q[2] = inside ? -1 : bd.split_ws;
             q[3] = inside ? 1 : 0;
+            q[4] = (inside ? inside_strict(bd.n, bd.count) : cky_strict(bd.n, bd.count)) ? 1 : 0;
             for (int t = 0; t < bd.count; ++t) q[crf::kRecHeader + t] = h.order[bd.first + t];
         }
         return r;
