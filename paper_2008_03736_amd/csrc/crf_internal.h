@@ -187,14 +187,6 @@ __host__ __device__ inline int64_t cky_chart_bytes(int n, int split_bytes) {
     const int64_t ld = cky_ld(n);
     return ld * ld * 8 + cky_split_bytes_of(n, split_bytes);
 }
-// The CKY tree walk follows the split table.  Bundles of fewer than
-// kDfsMinBundle sentences walk breadth first, one wavefront per sentence,
-// with a list of at most n - 1 internal nodes per wavefront; larger bundles
-// walk depth first, one lane per sentence, with a stack of n ints each.
-constexpr int kDfsMinBundle = 16;
-__host__ __device__ inline int64_t cky_walk_bytes(int n, int64_t count, int waves) {
-    return count < kDfsMinBundle ? 4 * (int64_t)(count < waves ? count : waves) * n : 4 * count * n;
-}
 
 // Shape of a width step with K split points per span: G lanes per span (a
 // power of two <= 64), C splits per lane (lane l takes splits l, l+G, ...),

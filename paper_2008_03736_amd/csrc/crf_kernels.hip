@@ -993,99 +993,46 @@ __device__ __forceinline__ void cky_sweep(const Cky_ctx<SP> &cx) {
 }
 
 // Order one wavefront's LDS accesses across its lanes.
-__device__ __forceinline__ void wave_sync() { __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront"); }
-
-// Tree nodes are spans (i, j) with their preorder row: once a node's split k
-// is known, its left child (i, k) takes the next row and its right child
-// (k, j) the row after the left subtree's 2(k-i)-1 rows.  A node (i, j, row)
-// packs into 31 bits (i, j < 1024, row < 2048).
-__device__ __forceinline__ uint32_t pack_node(int i, int j, int row) {
-    return (uint32_t)i | ((uint32_t)j << 10) | ((uint32_t)row << 20);
-}
 template <typename SP>
 __device__ __forceinline__ int split_of(const Cky_ctx<SP> &cx, int sb, int i, int j) {
     return i + 1 + cx.get_split(sb, cky_split_index(cx.n, j - i, i));
 }
-__device__ __forceinline__ void put_row(int32_t *out, int row, int i, int j) {
-    out[2 * row] = i;
-    out[2 * row + 1] = j;
-}
 
-// Write sentence sb's tree in preorder to out (its 2n-1 rows of the spans
-// output) on one wavefront, breadth first: each level's internal nodes,
-// one lane each, look up their splits, write both children and append the
-// children that are not single words to the node list `nodes` (LDS, at
-// most n - 1 ints), which thereby holds level after level.
+// Write the trees of all the bundle's sentences in preorder (the 2n-1 rows
+// of each sentence's spans output), one lane per word p of a sentence.  A
+// node (i, j) at row r with split k has its left child (i, k) at row r + 1
+// and its right child (k, j) at row r + 2(k - i) (a subtree of m words
+// holds 2m - 1 nodes).  Every node has one leftmost word; lane p walks down
+// from the root towards word p, following the split table and counting
+// rows, and writes the nodes whose leftmost word is p: once the walk reaches
+// a node starting at p, that node and its chain of left children down to
+// the word itself.  So each row is written once, and a lane's chain of
+// split lookups is as long as its word's depth.
 template <typename SP>
-__device__ void walk_bfs(const Cky_ctx<SP> &cx, int sb, int32_t *out, uint32_t *nodes) {
-    const int lane = threadIdx.x & 63, n = cx.n;
-    if (lane == 0) {
-        put_row(out, 0, 0, n);
-        nodes[0] = pack_node(0, n, 0);
-    }
-    wave_sync();
-    int lo = 0, hi = n >= 2 ? 1 : 0;   // the current level is nodes[lo, hi)
-    while (lo < hi) {
-        int tail = hi;
-        for (int base = lo; base < hi; base += 64) {
-            const int idx = base + lane;
-            const bool valid = idx < hi;
-            const uint32_t node = nodes[valid ? idx : lo];
-            const int i = node & 1023, j = (node >> 10) & 1023, row = node >> 20;
+__device__ void walk_trees(const Cky_ctx<SP> &cx, const int *sid, int32_t *spans, int R) {
+    const int n = cx.n, total = cx.nb * n;
+    const float inv_n = 1.0f / (float)n;
+    for (int t = threadIdx.x; t < total; t += blockDim.x) {
+        const int sb = div_small(t, n, inv_n), p = t - sb * n;
+        int2 *out = reinterpret_cast<int2 *>(spans + (size_t)sid[sb] * R * 2);
+        int i = 0, j = n, row = 0;
+        // (every split k lies in (i, j), so each pass moves i up or j down;
+        // the pass bounds only guard against a corrupt table)
+        for (int it = 0; i < p && it < n; ++it) {   // i < p < j: a node not starting at p
             const int k = split_of(cx, sb, i, j);
-            const int rl = row + 1, rr = row + 2 * (k - i);
-            if (valid) {
-                put_row(out, rl, i, k);
-                put_row(out, rr, k, j);
-            }
-            const bool li = valid && k - i >= 2, ri = valid && j - k >= 2;
-            const uint64_t ml = __ballot(li), mr = __ballot(ri);
-            const int nl = __popcll(ml);
-            if (li)
-                nodes[tail + __builtin_amdgcn_mbcnt_hi((uint32_t)(ml >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)ml, 0))] =
-                    pack_node(i, k, rl);
-            if (ri)
-                nodes[tail + nl + __builtin_amdgcn_mbcnt_hi((uint32_t)(mr >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mr, 0))] =
-                    pack_node(k, j, rr);
-            tail += nl + __popcll(mr);
-        }
-        wave_sync();
-        lo = hi;
-        hi = tail;
-    }
-}
-
-// Write the trees of all the bundle's sentences in preorder, one lane per
-// sentence, depth first: the walk goes left, with the right children still
-// to visit on the sentence's stack (LDS, at most n - 1 deep), and a left
-// child that is a single word is written at once and the walk goes right.
-template <typename SP>
-__device__ void walk_dfs(const Cky_ctx<SP> &cx, const int *sid, int32_t *spans, int R, uint32_t *stacks) {
-    const int n = cx.n;
-    for (int sb = threadIdx.x; sb < cx.nb; sb += blockDim.x) {
-        int32_t *out = spans + (size_t)sid[sb] * R * 2;
-        uint32_t *stack = stacks + (size_t)sb * n;
-        int i = 0, j = n, row = 0, top = 0;
-        for (int it = 0; it < 2 * n; ++it) {   // one row per pass: 2n-1 in all
-            put_row(out, row, i, j);
-            if (j - i >= 2) {
-                const int k = split_of(cx, sb, i, j);
-                if (k - i == 1) {   // left child is a word
-                    put_row(out, row + 1, i, k);
-                    row += 2;
-                    i = k;
-                } else {
-                    stack[top++] = pack_node(k, j, row + 2 * (k - i));
-                    ++row;
-                    j = k;
-                }
+            if (p < k) {
+                ++row;
+                j = k;
             } else {
-                if (top == 0) break;
-                const uint32_t node = stack[--top];
-                i = node & 1023;
-                j = (node >> 10) & 1023;
-                row = node >> 20;
+                row += 2 * (k - i);
+                i = k;
             }
+        }
+        for (int it = 0; it < n; ++it) {
+            out[row] = make_int2(i, j);
+            if (j - i < 2) break;
+            j = split_of(cx, sb, i, j);
+            ++row;
         }
     }
 }
@@ -1095,13 +1042,11 @@ __device__ __forceinline__ void cky_block(const KernelPlan &p, int block, const 
                                           const float *__restrict__ scores,
                                           int32_t *__restrict__ spans, float *__restrict__ best) {
     __shared__ int spill_id[1];
-    __shared__ uint32_t spill_scr[SPILL ? CRF_MAX_LEN : 1];
     const int NT = blockDim.x;
     const int tid = threadIdx.x;
     const int N1 = p.n1;
 
     int n, nb, *sid;
-    uint32_t *scratch;   // tree-walk scratch (cky_walk_bytes)
     char *chart0, *split0;
     int cstride, sstride;
     bool split_lds = false;
@@ -1116,7 +1061,6 @@ __device__ __forceinline__ void cky_block(const KernelPlan &p, int block, const 
         split0 = chart0 + (size_t)8 * lay.ld * lay.ld;
         sstride = 0;
         sid = spill_id;
-        scratch = spill_scr;
         if (tid == 0) sid[0] = b;
     } else {
         const int id0 = tid < p.rec_stride - kRecHeader ? rec[kRecHeader + tid] : 0;
@@ -1130,8 +1074,6 @@ __device__ __forceinline__ void cky_block(const KernelPlan &p, int block, const 
         split0 = split_lds ? chart0 + (size_t)8 * lay.ld * lay.ld : p.ws + (size_t)split_ws * 256;
         sstride = split_lds ? cstride : (int)cky_split_count(n);
         sid = reinterpret_cast<int *>(smem_raw + (size_t)nb * cstride);
-        // (then the room of bundle_extra_bytes, then the walk scratch)
-        scratch = reinterpret_cast<uint32_t *>(sid + nb) + n + 2;
         if (tid < nb) sid[tid] = id0;
     }
     const int ld = lay.ld;
@@ -1171,15 +1113,7 @@ __device__ __forceinline__ void cky_block(const KernelPlan &p, int block, const 
     }
     if (best != nullptr)
         for (int sb = tid; sb < nb; sb += NT) best[sid[sb]] = (float)cx.beta(sb)[n];
-    // Tree walks.  A few (long) sentences: one wavefront each, breadth first.
-    // Many (short) sentences: one lane each, depth first, all at once.
-    if (nb < kDfsMinBundle) {
-        const int wave = tid >> 6;
-        for (int sb = wave; sb < nb; sb += NT >> 6)
-            walk_bfs(cx, sb, spans + (size_t)sid[sb] * R * 2, scratch + (size_t)wave * n);
-    } else {
-        walk_dfs(cx, sid, spans, R, scratch);
-    }
+    walk_trees(cx, sid, spans, R);   // (the sweep's last barrier published the splits)
 }
 
 // Workgroups of 256, 512 or 1024 threads (the plan's choice) share one

@@ -370,14 +370,11 @@ int crf_plan_create(crf_plan **out, const int32_t *lengths_host, int32_t batch, 
     };
     auto inside_spill_bytes = [](int n) { return 4 * (int64_t)crf::inside_layout(n, 1, true).cs; };
     auto cky_spill_bytes = [](int n) { return crf::cky_chart_bytes(n, 2); };
-    // The CKY bundle's tail: the tree-walk scratch, padded so that the last
-    // chart's masked reads (into the ids, room and scratch behind it) stay
-    // inside the bundle.
-    constexpr int nwaves = crf::kThreadsDefault / 64;
+    // The CKY bundle's tail: padding so that the last chart's masked reads
+    // (into the ids and the room behind it) stay inside the bundle.
     auto cky_tail = [](int n, int64_t count) {
-        const int64_t walk = crf::cky_walk_bytes(n, count, nwaves);
-        const int64_t tables = 4 * count + crf::bundle_extra_bytes(n) + walk;
-        return walk + std::max<int64_t>(0, 8 * (int64_t)crf::masked_reach(n) - tables);
+        const int64_t tables = 4 * count + crf::bundle_extra_bytes(n);
+        return std::max<int64_t>(0, 8 * (int64_t)crf::masked_reach(n) - tables);
     };
     // A sentence's split table sits in LDS after its chart when a bundle of
     // one such sentence still fits in half the CU; longer sentences keep it
