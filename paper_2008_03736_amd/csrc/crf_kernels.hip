@@ -152,6 +152,16 @@ __device__ __forceinline__ double grp_max_d(double v) {
     return v;
 }
 template <int G>
+__device__ __forceinline__ double grp_sum_d(double v) {
+    if constexpr (G >= 2) v += dpp_d<DPP_XOR1>(v);
+    if constexpr (G >= 4) v += dpp_d<DPP_XOR2>(v);
+    if constexpr (G >= 8) v += dpp_d<DPP_HMIRROR>(v);
+    if constexpr (G >= 16) v += dpp_d<DPP_MIRROR>(v);
+    if constexpr (G >= 32) v += swz16_d(v);
+    if constexpr (G >= 64) v = readlane_d(v, 0) + readlane_d(v, 32);
+    return v;
+}
+template <int G>
 __device__ __forceinline__ int grp_min_i(int v) {
     if constexpr (G >= 2) v = min(v, dpp_i<DPP_XOR1>(v));
     if constexpr (G >= 4) v = min(v, dpp_i<DPP_XOR2>(v));
@@ -481,18 +491,29 @@ __device__ __forceinline__ void fwd_sweep(const Bundle_ctx<T> &bx, const float *
     }
 }
 
-// Fixed-order reductions over a wavefront (same result in every lane).
-__device__ __forceinline__ double wave_sum_d(double v) {
-    for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
-    return v;
-}
-__device__ __forceinline__ float wave_max_f(float v) {
-    for (int off = 32; off >= 1; off >>= 1) v = fmax_nn(v, __shfl_xor(v, off));
-    return v;
-}
-__device__ __forceinline__ float wave_sum_f(float v) {
-    for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
-    return v;
+
+// Per-sentence work of a bundle on groups of GS lanes, GS the smallest of
+// 8, 16, 32, 64 that covers `len` items per sentence (so that short
+// sentences share a wavefront and reduce with DPP moves, not through LDS):
+// group q of the workgroup takes sentences q, q + NG, ...  f(gs, sb, gl,
+// valid) runs on every lane of a wavefront that holds a sentence; a group
+// past the last sentence gets valid = false and the last sentence's index.
+// GS depends on len only, so a group's summation order is fixed.
+template <typename F>
+__device__ __forceinline__ void by_sentence_groups(int len, int nb, F &&f) {
+    auto run = [&](auto gs) {
+        constexpr int GS = decltype(gs)::value;
+        const int NG = blockDim.x / GS, q = threadIdx.x / GS, gl = threadIdx.x & (GS - 1);
+        const int q_wave = __builtin_amdgcn_readfirstlane((threadIdx.x & ~63) / GS);   // the wavefront's first group
+        for (int sb0 = 0; sb0 + q_wave < nb; sb0 += NG) {
+            const int sb = sb0 + q;
+            f(gs, sb < nb ? sb : nb - 1, gl, sb < nb);
+        }
+    };
+    if (len <= 8) run(std::integral_constant<int, 8>{});
+    else if (len <= 16) run(std::integral_constant<int, 16>{});
+    else if (len <= 32) run(std::integral_constant<int, 32>{});
+    else run(std::integral_constant<int, 64>{});
 }
 
 // Spans below a sentence's largest alpha of the probe width by more than this
@@ -514,25 +535,26 @@ constexpr float kShiftBand = 30.0f;
 template <typename T>
 __device__ void rescale_chart(const Bundle_ctx<T> &bx, int t0, float *dsh) {
     const int n = bx.n, ld = bx.ld, nb = bx.nb, w0 = t0 + 1, S = n - t0;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, NW = blockDim.x >> 6;
-    for (int sb = wave; sb < nb; sb += NW) {
+    const int tid = threadIdx.x;
+    by_sentence_groups(S, nb, [&](auto gs, int sb, int gl, bool valid) {
+        constexpr int GS = decltype(gs)::value;
         const T *P = bx.chart0 + (size_t)sb * bx.cstride;
         float m = NEG;
-        for (int i = lane; i < S; i += 64) m = fmax_nn(m, P[i * ld + w0 - 1]);
-        m = wave_max_f(m);
+        for (int i = gl; i < S; i += GS) m = fmax_nn(m, P[i * ld + w0 - 1]);
+        m = grp_max<GS>(m);
         const float floor_v = m - kShiftBand * (float)(w0 - 1);
         float acc = 0.f, cnt = 0.f;
-        for (int i = lane; i < S; i += 64) {
+        for (int i = gl; i < S; i += GS) {
             const float a = P[i * ld + w0 - 1];
             if (a >= floor_v) {
                 acc += a;
                 cnt += 1.f;
             }
         }
-        acc = wave_sum_f(acc);
-        cnt = wave_sum_f(cnt);
-        if (lane == 0) dsh[sb] = -acc / (cnt * (float)(w0 - 1));
-    }
+        acc = grp_sum<GS>(acc);
+        cnt = grp_sum<GS>(cnt);
+        if (valid && gl == 0) dsh[sb] = -acc / (cnt * (float)(w0 - 1));
+    });
     __syncthreads();
     // alpha of widths 2..w0: per sentence n rows x (w0-1) widths
     {
@@ -692,8 +714,8 @@ __device__ __forceinline__ void inside_block(const KernelPlan &p, int block, con
     __shared__ float spill_gv[1];
     __shared__ int spill_id[1];
     __shared__ float spill_dsh[1];
-    const int NT = blockDim.x, NW = NT >> 6;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int NT = blockDim.x;
+    const int tid = threadIdx.x;
     const int N1 = p.n1, L = p.L;
 
     int n, nb;
@@ -777,15 +799,16 @@ __device__ __forceinline__ void inside_block(const KernelPlan &p, int block, con
     };
     for_cells_loaded<LAB ? 1 : 8>(nb, n, score_at, load_score, put_score);
     __syncthreads();
-    // Forced-span sums, one wavefront per sentence, fixed order (deterministic).
-    for (int sb = wave; sb < nb; sb += NW) {
+    // Forced-span sums, a lane group per sentence, fixed order (deterministic).
+    by_sentence_groups(n, nb, [&](auto gs, int sb, int gl, bool valid) {
+        constexpr int GS = decltype(gs)::value;
         const float *P = chart0 + (size_t)sb * cstride;
         double acc = 0.0;
-        for (int i = lane; i < n; i += 64) acc += (double)P[(i + 1) * ld + n - 1];
-        if (lane == 0 && n >= 2) acc += (double)P[n];
-        acc = wave_sum_d(acc);
-        if (lane == 0) forced[sb] = acc;
-    }
+        for (int i = gl; i < n; i += GS) acc += (double)P[(i + 1) * ld + n - 1];
+        if (gl == 0 && n >= 2) acc += (double)P[n];
+        acc = grp_sum_d<GS>(acc);
+        if (valid && gl == 0) forced[sb] = acc;
+    });
 
     // Workspace charts lay spans side by side; LDS charts interleave them
     // when their layout allows (e = 0).
