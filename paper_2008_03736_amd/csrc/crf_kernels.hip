@@ -292,7 +292,9 @@ __device__ __forceinline__ int region_lanes(int nsp) {
 // at P[0][n].
 __host__ __device__ constexpr int rot_alpha_p(int w) { return w - 1; }
 template <typename T>
-__device__ __forceinline__ T *sq_p(const Bundle_ctx<T> &bx, int sb) { return bx.chart0 + (size_t)sb * bx.cstride; }
+__device__ __forceinline__ T *sq_p(const Bundle_ctx<T> &bx, int sb) {   // (sb < 256, cstride < 2^24)
+    return bx.chart0 + __umul24((uint32_t)sb, (uint32_t)bx.cstride);
+}
 
 // One span's log-sum-exp over the K split terms of a step: lane l of the
 // span's G lanes takes positions p = l + c*G, c < C, of the two runs a and b
@@ -333,8 +335,8 @@ __device__ __forceinline__ void inside_span(const Bundle_ctx<T> &bx, int w, int 
     const Lane_at at = lane_at<G, IL>(f, nsp, bx.nb, bx.mnb);
     const int i = at.i, l = at.l;
     T *pq = sq_p(bx, at.sb);
-    const int rp = (int)__umul24((uint32_t)i, (uint32_t)ld);                   // P row i
-    const int rq = rp + (int)__umul24((uint32_t)(ld + w), (uint32_t)ld);        // Q row j (uniform offset)
+    const int rp = (int)__umul24((uint32_t)i, (uint32_t)ld);              // P row i
+    const int rq = (int)__umul24((uint32_t)(i + ld + w), (uint32_t)ld);   // Q row j
     const int pa = rp + rot_alpha_p(w), qa = rq + n + 1 - w;                   // alpha(i,j) cells
     const float own = pq[pa] + (w < n ? dsh[at.sb] : 0.f);
     const float v = span_lse<G, C, MF>(pq + rp + l, pq + rq + (n + 2 - w) + l, K - l, own);
@@ -356,9 +358,8 @@ __device__ __forceinline__ void outside_span(const Bundle_ctx<T> &bx, int v, int
     const Lane_at at = lane_at<G, IL>(f, nsp, bx.nb, bx.mnb);
     const int i = at.i, l = at.l;
     T *pq = sq_p(bx, at.sb);
-    const int ri = (int)__umul24((uint32_t)i, (uint32_t)ld);
-    const int rp = ri + (int)__umul24((uint32_t)v, (uint32_t)ld);   // P row j (uniform offset)
-    const int rq = ri + (int)__umul24((uint32_t)ld, (uint32_t)ld);  // Q row i
+    const int rp = (int)__umul24((uint32_t)(i + v), (uint32_t)ld);    // P row j
+    const int rq = (int)__umul24((uint32_t)(i + ld), (uint32_t)ld);   // Q row i
     const int po = rp + n - v, qo = rq + v;                          // O'(i,j) cells
     const float own = pq[po] + dsh[at.sb];
     const float o = span_lse<G, C, MF>(pq + rp + l, pq + rq + v + 1 + l, K - l, own);
@@ -869,8 +870,8 @@ struct Cky_ctx {
     int n, ld, nb;
     uint32_t mnb;     // div_magic(nb)
     bool split_lds;   // split tables in LDS (else in global memory)
-    __device__ double *beta(int sb) const {
-        return reinterpret_cast<double *>(chart0 + (size_t)sb * cstride);
+    __device__ double *beta(int sb) const {   // (sb < 256, cstride < 2^24)
+        return reinterpret_cast<double *>(chart0 + __umul24((uint32_t)sb, (uint32_t)cstride));
     }
     // Split table entry e of sentence sb, through an LDS or a global pointer
     // (not a generic one: flat accesses cost more, and a flat store to LDS
