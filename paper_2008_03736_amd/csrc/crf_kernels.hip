@@ -940,25 +940,25 @@ __device__ __forceinline__ void cky_step(const Cky_ctx<SP> &cx, int w, int sp0) 
         const int rowo = rb + 1 + l, colo = cb + 1 + l;
         const double sij = be[rb + w];
         const int kl = K - l;
-        // Terms in chunks of up to 16.  Up to 16 splits per lane (one chunk),
-        // every float64 operand is loaded before the first is used; longer
-        // lanes interleave loads and arithmetic.  A chunk's max and its
-        // lowest term at the max pair up as a tree; chunks merge in order.
-        constexpr int CH = C < 16 ? C : 16;
+        // Terms in chunks of 16 (the last one shorter).  Up to 16 splits per
+        // lane (one chunk), every float64 operand is loaded before the first
+        // is used; longer lanes interleave loads and arithmetic.  A chunk's
+        // max and its lowest term at the max pair up as a tree; chunks merge
+        // in order.
         double m = -INFINITY;
         int kc = 0;   // this lane's first term at its max, as c * G
+        auto chunk = [&](auto c0_c, auto n_c) {
+            constexpr int c0 = decltype(c0_c)::value, CN = decltype(n_c)::value;
+            double xr[CN], xc[CN];
 #pragma unroll
-        for (int c0 = 0; c0 < C; c0 += CH) {
-            double xr[CH], xc[CH];
-#pragma unroll
-            for (int c = 0; c < CH; ++c) {
+            for (int c = 0; c < CN; ++c) {
                 xr[c] = be[rowo + (c0 + c) * G];
                 xc[c] = be[colo + (c0 + c) * G];
             }
             if constexpr (C <= 16) __builtin_amdgcn_sched_barrier(0);
-            double x[CH];
+            double x[CN];
 #pragma unroll
-            for (int c = 0; c < CH; ++c) {
+            for (int c = 0; c < CN; ++c) {
                 x[c] = xr[c] + xc[c];
                 // a split past the span's last: the high word alone makes it
                 // about -1.8e308, below any chart value (one select, not two)
@@ -968,15 +968,19 @@ __device__ __forceinline__ void cky_step(const Cky_ctx<SP> &cx, int w, int sp0) 
                     x[c] = __builtin_bit_cast(double, ((uint64_t)hi << 32) | (uint32_t)u);
                 }
             }
-            const Arg_max a = tree_arg_max<0, CH>(x, c0, G);
-            if (c0 == 0) {
+            const Arg_max a = tree_arg_max<0, CN>(x, c0, G);
+            if constexpr (c0 == 0) {
                 m = a.v;
                 kc = a.k;
             } else {
                 kc = a.v > m ? a.k : kc;
                 m = fmax(m, a.v);
             }
-        }
+        };
+        static_assert(C <= 48, "at most three chunks");
+        chunk(std::integral_constant<int, 0>{}, std::integral_constant<int, (C < 16 ? C : 16)>{});
+        if constexpr (C > 16) chunk(std::integral_constant<int, 16>{}, std::integral_constant<int, (C < 32 ? C - 16 : 16)>{});
+        if constexpr (C > 32) chunk(std::integral_constant<int, 32>{}, std::integral_constant<int, C - 32>{});
         const double mg = grp_max_d<G>(m);
         const int kb = min(grp_min_i<G>(m == mg ? kc + l : 0x7fffffff), K - 1);
         const double v = mg + sij;
