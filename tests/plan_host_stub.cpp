@@ -1,0 +1,102 @@
+// Host-only build of the plan code for the CPU tests: the HIP runtime calls
+// the plan makes are served from host memory (no device is touched), and
+// the launch entry points are never called.  Prints the plan's records:
+//   P n_mix fused_grid lds_inside lds_cky half_cu
+//   R kind n count split_ws strict ld cs e bytes id...
+// one R line per record of the fused queue, in queue order.
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <vector>
+
+#include "../paper_2008_03736_amd/csrc/crf_plan.cpp"
+
+extern "C" {
+hipError_t hipGetDevice(int *d) {
+    *d = 0;
+    return hipSuccess;
+}
+hipError_t hipSetDevice(int) { return hipSuccess; }
+hipError_t hipDeviceGetAttribute(int *v, hipDeviceAttribute_t a, int) {
+    *v = a == hipDeviceAttributeMaxSharedMemoryPerBlock ? 163840 : 256;   // MI355X: 160 KiB, 256 CUs
+    return hipSuccess;
+}
+hipError_t hipMalloc(void **p, size_t n) {
+    *p = std::malloc(n ? n : 1);
+    return *p ? hipSuccess : hipErrorOutOfMemory;
+}
+hipError_t hipFree(void *p) {
+    std::free(p);
+    return hipSuccess;
+}
+hipError_t hipMemcpy(void *d, const void *s, size_t n, hipMemcpyKind) {
+    std::memcpy(d, s, n);
+    return hipSuccess;
+}
+hipError_t hipMemset(void *d, int v, size_t n) {
+    std::memset(d, v, n);
+    return hipSuccess;
+}
+hipError_t hipDeviceSynchronize() { return hipSuccess; }
+hipError_t hipGetLastError() { return hipSuccess; }
+const char *hipGetErrorString(hipError_t) { return "host stub"; }
+}
+
+namespace crf {
+hipError_t launch_inside(const KernelPlan &, const float *, const float *, float *, float *, hipStream_t) {
+    return hipErrorNotSupported;
+}
+hipError_t launch_cky(const KernelPlan &, const float *, int32_t *, float *, hipStream_t) {
+    return hipErrorNotSupported;
+}
+hipError_t launch_parse(const KernelPlan &, const float *, const float *, float *, float *, int32_t *, float *,
+                        hipStream_t) {
+    return hipErrorNotSupported;
+}
+hipError_t set_kernel_attributes(int) { return hipSuccess; }
+}  // namespace crf
+
+int main(int argc, char **argv) {
+    if (argc < 2) return 2;
+    std::vector<int32_t> len;
+    FILE *f = std::fopen(argv[1], "r");
+    if (!f) return 2;
+    int x;
+    while (std::fscanf(f, "%d", &x) == 1) len.push_back(x);
+    std::fclose(f);
+    int n1 = 2;
+    for (int v : len) n1 = std::max(n1, v + 1);
+    crf_plan *p = nullptr;
+    const int rc = crf_plan_create(&p, len.data(), (int32_t)len.size(), n1, 1, 0);
+    if (rc != CRF_OK) {
+        std::printf("E %d\n", rc);
+        return 1;
+    }
+    const crf::KernelPlan &kp = p->kp;
+    const int half_cu = 163840 / 2 - crf::kReservedLds;
+    std::printf("P %d %d %d %d %d\n", kp.n_mix, kp.fused_grid, kp.inside.lds_bytes, kp.cky.lds_bytes, half_cu);
+    for (int b = 0; b < kp.n_mix; ++b) {
+        const int32_t *r = kp.mix + (size_t)b * kp.rec_stride;
+        const int n = r[0], count = r[1], split_ws = r[2], kind = r[3], strict = r[4];
+        int ld, cs, e;
+        long long bytes;
+        if (kind == 1) {
+            const crf::InsideLayout l = crf::inside_layout(n, count, strict != 0);
+            ld = l.ld;
+            cs = l.cs;
+            e = l.e;
+            bytes = crf::inside_bundle_bytes(n, count, strict != 0);
+        } else {
+            const crf::CkyLayout l = crf::cky_layout(n, count, split_ws < 0 ? 1 : 0, strict != 0);
+            ld = l.ld;
+            cs = l.cs;
+            e = l.e;
+            bytes = -1;   // (the CKY tail is the plan's; the test checks the strides)
+        }
+        std::printf("R %d %d %d %d %d %d %d %d %lld", kind, n, count, split_ws, strict, ld, cs, e, bytes);
+        for (int t = 0; t < count; ++t) std::printf(" %d", r[crf::kRecHeader + t]);
+        std::printf("\n");
+    }
+    crf_plan_destroy(p);
+    return 0;
+}

@@ -1,0 +1,98 @@
+"""Host logic of the plan (crf_plan.cpp), built for the CPU with stub HIP
+allocation calls (tests/plan_host_stub.cpp) and checked on synthetic batches:
+every sentence in exactly one inside and one CKY bundle, each bundle within
+the launch's LDS, the chart layouts' stride congruences (the condition under
+which the sweeps' LDS reads are bank-conflict free), and the fused queue.
+"""
+import os
+import shutil
+import subprocess
+
+import numpy as np
+import pytest
+
+from paper_2008_03736_amd import workloads as W
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+ROCM_INCLUDE = "/opt/rocm/include"
+
+
+@pytest.fixture(scope="module")
+def harness(tmp_path_factory):
+    cxx = shutil.which("g++")
+    if cxx is None or not os.path.isdir(ROCM_INCLUDE):
+        pytest.skip("needs g++ and the HIP headers")
+    out = str(tmp_path_factory.mktemp("plan") / "plan_host")
+    cmd = [cxx, "-O1", "-std=c++17", "-D__HIP_PLATFORM_AMD__", "-I" + ROCM_INCLUDE,
+           "-I" + os.path.join(HERE, "..", "include"), "-o", out, os.path.join(HERE, "plan_host_stub.cpp")]
+    subprocess.run(cmd, check=True, capture_output=True, text=True)
+    return out
+
+
+def plan_of(harness, tmp_path, lengths):
+    f = tmp_path / "lengths.txt"
+    f.write_text("\n".join(str(int(v)) for v in lengths))
+    res = subprocess.run([harness, str(f)], capture_output=True, text=True, check=True)
+    head, recs = None, []
+    for line in res.stdout.splitlines():
+        t = line.split()
+        if t[0] == "P":
+            head = dict(zip(["n_mix", "grid", "lds_in", "lds_ck", "half_cu"], map(int, t[1:])))
+        elif t[0] == "R":
+            v = list(map(int, t[1:]))
+            recs.append(dict(kind=v[0], n=v[1], count=v[2], split_ws=v[3], strict=v[4], ld=v[5], cs=v[6],
+                             e=v[7], bytes=v[8], ids=v[9:]))
+    return head, recs
+
+
+def check_plan(head, recs, lengths):
+    lengths = np.asarray(lengths)
+    assert head["n_mix"] == len(recs)
+    assert head["grid"] == min(len(recs), 512)
+    for kind in (0, 1):
+        ids = [i for r in recs if r["kind"] == kind for i in r["ids"]]
+        assert sorted(ids) == list(range(len(lengths))), "every sentence once per kind"
+    for r in recs:
+        assert r["count"] == len(r["ids"]) >= 1
+        assert all(lengths[i] == r["n"] for i in r["ids"])
+        n, nb, ld, cs = r["n"], r["count"], r["ld"], r["cs"]
+        if r["kind"] == 1:
+            assert ld >= n + 1 and 2 * ld * ld <= cs < 2 * ld * ld + 32
+            assert 0 < r["bytes"] <= head["lds_in"] <= head["half_cu"]
+            if r["strict"] and r["e"] == 0 and not (nb >= 32 and nb % 4 == 0):
+                # span g's runs start at sigma g (mod 32): cs = sigma odd, ld = nb sigma
+                assert cs % 2 == 1 and (ld - nb * cs) % 32 == 0, r
+        else:
+            assert ld >= n + 1 and cs % 8 == 0 and cs >= 8 * ld * ld
+            u = cs // 8
+            if r["strict"] and not (nb >= 16 and nb % 4 == 0):
+                assert u % 2 == 1 and (ld + 1 - nb * u) % 16 == 0, r
+            elif not r["strict"]:
+                assert u % 2 == 1 and ld % 2 == 0
+
+
+@pytest.mark.parametrize("name", ["tiny", "mixed"])
+def test_plan_of_workloads(harness, tmp_path, name):
+    b = W.make(name)
+    head, recs = plan_of(harness, tmp_path, b.lengths)
+    check_plan(head, recs, b.lengths)
+    if name == "mixed":
+        # both layouts occur, and most bundles take the strict one
+        for kind in (0, 1):
+            flags = [r["strict"] for r in recs if r["kind"] == kind]
+            assert 0 < sum(flags) and sum(flags) > len(flags) // 2
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_plan_of_random_batches(harness, tmp_path, seed):
+    rng = np.random.default_rng(seed)
+    lengths = rng.integers(1, 100, size=int(rng.integers(1, 3000)))
+    head, recs = plan_of(harness, tmp_path, lengths)
+    check_plan(head, recs, lengths)
+
+
+@pytest.mark.parametrize("n,count", [(9, 4), (14, 40), (17, 32), (20, 20), (30, 8), (45, 4), (99, 1)])
+def test_plan_of_one_length(harness, tmp_path, n, count):
+    lengths = [n] * count + [99] * 200
+    head, recs = plan_of(harness, tmp_path, lengths)
+    check_plan(head, recs, lengths)
