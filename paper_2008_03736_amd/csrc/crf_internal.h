@@ -216,6 +216,30 @@ __host__ __device__ inline StepShape step_shape_k(int K) {
     return 12 * g >= K ? StepShape{g, 12, 8} : StepShape{g, 16, 12};
 }
 
+// The first K' > K whose step shape differs from K's (the sweeps run the
+// steps of one shape as one loop; a closed form, since a scan over the
+// steps costs a chain of scalar instructions per step).
+__host__ __device__ inline int shape_run_end(int K) {
+    if (K <= 1) return 2;
+    if (K <= 2) return 3;
+    if (K <= 4) return 5;
+    if (K <= 8) return 9;
+    if (K <= 16) return 17;
+    if (K <= 32) return 33;
+    if (K <= 48) return 49;
+    if (K <= 64) return 65;
+    if (K <= 96) return 97;
+    if (K <= 128) return 129;
+    const StepShape s = step_shape_k(K);   // longer (workspace) sentences: scan
+    int k = K + 1;
+    while (k < (1 << 20)) {
+        const StepShape s2 = step_shape_k(k);
+        if (s2.G != s.G || s2.C != s.C) break;
+        ++k;
+    }
+    return k;
+}
+
 // Cells past its span's last split that a masked split read may reach, at
 // the widest step of a sentence of n words: (C - MF) G.
 __host__ __device__ inline int masked_reach(int n) {

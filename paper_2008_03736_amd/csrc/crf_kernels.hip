@@ -479,12 +479,7 @@ __device__ __forceinline__ void fwd_sweep(const Bundle_ctx<T> &bx, const float *
     int w = 2;
     while (w <= n) {
         const StepShape sh = step_shape_k(w - 1);
-        int w2 = w + 1;
-        while (w2 <= n) {
-            const StepShape s2 = step_shape_k(w2 - 1);
-            if (s2.G != sh.G || s2.C != sh.C) break;
-            ++w2;
-        }
+        const int w2 = min(shape_run_end(w - 1) + 1, n + 1);
 #define CRF_FWD_RUN(GG, CC, MM) fwd_run<GG, CC, MM, IL>(bx, w, w2, dsh)
         CRF_DISPATCH_SHAPE(sh, CRF_FWD_RUN);
 #undef CRF_FWD_RUN
@@ -603,12 +598,8 @@ __device__ __forceinline__ void io_sweep(const Bundle_ctx<T> &bx, float *dsh, in
     int t = 1;
     while (t <= n - 1) {
         const StepShape sh = step_shape_k(t);
-        int t2 = t + 1;
-        while (t2 <= n - 1 && t2 - 1 != t0) {
-            const StepShape s2 = step_shape_k(t2);
-            if (s2.G != sh.G || s2.C != sh.C) break;
-            ++t2;
-        }
+        int t2 = min(shape_run_end(t), n);
+        if (t <= t0 && t2 > t0 + 1) t2 = t0 + 1;   // the rescale follows step t0
 #define CRF_IO_RUN(GG, CC, MM) io_run<GG, CC, MM, IL>(bx, t, t2, dsh)
         CRF_DISPATCH_SHAPE(sh, CRF_IO_RUN);
 #undef CRF_IO_RUN
@@ -1007,12 +998,7 @@ __device__ __forceinline__ void cky_sweep(const Cky_ctx<SP> &cx) {
     int w = 2;
     while (w <= n) {
         const StepShape sh = step_shape_k(w - 1);
-        int w2 = w + 1;
-        while (w2 <= n) {
-            const StepShape s2 = step_shape_k(w2 - 1);
-            if (s2.G != sh.G || s2.C != sh.C) break;
-            ++w2;
-        }
+        const int w2 = min(shape_run_end(w - 1) + 1, n + 1);
 #define CRF_CKY_RUN(GG, CC, MM) cky_run<GG, CC, MM, IL>(cx, w, w2)
         CRF_DISPATCH_SHAPE(sh, CRF_CKY_RUN);
 #undef CRF_CKY_RUN
