@@ -266,11 +266,16 @@ struct Bundle {
 };
 
 // What a bundle's workgroup reads first: one record of rec_stride ints --
-// n, count, split_ws (CKY; -1 for inside), kind (1 inside, 0 CKY), the
-// strict flag of its chart layout (inside_layout, cky_layout), then the
-// count sentence ids -- so that its sentence ids arrive with its shape, one
-// memory round trip before its scores.
-constexpr int kRecHeader = 5;
+// n, count, split_ws (CKY; -1 for inside), kind (1 inside, 0 CKY), then its
+// chart layout (inside_layout or cky_layout, as the plan chose it: e, ld,
+// cs) and div_magic(count), then the count sentence ids -- so that its
+// sentence ids arrive with its shape, one memory round trip before its
+// scores, and the workgroup computes none of it.
+constexpr int kRecHeader = 8;
+enum RecField { kRecN = 0, kRecCount, kRecSplitWs, kRecKind, kRecE, kRecLd, kRecCs, kRecMagic };
+// g / S by multiply-high: 2^32 / S + 1, exact for g < 2^18, 2 <= S <= 1024;
+// 0 for S = 1 (the caller takes g itself).
+__host__ __device__ inline uint32_t div_magic(int S) { return S > 1 ? 0xFFFFFFFFu / (uint32_t)S + 1u : 0u; }
 
 // Which sentences run in LDS (in bundles) and which on the workspace kernel,
 // for one kind of chart.  Bundles and spilled sentences are ordered most

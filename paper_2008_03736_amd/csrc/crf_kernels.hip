@@ -205,7 +205,6 @@ struct Bundle_ctx {
     int e;          // the inside layout's bank exponent (inside_layout); 5 on the workspace
 };
 
-__device__ __forceinline__ uint32_t div_magic(int S) { return S > 1 ? 0xFFFFFFFFu / (uint32_t)S + 1u : 0u; }
 
 // Where lane f of a step's region works.  The region's nsp spans are numbered
 // sentence-minor, g = i nb + sb (sentence sb, span start i; g / nb by
@@ -717,6 +716,7 @@ __device__ __forceinline__ void inside_block(const KernelPlan &p, int block, con
     float *gv, *dsh;
     int *sid;
     InsideLayout lay;
+    uint32_t mnb = 0;   // div_magic(nb)
     if constexpr (SPILL) {
         const int b = p.inside.order_spill[block];
         n = p.len[b];
@@ -734,9 +734,10 @@ __device__ __forceinline__ void inside_block(const KernelPlan &p, int block, con
         // the record's ids are fetched with its header (a bundle holds at
         // most kMaxBundle <= blockDim.x sentences)
         const int id0 = tid < p.rec_stride - kRecHeader ? rec[kRecHeader + tid] : 0;
-        n = rec[0];
-        nb = rec[1];
-        lay = inside_layout(n, nb, rec[4] != 0);
+        n = rec[kRecN];
+        nb = rec[kRecCount];
+        lay = InsideLayout{rec[kRecLd], rec[kRecCs], rec[kRecE]};
+        mnb = (uint32_t)rec[kRecMagic];
         chart0 = reinterpret_cast<float *>(smem_raw);
         cstride = lay.cs;
         forced = reinterpret_cast<double *>(smem_raw + inside_tables_offset(nb, lay.cs));
@@ -746,7 +747,7 @@ __device__ __forceinline__ void inside_block(const KernelPlan &p, int block, con
         if (tid < nb) sid[tid] = id0;
     }
     const int ld = lay.ld;
-    const Bundle_ctx<float> bx{chart0, cstride, n, ld, nb, div_magic(nb), lay.e};
+    const Bundle_ctx<float> bx{chart0, cstride, n, ld, nb, mnb, lay.e};
     __syncthreads();
     for (int t = tid; t < nb; t += NT) {
         gv[t] = grad ? grad[sid[t]] : 1.0f;
@@ -1065,6 +1066,7 @@ __device__ __forceinline__ void cky_block(const KernelPlan &p, int block, const 
     int cstride, sstride;
     bool split_lds = false;
     CkyLayout lay;
+    uint32_t mnb = 0;   // div_magic(nb)
     if constexpr (SPILL) {
         const int b = p.cky.order_spill[block];
         n = p.len[b];
@@ -1078,11 +1080,12 @@ __device__ __forceinline__ void cky_block(const KernelPlan &p, int block, const 
         if (tid == 0) sid[0] = b;
     } else {
         const int id0 = tid < p.rec_stride - kRecHeader ? rec[kRecHeader + tid] : 0;
-        n = rec[0];
-        nb = rec[1];
-        const int split_ws = rec[2];
+        n = rec[kRecN];
+        nb = rec[kRecCount];
+        const int split_ws = rec[kRecSplitWs];
         split_lds = split_ws < 0;
-        lay = cky_layout(n, nb, split_lds ? 1 : 0, rec[4] != 0);
+        lay = CkyLayout{rec[kRecLd], rec[kRecCs], rec[kRecE]};
+        mnb = (uint32_t)rec[kRecMagic];
         chart0 = smem_raw;
         cstride = lay.cs;
         split0 = split_lds ? chart0 + (size_t)8 * lay.ld * lay.ld : p.ws + (size_t)split_ws * 256;
@@ -1092,7 +1095,7 @@ __device__ __forceinline__ void cky_block(const KernelPlan &p, int block, const 
     }
     const int ld = lay.ld;
     typedef typename std::conditional<SPILL, uint16_t, uint8_t>::type SP;
-    const Cky_ctx<SP> cx{chart0, cstride, split0, sstride, n, ld, nb, div_magic(nb), !SPILL && split_lds};
+    const Cky_ctx<SP> cx{chart0, cstride, split0, sstride, n, ld, nb, mnb, !SPILL && split_lds};
     __syncthreads();
 
     auto score_at = [&](int sb, int i, int j) -> const float * {
@@ -1173,7 +1176,7 @@ __global__ __launch_bounds__(kThreadsMax) void parse_kernel(KernelPlan p, const 
     int cur = blockIdx.x;
     for (;;) {
         const int32_t *rec = p.mix + (size_t)cur * p.rec_stride;
-        if (rec[3])
+        if (rec[kRecKind])
             inside_block<true, false, false>(p, 0, rec, smem_raw, scores, grad, logZ, marg);
         else
             cky_block<false>(p, 0, rec, smem_raw, scores, spans, best);

@@ -438,11 +438,23 @@ int crf_plan_create(crf_plan **out, const int32_t *lengths_host, int32_t batch, 
         for (size_t b = 0; b < h.bundles.size(); ++b) {
             const crf::Bundle &bd = h.bundles[b];
             int32_t *q = r.data() + b * stride;
-            q[0] = bd.n;
-            q[1] = bd.count;
-            q[2] = inside ? -1 : bd.split_ws;
-            q[3] = inside ? 1 : 0;
-            q[4] = (inside ? inside_strict(bd.n, bd.count) : cky_strict(bd.n, bd.count)) ? 1 : 0;
+            q[crf::kRecN] = bd.n;
+            q[crf::kRecCount] = bd.count;
+            q[crf::kRecSplitWs] = inside ? -1 : bd.split_ws;
+            q[crf::kRecKind] = inside ? 1 : 0;
+            if (inside) {
+                const crf::InsideLayout l = crf::inside_layout(bd.n, bd.count, inside_strict(bd.n, bd.count));
+                q[crf::kRecE] = l.e;
+                q[crf::kRecLd] = l.ld;
+                q[crf::kRecCs] = l.cs;
+            } else {
+                const crf::CkyLayout l =
+                    crf::cky_layout(bd.n, bd.count, split_in_lds(bd.n) ? 1 : 0, cky_strict(bd.n, bd.count));
+                q[crf::kRecE] = l.e;
+                q[crf::kRecLd] = l.ld;
+                q[crf::kRecCs] = l.cs;
+            }
+            q[crf::kRecMagic] = (int32_t)crf::div_magic(bd.count);
             for (int t = 0; t < bd.count; ++t) q[crf::kRecHeader + t] = h.order[bd.first + t];
         }
         return r;

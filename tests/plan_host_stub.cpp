@@ -77,21 +77,22 @@ int main(int argc, char **argv) {
     std::printf("P %d %d %d %d %d\n", kp.n_mix, kp.fused_grid, kp.inside.lds_bytes, kp.cky.lds_bytes, half_cu);
     for (int b = 0; b < kp.n_mix; ++b) {
         const int32_t *r = kp.mix + (size_t)b * kp.rec_stride;
-        const int n = r[0], count = r[1], split_ws = r[2], kind = r[3], strict = r[4];
-        int ld, cs, e;
-        long long bytes;
+        const int n = r[crf::kRecN], count = r[crf::kRecCount], split_ws = r[crf::kRecSplitWs];
+        const int kind = r[crf::kRecKind], e = r[crf::kRecE], ld = r[crf::kRecLd], cs = r[crf::kRecCs];
+        if ((uint32_t)r[crf::kRecMagic] != crf::div_magic(count)) {
+            std::printf("E magic\n");
+            return 1;
+        }
+        // which layout the plan chose: the strict one if the record holds it
+        int strict;
+        long long bytes = -1;   // (the CKY tail is the plan's; the test checks the strides)
         if (kind == 1) {
-            const crf::InsideLayout l = crf::inside_layout(n, count, strict != 0);
-            ld = l.ld;
-            cs = l.cs;
-            e = l.e;
+            const crf::InsideLayout l = crf::inside_layout(n, count, true);
+            strict = l.ld == ld && l.cs == cs && l.e == e;
             bytes = crf::inside_bundle_bytes(n, count, strict != 0);
         } else {
-            const crf::CkyLayout l = crf::cky_layout(n, count, split_ws < 0 ? 1 : 0, strict != 0);
-            ld = l.ld;
-            cs = l.cs;
-            e = l.e;
-            bytes = -1;   // (the CKY tail is the plan's; the test checks the strides)
+            const crf::CkyLayout l = crf::cky_layout(n, count, split_ws < 0 ? 1 : 0, true);
+            strict = l.ld == ld && l.cs == cs && l.e == e;
         }
         std::printf("R %d %d %d %d %d %d %d %d %lld", kind, n, count, split_ws, strict, ld, cs, e, bytes);
         for (int t = 0; t < count; ++t) std::printf(" %d", r[crf::kRecHeader + t]);
