@@ -198,7 +198,7 @@ __host__ __device__ inline int64_t cky_chart_bytes(int n, int split_bytes) {
 struct StepShape {
     int G, C, MF;
 };
-__host__ __device__ inline StepShape step_shape_k(int K) {
+__host__ __device__ constexpr StepShape step_shape_k(int K) {
     if (K <= 1) return StepShape{1, 1, 0};
     if (K <= 2) return StepShape{1, 2, 1};
     if (K <= 4) return StepShape{1, 4, 2};
@@ -215,6 +215,29 @@ __host__ __device__ inline StepShape step_shape_k(int K) {
     while (16 * g < K && g < 64) g <<= 1;
     return 12 * g >= K ? StepShape{g, 12, 8} : StepShape{g, 16, 12};
 }
+
+// The step shapes of steps of up to 128 splits as runs of K in [LO, HI]:
+// R(LO, HI, G, C, MF).  The sweeps call these runs one after the other,
+// with no shape dispatch (sentences of up to 129 words); steps of more
+// splits go through step_shape_k.
+#define CRF_FIXED_RUNS(R) \
+    R(1, 1, 1, 1, 0) R(2, 2, 1, 2, 1) R(3, 4, 1, 4, 2) R(5, 8, 1, 8, 4) R(9, 16, 2, 8, 4) R(17, 32, 4, 8, 4) \
+    R(33, 48, 4, 12, 8) R(49, 64, 4, 16, 12) R(65, 96, 4, 24, 16) R(97, 128, 4, 32, 24)
+constexpr int kFixedRunsMaxK = 128;
+constexpr bool fixed_runs_match_step_shapes() {
+    int next = 1;
+#define CRF_CHECK_RUN(LO, HI, GG, CC, MM)                                                 \
+    if (LO != next) return false;                                                       \
+    for (int K = LO; K <= HI; ++K) {                                                    \
+        const StepShape s = step_shape_k(K);                                            \
+        if (s.G != GG || s.C != CC || s.MF != MM) return false;                         \
+    }                                                                                   \
+    next = HI + 1;
+    CRF_FIXED_RUNS(CRF_CHECK_RUN)
+#undef CRF_CHECK_RUN
+    return next == kFixedRunsMaxK + 1;
+}
+static_assert(fixed_runs_match_step_shapes(), "CRF_FIXED_RUNS must list step_shape_k's runs");
 
 // The first K' > K whose step shape differs from K's (the sweeps run the
 // steps of one shape as one loop; a closed form, since a scan over the

@@ -427,44 +427,23 @@ __device__ __forceinline__ void io_run(const Bundle_ctx<T> &bx, int t0, int t1, 
     }
 }
 
-// Calls RUN(G, C, MF) for a step shape (step_shape_k never gives G = 8).
-// Charts in LDS hold at most 142 words (K <= 141), so their sweeps need
-// neither G >= 32 nor (16, 16); only the workspace (WIDE) kernels build
-// those shapes.
-#define CRF_DISPATCH_SHAPE(SH, RUN)                          \
+// Calls RUN(G, C, MF) for the shape of a step of more than 128 splits
+// (the fixed runs take the others).  Charts in LDS hold at most 142 words
+// (K <= 141), so their sweeps need only (16, 12); only the workspace (WIDE)
+// kernels build the wider shapes.
+#define CRF_DISPATCH_WIDE_SHAPE(SH, RUN)                     \
     do {                                                     \
-        switch ((SH).G) {                                    \
-            case 1:                                          \
-                switch ((SH).C) {                            \
-                    case 1: RUN(1, 1, 0); break;             \
-                    case 2: RUN(1, 2, 1); break;             \
-                    case 4: RUN(1, 4, 2); break;             \
-                    default: RUN(1, 8, 4); break;            \
-                }                                            \
-                break;                                       \
-            case 2: RUN(2, 8, 4); break;                     \
-            case 4:                                          \
-                if ((SH).C == 8) RUN(4, 8, 4);               \
-                else if ((SH).C == 12) RUN(4, 12, 8);        \
-                else if ((SH).C == 16) RUN(4, 16, 12);       \
-                else if ((SH).C == 24) RUN(4, 24, 16);       \
-                else RUN(4, 32, 24);                         \
-                break;                                       \
-            case 16:                                         \
-                if (!WIDE || (SH).C == 12) RUN(16, 12, 8);   \
-                else RUN(16, 16, 12);                        \
-                break;                                       \
-            default:                                         \
-                if constexpr (WIDE) {                        \
-                    if ((SH).G == 32) {                      \
-                        if ((SH).C == 12) RUN(32, 12, 8);    \
-                        else RUN(32, 16, 12);                \
-                    } else {                                 \
-                        if ((SH).C == 12) RUN(64, 12, 8);    \
-                        else RUN(64, 16, 12);                \
-                    }                                        \
-                }                                            \
-                break;                                       \
+        if (!WIDE || ((SH).G == 16 && (SH).C == 12)) {       \
+            RUN(16, 12, 8);                                  \
+        } else if constexpr (WIDE) {                         \
+            if ((SH).G == 16) RUN(16, 16, 12);               \
+            else if ((SH).G == 32) {                         \
+                if ((SH).C == 12) RUN(32, 12, 8);            \
+                else RUN(32, 16, 12);                        \
+            } else {                                         \
+                if ((SH).C == 12) RUN(64, 12, 8);            \
+                else RUN(64, 16, 12);                        \
+            }                                                \
         }                                                    \
     } while (0)
 
@@ -475,12 +454,15 @@ __device__ __forceinline__ void io_run(const Bundle_ctx<T> &bx, int t0, int t1, 
 template <bool WIDE, bool IL, typename T>
 __device__ __forceinline__ void fwd_sweep(const Bundle_ctx<T> &bx, const float *dsh) {
     const int n = bx.n;
-    int w = 2;
-    while (w <= n) {
+#define CRF_FWD_FIXED(LO, HI, GG, CC, MM) \
+    if (n >= LO + 1) fwd_run<GG, CC, MM, IL>(bx, LO + 1, min(HI + 2, n + 1), dsh);
+    CRF_FIXED_RUNS(CRF_FWD_FIXED)
+#undef CRF_FWD_FIXED
+    for (int w = kFixedRunsMaxK + 2; w <= n;) {
         const StepShape sh = step_shape_k(w - 1);
         const int w2 = min(shape_run_end(w - 1) + 1, n + 1);
 #define CRF_FWD_RUN(GG, CC, MM) fwd_run<GG, CC, MM, IL>(bx, w, w2, dsh)
-        CRF_DISPATCH_SHAPE(sh, CRF_FWD_RUN);
+        CRF_DISPATCH_WIDE_SHAPE(sh, CRF_FWD_RUN);
 #undef CRF_FWD_RUN
         w = w2;
     }
@@ -594,16 +576,24 @@ __device__ void rescale_chart(const Bundle_ctx<T> &bx, int t0, float *dsh) {
 template <bool WIDE, bool IL, typename T>
 __device__ __forceinline__ void io_sweep(const Bundle_ctx<T> &bx, float *dsh, int t0) {
     const int n = bx.n;
-    int t = 1;
-    while (t <= n - 1) {
-        const StepShape sh = step_shape_k(t);
-        int t2 = min(shape_run_end(t), n);
-        if (t <= t0 && t2 > t0 + 1) t2 = t0 + 1;   // the rescale follows step t0
+    // two phases, steps [1, t0] and [t0+1, n-1], with the rescale between
+    // (one copy of each run in the code)
+    for (int ph = 0; ph < 2; ++ph) {
+        const int lo = ph == 0 ? 1 : t0 + 1, hi = ph == 0 ? t0 + 1 : n;   // steps [lo, hi)
+#define CRF_IO_FIXED(LO, HI, GG, CC, MM)                              \
+        if (max(lo, LO) < min(hi, HI + 1))                            \
+            io_run<GG, CC, MM, IL>(bx, max(lo, LO), min(hi, HI + 1), dsh);
+        CRF_FIXED_RUNS(CRF_IO_FIXED)
+#undef CRF_IO_FIXED
+        for (int t = max(lo, kFixedRunsMaxK + 1); t < hi;) {
+            const StepShape sh = step_shape_k(t);
+            const int t2 = min(shape_run_end(t), hi);
 #define CRF_IO_RUN(GG, CC, MM) io_run<GG, CC, MM, IL>(bx, t, t2, dsh)
-        CRF_DISPATCH_SHAPE(sh, CRF_IO_RUN);
+            CRF_DISPATCH_WIDE_SHAPE(sh, CRF_IO_RUN);
 #undef CRF_IO_RUN
-        if (t2 - 1 == t0) rescale_chart(bx, t0, dsh);
-        t = t2;
+            t = t2;
+        }
+        if (ph == 0 && t0 > 0) rescale_chart(bx, t0, dsh);
     }
 }
 
@@ -996,12 +986,15 @@ __device__ __forceinline__ void cky_run(const Cky_ctx<SP> &cx, int w0, int w1) {
 template <bool WIDE, bool IL, typename SP>
 __device__ __forceinline__ void cky_sweep(const Cky_ctx<SP> &cx) {
     const int n = cx.n;
-    int w = 2;
-    while (w <= n) {
+#define CRF_CKY_FIXED(LO, HI, GG, CC, MM) \
+    if (n >= LO + 1) cky_run<GG, CC, MM, IL>(cx, LO + 1, min(HI + 2, n + 1));
+    CRF_FIXED_RUNS(CRF_CKY_FIXED)
+#undef CRF_CKY_FIXED
+    for (int w = kFixedRunsMaxK + 2; w <= n;) {
         const StepShape sh = step_shape_k(w - 1);
         const int w2 = min(shape_run_end(w - 1) + 1, n + 1);
 #define CRF_CKY_RUN(GG, CC, MM) cky_run<GG, CC, MM, IL>(cx, w, w2)
-        CRF_DISPATCH_SHAPE(sh, CRF_CKY_RUN);
+        CRF_DISPATCH_WIDE_SHAPE(sh, CRF_CKY_RUN);
 #undef CRF_CKY_RUN
         w = w2;
     }
