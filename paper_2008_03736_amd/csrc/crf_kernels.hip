@@ -21,6 +21,11 @@
 //     the first use.  The split-point log-sum-exp is a max / sum-exp per lane
 //     finished by a butterfly over the G lanes (DPP inside a 16-lane row,
 //     ds_swizzle across rows, readlane across the two halves of the wave).
+//   * Span order.  A step numbers its spans sentence-minor (span start i,
+//     then sentence), spread over the 32-lane (4-byte words) or 16-lane
+//     (8-byte words) groups of a wavefront, and the plan pads each bundle's
+//     row and chart strides (inside_layout, cky_layout) so that every group
+//     reads its split operands from distinct LDS banks.
 //   * alpha and the outside values are each stored twice, in two squares
 //     whose rows are stored rotated, so that every split operand of the
 //     inside and of the outside is a contiguous run (see the inside chart
@@ -45,9 +50,9 @@
 //     and exact max, so the tree is reproducible bit for bit; ties keep the
 //     lowest split, which the sweep records per span in a split table.  The
 //     tree walk only looks splits up: a node (i,j) written at preorder row r
-//     with split k puts (i,k) at row r+1 and (k,j) at row r+2(k-i).  Bundles
-//     of few (long) sentences walk breadth first, one wavefront per sentence;
-//     bundles of many (short) sentences depth first, one lane per sentence.
+//     with split k puts (i,k) at row r+1 and (k,j) at row r+2(k-i).  One
+//     lane per word p of every sentence walks down from the root towards p
+//     and writes the nodes whose leftmost word is p.
 //   * The fused launch is persistent: one workgroup per slot runs a chain of
 //     bundles, claiming each next one from a device counter as it frees up.
 #include <hip/hip_runtime.h>
