@@ -672,13 +672,41 @@ __device__ __forceinline__ void for_cells_loaded(int nb, int n, AD &&addr, LD &&
     }
 }
 
-// Log-sum-exp over labels of one span, in log2 units.
+// Log-sum-exp (log2 units) of the L label scores of one span at s: blocks
+// of 32 labels, each block's loads issued together (clamped to the last
+// label, so every load is in bounds) and its terms kept in registers;
+// label_block folds one block into the running max m and sum acc.
+__device__ __forceinline__ void label_block(const float (&v)[32], int q0, int L, float &m, float &acc) {
+    float mb = -INFINITY;
+#pragma unroll
+    for (int k = 0; k < 32; ++k) mb = q0 + k < L ? fmax_nn(mb, v[k]) : mb;
+    const float mn = fmax_nn(m, mb * LOG2E_F);
+    acc *= fast_exp2(m - mn);   // (0 * exp2(-inf) = 0 on the first block)
+#pragma unroll
+    for (int k = 0; k < 32; ++k) acc += q0 + k < L ? fast_exp2(v[k] * LOG2E_F - mn) : 0.f;
+    m = mn;
+}
 __device__ __forceinline__ float label_lse2(const float *s, int L) {
-    float m = -INFINITY;
-    for (int q = 0; q < L; ++q) m = fmax_nn(m, s[q] * LOG2E_F);
-    float acc = 0.f;
-    for (int q = 0; q < L; ++q) acc += fast_exp2(s[q] * LOG2E_F - m);
+    float m = -INFINITY, acc = 0.f;
+    for (int q0 = 0; q0 < L; q0 += 32) {
+        float v[32];
+#pragma unroll
+        for (int k = 0; k < 32; ++k) v[k] = s[min(q0 + k, L - 1)];
+        label_block(v, q0, L, m, acc);
+    }
     return m + fast_log2(acc);
+}
+// o[q] = mu exp2(s[q] log2e - lse2) for the L labels of one span, in blocks
+// of 32 as above.
+__device__ __forceinline__ void label_marginals(const float *s, int L, float mu, float lse2, float *o) {
+    for (int q0 = 0; q0 < L; q0 += 32) {
+        float v[32];
+#pragma unroll
+        for (int k = 0; k < 32; ++k) v[k] = s[min(q0 + k, L - 1)];
+#pragma unroll
+        for (int k = 0; k < 32; ++k)
+            if (q0 + k < L) o[q0 + k] = mu * fast_exp2(v[k] * LOG2E_F - lse2);
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -760,7 +788,7 @@ __device__ __forceinline__ void inside_block(const KernelPlan &p, int block, con
     };
     auto load_score = [&](const float *q) -> float {
         if constexpr (LAB)
-            return label_lse2(q, L) * (float)LN2_D;
+            return label_lse2(q, L) * (float)LN2_D;   // the label log-sum-exp is the span's score
         else
             return *q;
     };
@@ -823,25 +851,63 @@ __device__ __forceinline__ void inside_block(const KernelPlan &p, int block, con
     // Epilogue: marginals of the valid cells (coalesced stores along rows),
     //   mu(i,j) = g exp2(alpha~(i,j) + O'(i,j) - (s(i,j) + d) - alpha~(0,n)),
     // and exactly g on forced spans.
-    for_cells_loaded<LAB ? 1 : 8>(nb, n, score_at, load_score, [&](int sb, int i, int j, float s) {
-        const size_t rowoff = (size_t)sid[sb] * sent_stride + (size_t)i * row_stride;
+    // mu of a valid cell whose own score (log2 units) is own2
+    auto span_mu = [&](int sb, int i, int j, float own2) {
         const float *P = chart0 + (size_t)sb * cstride, *Q = P + (size_t)ld * ld;
         const bool forced_span = (j == i + 1) || (i == 0 && j == n);
         float mu = gv[sb];
         if (!forced_span) {
-            const float own = s * LOG2E_F + dsh[sb];
             const int w = j - i;
-            mu *= fast_exp2(((P[i * ld + w - 1] - P[n - 1]) + Q[i * ld + w]) - own);
+            mu *= fast_exp2(((P[i * ld + w - 1] - P[n - 1]) + Q[i * ld + w]) - (own2 + dsh[sb]));
         }
-        if constexpr (LAB) {
-            const float *sl = scores + rowoff + (size_t)j * L;
-            const float lse2 = label_lse2(sl, L);
-            float *o = marg + rowoff + (size_t)j * L;
-            for (int q = 0; q < L; ++q) o[q] = mu * fast_exp2(sl[q] * LOG2E_F - lse2);
+        return mu;
+    };
+    if constexpr (LAB) {
+        // Up to 32 labels: one load of a span's labels serves its log-sum-exp
+        // (the same arithmetic as the prologue's, so the same own score) and
+        // its per-label marginals, two spans per thread at a time.
+        if (L <= 32) {
+            const Cell_walk cw(nb, n);
+            for (int c0 = tid; c0 < cw.total; c0 += NT * 2) {
+                Cell e[2];
+                const float *q[2];
+                float v[2][32];
+#pragma unroll
+                for (int u = 0; u < 2; ++u) {
+                    e[u] = cw.at(c0 + u * NT);
+                    q[u] = score_at(e[u].sb, e[u].i, e[u].j);
+                }
+#pragma unroll
+                for (int u = 0; u < 2; ++u)
+#pragma unroll
+                    for (int k = 0; k < 32; ++k) v[u][k] = q[u][min(k, L - 1)];
+                __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                for (int u = 0; u < 2; ++u) {
+                    float m = -INFINITY, acc = 0.f;
+                    label_block(v[u], 0, L, m, acc);
+                    const float own2 = ((m + fast_log2(acc)) * (float)LN2_D) * LOG2E_F;   // as the chart holds it
+                    const float mu = span_mu(e[u].sb, e[u].i, e[u].j, own2);
+                    if (e[u].ok) {
+                        float *o = marg + (q[u] - scores);
+#pragma unroll
+                        for (int k = 0; k < 32; ++k)
+                            if (k < L) o[k] = mu * fast_exp2(v[u][k] * LOG2E_F - own2);
+                    }
+                }
+            }
         } else {
-            marg[rowoff + j] = mu;
+            for_cells_loaded<1>(nb, n, score_at, load_score, [&](int sb, int i, int j, float s) {
+                const float mu = span_mu(sb, i, j, s * LOG2E_F);
+                const size_t cell = (size_t)sid[sb] * sent_stride + (size_t)i * row_stride + (size_t)j * L;
+                label_marginals(scores + cell, L, mu, s * LOG2E_F, marg + cell);
+            });
         }
-    });
+    } else {
+        for_cells_loaded<8>(nb, n, score_at, load_score, [&](int sb, int i, int j, float s) {
+            marg[(size_t)sid[sb] * sent_stride + (size_t)i * row_stride + j] = span_mu(sb, i, j, s * LOG2E_F);
+        });
+    }
 }
 
 // ---------------------------------------------------------------------------

@@ -88,10 +88,14 @@ struct HostSchedule {
 };
 
 // Cost model of one sentence for sizing bundles: split points plus a latency
-// term per width step.
-inline double sentence_cost(int n) {
+// term per width step, plus, for labelled scores, a term per label of every
+// span (each is read twice and written once, 32 labels of a span per lane
+// group; about 30 split points' worth, measured on 26 labels).
+constexpr double kLabelCellCost = 30.0;
+inline double sentence_cost(int n, int labels = 1) {
     const double T = (double)(n + 1) * n * (n - 1) / 6.0;
-    return T + 200.0 * (n - 1);
+    const double cells = labels > 1 ? (double)n * (n + 1) / 2.0 * labels : 0.0;
+    return T + 200.0 * (n - 1) + kLabelCellCost * cells;
 }
 
 // Predicted duration (microseconds on MI355X, two workgroups per CU) of a
@@ -219,6 +223,9 @@ void plan_fused_launch(std::vector<crf::Bundle> &in, std::vector<crf::Bundle> &c
 // little, and fewer, fuller bundles measured 3-5% faster on the 5,000-sentence
 // mixed batch than an even share; CKY bundles take the share.
 constexpr double kInsideTargetScale = 2.0, kCkyTargetScale = 1.0;
+// Labelled bundles spend most of their time reading and writing labels, a
+// latency-bound pass per bundle: they aim at one slot's share.
+constexpr double kLabelTargetScale = 1.0;
 
 // `order` is sorted by decreasing length.  `bundle_bytes(n, count)` is the
 // LDS of a bundle of `count` sentences of n words, `spill_chart(n)` a
@@ -229,7 +236,7 @@ constexpr double kInsideTargetScale = 2.0, kCkyTargetScale = 1.0;
 template <typename BB, typename FS>
 HostSchedule make_schedule(const std::vector<int32_t> &order, const int32_t *len, int lds_cap,
                            bool force_spill, int64_t ws_base, BB &&bundle_bytes, FS &&spill_chart,
-                           double target_scale) {
+                           double target_scale, int labels = 1) {
     HostSchedule s;
     s.threads = crf::kThreadsDefault;
     // Workgroup LDS budget: half the CU when every eligible sentence fits in
@@ -260,7 +267,7 @@ HostSchedule make_schedule(const std::vector<int32_t> &order, const int32_t *len
     // Target cost per bundle: spread the total over the workgroup slots, but
     // never split below one sentence.
     double total = 0.0;
-    for (int32_t b : eligible) total += sentence_cost(len[b]);
+    for (int32_t b : eligible) total += sentence_cost(len[b], labels);
     const double target = std::max(total / slots, 1.0) * target_scale;
 
     struct Tmp { crf::Bundle bd; double cost; };
@@ -273,7 +280,7 @@ HostSchedule make_schedule(const std::vector<int32_t> &order, const int32_t *len
         const int count = (int)(e - a);
         int by_lds = 1;
         while (by_lds < crf::kMaxBundle && bundle_bytes(n, by_lds + 1) <= budget) ++by_lds;
-        const int by_cost = std::max(1, (int)(target / sentence_cost(n)));
+        const int by_cost = std::max(1, (int)(target / sentence_cost(n, labels)));
         const int per = std::min(by_lds, std::max(1, by_cost));
         const int nbund = (count + per - 1) / per;
         for (int q = 0; q < nbund; ++q) {
@@ -283,7 +290,7 @@ HostSchedule make_schedule(const std::vector<int32_t> &order, const int32_t *len
             t.bd.count = hi - lo;
             t.bd.n = n;
             t.bd.split_ws = -1;
-            t.cost = (hi - lo) * (sentence_cost(n) - 200.0 * (n - 1)) + 200.0 * (n - 1);
+            t.cost = (hi - lo) * (sentence_cost(n, labels) - 200.0 * (n - 1)) + 200.0 * (n - 1);
             tmp.push_back(t);
             s.lds_bytes = std::max<int32_t>(s.lds_bytes, (int32_t)bundle_bytes(n, hi - lo));
         }
@@ -392,7 +399,8 @@ int crf_plan_create(crf_plan **out, const int32_t *lengths_host, int32_t batch, 
     auto cky_strict = [=](int n, int64_t count) { return cky_bytes_with(n, count, true) <= half_cu; };
     auto cky_bundle_bytes = [=](int n, int64_t count) { return cky_bytes_with(n, count, cky_strict(n, count)); };
     HostSchedule si = make_schedule(order, lengths_host, lds_cap, force, 0, inside_bundle_bytes,
-                                    inside_spill_bytes, kInsideTargetScale);
+                                    inside_spill_bytes, num_labels > 1 ? kLabelTargetScale : kInsideTargetScale,
+                                    num_labels);
     HostSchedule sc = make_schedule(order, lengths_host, lds_cap, force, si.ws_bytes, cky_bundle_bytes,
                                     cky_spill_bytes, kCkyTargetScale);
     int64_t split_cursor = si.ws_bytes + sc.ws_bytes;

@@ -3,7 +3,8 @@
 // the launch entry points are never called.  Prints the plan's records:
 //   P n_mix fused_grid lds_inside lds_cky half_cu
 //   R kind n count split_ws strict ld cs e bytes id...
-// one R line per record of the fused queue, in queue order.
+// one R line per record of the fused queue, in queue order.  Arguments: a file
+// of sentence lengths, and optionally the number of labels.
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
@@ -67,7 +68,8 @@ int main(int argc, char **argv) {
     int n1 = 2;
     for (int v : len) n1 = std::max(n1, v + 1);
     crf_plan *p = nullptr;
-    const int rc = crf_plan_create(&p, len.data(), (int32_t)len.size(), n1, 1, 0);
+    const int labels = argc > 2 ? std::atoi(argv[2]) : 1;
+    const int rc = crf_plan_create(&p, len.data(), (int32_t)len.size(), n1, labels, 0);
     if (rc != CRF_OK) {
         std::printf("E %d\n", rc);
         return 1;
@@ -97,6 +99,12 @@ int main(int argc, char **argv) {
         std::printf("R %d %d %d %d %d %d %d %d %lld", kind, n, count, split_ws, strict, ld, cs, e, bytes);
         for (int t = 0; t < count; ++t) std::printf(" %d", r[crf::kRecHeader + t]);
         std::printf("\n");
+    }
+    // Labelled plans have no fused queue: their inside bundles, as
+    //   I n count
+    for (int b = 0; kp.n_mix == 0 && b < kp.inside.n_bundles; ++b) {
+        const int32_t *r = kp.inside.recs + (size_t)b * kp.rec_stride;
+        std::printf("I %d %d\n", r[crf::kRecN], r[crf::kRecCount]);
     }
     crf_plan_destroy(p);
     return 0;
