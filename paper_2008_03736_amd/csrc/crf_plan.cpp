@@ -366,11 +366,15 @@ int crf_plan_create(crf_plan **out, const int32_t *lengths_host, int32_t batch, 
                      [&](int32_t a, int32_t b) { return lengths_host[a] > lengths_host[b]; });
 
     const bool force = (flags & CRF_FORCE_SPILL) != 0;
-    // Inside bundles take the strict chart layout when it fits in half a CU,
-    // else the loose one (inside_layout).
-    const int64_t half_cu = lds_cap / 2 - crf::kReservedLds;
+    // Bundles take the strict chart layout when it fits in half a CU, or,
+    // for a bundle that needs a whole CU in either layout, in the whole CU;
+    // else the loose one (inside_layout, cky_layout).
+    const int64_t half_cu = lds_cap / 2 - crf::kReservedLds, full_cu = lds_cap - crf::kReservedLds;
+    auto strict_fits = [=](int64_t strict_bytes, int64_t loose_bytes) {
+        return strict_bytes <= half_cu || (loose_bytes > half_cu && strict_bytes <= full_cu);
+    };
     auto inside_strict = [=](int n, int64_t count) {
-        return crf::inside_bundle_bytes(n, (int)count, true) <= half_cu;
+        return strict_fits(crf::inside_bundle_bytes(n, (int)count, true), crf::inside_bundle_bytes(n, (int)count, false));
     };
     auto inside_bundle_bytes = [=](int n, int64_t count) {
         return crf::inside_bundle_bytes(n, (int)count, inside_strict(n, count));
@@ -396,7 +400,9 @@ int crf_plan_create(crf_plan **out, const int32_t *lengths_host, int32_t batch, 
         const int cs = crf::cky_layout(n, (int)count, split_in_lds(n) ? 1 : 0, strict).cs;
         return count * (cs + 4) + crf::bundle_extra_bytes(n) + cky_tail(n, count);
     };
-    auto cky_strict = [=](int n, int64_t count) { return cky_bytes_with(n, count, true) <= half_cu; };
+    auto cky_strict = [=](int n, int64_t count) {
+        return strict_fits(cky_bytes_with(n, count, true), cky_bytes_with(n, count, false));
+    };
     auto cky_bundle_bytes = [=](int n, int64_t count) { return cky_bytes_with(n, count, cky_strict(n, count)); };
     HostSchedule si = make_schedule(order, lengths_host, lds_cap, force, 0, inside_bundle_bytes,
                                     inside_spill_bytes, num_labels > 1 ? kLabelTargetScale : kInsideTargetScale,
