@@ -686,12 +686,35 @@ __device__ __forceinline__ void label_block(const float (&v)[32], int q0, int L,
     for (int k = 0; k < 32; ++k) acc += q0 + k < L ? fast_exp2(v[k] * LOG2E_F - mn) : 0.f;
     m = mn;
 }
-__device__ __forceinline__ float label_lse2(const float *s, int L) {
+// The first 32 labels of a span into v (clamped to the last label), with
+// 8-byte loads when `wide`: an even count on an 8-byte aligned score tensor
+// (every span's offset is then a multiple of 2 floats).  The values are the
+// same either way.
+__device__ __forceinline__ void label_load32(const float *s, int L, bool wide, float (&v)[32]) {
+    if (wide) {
+        const float2 *s2 = reinterpret_cast<const float2 *>(s);
+        const int last = L / 2 - 1;
+#pragma unroll
+        for (int k = 0; k < 16; ++k) {
+            const float2 x = s2[min(k, last)];
+            v[2 * k] = x.x;
+            v[2 * k + 1] = x.y;
+        }
+    } else {
+#pragma unroll
+        for (int k = 0; k < 32; ++k) v[k] = s[min(k, L - 1)];
+    }
+}
+__device__ __forceinline__ float label_lse2(const float *s, int L, bool wide) {
     float m = -INFINITY, acc = 0.f;
     for (int q0 = 0; q0 < L; q0 += 32) {
         float v[32];
+        if (q0 == 0) {
+            label_load32(s, L, wide, v);
+        } else {
 #pragma unroll
-        for (int k = 0; k < 32; ++k) v[k] = s[min(q0 + k, L - 1)];
+            for (int k = 0; k < 32; ++k) v[k] = s[min(q0 + k, L - 1)];
+        }
         label_block(v, q0, L, m, acc);
     }
     return m + fast_log2(acc);
@@ -786,9 +809,12 @@ __device__ __forceinline__ void inside_block(const KernelPlan &p, int block, con
     auto score_at = [&](int sb, int i, int j) -> const float * {
         return scores + (size_t)sid[sb] * sent_stride + (size_t)i * row_stride + (size_t)j * (LAB ? L : 1);
     };
+    // 8-byte label accesses: an even label count on 8-byte aligned tensors
+    const bool wide_in = LAB && (L & 1) == 0 && ((uintptr_t)scores & 7) == 0;
+    const bool wide_out = wide_in && ((uintptr_t)marg & 7) == 0;
     auto load_score = [&](const float *q) -> float {
         if constexpr (LAB)
-            return label_lse2(q, L) * (float)LN2_D;   // the label log-sum-exp is the span's score
+            return label_lse2(q, L, wide_in) * (float)LN2_D;   // the label log-sum-exp is the span's score
         else
             return *q;
     };
@@ -878,9 +904,7 @@ __device__ __forceinline__ void inside_block(const KernelPlan &p, int block, con
                     q[u] = score_at(e[u].sb, e[u].i, e[u].j);
                 }
 #pragma unroll
-                for (int u = 0; u < 2; ++u)
-#pragma unroll
-                    for (int k = 0; k < 32; ++k) v[u][k] = q[u][min(k, L - 1)];
+                for (int u = 0; u < 2; ++u) label_load32(q[u], L, wide_in, v[u]);
                 __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
                 for (int u = 0; u < 2; ++u) {
@@ -890,9 +914,18 @@ __device__ __forceinline__ void inside_block(const KernelPlan &p, int block, con
                     const float mu = span_mu(e[u].sb, e[u].i, e[u].j, own2);
                     if (e[u].ok) {
                         float *o = marg + (q[u] - scores);
+                        if (wide_out) {   // 8-byte stores
+                            float2 *o2 = reinterpret_cast<float2 *>(o);
 #pragma unroll
-                        for (int k = 0; k < 32; ++k)
-                            if (k < L) o[k] = mu * fast_exp2(v[u][k] * LOG2E_F - own2);
+                            for (int k = 0; k < 16; ++k)
+                                if (2 * k < L)
+                                    o2[k] = make_float2(mu * fast_exp2(v[u][2 * k] * LOG2E_F - own2),
+                                                        mu * fast_exp2(v[u][2 * k + 1] * LOG2E_F - own2));
+                        } else {
+#pragma unroll
+                            for (int k = 0; k < 32; ++k)
+                                if (k < L) o[k] = mu * fast_exp2(v[u][k] * LOG2E_F - own2);
+                        }
                     }
                 }
             }

@@ -195,6 +195,27 @@ def test_labeled_small(torch):
     check_marg(out["marg"], mu, b.lengths, b.n1, labeled=True)
 
 
+@pytest.mark.parametrize("offset", [0, 1])
+@pytest.mark.parametrize("labels", [6, 7])
+def test_labeled_alignment(torch, offset, labels):
+    # labelled scores and marginals 8-byte aligned (offset 0) or only 4-byte
+    # aligned (offset 1 float), with an even and an odd label count: the
+    # 8-byte label accesses are taken only for even counts on aligned
+    # tensors, and every case gives the same results
+    b = W.custom([5, 12, 30, 31], seed=41 + labels, sd=1.0, labels=labels)
+    dev = torch.device("cuda", 0)
+    size = b.scores.size
+    s = torch.empty(size + 1, dtype=torch.float32, device=dev)[offset:offset + size].view(b.scores.shape)
+    s.copy_(torch.from_numpy(b.scores))
+    m = torch.full((size + 1,), float("nan"), dtype=torch.float32, device=dev)[offset:offset + size].view(b.scores.shape)
+    with B.Plan(b.lengths, n1=b.n1, num_labels=b.num_labels, device=dev) as plan:
+        lz, mu_gpu = plan.inside_fwd_bwd(s, marginals=m)
+        torch.cuda.synchronize()
+    lz_ref, mu_ref = orc.labeled(b.scores, b.lengths)
+    check_logz(lz.cpu().numpy(), lz_ref)
+    check_marg(mu_gpu.cpu().numpy(), mu_ref, b.lengths, b.n1, labeled=True)
+
+
 @pytest.mark.parametrize("name", ["tiny", "mixed"])
 def test_fused_call_matches_separate_calls(torch, name):
     # one launch for inside + reverse + CKY gives the separate calls' bits
