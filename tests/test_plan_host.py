@@ -48,7 +48,9 @@ def plan_of(harness, tmp_path, lengths):
 def check_plan(head, recs, lengths):
     lengths = np.asarray(lengths)
     assert head["n_mix"] == len(recs)
-    assert head["grid"] == min(len(recs), 512)
+    # one workgroup slot per CU per bundle LDS that fits (256 CUs, 160 KiB each)
+    per_cu = min(4, max(1, 163840 // max(head["lds_in"], head["lds_ck"])))
+    assert head["grid"] == min(len(recs), 256 * per_cu)
     for kind in (0, 1):
         ids = [i for r in recs if r["kind"] == kind for i in r["ids"]]
         assert sorted(ids) == list(range(len(lengths))), "every sentence once per kind"
@@ -58,7 +60,7 @@ def check_plan(head, recs, lengths):
         n, nb, ld, cs = r["n"], r["count"], r["ld"], r["cs"]
         if r["kind"] == 1:
             assert ld >= n + 1 and 2 * ld * ld <= cs < 2 * ld * ld + 32
-            assert 0 < r["bytes"] <= head["lds_in"] <= head["half_cu"]
+            assert 0 < r["bytes"] <= head["lds_in"] <= 2 * head["half_cu"] + 256
             if r["strict"] and r["e"] == 0 and not (nb >= 32 and nb % 4 == 0):
                 # span g's runs start at sigma g (mod 32): cs = sigma odd, ld = nb sigma
                 assert cs % 2 == 1 and (ld - nb * cs) % 32 == 0, r
@@ -71,12 +73,19 @@ def check_plan(head, recs, lengths):
                 assert u % 2 == 1 and ld % 2 == 0
 
 
-@pytest.mark.parametrize("name", ["tiny", "mixed"])
+@pytest.mark.parametrize("name", ["tiny", "mixed", "longer"])
 def test_plan_of_workloads(harness, tmp_path, name):
     b = W.make(name)
     head, recs = plan_of(harness, tmp_path, b.lengths)
     check_plan(head, recs, b.lengths)
+    if name == "longer":
+        # sentences of more than 99 words need a whole CU in either layout:
+        # the launch runs one workgroup per CU, and those bundles take the
+        # strict layout there
+        assert head["lds_in"] > head["half_cu"]
+        assert all(r["strict"] for r in recs if r["kind"] == 1 and r["n"] > 99)
     if name == "mixed":
+        assert head["lds_in"] <= head["half_cu"]
         # both layouts occur, and most bundles take the strict one
         for kind in (0, 1):
             flags = [r["strict"] for r in recs if r["kind"] == kind]
