@@ -101,10 +101,12 @@ int main(int argc, char **argv) {
         std::printf("\n");
     }
     // Labelled plans have no fused queue: their inside bundles, as
-    //   I n count
+    //   I n count id...
     for (int b = 0; kp.n_mix == 0 && b < kp.inside.n_bundles; ++b) {
         const int32_t *r = kp.inside.recs + (size_t)b * kp.rec_stride;
-        std::printf("I %d %d\n", r[crf::kRecN], r[crf::kRecCount]);
+        std::printf("I %d %d", r[crf::kRecN], r[crf::kRecCount]);
+        for (int t = 0; t < r[crf::kRecCount]; ++t) std::printf(" %d", r[crf::kRecHeader + t]);
+        std::printf("\n");
     }
     crf_plan_destroy(p);
     return 0;

@@ -29,10 +29,11 @@ def harness(tmp_path_factory):
     return out
 
 
-def plan_of(harness, tmp_path, lengths):
+def plan_of(harness, tmp_path, lengths, labels=None):
     f = tmp_path / "lengths.txt"
     f.write_text("\n".join(str(int(v)) for v in lengths))
-    res = subprocess.run([harness, str(f)], capture_output=True, text=True, check=True)
+    args = [harness, str(f)] + ([str(labels)] if labels is not None else [])
+    res = subprocess.run(args, capture_output=True, text=True, check=True)
     head, recs = None, []
     for line in res.stdout.splitlines():
         t = line.split()
@@ -42,6 +43,9 @@ def plan_of(harness, tmp_path, lengths):
             v = list(map(int, t[1:]))
             recs.append(dict(kind=v[0], n=v[1], count=v[2], split_ws=v[3], strict=v[4], ld=v[5], cs=v[6],
                              e=v[7], bytes=v[8], ids=v[9:]))
+        elif t[0] == "I":
+            v = list(map(int, t[1:]))
+            recs.append(dict(kind=1, n=v[0], count=v[1], ids=v[2:]))
     return head, recs
 
 
@@ -105,3 +109,18 @@ def test_plan_of_one_length(harness, tmp_path, n, count):
     lengths = [n] * count + [99] * 200
     head, recs = plan_of(harness, tmp_path, lengths)
     check_plan(head, recs, lengths)
+
+
+@pytest.mark.parametrize("labels,seed", [(2, 0), (7, 1), (32, 2), (33, 3), (100, 4)])
+def test_plan_of_labelled_batches(harness, tmp_path, labels, seed):
+    # labelled plans run inside bundles only (no fused queue); each sentence
+    # in exactly one bundle of sentences of its own length
+    rng = np.random.default_rng(seed)
+    lengths = rng.integers(1, 100, size=int(rng.integers(1, 2000)))
+    head, recs = plan_of(harness, tmp_path, lengths, labels)
+    assert head["n_mix"] == 0 and recs
+    ids = [i for r in recs for i in r["ids"]]
+    assert sorted(ids) == list(range(len(lengths)))
+    for r in recs:
+        assert r["count"] == len(r["ids"]) >= 1
+        assert all(lengths[i] == r["n"] for i in r["ids"])
