@@ -3,8 +3,8 @@
 
 One step = one pass of the whole path over the batch: inside (log Z), span
 marginals (the derivative of log Z, as inside x outside) and CKY decode
-(1-best trees), in one fused launch.  Inputs are resident in HBM before timing starts.  Prints one JSON
-line.
+(1-best trees), in one fused launch.  Inputs are resident in HBM before
+timing starts.  Prints one JSON line.
 
   python bench.py [--steps K] [--warmup W] [--workload mixed] [--no-cpu-baseline]
 
@@ -12,21 +12,29 @@ Roofline: the hot path is one launch (parse_kernel: inside + marginal and CKY
 workgroups side by side).  It is bound by plain vector-ALU work and by the
 dependency chain of width steps, not by HBM and not by MFMA.  Algorithmic work
 per sentence of n words, with T(n) = (n+1)n(n-1)/6 split points and
-P(n) = n(n+1)/2 spans, in VALU issue slots (a transcendental v_exp/v_log/v_rcp
-costs 2 slots, as measured on gfx950), counting the marginals as a reverse-mode
-pass (the cheaper formulation; the kernel's outside pass does more):
-  inside   per split: add, max, sub, exp, add          = 6
-           per span:  log, 2 adds                      = 4
-  reverse  per split: sub, exp, mul, 2 adds            = 6
-           per span:  add, rcp                         = 2
-  CKY      per split: add, compare, select             = 3
-           per span:  add                              = 1
+P(n) = n(n+1)/2 spans, in VALU issue slots, counting the marginals as a
+reverse-mode pass (the cheaper formulation; the kernel's outside pass does
+more).  Per split: inside 1 exp + 4 VALU, reverse 1 exp + 4 VALU, CKY 3 VALU;
+per span: inside 1 log + 2, reverse 2, CKY 1.  Labelled scores add, per span
+and label, 1 exp + 3 (label log-sum-exp) and 1 exp + 2 (per-label marginal).
+A transcendental is priced two ways:
+  frac                     4 slots (the scope document's op model, quarter rate)
+  frac_measured_trans_rate 2 slots (v_exp_f32 / v_log_f32 measured at half the
+                           fp32 add rate on gfx950 and not co-issued; see
+                           --ceilings and profiles/ceilings_gfx950.txt)
 Peak = 256 CUs x 64 lanes x 2.4 GHz = 39.32 T lane-slots/s.
+
+  python bench.py --ceilings   measures the ceilings the model rests on
+                               (fp32 add / FMA, fp64 add, exp2, log2, exp2 with
+                               independent adds, LDS reads, barrier round trip)
+                               with the microbenchmark kernels of
+                               libcrfceilings.so and prints one JSON line.
 """
 import argparse
 import ctypes
 import json
 import os
+import platform
 import sys
 import time
 
@@ -37,58 +45,118 @@ sys.path.insert(0, ROOT)
 
 PEAK_SLOTS = 256 * 64 * 2.4e9   # VALU lane-slots per second
 HBM_PEAK = 8.0e12               # bytes per second
-# HBM bytes per launch of the timed kernel from rocprofv3 FETCH_SIZE / WRITE_SIZE,
-# scaled by the same counters on a plain copy of known size, keyed by workload
-# and by the kernel source they were taken on (reported only while it matches).
-MEASURED_TRAFFIC = {"mixed": (76.01e6, "dd5a193d65ff39e9")}
+# HBM bytes per launch of the timed kernel from rocprofv3 FETCH_SIZE /
+# WRITE_SIZE, each scaled by the same counter on a plain copy of known size,
+# keyed by workload and by the kernel source they were taken on: reported only
+# while that source is unchanged (else null).  `profile` names the committed
+# summary that holds the counters and the scaling.
+MEASURED_TRAFFIC = {
+    "mixed": {"bytes": 76.01e6, "source_sha16": "dd5a193d65ff39e9",
+              "profile": "profiles/parse_kernel_mixed5000.txt"},
+}
 METRIC = "sentences/sec for inside fwd+bwd and CKY decode; % of binding roofline"
 
 
-def work_model(lengths, labels=1):
+def work_model(lengths, labels=1, trans_slots=4):
+    """Algorithmic VALU issue slots and HBM bytes of one pass (see the module
+    docstring), with a transcendental priced at trans_slots."""
     n = lengths.astype(np.int64)
-    T = (n + 1) * n * (n - 1) // 6
-    P = n * (n + 1) // 2
-    slots_inside = 12 * T.sum() + 6 * P.sum()
-    if labels > 1:   # label log-sum-exp and per-label marginals: (exp + 3) + (exp + 2) per label
-        slots_inside += P.sum() * labels * (2 + 3 + 2 + 2)
-    slots_cky = 3 * T.sum() + P.sum()
-    bytes_inside = 4 * P.sum() * labels * 2 + 4 * len(n)      # scores in, marginals out, logZ
-    bytes_cky = 4 * P.sum() + 8 * (2 * n - 1).sum() + 4 * len(n)
-    return dict(T=int(T.sum()), P=int(P.sum()), slots_inside=int(slots_inside),
-                slots_cky=int(slots_cky), bytes_inside=int(bytes_inside), bytes_cky=int(bytes_cky))
+    T = int(((n + 1) * n * (n - 1) // 6).sum())
+    P = int((n * (n + 1) // 2).sum())
+    e = trans_slots
+    slots_inside = (e + 4) * T + (e + 2) * P + (e + 4) * T + 2 * P
+    if labels > 1:
+        slots_inside += P * labels * ((e + 3) + (e + 2))
+    slots_cky = 3 * T + P
+    bytes_inside = 4 * P * labels * 2 + 4 * len(n)      # scores in, marginals out, logZ
+    bytes_cky = 4 * P + 8 * int((2 * n - 1).sum()) + 4 * len(n)
+    return dict(T=T, P=P, slots_inside=int(slots_inside), slots_cky=int(slots_cky),
+                bytes_inside=int(bytes_inside), bytes_cky=int(bytes_cky))
+
+
+def source_sha16():
+    import hashlib
+
+    src = os.path.join(ROOT, "paper_2008_03736_amd", "csrc", "crf_kernels.hip")
+    with open(src, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
 def measured_traffic(workload):
-    import hashlib
-
-    if workload not in MEASURED_TRAFFIC:
-        return None
-    nbytes, digest = MEASURED_TRAFFIC[workload]
-    src = os.path.join(ROOT, "paper_2008_03736_amd", "csrc", "crf_kernels.hip")
-    with open(src, "rb") as f:
-        now = hashlib.sha256(f.read()).hexdigest()[:16]
-    return nbytes if now == digest else None
+    m = MEASURED_TRAFFIC.get(workload)
+    if m is None or m["source_sha16"] != source_sha16():
+        return None, None
+    return m["bytes"], m["profile"]
 
 
-def cpu_baseline(batch, threads, budget_s=12.0):
-    """The float64 oracle (marginals + CKY) on the host, repeated over the
-    workload until about budget_s seconds have been spent."""
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or "unknown"
+
+
+def oracle_rate(batch, threads, budget_s):
+    """Sentences/s of the float64 oracle (marginals by the reverse-mode
+    adjoint, then CKY) over whole passes of the batch, or over a prefix of it
+    when one pass would take much longer than the budget."""
     from oracle import oracle as orc
 
     out = np.empty((batch.B, batch.n1, batch.n1), np.float64)
     orc.marginals(batch.scores[:8], batch.lengths[:8], threads=1)   # load / build
+    # size the sample from a first timed chunk
+    k = min(batch.B, 64)
+    t0 = time.perf_counter()
+    orc.marginals(batch.scores[:k], batch.lengths[:k], threads=threads, out=out[:k])
+    orc.cky(batch.scores[:k], batch.lengths[:k], threads=threads)
+    per = (time.perf_counter() - t0) / k
+    m = int(min(batch.B, max(k, budget_s / max(per, 1e-9))))
     done, t0 = 0, time.perf_counter()
     while True:
-        orc.marginals(batch.scores, batch.lengths, threads=threads, out=out)
-        orc.cky(batch.scores, batch.lengths, threads=threads)
-        done += batch.B
+        orc.marginals(batch.scores[:m], batch.lengths[:m], threads=threads, out=out[:m])
+        orc.cky(batch.scores[:m], batch.lengths[:m], threads=threads)
+        done += m
         el = time.perf_counter() - t0
         if el >= budget_s:
             break
-    return {"value": round(done / el, 1), "unit": "sentences/s", "cores": threads,
-            "kind": "oracle",
-            "sample": f"whole {batch.name} batch ({batch.B} sentences) x {done // batch.B} passes "
-                      f"of float64 marginals (reverse-mode) + CKY, {el:.1f} s, {threads} threads"}
+    passes = done / batch.B
+    what = (f"{done // m} passes over the whole {batch.name} batch ({batch.B} sentences)" if m == batch.B
+            else f"{done // m} passes over its first {m} of {batch.B} sentences")
+    return done / el, f"{what}: float64 marginals (reverse-mode) + CKY, {el:.1f} s, {threads} thread(s)", passes
+
+
+def cpu_baseline(batch, threads, budget_s=10.0):
+    """The oracle as it stands, timed on the host cores: all-core (threads)
+    and single-threaded."""
+    v_all, s_all, _ = oracle_rate(batch, threads, budget_s)
+    v_one, s_one, _ = oracle_rate(batch, 1, budget_s)
+    return {"value": round(v_all, 1), "unit": "sentences/s", "cores": threads, "kind": "oracle",
+            "sample": s_all, "cpu_model": cpu_model(), "nproc": os.cpu_count(),
+            "single_thread": {"value": round(v_one, 1), "cores": 1, "sample": s_one}}
+
+
+def stats_ms(samples):
+    a = np.asarray(samples, np.float64)
+    return {"mean": round(float(a.mean()), 5), "median": round(float(np.median(a)), 5),
+            "p10": round(float(np.percentile(a, 10)), 5), "p90": round(float(np.percentile(a, 90)), 5),
+            "n": int(a.size)}
+
+
+def run_ceilings():
+    """Microbenchmarked ceilings of gfx950 (lane-operations per second)."""
+    import torch
+
+    from paper_2008_03736_amd import ceilings as C
+
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    res = C.measure_all(torch, dev)
+    line = {"metric": "gfx950 ceilings", "peak_lane_slots_per_s": PEAK_SLOTS, "ceilings": res}
+    print(json.dumps(line), flush=True)
 
 
 def main():
@@ -96,6 +164,8 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--launches", type=int, default=100,
+                    help="per-launch event-timed launches for median/p10/p90 (at least 100)")
     ap.add_argument("--workload", default="mixed")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -103,12 +173,16 @@ def main():
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="after timing, run a plain device copy of this many MiB a few times "
                          "(a known-size kernel to scale HBM counters by)")
+    ap.add_argument("--ceilings", action="store_true", help="measure the ALU / LDS ceilings and exit")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); "
               "sentences are independent and would be sharded by sentence, see DESIGN.md",
               file=sys.stderr)
         sys.exit(2)
+    if args.ceilings:
+        run_ceilings()
+        return
 
     import torch
 
@@ -164,21 +238,28 @@ def main():
     torch.cuda.synchronize()
     ms_per_step = e0.elapsed_time(e1) / args.steps
 
+    # Labelled scores (877 MB padded, 38.6 MB valid) would otherwise be served
+    # from the 256 MB Infinity Cache between launches: a 512 MiB fill between
+    # timed launches evicts them, and each event pair brackets the launch alone.
+    flush = torch.empty(512 << 18, dtype=torch.float32, device=dev) if not decode else None
+
     # Per-launch durations, one event pair per launch on the launch stream.
-    def per_launch_ms(fn, reps):
+    def per_launch(fn, reps):
         evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
                for _ in range(reps)]
         for a, b in evs:
+            if flush is not None:
+                flush.fill_(1.0)
             a.record(stream)
             fn()
             b.record(stream)
         torch.cuda.synchronize()
-        return float(np.mean([a.elapsed_time(b) for a, b in evs]))
+        return stats_ms([a.elapsed_time(b) for a, b in evs])
 
-    reps = max(10, args.steps)
-    t_step = per_launch_ms(step, reps)
-    t_inside = per_launch_ms(fwd_bwd, reps)
-    t_cky = per_launch_ms(cky, reps) if decode else None
+    reps = max(100, args.launches)
+    t_step = per_launch(step, reps)
+    t_inside = per_launch(fwd_bwd, reps) if decode else t_step
+    t_cky = per_launch(cky, reps) if decode else None
 
     # The longest sentence alone: the dependency chain no batch can beat.
     longest = int(np.argmax(batch.lengths))
@@ -186,29 +267,41 @@ def main():
     s1 = torch.from_numpy(one.scores).to(dev)
     plan1 = B.Plan(one.lengths, n1=one.n1, num_labels=labels, device=dev)
     if decode:
-        t_one = per_launch_ms(lambda: plan1.parse(s1), reps)
+        t_one = per_launch(lambda: plan1.parse(s1), reps)
     else:
-        t_one = per_launch_ms(lambda: plan1.inside_fwd_bwd(s1), reps)
+        t_one = per_launch(lambda: plan1.inside_fwd_bwd(s1), reps)
     plan1.close()
 
-    wm = work_model(batch.lengths, labels)
-    slots = wm["slots_inside"] + (wm["slots_cky"] if decode else 0)
+    def slots_of(trans):
+        wm = work_model(batch.lengths, labels, trans)
+        return wm, wm["slots_inside"] + (wm["slots_cky"] if decode else 0)
+
+    wm, slots = slots_of(4)
+    _, slots2 = slots_of(2)
     hbm = wm["bytes_inside"] + (wm["bytes_cky"] if decode else 0)
-    ach = slots / (t_step * 1e-3)
+    avg_s = t_step["mean"] * 1e-3
+    ach = slots / avg_s
+    traffic, traffic_src = measured_traffic(batch.name) if decode else (None, None)
     roof = {"bound": "alu",
-            "kernel": "parse_kernel (inside + marginals + CKY, one launch)" if decode else "inside_kernel (inside + marginals)",
+            "kernel": "parse_kernel (inside + marginals + CKY, one launch)" if decode
+            else "inside_kernel (inside + marginals)",
             "achieved": round(ach / 1e12, 4), "peak": round(PEAK_SLOTS / 1e12, 3),
             "unit": "T VALU lane-slots/s", "frac": round(ach / PEAK_SLOTS, 5),
-            "traffic": measured_traffic(batch.name) if decode else None, "avg_ms": round(t_step, 4),
-            "algorithmic_slots": int(slots), "algorithmic_bytes": int(hbm),
-            "hbm_frac": round(hbm / (t_step * 1e-3) / HBM_PEAK, 5),
-            "latency_floor_ms": round(t_one, 4),
+            "frac_measured_trans_rate": round(slots2 / avg_s / PEAK_SLOTS, 5),
+            "traffic": traffic, "traffic_profile": traffic_src,
+            "avg_ms": t_step["mean"], "launch_ms": t_step,
+            "algorithmic_slots": int(slots), "algorithmic_slots_trans2": int(slots2),
+            "algorithmic_bytes": int(hbm),
+            "hbm_frac": round(hbm / avg_s / HBM_PEAK, 5),
+            "latency_floor_ms": t_one["median"],
             "latency_floor": f"the longest sentence (n={int(one.lengths[0])}) alone"}
-    extra = {"fwd_bwd_ms": round(t_inside, 4),
-             "fwd_bwd_sentences_per_s": round(batch.B / (t_inside * 1e-3), 1)}
+    if flush is not None:
+        roof["mall"] = "defeated: a 512 MiB fill between timed launches"
+    extra = {"fwd_bwd_ms": t_inside,
+             "fwd_bwd_sentences_per_s": round(batch.B / (t_inside["median"] * 1e-3), 1)}
     if decode:
-        extra["decode_ms"] = round(t_cky, 4)
-        extra["decode_sentences_per_s"] = round(batch.B / (t_cky * 1e-3), 1)
+        extra["decode_ms"] = t_cky
+        extra["decode_sentences_per_s"] = round(batch.B / (t_cky["median"] * 1e-3), 1)
 
     if args.copy_mib > 0:
         src = torch.empty(args.copy_mib << 18, dtype=torch.float32, device=dev).fill_(1.0)

@@ -38,9 +38,13 @@
  *   nothing.
  *
  *   Streams.  `stream` is a hipStream_t (NULL = the null stream).  Compute
- *   calls only enqueue work and never synchronise.  Calls on one plan may run
- *   concurrently on different streams, except that two calls touching
- *   sentences that use the workspace (crf_plan_info: spill_count > 0) race.
+ *   calls only enqueue work and never synchronise.  Calls on one plan must
+ *   not overlap on the device: issue them on one stream, or order them with
+ *   events.  A plan owns device state that its calls use while they run --
+ *   the fused launches' work counter, and the workspace that holds the charts
+ *   and CKY split tables of sentences too long for LDS (crf_plan_info:
+ *   workspace_users) -- and two overlapping calls would share it.  Different
+ *   plans share nothing and may run concurrently on any streams.
  *
  *   Errors.  Every call returns a status (CRF_OK = 0).  Arguments are checked
  *   on the host before any HIP call is made, so a rejected call has no effect
@@ -78,11 +82,18 @@ typedef struct {
     int32_t n1;              /* padded side N1 */
     int32_t num_labels;      /* L (1 = unlabelled) */
     int32_t max_len;         /* longest sentence */
-    int32_t lds_count;       /* sentences whose chart lives in LDS */
-    int32_t spill_count;     /* sentences whose chart lives in the workspace */
+    int32_t lds_count;       /* sentences whose inside chart lives in LDS */
+    int32_t spill_count;     /* sentences whose inside chart lives in the workspace */
     int64_t workspace_bytes; /* device workspace owned by the plan */
     int32_t lds_bytes_inside;/* dynamic LDS per workgroup, inside kernels */
     int32_t lds_bytes_cky;   /* dynamic LDS per workgroup, CKY kernel */
+    int32_t cky_spill_count; /* sentences whose CKY chart lives in the workspace */
+    int32_t split_ws_count;  /* sentences whose CKY chart is in LDS but whose
+                                split table is in the workspace */
+    int32_t workspace_users; /* sentences that use the workspace in some call
+                                (any of the three above) */
+    int32_t fused_queue;     /* 1 if the fused launches pull work from the
+                                plan's counter */
 } crf_plan_stats;
 
 /*

@@ -48,6 +48,10 @@ class PlanStats(ctypes.Structure):
         ("workspace_bytes", ctypes.c_int64),
         ("lds_bytes_inside", ctypes.c_int32),
         ("lds_bytes_cky", ctypes.c_int32),
+        ("cky_spill_count", ctypes.c_int32),
+        ("split_ws_count", ctypes.c_int32),
+        ("workspace_users", ctypes.c_int32),
+        ("fused_queue", ctypes.c_int32),
     ]
 
 
@@ -199,11 +203,16 @@ class Plan:
         return scores.data_ptr()
 
     def _vec(self, v, name):
+        """Pointer of a float32 [B] vector.  Outputs and inputs alike must be
+        contiguous: a pointer into a temporary copy would let the kernel write
+        results that the caller never sees."""
         if v is None:
             return None
         if tuple(v.shape) != (self.B,) or v.dtype != self._torch.float32 or v.device != self.device:
             raise ValueError(f"{name} must be float32 [{self.B}] on {self.device}")
-        return v.contiguous().data_ptr()
+        if not v.is_contiguous():
+            raise ValueError(f"{name} must be contiguous")
+        return v.data_ptr()
 
     def inside_fwd(self, scores, logZ=None):
         """log Z per sentence (float32 [B])."""
@@ -294,6 +303,7 @@ def log_partition(scores, plan):
         @staticmethod
         def backward(ctx, g):
             (s,) = ctx.saved_tensors
-            return plan.inside_bwd(s, grad_logZ=g.contiguous().float())
+            g = g.float().contiguous()   # held by this frame until the call has been enqueued
+            return plan.inside_bwd(s, grad_logZ=g)
 
     return _LogZ.apply(scores)

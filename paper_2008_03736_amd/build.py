@@ -8,6 +8,9 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 SOURCES = [os.path.join(CSRC, "crf_kernels.hip"), os.path.join(CSRC, "crf_plan.cpp")]
 LIB = os.path.join(PKG, "libcrfinside.so")
+# microbenchmarks of the ceilings behind the roofline (bench.py --ceilings)
+CEIL_SOURCES = [os.path.join(CSRC, "crf_ceilings.hip")]
+CEIL_LIB = os.path.join(PKG, "libcrfceilings.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [
@@ -25,14 +28,20 @@ FLAGS = [
 ]
 
 
-def build(verbose: bool = False) -> str:
-    """Compile every HIP source into ``libcrfinside.so`` (always recompiles)."""
-    tmp = LIB + ".tmp"
-    cmd = [HIPCC, *FLAGS, "-o", tmp, *SOURCES]
+def _compile(sources, lib, verbose):
+    tmp = lib + ".tmp"
+    cmd = [HIPCC, *FLAGS, "-o", tmp, *sources]
     if verbose:
         print(" ".join(cmd), file=sys.stderr)
     subprocess.run(cmd, check=True)
-    os.replace(tmp, LIB)
+    os.replace(tmp, lib)
+
+
+def build(verbose: bool = False) -> str:
+    """Compile every HIP source: ``libcrfinside.so`` (the CRF library) and
+    ``libcrfceilings.so`` (ceiling microbenchmarks).  Always recompiles."""
+    _compile(SOURCES, LIB, verbose)
+    _compile(CEIL_SOURCES, CEIL_LIB, verbose)
     return LIB
 
 

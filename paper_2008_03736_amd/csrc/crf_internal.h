@@ -76,9 +76,12 @@ __host__ __device__ inline int pow2_mod32(int x) {   // the power of two in x mo
     return b;
 }
 __host__ __device__ inline int inverse_mod32(int m) {   // m odd: m x = 1 (mod 32)
-    int x = m;
-    for (int k = 0; k < 4; ++k) x *= 2 - m * x;   // Newton: each step doubles the correct low bits
-    return x & 31;
+    // Newton: each step doubles the correct low bits.  Unsigned, since the
+    // products wrap (only the low five bits are kept).
+    const uint32_t mu = (uint32_t)m;
+    uint32_t x = mu;
+    for (int k = 0; k < 4; ++k) x *= 2u - mu * x;
+    return (int)(x & 31u);
 }
 constexpr int kInsideLdCap = 100;
 __host__ __device__ inline InsideLayout inside_layout(int n, int nb, bool strict) {

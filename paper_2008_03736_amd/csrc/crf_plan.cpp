@@ -53,6 +53,8 @@ struct crf_plan {
     std::vector<void *> allocations;
     crf::KernelPlan kp{};
     int64_t ws_bytes = 0;
+    int32_t split_ws_count = 0;    // sentences with CKY split tables in the workspace
+    int32_t workspace_users = 0;   // sentences using the workspace in some call
 };
 
 namespace {
@@ -410,13 +412,19 @@ int crf_plan_create(crf_plan **out, const int32_t *lengths_host, int32_t batch, 
     HostSchedule sc = make_schedule(order, lengths_host, lds_cap, force, si.ws_bytes, cky_bundle_bytes,
                                     cky_spill_bytes, kCkyTargetScale);
     int64_t split_cursor = si.ws_bytes + sc.ws_bytes;
+    std::vector<char> uses_ws(batch, 0);
+    for (int32_t b : si.spill) uses_ws[b] = 1;
+    for (int32_t b : sc.spill) uses_ws[b] = 1;
     for (crf::Bundle &bd : sc.bundles) {
         if (split_in_lds(bd.n)) continue;
         bd.split_ws = (int32_t)(split_cursor / 256);
         split_cursor += (bd.count * crf::cky_split_count(bd.n) + 255) / 256 * 256;
+        p->split_ws_count += bd.count;
+        for (int q = 0; q < bd.count; ++q) uses_ws[sc.order[bd.first + q]] = 1;
     }
     sc.ws_bytes = split_cursor - si.ws_bytes;
     p->ws_bytes = si.ws_bytes + sc.ws_bytes;
+    p->workspace_users = (int32_t)std::count(uses_ws.begin(), uses_ws.end(), 1);
 
     std::vector<int32_t> len(lengths_host, lengths_host + batch);
     crf::KernelPlan &kp = p->kp;
@@ -559,6 +567,10 @@ int crf_plan_info(const crf_plan *plan, crf_plan_stats *out) {
     out->workspace_bytes = plan->ws_bytes;
     out->lds_bytes_inside = plan->kp.inside.lds_bytes;
     out->lds_bytes_cky = plan->kp.cky.lds_bytes;
+    out->cky_spill_count = plan->kp.cky.n_spill;
+    out->split_ws_count = plan->split_ws_count;
+    out->workspace_users = plan->workspace_users;
+    out->fused_queue = plan->kp.counter != nullptr ? 1 : 0;
     return ok();
 }
 

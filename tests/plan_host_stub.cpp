@@ -2,6 +2,7 @@
 // the plan makes are served from host memory (no device is touched), and
 // the launch entry points are never called.  Prints the plan's records:
 //   P n_mix fused_grid lds_inside lds_cky half_cu
+//   W spill cky_spill split_ws workspace_users workspace_bytes fused_queue
 //   R kind n count split_ws strict ld cs e bytes id...
 // one R line per record of the fused queue, in queue order.  Arguments: a file
 // of sentence lengths, and optionally the number of labels.
@@ -77,6 +78,13 @@ int main(int argc, char **argv) {
     const crf::KernelPlan &kp = p->kp;
     const int half_cu = 163840 / 2 - crf::kReservedLds;
     std::printf("P %d %d %d %d %d\n", kp.n_mix, kp.fused_grid, kp.inside.lds_bytes, kp.cky.lds_bytes, half_cu);
+    crf_plan_stats st;
+    if (crf_plan_info(p, &st) != CRF_OK) {
+        std::printf("E info\n");
+        return 1;
+    }
+    std::printf("W %d %d %d %d %lld %d\n", st.spill_count, st.cky_spill_count, st.split_ws_count, st.workspace_users,
+                (long long)st.workspace_bytes, st.fused_queue);
     for (int b = 0; b < kp.n_mix; ++b) {
         const int32_t *r = kp.mix + (size_t)b * kp.rec_stride;
         const int n = r[crf::kRecN], count = r[crf::kRecCount], split_ws = r[crf::kRecSplitWs];

@@ -113,3 +113,21 @@ def test_product_package_never_touches_the_oracle():
                 text = open(os.path.join(dirpath, f)).read()
                 assert "oracle" not in text.lower() or f == "workloads.py", f
                 assert "import oracle" not in text and "from oracle" not in text, f
+
+
+def test_ceilings_library_exports_its_header():
+    # the microbenchmark library behind bench.py --ceilings
+    from paper_2008_03736_amd import ceilings as C
+
+    text = open(os.path.join(ROOT, "include", "crf_ceilings.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    declared = sorted(set(re.findall(r"\b(crf_[a-z_]+)\s*\(", text)))
+    assert declared == sorted(C.SIGNATURES)
+    if not os.path.exists(C.LIB_PATH):
+        pytest.fail("libcrfceilings.so is not built (run __graft_entry__.build())")
+    lib = C.load()
+    for name in declared:
+        assert hasattr(lib, name), name
+    # bad arguments are rejected before any launch (no GPU needed)
+    assert lib.crf_ceiling_run(9, 1, 64, 1, None, None) != 0
+    assert lib.crf_ceiling_run(0, 1, 100, 1, None, None) != 0

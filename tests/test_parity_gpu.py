@@ -44,6 +44,11 @@ def gpu_run(torch, batch, flags=0, grad=None, decode=True, marg_fill=0.0):
         if decode and batch.num_labels == 1:
             spans, best = plan.cky_decode(s)
             out["spans"], out["best"] = spans, best
+            # the fused launch (inside, marginals and CKY together) that the
+            # benchmark times, on its own outputs
+            pm = torch.full_like(s, marg_fill)
+            plz, pm, psp, pbe = plan.parse(s, grad_logZ=g, marginals=pm)
+            out.update(p_logZ=plz, p_marg=pm, p_spans=psp, p_best=pbe)
         torch.cuda.synchronize()
     return {k: (v.cpu().numpy() if hasattr(v, "cpu") else v) for k, v in out.items()}
 
@@ -65,21 +70,27 @@ def check_marg(gpu, ref, lengths, n1, labeled=False):
     return worst
 
 
-def check_cky(out, batch):
-    spans_ref, best_ref = orc.cky(batch.scores, batch.lengths, threads=ORACLE_THREADS)
-    bad = np.nonzero((out["spans"] != spans_ref).any(axis=(1, 2)))[0]
+def check_cky(spans, best, batch, ref=None):
+    spans_ref, best_ref = ref if ref is not None else orc.cky(batch.scores, batch.lengths, threads=ORACLE_THREADS)
+    bad = np.nonzero((spans != spans_ref).any(axis=(1, 2)))[0]
     assert bad.size == 0, f"trees differ for sentences {bad[:10]}"
-    assert np.array_equal(out["best"], best_ref.astype(np.float32))
+    assert np.array_equal(best, best_ref.astype(np.float32))
+    return spans_ref, best_ref
 
 
 def full_check(torch, batch, flags=0, grad=None, decode=True):
+    """Every entry point against the oracle: inside_fwd, inside_fwd_bwd,
+    cky_decode, and the fused parse launch (each on its own outputs)."""
     out = gpu_run(torch, batch, flags=flags, grad=grad, decode=decode)
     lz, mu = orc.marginals(batch.scores, batch.lengths, grad=grad, threads=ORACLE_THREADS)
     check_logz(out["logZ"], lz)
     check_logz(out["logZ_fwd"], lz)
     worst = check_marg(out["marg"], mu, batch.lengths, batch.n1)
     if decode:
-        check_cky(out, batch)
+        ref = check_cky(out["spans"], out["best"], batch)
+        check_logz(out["p_logZ"], lz)
+        worst = max(worst, check_marg(out["p_marg"], mu, batch.lengths, batch.n1))
+        check_cky(out["p_spans"], out["p_best"], batch, ref)
     return out, worst
 
 
@@ -111,20 +122,42 @@ def test_stress_full_batch(torch):
     print(f"stress: max |marginal error| {worst:.2e}")
 
 
-def test_labeled_sampled(torch):
+def check_labeled_chunks(out, b, chunk=125):
+    """All sentences of a labelled batch against the oracle, a chunk of
+    sentences at a time (each re-padded to its own longest sentence)."""
+    worst = 0.0
+    for c0 in range(0, b.B, chunk):
+        idx = np.arange(c0, min(b.B, c0 + chunk))
+        sub = W.subset(b, idx)
+        lz, mu = orc.labeled(sub.scores, sub.lengths, threads=ORACLE_THREADS)
+        check_logz(out["logZ"][idx], lz)
+        check_logz(out["logZ_fwd"][idx], lz)
+        n1 = sub.n1
+        worst = max(worst, check_marg(out["marg"][idx][:, :n1, :n1], mu, sub.lengths, n1, labeled=True))
+    return worst
+
+
+def test_labeled_full_batch(torch):
+    # all 1,000 sentences of the labelled batch (L = 26)
     b = W.make("labeled")
     out = gpu_run(torch, b, decode=False)
-    order = np.argsort(-b.lengths, kind="stable")
-    idx = np.unique(np.concatenate([order[:8], order[-8:], np.arange(0, b.B, 37)]))
-    sub = W.subset(b, idx)
-    lz, mu = orc.labeled(sub.scores, sub.lengths, threads=ORACLE_THREADS)
-    check_logz(out["logZ"][idx], lz)
-    n1 = sub.n1
-    check_marg(out["marg"][idx][:, :n1, :n1], mu, sub.lengths, n1, labeled=True)
+    worst = check_labeled_chunks(out, b)
     # label marginals sum to the span marginal, which is 1 on forced spans
-    for k, bi in enumerate(idx[:4]):
+    for bi in range(4):
         n = int(b.lengths[bi])
         assert abs(out["marg"][bi, 0, n].sum() - 1.0) < 1e-5
+    print(f"labeled: max |marginal error| {worst:.2e}")
+
+
+@pytest.mark.parametrize("labels", [33, 64, 138, 139])
+def test_labeled_many_labels(torch, labels):
+    # more than 32 labels per span: the label log-sum-exp and the per-label
+    # marginals run in blocks of 32 (the second and later blocks, even and
+    # odd counts); 138 is the size of the paper's CNF label set for English
+    b = W.custom([1, 2, 5, 17, 40, 41, 64], seed=300 + labels, sd=1.0, labels=labels)
+    out = gpu_run(torch, b, decode=False)
+    worst = check_labeled_chunks(out, b, chunk=b.B)
+    print(f"L = {labels}: max |marginal error| {worst:.2e}")
 
 
 # --------------------------------------------------------------------------

@@ -23,7 +23,10 @@ def harness(tmp_path_factory):
     if cxx is None or not os.path.isdir(ROCM_INCLUDE):
         pytest.skip("needs g++ and the HIP headers")
     out = str(tmp_path_factory.mktemp("plan") / "plan_host")
-    cmd = [cxx, "-O1", "-std=c++17", "-D__HIP_PLATFORM_AMD__", "-I" + ROCM_INCLUDE,
+    # host code only (g++, no GPU code): built with the address and
+    # undefined-behaviour sanitizers, which abort the run on a finding
+    cmd = [cxx, "-O1", "-g", "-std=c++17", "-fsanitize=address,undefined", "-fno-sanitize-recover=all",
+           "-fno-omit-frame-pointer", "-D__HIP_PLATFORM_AMD__", "-I" + ROCM_INCLUDE,
            "-I" + os.path.join(HERE, "..", "include"), "-o", out, os.path.join(HERE, "plan_host_stub.cpp")]
     subprocess.run(cmd, check=True, capture_output=True, text=True)
     return out
@@ -33,12 +36,18 @@ def plan_of(harness, tmp_path, lengths, labels=None):
     f = tmp_path / "lengths.txt"
     f.write_text("\n".join(str(int(v)) for v in lengths))
     args = [harness, str(f)] + ([str(labels)] if labels is not None else [])
-    res = subprocess.run(args, capture_output=True, text=True, check=True)
+    env = dict(os.environ, ASAN_OPTIONS="detect_leaks=1:abort_on_error=0", UBSAN_OPTIONS="print_stacktrace=1")
+    res = subprocess.run(args, capture_output=True, text=True, env=env)
+    assert res.returncode == 0, res.stdout[-2000:] + res.stderr[-4000:]
+    assert "runtime error" not in res.stderr and "AddressSanitizer" not in res.stderr, res.stderr[-4000:]
     head, recs = None, []
     for line in res.stdout.splitlines():
         t = line.split()
         if t[0] == "P":
             head = dict(zip(["n_mix", "grid", "lds_in", "lds_ck", "half_cu"], map(int, t[1:])))
+        elif t[0] == "W":
+            head.update(zip(["spill", "cky_spill", "split_ws", "ws_users", "ws_bytes", "fused_queue"],
+                            map(int, t[1:])))
         elif t[0] == "R":
             v = list(map(int, t[1:]))
             recs.append(dict(kind=v[0], n=v[1], count=v[2], split_ws=v[3], strict=v[4], ld=v[5], cs=v[6],
@@ -124,3 +133,22 @@ def test_plan_of_labelled_batches(harness, tmp_path, labels, seed):
     for r in recs:
         assert r["count"] == len(r["ids"]) >= 1
         assert all(lengths[i] == r["n"] for i in r["ids"])
+
+
+def test_workspace_users_reported(harness, tmp_path):
+    # The mixed batch keeps every chart in LDS, yet its 99-word sentence's CKY
+    # split table lives in the plan's workspace: plan info must count it as a
+    # workspace user (calls on one plan are stream-ordered for that reason).
+    b = W.make("mixed")
+    head, _ = plan_of(harness, tmp_path, b.lengths)
+    assert head["spill"] == 0 and head["cky_spill"] == 0
+    long_ones = int(np.sum(b.lengths >= 97))
+    assert long_ones >= 1
+    assert head["split_ws"] == long_ones and head["ws_users"] == long_ones
+    assert head["ws_bytes"] > 0 and head["fused_queue"] == 1
+    # a batch of short sentences uses no workspace at all
+    head, _ = plan_of(harness, tmp_path, [5, 9, 30, 60] * 10)
+    assert head["ws_users"] == 0 and head["ws_bytes"] == 0
+    # sentences past the LDS limit use it for both charts
+    head, _ = plan_of(harness, tmp_path, [200, 150, 10])
+    assert head["spill"] == 2 and head["cky_spill"] == 2 and head["ws_users"] == 2
