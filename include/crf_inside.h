@@ -163,6 +163,27 @@ int crf_inside_fwd_bwd_cky(const crf_plan *plan, const float *scores, const floa
                            float *logZ, float *marginals, int32_t *spans, float *best,
                            void *stream);
 
+/*
+ * crf_inside_fwd_bwd_cky_noalloc -- crf_inside_fwd_bwd_cky for callers that
+ * cannot allocate device memory or must not touch the plan's device state
+ * while they run (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation).  Same arguments and results as
+ * crf_inside_fwd_bwd_cky; the plan's workspace and work counter are not
+ * used: the call takes them from a static scratch array of the library,
+ * 8 MiB per GPU, held from the library's first use on a device until the
+ * process ends.  It calls no allocation routine; it enqueues a small kernel
+ * that clears the array's counter, then the launches of the fused call.
+ *   Returns CRF_EINVAL when the plan needs more workspace than the array
+ *   holds (8 MiB less 256 bytes; crf_plan_info: workspace_bytes), e.g. a
+ *   batch with many sentences longer than 142 words.
+ *   Every such call on one GPU shares that GPU's array, whatever the plan:
+ *   calls of this entry point that overlap on one GPU race (issue them on
+ *   one stream, or order them with events).
+ */
+int crf_inside_fwd_bwd_cky_noalloc(const crf_plan *plan, const float *scores, const float *grad_logZ,
+                                   float *logZ, float *marginals, int32_t *spans, float *best,
+                                   void *stream);
+
 /* Static description of a status code. */
 const char *crf_status_string(int status);
 

@@ -32,6 +32,7 @@ SIGNATURES = {
     "crf_inside_fwd_bwd": (ctypes.c_int, [_P, _P, _P, _P, _P, _P]),
     "crf_cky_decode": (ctypes.c_int, [_P, _P, _P, _P, _P]),
     "crf_inside_fwd_bwd_cky": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _P]),
+    "crf_inside_fwd_bwd_cky_noalloc": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _P]),
     "crf_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "crf_last_error": (ctypes.c_char_p, []),
 }
@@ -128,6 +129,11 @@ def crf_cky_decode(plan, scores, spans, best, stream):
 def crf_inside_fwd_bwd_cky(plan, scores, grad_logZ, logZ, marginals, spans, best, stream):
     _check(load().crf_inside_fwd_bwd_cky(plan, scores, grad_logZ, logZ, marginals, spans, best,
                                          stream), "crf_inside_fwd_bwd_cky")
+
+
+def crf_inside_fwd_bwd_cky_noalloc(plan, scores, grad_logZ, logZ, marginals, spans, best, stream):
+    _check(load().crf_inside_fwd_bwd_cky_noalloc(plan, scores, grad_logZ, logZ, marginals, spans, best,
+                                                 stream), "crf_inside_fwd_bwd_cky_noalloc")
 
 
 def crf_status_string(status):

@@ -331,6 +331,21 @@ struct KernelPlan {
     int32_t B, n1, L;
 };
 
+// The no-allocation entry point's scratch: a file-scope device array of
+// kScratchBytes per GPU (the first kScratchCounterBytes hold the fused
+// launch's claim counter, the rest stands in for the plan's workspace).
+constexpr int64_t kScratchBytes = (int64_t)8 << 20;
+constexpr int64_t kScratchCounterBytes = 256;
+constexpr int kMaxDevices = 64;
+// Device address of the current device's scratch array (resolved once per
+// device, with that device current, and kept).
+hipError_t scratch_address(int device, char **out);
+// crf_inside_fwd_bwd_cky on the scratch array instead of the plan's
+// workspace and counter: clears the counter with a kernel, then launches as
+// launch_parse does.  The caller has checked the plan's workspace fits.
+hipError_t launch_parse_scratch(const KernelPlan &p, char *scratch, const float *scores, const float *grad,
+                                float *logZ, float *marg, int32_t *spans, float *best, hipStream_t stream);
+
 hipError_t launch_inside(const KernelPlan &p, const float *scores, const float *grad,
                          float *logZ, float *marg, hipStream_t stream);
 hipError_t launch_cky(const KernelPlan &p, const float *scores, int32_t *spans, float *best,

@@ -59,6 +59,7 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <mutex>
 #include <type_traits>
 
 #include "crf_internal.h"
@@ -1290,10 +1291,49 @@ __global__ __launch_bounds__(kThreadsMax) void parse_kernel(KernelPlan p, const 
     }
 }
 
+// Zeroes n words (the no-allocation entry point's claim counter): a kernel,
+// not hipMemsetAsync, so that the call stays a plain kernel node when a
+// caller captures it into a graph.
+__global__ void zero_words(int32_t *p, int n) {
+    for (int t = threadIdx.x; t < n; t += blockDim.x) p[t] = 0;
+}
+
+// Scratch of the no-allocation entry point, one per GPU for the life of the
+// process.  In host code `scratch` names a host-side stand-in, not device
+// memory: host code only ever uses the address scratch_address() resolved.
+__device__ __align__(256) char scratch[kScratchBytes];
+
 }  // namespace
 
 // ---------------------------------------------------------------------------
 // Launchers.
+
+hipError_t scratch_address(int device, char **out) {
+    static std::mutex mu;
+    static char *addr[kMaxDevices] = {};
+    *out = nullptr;
+    if (device < 0 || device >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(mu);
+    if (addr[device] == nullptr) {
+        void *ptr = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        addr[device] = static_cast<char *>(ptr);
+    }
+    *out = addr[device];
+    return hipSuccess;
+}
+
+hipError_t launch_parse_scratch(const KernelPlan &p, char *scr, const float *scores, const float *grad,
+                                float *logZ, float *marg, int32_t *spans, float *best, hipStream_t stream) {
+    KernelPlan q = p;
+    q.counter = reinterpret_cast<int32_t *>(scr);
+    q.ws = scr + kScratchCounterBytes;
+    hipLaunchKernelGGL(zero_words, dim3(1), dim3(64), 0, stream, q.counter, (int)(kScratchCounterBytes / 4));
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    return launch_parse(q, scores, grad, logZ, marg, spans, best, stream);
+}
 
 hipError_t set_kernel_attributes(int max_lds_bytes) {
     const void *fns[] = {

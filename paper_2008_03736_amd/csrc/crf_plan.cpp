@@ -539,6 +539,10 @@ int crf_plan_create(crf_plan **out, const int32_t *lengths_host, int32_t batch, 
     // limit without this attribute; a real shortfall surfaces as a launch error.
     if (crf::set_kernel_attributes(std::max(si.lds_bytes, sc.lds_bytes)) != hipSuccess)
         (void)hipGetLastError();
+    // Resolve this device's scratch address for the no-allocation entry
+    // point now (it retries, and reports a failure, on its first call).
+    char *scr = nullptr;
+    if (crf::scratch_address(p->device, &scr) != hipSuccess) (void)hipGetLastError();
     *out = p;
     return ok();
 }
@@ -624,6 +628,29 @@ int crf_inside_fwd_bwd_cky(const crf_plan *plan, const float *scores, const floa
     hipError_t e = crf::launch_parse(plan->kp, scores, grad_logZ, logZ, marginals, spans, best,
                                      static_cast<hipStream_t>(stream));
     return e == hipSuccess ? ok() : hip_fail(e, "crf_inside_fwd_bwd_cky launch");
+}
+
+int crf_inside_fwd_bwd_cky_noalloc(const crf_plan *plan, const float *scores, const float *grad_logZ,
+                                   float *logZ, float *marginals, int32_t *spans, float *best,
+                                   void *stream) {
+    if (plan == nullptr) return fail(CRF_EINVAL, "plan is NULL");
+    if (scores == nullptr || marginals == nullptr || spans == nullptr)
+        return fail(CRF_EINVAL, "scores/marginals/spans is NULL");
+    if (plan->L != 1)
+        return fail(CRF_EUNSUPPORTED, "CKY decode of labelled scores (L = %d)", plan->L);
+    if (plan->ws_bytes > crf::kScratchBytes - crf::kScratchCounterBytes)
+        return fail(CRF_EINVAL,
+                    "the plan needs %lld bytes of workspace, more than the %lld bytes of static scratch "
+                    "(use crf_inside_fwd_bwd_cky)",
+                    (long long)plan->ws_bytes, (long long)(crf::kScratchBytes - crf::kScratchCounterBytes));
+    int rc = check_device(plan);
+    if (rc != CRF_OK) return rc;
+    char *scr = nullptr;
+    hipError_t e = crf::scratch_address(plan->device, &scr);
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+    e = crf::launch_parse_scratch(plan->kp, scr, scores, grad_logZ, logZ, marginals, spans, best,
+                                  static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? ok() : hip_fail(e, "crf_inside_fwd_bwd_cky_noalloc launch");
 }
 
 int crf_cky_decode(const crf_plan *plan, const float *scores, int32_t *spans, float *best,

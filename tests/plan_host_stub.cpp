@@ -56,6 +56,14 @@ hipError_t launch_parse(const KernelPlan &, const float *, const float *, float 
     return hipErrorNotSupported;
 }
 hipError_t set_kernel_attributes(int) { return hipSuccess; }
+hipError_t scratch_address(int, char **out) {
+    *out = nullptr;
+    return hipErrorNotSupported;
+}
+hipError_t launch_parse_scratch(const KernelPlan &, char *, const float *, const float *, float *, float *, int32_t *,
+                                float *, hipStream_t) {
+    return hipErrorNotSupported;
+}
 }  // namespace crf
 
 int main(int argc, char **argv) {

@@ -95,6 +95,7 @@ def test_compute_calls_reject_null_plan(lib):
     assert lib.crf_inside_fwd_bwd(None, dummy, None, dummy, dummy, None) == B.CRF_EINVAL
     assert lib.crf_cky_decode(None, dummy, dummy, None, None) == B.CRF_EINVAL
     assert lib.crf_inside_fwd_bwd_cky(None, dummy, None, dummy, dummy, dummy, None, None) == B.CRF_EINVAL
+    assert lib.crf_inside_fwd_bwd_cky_noalloc(None, dummy, None, dummy, dummy, dummy, None, None) == B.CRF_EINVAL
     assert lib.crf_plan_info(None, None) == B.CRF_EINVAL
     assert lib.crf_plan_destroy(None) == B.CRF_OK
 
