@@ -11,6 +11,9 @@ by listing all legal trees -- no dynamic programming at all:
   * p((i,j)|x) = sum of p(y|x) over trees containing (i,j)  (Eq. partial-derivative)
   * the best tree maximises s(x,y)                           (Eq. tree-argmax)
   * one-stage labelled score: sum of s(i,j,l) over labelled spans (Eq. tree-label-score)
+  * gold-tree loss -log p(y|x) = log Z - s(x,y)              (Eq. bracket-loss)
+  * MBR decoding: the tree maximising the sum of its spans' marginals (Sec. 3.3)
+  * labelling: each span of a tree takes its best label      (Eq. label-argmax)
 
 Ties between best trees are resolved by the lowest split point, which on
 exactly representable scores is the optimal tree whose preorder sequence of
@@ -86,3 +89,35 @@ def labeled(s4, n, L):
         for (i, j), l in zip(spans, labels):
             mu[(i, j, l)] += p
     return lz, mu
+
+
+def loss(s, n, gold):
+    """-log p(y|x) for the gold tree y (a list of spans), by enumeration."""
+    lz = log_z(s, n)
+    return lz - sum(float(s[i][j]) for i, j in gold)
+
+
+def best_labeled_tree(s4, n, L):
+    """(best score, preorder spans, labels) over every tree and labelling.
+
+    Among optimal labelled trees, the one whose preorder split sequence is
+    lexicographically smallest, then whose preorder label sequence is.
+    """
+    cands = []
+    for spans, splits in trees(0, n):
+        for labels in itertools.product(range(L), repeat=len(spans)):
+            tot = sum(float(s4[i][j][l]) for (i, j), l in zip(spans, labels))
+            cands.append((tot, splits, labels, spans))
+    top = max(c[0] for c in cands)
+    opt = sorted((c for c in cands if c[0] == top), key=lambda c: (c[1], c[2]))
+    return top, opt[0][3], list(opt[0][2])
+
+
+def mbr_tree(s, n):
+    """MBR decoding by enumeration: (best, preorder spans, gap to the runner-up)
+    of the tree maximising the sum of its spans' marginals."""
+    mu = marginals(s, n)
+    scored = sorted(((sum(mu[sp] for sp in spans), spans) for spans, _ in trees(0, n)),
+                    key=lambda t: -t[0])
+    gap = scored[0][0] - scored[1][0] if len(scored) > 1 else float("inf")
+    return scored[0][0], scored[0][1], gap

@@ -172,19 +172,38 @@ static double cky(int n, int ld, const double *s, double *beta, int32_t *bp,
 }
 
 /* ------------------------------------------------------------------------ */
+/* Second stage of the two-stage parser, labelling (Sec. 2.1, Eq. label-argmax):
+ * every span of a given tree independently takes argmax_l s(i,j,l).  Among
+ * equal maxima the lowest label index is kept.  s4 points at one sentence's
+ * [ld][ld][L] block.                                                        */
+static int32_t best_label(const float *s4, int ld, int L, int i, int j)
+{
+    const float *v = s4 + IDX(i, j, ld) * (size_t)L;
+    int32_t bl = 0;
+    for (int l = 1; l < L; ++l)
+        if (v[l] > v[bl]) bl = l;
+    return bl;
+}
+
+/* Whether (i,j) is a span of an n-word sentence. */
+static int valid_span(int n, int i, int j) { return 0 <= i && i < j && j <= n; }
+
+/* ------------------------------------------------------------------------ */
 /* Batch drivers.  Sentences are independent (Algorithm 1 parallelises over
  * the batch), so worker threads take whole sentences from a shared counter. */
 
-enum { JOB_LOGZ = 0, JOB_MARG_ADJ = 1, JOB_MARG_OUT = 2, JOB_CKY = 3, JOB_LABEL = 4 };
+enum { JOB_LOGZ = 0, JOB_MARG_ADJ = 1, JOB_MARG_OUT = 2, JOB_CKY = 3, JOB_LABEL = 4, JOB_LOSS = 5,
+       JOB_LCKY = 6, JOB_LSPANS = 7 };
 
 typedef struct {
     int job, B, ld, L;
     const int32_t *len;
     const float *s;          /* [B][ld][ld] or [B][ld][ld][L] */
     const double *g;         /* [B] upstream gradient, NULL = 1 */
-    double *logZ;            /* [B] (or best score for CKY), may be NULL */
+    double *logZ;            /* [B] (or best score for CKY, loss for JOB_LOSS), may be NULL */
     double *mu;              /* [B][ld][ld] or [B][ld][ld][L], may be NULL */
-    int32_t *spans;          /* [B][2(ld-1)-1][2] */
+    int32_t *spans;          /* [B][2(ld-1)-1][2] (input for JOB_LOSS and JOB_LSPANS) */
+    int32_t *labels;         /* [B][2(ld-1)-1] (JOB_LCKY, JOB_LSPANS) */
     volatile int next;
     volatile int status;
 } job_t;
@@ -198,6 +217,43 @@ static void run_one(job_t *J, int b, double *buf)
     double *c2 = c1 + (size_t)st * st;         /* st*st: outside / adjoint   */
     double *tmp = c2 + (size_t)st * st;        /* 2*st scratch terms         */
     const double g = J->g ? J->g[b] : 1.0;
+
+    const int R = 2 * (ld - 1) - 1;   /* rows of a span list */
+
+    if (J->job == JOB_LSPANS) {
+        /* Labelling stage on a given tree: every listed row that is a span of
+         * this sentence gets its best label; every other row gets -1.       */
+        const float *s4 = J->s + (size_t)b * blk * J->L;
+        const int32_t *sp = J->spans + (size_t)b * R * 2;
+        int32_t *lab = J->labels + (size_t)b * R;
+        for (int r = 0; r < R; ++r)
+            lab[r] = valid_span(n, sp[2 * r], sp[2 * r + 1]) ? best_label(s4, ld, J->L, sp[2 * r], sp[2 * r + 1]) : -1;
+        return;
+    }
+
+    if (J->job == JOB_LCKY) {
+        /* One-stage labelled decoding (Sec. 4.2, Eq. tree-label-score; the
+         * time-complexity paragraph of Sec. 2.1: CKY picks the best label of
+         * every span).  A labelled tree scores the sum of s(i,j,l) over its
+         * labelled spans, and each span's label is free, so the best labelled
+         * tree is the CKY tree over s'(i,j) = max_l s(i,j,l) with each of its
+         * spans labelled argmax_l s(i,j,l) (lowest label on ties).  s' is a
+         * float32 value (an exact max), decoded by the float64 CKY above.   */
+        const int L = J->L;
+        const float *s4 = J->s + (size_t)b * blk * L;
+        for (int i = 0; i < n; ++i)
+            for (int j = i + 1; j <= n; ++j)
+                sd[IDX(i, j, ld)] = (double)s4[IDX(i, j, ld) * L + best_label(s4, ld, L, i, j)];
+        int32_t *bp = (int32_t *)c2;
+        int32_t *stack = (int32_t *)tmp;
+        int32_t *sp = J->spans + (size_t)b * R * 2;
+        int32_t *lab = J->labels + (size_t)b * R;
+        for (int r = 0; r < R * 2; ++r) sp[r] = -1;
+        const double best = cky(n, ld, sd, c1, bp, stack, sp);
+        for (int r = 0; r < R; ++r) lab[r] = r < 2 * n - 1 ? best_label(s4, ld, L, sp[2 * r], sp[2 * r + 1]) : -1;
+        if (J->logZ) J->logZ[b] = best;
+        return;
+    }
 
     if (J->job == JOB_LABEL) {
         /* One-stage labelled CRF (Sec. 4.2, Eq. tree-label-score): a tree's
@@ -252,6 +308,33 @@ static void run_one(job_t *J, int b, double *buf)
     }
 
     const double lz = inside(n, ld, sd, c1, tmp);
+    if (J->job == JOB_LOSS) {
+        /* Gold-tree CRF loss (Sec. 2.3, Eq. bracket-loss):
+         *   L = -s(x,y) + log Z(x),  s(x,y) = sum of the scores of y's spans
+         * (Eq. tree-score), and its gradient, the marginals minus the gold
+         * indicator: dL/ds(i,j) = p((i,j)|x) - 1[(i,j) in y] (Sec. 3.2),
+         * the gradient times the upstream gradient g.  y is the set of the first
+         * 2n-1 rows of the span list; every one must be a span of this
+         * sentence (else the job fails); a repeated row adds its score again
+         * but the indicator of a set.                                        */
+        const int32_t *gy = J->spans + (size_t)b * R * 2;
+        double *mu = J->mu + (size_t)b * blk;
+        adjoint_marginals(n, ld, c1, g, c2, tmp, mu);
+        char *hit = (char *)c2;               /* c2 is free again: st*st flags */
+        memset(hit, 0, (size_t)st * st);
+        double gold = 0.0;
+        for (int r = 0; r < 2 * n - 1; ++r) {
+            const int i = gy[2 * r], j = gy[2 * r + 1];
+            if (!valid_span(n, i, j)) { J->status = 1; return; }
+            gold += sd[IDX(i, j, ld)];
+            if (!hit[IDX(i, j, st)]) {
+                hit[IDX(i, j, st)] = 1;
+                mu[IDX(i, j, ld)] -= g;
+            }
+        }
+        if (J->logZ) J->logZ[b] = lz - gold;
+        return;
+    }
     if (J->logZ) J->logZ[b] = lz;
     if (J->job == JOB_LOGZ || !J->mu) return;
     double *mu = J->mu + (size_t)b * blk;
@@ -308,7 +391,7 @@ static int run_job(job_t *J, int nthreads)
 /* log Z per sentence (Eq. tree-prob, Algorithm 1). */
 int orc_logz(int B, int ld, const int32_t *len, const float *s, double *logZ, int nthreads)
 {
-    job_t J = {JOB_LOGZ, B, ld, 1, len, s, NULL, logZ, NULL, NULL, 0, 0};
+    job_t J = {JOB_LOGZ, B, ld, 1, len, s, NULL, logZ, NULL, NULL, NULL, 0, 0};
     return run_job(&J, nthreads);
 }
 
@@ -320,7 +403,7 @@ int orc_marginals(int B, int ld, const int32_t *len, const float *s, const doubl
 {
     if (!mu) return 1;
     job_t J = {method == 1 ? JOB_MARG_OUT : JOB_MARG_ADJ, B, ld, 1, len, s, g, logZ, mu,
-               NULL, 0, 0};
+               NULL, NULL, 0, 0};
     return run_job(&J, nthreads);
 }
 
@@ -330,7 +413,7 @@ int orc_cky(int B, int ld, const int32_t *len, const float *s, int32_t *spans, d
             int nthreads)
 {
     if (!spans) return 1;
-    job_t J = {JOB_CKY, B, ld, 1, len, s, NULL, best, NULL, spans, 0, 0};
+    job_t J = {JOB_CKY, B, ld, 1, len, s, NULL, best, NULL, spans, NULL, 0, 0};
     return run_job(&J, nthreads);
 }
 
@@ -340,6 +423,40 @@ int orc_labeled(int B, int ld, int L, const int32_t *len, const float *s, const 
                 double *logZ, double *mu, int nthreads)
 {
     if (L < 1) return 1;
-    job_t J = {JOB_LABEL, B, ld, L, len, s, g, logZ, mu, NULL, 0, 0};
+    job_t J = {JOB_LABEL, B, ld, L, len, s, g, logZ, mu, NULL, NULL, 0, 0};
+    return run_job(&J, nthreads);
+}
+
+/* Gold-tree CRF loss and its gradient (Sec. 2.3, Eq. bracket-loss; Sec. 3.2):
+ * gold is [B][2(ld-1)-1][2], its first 2n_b-1 rows the gold tree's spans;
+ * loss[b] = log Z - s(x,y); grad is [B][ld][ld] with
+ * g[b] (p((i,j)|x) - 1[(i,j) in y]) on valid cells.
+ * Returns 1 if a gold row is not a span of its sentence.                   */
+int orc_loss(int B, int ld, const int32_t *len, const float *s, const int32_t *gold, const double *g,
+             double *loss, double *grad, int nthreads)
+{
+    if (!gold || !grad) return 1;
+    job_t J = {JOB_LOSS, B, ld, 1, len, s, g, loss, grad, (int32_t *)gold, NULL, 0, 0};
+    return run_job(&J, nthreads);
+}
+
+/* One-stage labelled decoding: s is [B][ld][ld][L]; spans [B][2(ld-1)-1][2]
+ * and labels [B][2(ld-1)-1] of the best labelled tree (rows past 2n_b-1 are
+ * -1); best[b] (nullable) its score.                                        */
+int orc_labeled_cky(int B, int ld, int L, const int32_t *len, const float *s, int32_t *spans,
+                    int32_t *labels, double *best, int nthreads)
+{
+    if (L < 1 || !spans || !labels) return 1;
+    job_t J = {JOB_LCKY, B, ld, L, len, s, NULL, best, NULL, spans, labels, 0, 0};
+    return run_job(&J, nthreads);
+}
+
+/* Labelling stage on given trees: labels[b][r] = argmax_l s(i,j,l) for every
+ * row r of spans[b] that is a span of sentence b, else -1.                  */
+int orc_label_spans(int B, int ld, int L, const int32_t *len, const float *s, const int32_t *spans,
+                    int32_t *labels, int nthreads)
+{
+    if (L < 1 || !spans || !labels) return 1;
+    job_t J = {JOB_LSPANS, B, ld, L, len, s, NULL, NULL, NULL, (int32_t *)spans, labels, 0, 0};
     return run_job(&J, nthreads);
 }

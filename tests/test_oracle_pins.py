@@ -282,3 +282,181 @@ def test_fig1b_tree_is_decoded_and_dominates():
             assert mu[0, i, j] > 0.95
         else:
             assert mu[0, i, j] < 0.05
+
+
+# --------------------------------------------------------------------------
+# Gold-tree loss (Eq. bracket-loss), labelled decoding (Eq. tree-label-score),
+# labelling (Eq. label-argmax) and MBR decoding (Sec. 3.3)
+
+
+def _span_list(trees_rows, ld):
+    """[B, 2(ld-1)-1, 2] int32 span list, rows past each tree = -1."""
+    R = 2 * (ld - 1) - 1
+    out = np.full((len(trees_rows), R, 2), -1, np.int32)
+    for b, rows in enumerate(trees_rows):
+        out[b, : len(rows)] = rows
+    return out
+
+
+@pytest.mark.parametrize("n", [1, 2, 3, 4, 5, 6, 7])
+def test_bruteforce_loss_and_gradient(n):
+    rng = np.random.default_rng(40 + n)
+    all_trees = list(bf.trees(0, n))
+    for t in range(3):
+        b = W.custom([n], seed=60 + 7 * n + t, sd=1.5)
+        spans, _ = all_trees[int(rng.integers(len(all_trees)))]
+        gold = _span_list([spans], b.n1)
+        g = [1.75]
+        lv, gr = orc.loss(b.scores, b.lengths, gold, grad=g)
+        ref = bf.loss(b.scores[0], n, spans)
+        assert abs(lv[0] - ref) <= 1e-12 * max(1.0, abs(ref))
+        assert lv[0] > 0.0 or n <= 2          # p(y|x) < 1 whenever there is a choice (n > 2)
+        mu = bf.marginals(b.scores[0], n)
+        for (i, j), v in mu.items():
+            ind = 1.0 if (i, j) in spans else 0.0
+            assert abs(gr[0, i, j] - g[0] * (v - ind)) <= 1e-12, (i, j)
+        # the gold tree has 2n-1 spans and the marginals sum to 2n-1
+        v = W.valid_mask(b.lengths, b.n1)
+        assert abs(gr[v].sum()) <= 1e-10
+        # forced spans are in every tree: zero gradient
+        assert all(abs(gr[0, i, i + 1]) <= 1e-12 for i in range(n)) and abs(gr[0, 0, n]) <= 1e-12
+
+
+def test_loss_finite_differences():
+    n = 11
+    rng = np.random.default_rng(8)
+    s = rng.standard_normal((n + 1, n + 1))
+    sc, ln = _one(n, s)
+    gold_rows, _ = orc.cky(sc + np.float32(0.0), ln)
+    # a gold tree other than the best one: right-branching
+    rb = []
+    for i in range(n - 1):
+        rb += [(i, n), (i, i + 1)]
+    rb.append((n - 1, n))
+    for gold in (gold_rows, _span_list([rb], n + 1)):
+        h = 2.0 ** -10
+        _, gr = orc.loss(sc, ln, gold)
+        for i, j in [(0, 11), (0, 5), (3, 9), (5, 6), (2, 11), (6, 11), (1, 3)]:
+            base = float(np.float32(s[i][j]))
+            vals = []
+            for d in (h, -h):
+                s2 = s.copy()
+                s2[i][j] = base + d
+                sc2, _ = _one(n, s2)
+                vals.append(orc.loss(sc2, ln, gold)[0][0])
+            fd = (vals[0] - vals[1]) / (2 * h)
+            assert abs(fd - gr[0, i, j]) <= 2e-7, (i, j, fd, gr[0, i, j])
+
+
+def test_loss_upstream_gradient_and_rows():
+    b = W.custom([9, 4], seed=12, sd=1.0)
+    spans, _ = orc.cky(b.scores, b.lengths)
+    l1, g1 = orc.loss(b.scores, b.lengths, spans)
+    l2, g2 = orc.loss(b.scores, b.lengths, spans, grad=[2.0, -0.5])
+    assert np.array_equal(l1, l2)             # the loss value is not scaled
+    v = W.valid_mask(b.lengths, b.n1)
+    ref = (g1 * np.array([2.0, -0.5])[:, None, None])[v]
+    assert np.max(np.abs(g2[v] - ref)) <= 1e-12
+    # the best tree's loss is the smallest over trees: log Z - best
+    _, best = orc.cky(b.scores, b.lengths)
+    lz = orc.logz(b.scores, b.lengths)
+    assert np.allclose(l1, lz - best, rtol=0, atol=1e-12)
+    bad = spans.copy()
+    bad[0, 3] = (4, 2)                         # not a span
+    with pytest.raises(RuntimeError):
+        orc.loss(b.scores, b.lengths, bad)
+
+
+@pytest.mark.parametrize("n", [1, 2, 3, 4])
+@pytest.mark.parametrize("integer", [False, True])
+def test_bruteforce_labeled_cky(n, integer):
+    L = 3
+    for seed in range(6 if integer else 3):
+        if integer:
+            b = W.custom([n], seed=500 + seed, labels=L, integer=(-1, 1))
+        else:
+            b = W.custom([n], seed=520 + seed, sd=1.0, labels=L)
+        top, tree, labs = bf.best_labeled_tree(b.scores[0], n, L)
+        spans, labels, best = orc.labeled_cky(b.scores, b.lengths)
+        assert [tuple(r) for r in spans[0, : 2 * n - 1]] == tree, seed
+        assert list(labels[0, : 2 * n - 1]) == labs, seed
+        assert (spans[0, 2 * n - 1:] == -1).all() and (labels[0, 2 * n - 1:] == -1).all()
+        assert abs(best[0] - top) <= 1e-12 * max(1.0, abs(top))
+
+
+def test_fig1b_labeled_tree_is_decoded():
+    # the labelled CNF tree of Fig. 1b, planted in one-stage label scores
+    rows = []
+    with open(os.path.join(GOLDEN, "fig1b_cnf_tree.txt")) as f:
+        for line in f:
+            if line.startswith("#") or not line.strip():
+                continue
+            i, j, lab = line.split()
+            rows.append((int(i), int(j), lab))
+    names = sorted({r[2] for r in rows})
+    L, n = len(names), 5
+    rng = np.random.default_rng(1)
+    s4 = np.full((1, n + 1, n + 1, L), np.nan, np.float32)
+    for i in range(n):
+        for j in range(i + 1, n + 1):
+            s4[0, i, j] = 0.1 * rng.standard_normal(L)
+    for i, j, lab in rows:
+        s4[0, i, j, names.index(lab)] += 4.0
+    spans, labels, _ = orc.labeled_cky(s4, np.array([n], np.int32))
+    assert [tuple(r) for r in spans[0, : 2 * n - 1]] == [(i, j) for i, j, _ in rows]
+    assert [names[k] for k in labels[0, : 2 * n - 1]] == [lab for _, _, lab in rows]
+
+
+def test_label_spans_is_first_argmax():
+    # every listed span takes the lowest index among its equal best labels
+    # (numpy's argmax returns the first maximum); rows that are not spans of
+    # the sentence get -1
+    for integer in (None, (-2, 2)):
+        b = W.custom([7, 1, 12], seed=33, labels=9, integer=integer, sd=1.0)
+        rng = np.random.default_rng(2)
+        R = 2 * (b.n1 - 1) - 1
+        sp = np.full((b.B, R, 2), -1, np.int32)
+        for bi, n in enumerate(b.lengths):
+            for r in range(R):
+                i = int(rng.integers(0, n))
+                sp[bi, r] = (i, int(rng.integers(i + 1, n + 1)))
+        sp[0, 3] = (5, 3)                      # not a span
+        sp[2, 0] = (0, 13)                     # past the sentence
+        sp[1, 2] = (-1, -1)
+        labels = orc.label_spans(b.scores, b.lengths, sp)
+        for bi, n in enumerate(b.lengths):
+            for r in range(R):
+                i, j = sp[bi, r]
+                if 0 <= i < j <= n:
+                    assert labels[bi, r] == int(np.argmax(b.scores[bi, i, j])), (bi, r)
+                else:
+                    assert labels[bi, r] == -1
+
+
+@pytest.mark.parametrize("n", [2, 3, 4, 5, 6, 7])
+def test_bruteforce_mbr(n):
+    compared = 0
+    for seed in range(6):
+        b = W.custom([n], seed=700 + 10 * n + seed, sd=1.5)
+        top, tree, gap = bf.mbr_tree(b.scores[0], n)
+        if gap <= 1e-5:        # float32 marginals may legitimately flip a near tie
+            continue
+        spans, best, mu32 = orc.mbr(b.scores, b.lengths)
+        assert [tuple(r) for r in spans[0, : 2 * n - 1]] == tree, seed
+        assert abs(best[0] - top) <= 2 * n * 1e-7
+        compared += 1
+    assert compared >= 3
+
+
+def test_mbr_invariants():
+    # forced spans have marginal 1, so an MBR tree scores between n+1 (all its
+    # other spans improbable) and 2n-1; it beats the plain CKY tree's marginal
+    # sum
+    b = W.make("tiny")
+    spans, best, mu32 = orc.mbr(b.scores, b.lengths, threads=4)
+    sp_cky, _ = orc.cky(b.scores, b.lengths, threads=4)
+    for bi, n in enumerate(b.lengths):
+        n = int(n)
+        assert n + 1 - 1e-5 <= best[bi] <= 2 * n - 1 + 1e-5
+        cky_sum = sum(float(mu32[bi, i, j]) for i, j in sp_cky[bi, : 2 * n - 1])
+        assert best[bi] >= cky_sum - 1e-9
