@@ -13,7 +13,11 @@
  *   - the 1-best tree argmax_y s(x,y) (Sec. 2.1, Eq. tree-argmax) by CKY,
  *     the same recursion with max in place of sum (Sec. 3.3);
  *   - for the one-stage labelled CRF (Sec. 4.2, Eq. tree-label-score),
- *     log Z and the per-label span marginals p((i,j,l)|x).
+ *     log Z, the per-label span marginals p((i,j,l)|x) and the best
+ *     labelled tree;
+ *   - MBR decoding over the marginals (Sec. 3.3), the gold-tree CRF loss
+ *     and its gradient (Sec. 2.3, Eq. bracket-loss), and the labelling stage
+ *     of the two-stage parser (Sec. 2.1, Eq. label-argmax).
  *
  * Conventions
  *   Fence posts.  A sentence of n words has boundaries 0..n; span (i,j),
@@ -94,6 +98,8 @@ typedef struct {
                                 (any of the three above) */
     int32_t fused_queue;     /* 1 if the fused launches pull work from the
                                 plan's counter */
+    int32_t mbr_fused;       /* 1 if crf_mbr_decode runs as one launch per
+                                bundle queue (else as separate launches) */
 } crf_plan_stats;
 
 /*
@@ -162,6 +168,77 @@ int crf_cky_decode(const crf_plan *plan, const float *scores, int32_t *spans, fl
 int crf_inside_fwd_bwd_cky(const crf_plan *plan, const float *scores, const float *grad_logZ,
                            float *logZ, float *marginals, int32_t *spans, float *best,
                            void *stream);
+
+/*
+ * crf_mbr_decode -- MBR decoding (Sec. 3.3, "Decoding"): the CKY tree with the
+ * span marginals p((i,j)|x) in place of the span scores in Eq. tree-score and
+ * Eq. tree-argmax, i.e. the tree whose spans' marginals sum highest.  One
+ * pass: the inside and outside sweeps write the marginals, and the same
+ * workgroup then runs CKY over them (float64 chart, lowest split on ties, as
+ * crf_cky_decode) while its bundle is still on chip.
+ *   logZ       device float32[B] or NULL: log Z(x_b).
+ *   marginals  device float32, layout of scores (required, must not alias
+ *              scores): p((i,j)|x_b) on valid cells; the trees are decoded
+ *              from exactly these float32 values.
+ *   spans      device int32[B][2*(N1-1)-1][2], as crf_cky_decode.
+ *   best       device float32[B] or NULL: the sum of the marginals over the
+ *              tree (float64 chart, rounded).
+ * Unlabelled plans only (CRF_EUNSUPPORTED otherwise).
+ */
+int crf_mbr_decode(const crf_plan *plan, const float *scores, float *logZ, float *marginals, int32_t *spans,
+                   float *best, void *stream);
+
+/*
+ * crf_gold_loss -- the sentence-level CRF loss of a gold tree (Sec. 2.3,
+ * Eq. bracket-loss), L = log Z(x) - s(x,y), with s(x,y) the sum of the gold
+ * spans' scores (Eq. tree-score), and its gradient with respect to the scores,
+ * dL/ds(i,j) = p((i,j)|x) - 1[(i,j) in y] (the marginals of Sec. 3.2 minus
+ * the gold indicator).
+ *   gold_spans  device int32[B][2*(N1-1)-1][2]: the first 2n_b-1 rows of
+ *               sentence b are its gold tree's spans (i,j) (the layout
+ *               crf_cky_decode writes; any order).  Rows that are not spans
+ *               of the sentence (0 <= i < j <= n_b) are skipped; a repeated
+ *               span adds its score to s(x,y) again but 1 to the indicator.
+ *   grad_loss   device float32[B] upstream gradient dOut/dL, or NULL for 1.
+ *   loss        device float32[B]: L (not scaled by grad_loss).
+ *   grad_scores device float32, layout of scores (must not alias scores):
+ *               grad_loss[b] * (p((i,j)|x_b) - 1[(i,j) in y_b]) on valid cells
+ *               only.
+ * Unlabelled plans only (CRF_EUNSUPPORTED otherwise).
+ */
+int crf_gold_loss(const crf_plan *plan, const float *scores, const int32_t *gold_spans, const float *grad_loss,
+                  float *loss, float *grad_scores, void *stream);
+
+/*
+ * crf_cky_decode_labeled -- one-stage labelled decoding (Sec. 4.2,
+ * Eq. tree-label-score; Sec. 2.1, time-complexity paragraph): the labelled
+ * tree maximising the sum of s(i,j,l) over its labelled spans.  Each span's
+ * label is free, so this is CKY (as crf_cky_decode) over the float32 maxima
+ * max_l s(i,j,l), each of the tree's spans labelled with the lowest label
+ * attaining its maximum.
+ *   scores  device float32 [B][N1][N1][L], L = the plan's num_labels.
+ *   spans   device int32[B][2*(N1-1)-1][2], as crf_cky_decode.
+ *   labels  device int32[B][2*(N1-1)-1]: the label of each span row, -1 on
+ *           the rows past the tree.
+ *   best    device float32[B] or NULL: the labelled tree's score.
+ */
+int crf_cky_decode_labeled(const crf_plan *plan, const float *scores, int32_t *spans, int32_t *labels, float *best,
+                           void *stream);
+
+/*
+ * crf_label_spans -- the labelling stage of the two-stage parser (Sec. 2.1,
+ * Eq. label-argmax): every span (i,j) of a given tree independently takes
+ * argmax_l s(i,j,l) (the lowest such label on ties).
+ *   label_scores  device float32 [B][N1][N1][num_labels] (N1 and B of the
+ *                 plan; the plan's own num_labels is not used).
+ *   num_labels    1 <= num_labels <= CRF_MAX_LABELS.
+ *   spans         device int32[B][2*(N1-1)-1][2], e.g. crf_cky_decode's or
+ *                 crf_mbr_decode's output.
+ *   labels        device int32[B][2*(N1-1)-1]: the label of every row that is
+ *                 a span of its sentence (0 <= i < j <= n_b), else -1.
+ */
+int crf_label_spans(const crf_plan *plan, const float *label_scores, int32_t num_labels, const int32_t *spans,
+                    int32_t *labels, void *stream);
 
 /*
  * crf_inside_fwd_bwd_cky_noalloc -- crf_inside_fwd_bwd_cky for callers that

@@ -33,6 +33,10 @@ SIGNATURES = {
     "crf_cky_decode": (ctypes.c_int, [_P, _P, _P, _P, _P]),
     "crf_inside_fwd_bwd_cky": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _P]),
     "crf_inside_fwd_bwd_cky_noalloc": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _P]),
+    "crf_mbr_decode": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P]),
+    "crf_gold_loss": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P]),
+    "crf_cky_decode_labeled": (ctypes.c_int, [_P, _P, _P, _P, _P, _P]),
+    "crf_label_spans": (ctypes.c_int, [_P, _P, _I32, _P, _P, _P]),
     "crf_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "crf_last_error": (ctypes.c_char_p, []),
 }
@@ -53,6 +57,7 @@ class PlanStats(ctypes.Structure):
         ("split_ws_count", ctypes.c_int32),
         ("workspace_users", ctypes.c_int32),
         ("fused_queue", ctypes.c_int32),
+        ("mbr_fused", ctypes.c_int32),
     ]
 
 
@@ -134,6 +139,22 @@ def crf_inside_fwd_bwd_cky(plan, scores, grad_logZ, logZ, marginals, spans, best
 def crf_inside_fwd_bwd_cky_noalloc(plan, scores, grad_logZ, logZ, marginals, spans, best, stream):
     _check(load().crf_inside_fwd_bwd_cky_noalloc(plan, scores, grad_logZ, logZ, marginals, spans, best,
                                                  stream), "crf_inside_fwd_bwd_cky_noalloc")
+
+
+def crf_mbr_decode(plan, scores, logZ, marginals, spans, best, stream):
+    _check(load().crf_mbr_decode(plan, scores, logZ, marginals, spans, best, stream), "crf_mbr_decode")
+
+
+def crf_gold_loss(plan, scores, gold_spans, grad_loss, loss, grad_scores, stream):
+    _check(load().crf_gold_loss(plan, scores, gold_spans, grad_loss, loss, grad_scores, stream), "crf_gold_loss")
+
+
+def crf_cky_decode_labeled(plan, scores, spans, labels, best, stream):
+    _check(load().crf_cky_decode_labeled(plan, scores, spans, labels, best, stream), "crf_cky_decode_labeled")
+
+
+def crf_label_spans(plan, label_scores, num_labels, spans, labels, stream):
+    _check(load().crf_label_spans(plan, label_scores, num_labels, spans, labels, stream), "crf_label_spans")
 
 
 def crf_status_string(status):
@@ -278,6 +299,93 @@ class Plan:
                                self._vec(logZ, "logZ"), marginals.data_ptr(), spans.data_ptr(),
                                self._vec(best, "best"), _stream_ptr(t, self.device))
         return logZ, marginals, spans, best
+
+    def _spans_out(self, spans):
+        t = self._torch
+        R = 2 * (self.n1 - 1) - 1
+        if spans is None:
+            return t.empty((self.B, R, 2), dtype=t.int32, device=self.device)
+        if tuple(spans.shape) != (self.B, R, 2) or spans.dtype != t.int32 or not spans.is_contiguous():
+            raise ValueError(f"spans must be contiguous int32 [{self.B}, {R}, 2]")
+        if spans.device != self.device:
+            raise ValueError(f"spans on {spans.device}, plan on {self.device}")
+        return spans
+
+    def _labels_out(self, labels):
+        t = self._torch
+        R = 2 * (self.n1 - 1) - 1
+        if labels is None:
+            return t.empty((self.B, R), dtype=t.int32, device=self.device)
+        if tuple(labels.shape) != (self.B, R) or labels.dtype != t.int32 or not labels.is_contiguous():
+            raise ValueError(f"labels must be contiguous int32 [{self.B}, {R}]")
+        if labels.device != self.device:
+            raise ValueError(f"labels on {labels.device}, plan on {self.device}")
+        return labels
+
+    def mbr_decode(self, scores, logZ=None, marginals=None, spans=None, best=None):
+        """MBR decoding (Sec. 3.3): (logZ, marginals, spans, best), the trees
+        decoded by CKY over the marginals."""
+        t = self._torch
+        sp = self._scores(scores)
+        if logZ is None:
+            logZ = t.empty(self.B, dtype=t.float32, device=self.device)
+        if marginals is None:
+            marginals = t.zeros_like(scores)
+        elif tuple(marginals.shape) != tuple(scores.shape) or not marginals.is_contiguous():
+            raise ValueError("marginals must be a contiguous tensor shaped like scores")
+        spans = self._spans_out(spans)
+        if best is None:
+            best = t.empty(self.B, dtype=t.float32, device=self.device)
+        crf_mbr_decode(self._handle, sp, self._vec(logZ, "logZ"), marginals.data_ptr(), spans.data_ptr(),
+                       self._vec(best, "best"), _stream_ptr(t, self.device))
+        return logZ, marginals, spans, best
+
+    def gold_loss(self, scores, gold_spans, grad_loss=None, loss=None, grad_scores=None):
+        """Gold-tree CRF loss (Sec. 2.3, Eq. bracket-loss): (loss [B],
+        gradient shaped like scores, valid cells only; a fresh buffer is
+        zero-filled)."""
+        t = self._torch
+        sp = self._scores(scores)
+        R = 2 * (self.n1 - 1) - 1
+        if (tuple(gold_spans.shape) != (self.B, R, 2) or gold_spans.dtype != t.int32
+                or not gold_spans.is_contiguous() or gold_spans.device != self.device):
+            raise ValueError(f"gold_spans must be contiguous int32 [{self.B}, {R}, 2] on {self.device}")
+        if loss is None:
+            loss = t.empty(self.B, dtype=t.float32, device=self.device)
+        if grad_scores is None:
+            grad_scores = t.zeros_like(scores)
+        elif tuple(grad_scores.shape) != tuple(scores.shape) or not grad_scores.is_contiguous():
+            raise ValueError("grad_scores must be a contiguous tensor shaped like scores")
+        crf_gold_loss(self._handle, sp, gold_spans.data_ptr(), self._vec(grad_loss, "grad_loss"),
+                      self._vec(loss, "loss"), grad_scores.data_ptr(), _stream_ptr(t, self.device))
+        return loss, grad_scores
+
+    def cky_decode_labeled(self, scores, spans=None, labels=None, best=None):
+        """One-stage labelled decoding (Sec. 4.2): (spans, labels, best)."""
+        t = self._torch
+        sp = self._scores(scores)
+        spans = self._spans_out(spans)
+        labels = self._labels_out(labels)
+        if best is None:
+            best = t.empty(self.B, dtype=t.float32, device=self.device)
+        crf_cky_decode_labeled(self._handle, sp, spans.data_ptr(), labels.data_ptr(), self._vec(best, "best"),
+                               _stream_ptr(t, self.device))
+        return spans, labels, best
+
+    def label_spans(self, label_scores, spans, labels=None):
+        """Labelling stage (Sec. 2.1, Eq. label-argmax) of given trees:
+        label_scores [B, N1, N1, L'] float32 (any L'), spans as cky_decode
+        writes them; returns int32 [B, 2(N1-1)-1]."""
+        t = self._torch
+        if (label_scores.dim() != 4 or tuple(label_scores.shape[:3]) != (self.B, self.n1, self.n1)
+                or label_scores.dtype != t.float32 or not label_scores.is_contiguous()
+                or label_scores.device != self.device):
+            raise ValueError(f"label_scores must be contiguous float32 [{self.B}, {self.n1}, {self.n1}, L]")
+        spans = self._spans_out(spans)
+        labels = self._labels_out(labels)
+        crf_label_spans(self._handle, label_scores.data_ptr(), int(label_scores.shape[3]), spans.data_ptr(),
+                        labels.data_ptr(), _stream_ptr(t, self.device))
+        return labels
 
     def cky_decode(self, scores, spans=None, best=None):
         """(spans int32 [B, 2(N1-1)-1, 2] preorder padded with -1, best float32 [B])."""

@@ -292,13 +292,15 @@ struct Bundle {
 };
 
 // What a bundle's workgroup reads first: one record of rec_stride ints --
-// n, count, split_ws (CKY; -1 for inside), kind (1 inside, 0 CKY), then its
-// chart layout (inside_layout or cky_layout, as the plan chose it: e, ld,
-// cs) and div_magic(count), then the count sentence ids -- so that its
-// sentence ids arrive with its shape, one memory round trip before its
-// scores, and the workgroup computes none of it.
-constexpr int kRecHeader = 8;
-enum RecField { kRecN = 0, kRecCount, kRecSplitWs, kRecKind, kRecE, kRecLd, kRecCs, kRecMagic };
+// n, count, split_ws (CKY; -1 for inside), kind (kKindInside, kKindCky or
+// kKindMbr), then its chart layout (inside_layout or cky_layout, as the plan
+// chose it: e, ld, cs) and div_magic(count), then a second layout (the CKY
+// chart of an MBR bundle, whose first layout is its inside chart), then the
+// count sentence ids -- so that its sentence ids arrive with its shape, one
+// memory round trip before its scores, and the workgroup computes none of it.
+constexpr int kRecHeader = 12;
+enum RecField { kRecN = 0, kRecCount, kRecSplitWs, kRecKind, kRecE, kRecLd, kRecCs, kRecMagic, kRecE2, kRecLd2, kRecCs2 };
+enum RecKind { kKindCky = 0, kKindInside = 1, kKindMbr = 2 };
 // g / S by multiply-high: 2^32 / S + 1, exact for g < 2^18, 2 <= S <= 1024;
 // 0 for S = 1 (the caller takes g itself).
 __host__ __device__ inline uint32_t div_magic(int S) { return S > 1 ? 0xFFFFFFFFu / (uint32_t)S + 1u : 0u; }
@@ -326,7 +328,11 @@ struct KernelPlan {
     const int32_t *mix;          // [n_mix] records, or NULL when the fused kernel is not used
     int32_t n_mix;
     int32_t fused_grid;          // workgroups of the fused kernel (<= n_mix)
-    int32_t *counter;            // the fused kernel's bundle claims; zero between launches
+    // MBR decoding: records of bundles that run inside + marginals and then
+    // CKY over the marginals, or NULL (then the two run as separate launches)
+    const int32_t *mbr;
+    int32_t n_mbr, mbr_grid, mbr_lds;
+    int32_t *counter;            // the fused kernels' bundle claims; zero between launches
     int32_t rec_stride;          // ints per record: kRecHeader + the largest bundle
     int32_t B, n1, L;
 };
@@ -348,8 +354,19 @@ hipError_t launch_parse_scratch(const KernelPlan &p, char *scratch, const float 
 
 hipError_t launch_inside(const KernelPlan &p, const float *scores, const float *grad,
                          float *logZ, float *marg, hipStream_t stream);
+// CKY; labels != NULL: labelled scores, max over labels per span, and the
+// tree's spans' best labels (one-stage labelled decoding)
 hipError_t launch_cky(const KernelPlan &p, const float *scores, int32_t *spans, float *best,
-                      hipStream_t stream);
+                      hipStream_t stream, int32_t *labels = nullptr);
+// MBR decoding: inside + marginals, then CKY over the marginals
+hipError_t launch_mbr(const KernelPlan &p, const float *scores, float *logZ, float *marg, int32_t *spans,
+                      float *best, hipStream_t stream);
+// Gold-tree loss and its gradient (unlabelled)
+hipError_t launch_loss(const KernelPlan &p, const float *scores, const int32_t *gold, const float *grad,
+                       float *loss, float *grad_scores, hipStream_t stream);
+// Labelling stage: labels of given spans from [B][N1][N1][L] label scores
+hipError_t launch_label_spans(const KernelPlan &p, const float *label_scores, int L, const int32_t *spans,
+                              int32_t *labels, hipStream_t stream);
 hipError_t launch_parse(const KernelPlan &p, const float *scores, const float *grad, float *logZ,
                         float *marg, int32_t *spans, float *best, hipStream_t stream);
 hipError_t set_kernel_attributes(int max_lds_bytes);

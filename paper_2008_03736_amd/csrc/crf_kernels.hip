@@ -733,6 +733,43 @@ __device__ __forceinline__ void label_marginals(const float *s, int L, float mu,
     }
 }
 
+// Max over the L labels of one span at s (an exact float32 max), for the
+// one-stage labelled CKY: blocks of 32 labels, each block's loads issued
+// together (clamped to the last label).
+__device__ __forceinline__ float label_max(const float *s, int L, bool wide) {
+    float m = -INFINITY;
+    for (int q0 = 0; q0 < L; q0 += 32) {
+        float v[32];
+        if (q0 == 0) {
+            label_load32(s, L, wide, v);
+        } else {
+#pragma unroll
+            for (int k = 0; k < 32; ++k) v[k] = s[min(q0 + k, L - 1)];
+        }
+#pragma unroll
+        for (int k = 0; k < 32; ++k) m = fmax_nn(m, v[k]);   // (clamped copies repeat the last label)
+    }
+    return m;
+}
+// The lowest label attaining the max of one span's L labels (Eq. label-argmax
+// with the lowest-label tie rule): blocks of 32, strict '>' in label order.
+__device__ __forceinline__ int label_argmax(const float *s, int L) {
+    float m = -INFINITY;
+    int bl = 0;
+    for (int q0 = 0; q0 < L; q0 += 32) {
+        float v[32];
+#pragma unroll
+        for (int k = 0; k < 32; ++k) v[k] = s[min(q0 + k, L - 1)];
+#pragma unroll
+        for (int k = 0; k < 32; ++k)
+            if (q0 + k < L && v[k] > m) {
+                m = v[k];
+                bl = q0 + k;
+            }
+    }
+    return bl;
+}
+
 // ---------------------------------------------------------------------------
 // Inside (+ marginals).  One workgroup per bundle (or, SPILL, per long
 // sentence with its chart in the workspace).
@@ -743,11 +780,22 @@ __device__ __forceinline__ void label_marginals(const float *s, int L, float mu,
 // bundle_extra_bytes gives every bundle.
 // Chart of a sentence: the rotated squares P and Q of the inside chart
 // layout (ld x ld floats each).
-template <bool REV, bool LAB, bool SPILL>
+// GOLD (with REV, unlabelled): the gold-tree CRF loss (Sec. 2.3,
+//   Eq. bracket-loss) L = log Z - s(x,y) into loss[b], and in marg its
+//   gradient g (p((i,j)|x) - 1[(i,j) in y]), y = the first 2n-1 rows of the
+//   sentence's span list in `gold` (rows that are not spans of the sentence
+//   are skipped).  Gold spans are marked in their O' mirror cell P[j][n-w],
+//   which nothing reads once the sweep is done, so the epilogue subtracts g
+//   once per distinct span.
+constexpr int kGoldMark = 0x7FBADBAD;   // a NaN bit pattern: no finite chart value has it
+template <bool REV, bool LAB, bool SPILL, bool GOLD = false>
 __device__ __forceinline__ void inside_block(const KernelPlan &p, int block, const int32_t *rec, char *smem_raw,
                                              const float *__restrict__ scores,
                                              const float *__restrict__ grad,
-                                             float *__restrict__ logZ, float *__restrict__ marg) {
+                                             float *__restrict__ logZ, float *__restrict__ marg,
+                                             const int32_t *__restrict__ gold = nullptr,
+                                             float *__restrict__ loss = nullptr) {
+    static_assert(!GOLD || (REV && !LAB), "the gold-tree loss is unlabelled and needs the marginals");
     __shared__ double spill_forced[1];
     __shared__ float spill_gv[1];
     __shared__ int spill_id[1];
@@ -868,12 +916,35 @@ __device__ __forceinline__ void inside_block(const KernelPlan &p, int block, con
         else io_sweep<false, false>(bx, dsh, t0);
     }
     // log Z = (alpha~(0,n) - (n-2) d) ln 2 + forced sum.
+    auto log_z = [&](int sb) {
+        const double z2 = (double)chart0[(size_t)sb * cstride + n - 1] - (double)dsh[sb] * (n >= 2 ? n - 2 : 0);
+        return z2 * LN2_D + forced[sb];
+    };
     if (logZ != nullptr)
-        for (int sb = tid; sb < nb; sb += NT) {
-            const double z2 = (double)chart0[(size_t)sb * cstride + n - 1] - (double)dsh[sb] * (n >= 2 ? n - 2 : 0);
-            logZ[sid[sb]] = (float)(z2 * LN2_D + forced[sb]);
-        }
+        for (int sb = tid; sb < nb; sb += NT) logZ[sid[sb]] = (float)log_z(sb);
     if constexpr (!REV) return;
+
+    if constexpr (GOLD) {
+        // Gold rows of each sentence: mark the span, sum its score (float64,
+        // a lane group per sentence in a fixed order), loss = log Z - sum.
+        const int R = 2 * (N1 - 1) - 1, rows = 2 * n - 1;
+        by_sentence_groups(rows, nb, [&](auto gs, int sb, int gl, bool valid) {
+            constexpr int GS = decltype(gs)::value;
+            float *P = chart0 + (size_t)sb * cstride;
+            const int32_t *g2 = gold + (size_t)sid[sb] * R * 2;
+            double acc = 0.0;
+            for (int r = gl; r < rows; r += GS) {
+                const int i = g2[2 * r], j = g2[2 * r + 1];
+                if (0 <= i && i < j && j <= n) {
+                    acc += (double)*score_at(sb, i, j);
+                    if (valid) P[j * ld + n - (j - i)] = __builtin_bit_cast(float, kGoldMark);
+                }
+            }
+            acc = grp_sum_d<GS>(acc);
+            if (valid && gl == 0) loss[sid[sb]] = (float)(log_z(sb) - acc);
+        });
+        __syncthreads();
+    }
 
     // Epilogue: marginals of the valid cells (coalesced stores along rows),
     //   mu(i,j) = g exp2(alpha~(i,j) + O'(i,j) - (s(i,j) + d) - alpha~(0,n)),
@@ -882,11 +953,11 @@ __device__ __forceinline__ void inside_block(const KernelPlan &p, int block, con
     auto span_mu = [&](int sb, int i, int j, float own2) {
         const float *P = chart0 + (size_t)sb * cstride, *Q = P + (size_t)ld * ld;
         const bool forced_span = (j == i + 1) || (i == 0 && j == n);
+        const int w = j - i;
         float mu = gv[sb];
-        if (!forced_span) {
-            const int w = j - i;
-            mu *= fast_exp2(((P[i * ld + w - 1] - P[n - 1]) + Q[i * ld + w]) - (own2 + dsh[sb]));
-        }
+        if (!forced_span) mu *= fast_exp2(((P[i * ld + w - 1] - P[n - 1]) + Q[i * ld + w]) - (own2 + dsh[sb]));
+        if constexpr (GOLD)
+            if (__builtin_bit_cast(int, P[j * ld + n - w]) == kGoldMark) mu -= gv[sb];
         return mu;
     };
     if constexpr (LAB) {
@@ -1121,13 +1192,18 @@ __device__ __forceinline__ int split_of(const Cky_ctx<SP> &cx, int sb, int i, in
 // a node starting at p, that node and its chain of left children down to
 // the word itself.  So each row is written once, and a lane's chain of
 // split lookups is as long as its word's depth.
-template <typename SP>
-__device__ void walk_trees(const Cky_ctx<SP> &cx, const int *sid, int32_t *spans, int R) {
+// With labels (one-stage labelled decoding), every node written also gets
+// the lowest of its span's best labels, from the [B][N1][N1][L] scores s4.
+template <bool LAB, typename SP>
+__device__ void walk_trees(const Cky_ctx<SP> &cx, const int *sid, int32_t *spans, int R, int32_t *labels,
+                           const float *s4, int N1, int L) {
     const int n = cx.n, total = cx.nb * n;
     const float inv_n = 1.0f / (float)n;
     for (int t = threadIdx.x; t < total; t += blockDim.x) {
         const int sb = div_small(t, n, inv_n), p = t - sb * n;
         int2 *out = reinterpret_cast<int2 *>(spans + (size_t)sid[sb] * R * 2);
+        int32_t *lab = LAB ? labels + (size_t)sid[sb] * R : nullptr;
+        const float *sent = LAB ? s4 + (size_t)sid[sb] * N1 * N1 * L : nullptr;
         int i = 0, j = n, row = 0;
         // (every split k lies in (i, j), so each pass moves i up or j down;
         // the pass bounds only guard against a corrupt table)
@@ -1143,6 +1219,7 @@ __device__ void walk_trees(const Cky_ctx<SP> &cx, const int *sid, int32_t *spans
         }
         for (int it = 0; it < n; ++it) {
             out[row] = make_int2(i, j);
+            if constexpr (LAB) lab[row] = label_argmax(sent + ((size_t)i * N1 + j) * L, L);
             if (j - i < 2) break;
             j = split_of(cx, sb, i, j);
             ++row;
@@ -1150,14 +1227,20 @@ __device__ void walk_trees(const Cky_ctx<SP> &cx, const int *sid, int32_t *spans
     }
 }
 
-template <bool SPILL>
+// LAB: labelled scores [B][N1][N1][L]; each span's score is its best label's
+// (an exact max), and the tree's spans get their best labels (one-stage
+// labelled decoding, Sec. 4.2, Eq. tree-label-score).  second: take the chart
+// layout from the record's second layout (an MBR bundle's CKY chart).
+template <bool SPILL, bool LAB = false>
 __device__ __forceinline__ void cky_block(const KernelPlan &p, int block, const int32_t *rec, char *smem_raw,
                                           const float *__restrict__ scores,
-                                          int32_t *__restrict__ spans, float *__restrict__ best) {
+                                          int32_t *__restrict__ spans, float *__restrict__ best,
+                                          int32_t *__restrict__ labels = nullptr, bool second = false) {
     __shared__ int spill_id[1];
     const int NT = blockDim.x;
     const int tid = threadIdx.x;
     const int N1 = p.n1;
+    const int L = LAB ? p.L : 1;
 
     int n, nb, *sid;
     char *chart0, *split0;
@@ -1182,7 +1265,7 @@ __device__ __forceinline__ void cky_block(const KernelPlan &p, int block, const 
         nb = rec[kRecCount];
         const int split_ws = rec[kRecSplitWs];
         split_lds = split_ws < 0;
-        lay = CkyLayout{rec[kRecLd], rec[kRecCs], rec[kRecE]};
+        lay = second ? CkyLayout{rec[kRecLd2], rec[kRecCs2], rec[kRecE2]} : CkyLayout{rec[kRecLd], rec[kRecCs], rec[kRecE]};
         mnb = (uint32_t)rec[kRecMagic];
         chart0 = smem_raw;
         cstride = lay.cs;
@@ -1197,16 +1280,20 @@ __device__ __forceinline__ void cky_block(const KernelPlan &p, int block, const 
     __syncthreads();
 
     auto score_at = [&](int sb, int i, int j) -> const float * {
-        return scores + ((size_t)sid[sb] * N1 + i) * N1 + j;
+        return scores + (((size_t)sid[sb] * N1 + i) * N1 + j) * L;
     };
-    auto load_score = [](const float *q) -> float { return *q; };
+    const bool wide_in = LAB && (L & 1) == 0 && ((uintptr_t)scores & 7) == 0;
+    auto load_score = [&](const float *q) -> float {
+        if constexpr (LAB) return label_max(q, L, wide_in);
+        else return *q;
+    };
     auto put_score = [&](int sb, int i, int j, float sf) {
         double *be = cx.beta(sb);
         const double s = (double)sf;
         be[i * ld + j] = s;
         if (j == i + 1) be[j * ld + i] = s;
     };
-    for_cells_loaded<8>(nb, n, score_at, load_score, put_score);
+    for_cells_loaded<LAB ? 1 : 8>(nb, n, score_at, load_score, put_score);
     __syncthreads();
     // Workspace charts lay spans side by side; LDS charts interleave them
     // when their layout allows (e = 0).
@@ -1224,11 +1311,13 @@ __device__ __forceinline__ void cky_block(const KernelPlan &p, int block, const 
             int32_t *o = spans + ((size_t)sid[sbb] * R + r) * 2;
             o[0] = -1;
             o[1] = -1;
+            if constexpr (LAB) labels[(size_t)sid[sbb] * R + r] = -1;
         }
     }
     if (best != nullptr)
         for (int sb = tid; sb < nb; sb += NT) best[sid[sb]] = (float)cx.beta(sb)[n];
-    walk_trees(cx, sid, spans, R);   // (the sweep's last barrier published the splits)
+    // (the sweep's last barrier published the splits)
+    walk_trees<LAB>(cx, sid, spans, R, labels, scores, N1, L);
 }
 
 // Workgroups of 256, 512 or 1024 threads (the plan's choice) share one
@@ -1243,13 +1332,102 @@ __global__ __launch_bounds__(kThreadsMax) void inside_kernel(KernelPlan p, const
                                   smem_raw, scores, grad, logZ, marg);
 }
 
+// The gold-tree loss: the inside kernel with marginals, minus the gold
+// indicator (inside_block, GOLD).
 template <bool SPILL>
+__global__ __launch_bounds__(kThreadsMax) void loss_kernel(KernelPlan p, const float *__restrict__ scores,
+                                                           const int32_t *__restrict__ gold,
+                                                           const float *__restrict__ grad,
+                                                           float *__restrict__ loss,
+                                                           float *__restrict__ marg) {
+    extern __shared__ __align__(16) char smem_raw[];
+    inside_block<true, false, SPILL, true>(p, blockIdx.x,
+                                           SPILL ? nullptr : p.inside.recs + (size_t)blockIdx.x * p.rec_stride,
+                                           smem_raw, scores, grad, nullptr, marg, gold, loss);
+}
+
+template <bool SPILL, bool LAB>
 __global__ __launch_bounds__(kThreadsMax) void cky_kernel(KernelPlan p, const float *__restrict__ scores,
+                                                          int32_t *__restrict__ spans,
+                                                          float *__restrict__ best,
+                                                          int32_t *__restrict__ labels) {
+    extern __shared__ __align__(16) char smem_raw[];
+    cky_block<SPILL, LAB>(p, blockIdx.x, SPILL ? nullptr : p.cky.recs + (size_t)blockIdx.x * p.rec_stride,
+                          smem_raw, scores, spans, best, labels);
+}
+
+// Claim the next bundle of a persistent launch over n_rec records (see
+// parse_kernel): returns its index, n_rec or more when none is left.
+__device__ __forceinline__ int claim_next(int32_t *counter, int n_rec, int *slot) {
+    if (threadIdx.x == 0) {
+        const int ticket = atomicAdd(counter, 1);
+        if (ticket == n_rec - 1) atomicExch(counter, 0);
+        *slot = (int)gridDim.x + ticket;
+    }
+    __syncthreads();   // the claim is published and the bundle's LDS is free
+    const int cur = *slot;
+    __syncthreads();   // every thread has read the slot
+    return cur;
+}
+
+// MBR decoding (Sec. 3.3) in one launch: each bundle runs the inside sweep
+// with the outside and writes the marginals, then CKY with the marginals in
+// place of the scores, in the same workgroup.  The CKY prologue reads back
+// exactly the cells this thread wrote (the same cell walk over the same
+// bundle), so the marginals come from this CU's cache, and the LDS charts are
+// reused.  Persistent, bundles claimed as in parse_kernel.
+__global__ __launch_bounds__(kThreadsMax) void mbr_kernel(KernelPlan p, const float *__restrict__ scores,
+                                                          float *__restrict__ logZ, float *marg,
                                                           int32_t *__restrict__ spans,
                                                           float *__restrict__ best) {
     extern __shared__ __align__(16) char smem_raw[];
-    cky_block<SPILL>(p, blockIdx.x, SPILL ? nullptr : p.cky.recs + (size_t)blockIdx.x * p.rec_stride, smem_raw,
-                     scores, spans, best);
+    __shared__ int slot;
+    int cur = blockIdx.x;
+    for (;;) {
+        const int32_t *rec = p.mbr + (size_t)cur * p.rec_stride;
+        inside_block<true, false, false>(p, 0, rec, smem_raw, scores, nullptr, logZ, marg);
+        __syncthreads();   // the marginals are written and the inside charts are free
+        cky_block<false>(p, 0, rec, smem_raw, marg, spans, best, nullptr, true);
+        if ((int)gridDim.x >= p.n_mbr) break;
+        cur = claim_next(p.counter, p.n_mbr, &slot);
+        if (cur >= p.n_mbr) break;
+    }
+}
+
+// Labelling stage (Sec. 2.1, Eq. label-argmax): row r of sentence b's span
+// list gets the lowest label attaining max_l s(i,j,l) when it is a span of
+// sentence b, else -1.  A group of kLabelLanes lanes per row: lane q reads
+// labels q, q + kLabelLanes, ... of the row's contiguous label scores (keeping
+// its first maximum), then the group takes the max and the lowest label at it.
+constexpr int kLabelLanes = 16;
+__global__ __launch_bounds__(256) void label_spans_kernel(const int32_t *__restrict__ len,
+                                                          const float *__restrict__ s4, int n1, int L, int B,
+                                                          const int32_t *__restrict__ spans,
+                                                          int32_t *__restrict__ labels) {
+    const int R = 2 * (n1 - 1) - 1;
+    const int64_t rows = (int64_t)B * R;
+    const int64_t row = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / kLabelLanes;
+    const int q = threadIdx.x & (kLabelLanes - 1);
+    const bool ok = row < rows;          // the same for every lane of a group
+    const int64_t rr = ok ? row : rows - 1;
+    const int b = (int)(rr / R);
+    const int i = spans[2 * rr], j = spans[2 * rr + 1], n = len[b];
+    const bool valid = ok && 0 <= i && i < j && j <= n;
+    float m = -INFINITY;
+    int bl = 0x7fffffff;
+    if (valid) {
+        const float *v = s4 + (((size_t)b * n1 + i) * n1 + j) * L;
+        for (int l = q; l < L; l += kLabelLanes) {
+            const float x = v[l];
+            if (x > m) {
+                m = x;
+                bl = l;
+            }
+        }
+    }
+    const float mg = grp_max<kLabelLanes>(m);
+    const int k = grp_min_i<kLabelLanes>(m == mg ? bl : 0x7fffffff);
+    if (ok && q == 0) labels[rr] = valid ? k : -1;
 }
 
 // The whole pass -- inside, marginals and CKY -- in one launch of at most
@@ -1274,19 +1452,12 @@ __global__ __launch_bounds__(kThreadsMax) void parse_kernel(KernelPlan p, const 
     int cur = blockIdx.x;
     for (;;) {
         const int32_t *rec = p.mix + (size_t)cur * p.rec_stride;
-        if (rec[kRecKind])
+        if (rec[kRecKind] == kKindInside)
             inside_block<true, false, false>(p, 0, rec, smem_raw, scores, grad, logZ, marg);
         else
             cky_block<false>(p, 0, rec, smem_raw, scores, spans, best);
         if ((int)gridDim.x >= p.n_mix) break;   // one bundle per workgroup: no claims at all
-        if (threadIdx.x == 0) {
-            const int ticket = atomicAdd(p.counter, 1);
-            if (ticket == p.n_mix - 1) atomicExch(p.counter, 0);
-            slot = (int)gridDim.x + ticket;
-        }
-        __syncthreads();   // the claim is published and the bundle's LDS is free
-        cur = slot;
-        __syncthreads();   // every thread has read the slot
+        cur = claim_next(p.counter, p.n_mix, &slot);
         if (cur >= p.n_mix) break;
     }
 }
@@ -1339,7 +1510,9 @@ hipError_t set_kernel_attributes(int max_lds_bytes) {
     const void *fns[] = {
         (const void *)inside_kernel<false, false, false>, (const void *)inside_kernel<true, false, false>,
         (const void *)inside_kernel<false, true, false>,  (const void *)inside_kernel<true, true, false>,
-        (const void *)cky_kernel<false>,                  (const void *)parse_kernel,
+        (const void *)cky_kernel<false, false>,           (const void *)cky_kernel<false, true>,
+        (const void *)loss_kernel<false>,                 (const void *)parse_kernel,
+        (const void *)mbr_kernel,
     };
     for (const void *f : fns) {
         hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, max_lds_bytes);
@@ -1374,19 +1547,80 @@ hipError_t launch_inside(const KernelPlan &p, const float *scores, const float *
     return hipSuccess;
 }
 
-hipError_t launch_cky(const KernelPlan &p, const float *scores, int32_t *spans, float *best,
-                      hipStream_t stream) {
+template <bool LAB>
+static hipError_t launch_cky_k(const KernelPlan &p, const float *scores, int32_t *spans, float *best,
+                               hipStream_t stream, int32_t *labels) {
     const Schedule &q = p.cky;
     hipError_t e;
     if (q.n_bundles > 0) {
-        hipLaunchKernelGGL((cky_kernel<false>), dim3(q.n_bundles), dim3(q.threads), (size_t)q.lds_bytes, stream, p, scores, spans, best);
+        hipLaunchKernelGGL((cky_kernel<false, LAB>), dim3(q.n_bundles), dim3(q.threads), (size_t)q.lds_bytes, stream, p,
+                           scores, spans, best, labels);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     if (q.n_spill > 0) {
-        hipLaunchKernelGGL((cky_kernel<true>), dim3(q.n_spill), dim3(kThreadsMax), 0, stream, p, scores, spans, best);
+        hipLaunchKernelGGL((cky_kernel<true, LAB>), dim3(q.n_spill), dim3(kThreadsMax), 0, stream, p, scores, spans,
+                           best, labels);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     return hipSuccess;
+}
+
+hipError_t launch_cky(const KernelPlan &p, const float *scores, int32_t *spans, float *best,
+                      hipStream_t stream, int32_t *labels) {
+    return labels != nullptr ? launch_cky_k<true>(p, scores, spans, best, stream, labels)
+                             : launch_cky_k<false>(p, scores, spans, best, stream, nullptr);
+}
+
+hipError_t launch_mbr(const KernelPlan &p, const float *scores, float *logZ, float *marg, int32_t *spans,
+                      float *best, hipStream_t stream) {
+    if (p.mbr == nullptr || p.counter == nullptr || p.mbr_grid < 1) {
+        // separate launches, in stream order: inside + marginals, then CKY
+        // over the marginals
+        hipError_t e = launch_inside(p, scores, nullptr, logZ, marg, stream);
+        if (e != hipSuccess) return e;
+        return launch_cky(p, marg, spans, best, stream);
+    }
+    hipLaunchKernelGGL(mbr_kernel, dim3(p.mbr_grid), dim3(p.inside.threads), (size_t)p.mbr_lds, stream, p, scores,
+                       logZ, marg, spans, best);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    // sentences too long for LDS (the plan has checked that the inside and
+    // CKY workspace lists hold the same sentences): their marginals, then
+    // CKY over them
+    if (p.inside.n_spill > 0) {
+        launch_inside_k<true>(p, dim3(p.inside.n_spill), kThreadsMax, 0, stream, scores, nullptr, logZ, marg);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        hipLaunchKernelGGL((cky_kernel<true, false>), dim3(p.cky.n_spill), dim3(kThreadsMax), 0, stream, p, marg, spans,
+                           best, nullptr);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
+hipError_t launch_loss(const KernelPlan &p, const float *scores, const int32_t *gold, const float *grad,
+                       float *loss, float *grad_scores, hipStream_t stream) {
+    const Schedule &q = p.inside;
+    hipError_t e;
+    if (q.n_bundles > 0) {
+        hipLaunchKernelGGL((loss_kernel<false>), dim3(q.n_bundles), dim3(q.threads), (size_t)q.lds_bytes, stream, p,
+                           scores, gold, grad, loss, grad_scores);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    if (q.n_spill > 0) {
+        hipLaunchKernelGGL((loss_kernel<true>), dim3(q.n_spill), dim3(kThreadsMax), 0, stream, p, scores, gold, grad,
+                           loss, grad_scores);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
+hipError_t launch_label_spans(const KernelPlan &p, const float *label_scores, int L, const int32_t *spans,
+                              int32_t *labels, hipStream_t stream) {
+    const int64_t rows = (int64_t)p.B * (2 * (p.n1 - 1) - 1);
+    const int64_t blocks = (rows * kLabelLanes + 255) / 256;
+    hipLaunchKernelGGL(label_spans_kernel, dim3((unsigned)blocks), dim3(256), 0, stream, p.len, label_scores, p.n1, L,
+                       p.B, spans, labels);
+    return hipGetLastError();
 }
 
 hipError_t launch_parse(const KernelPlan &p, const float *scores, const float *grad, float *logZ,
@@ -1407,7 +1641,8 @@ hipError_t launch_parse(const KernelPlan &p, const float *scores, const float *g
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     if (qc.n_spill > 0) {
-        hipLaunchKernelGGL((cky_kernel<true>), dim3(qc.n_spill), dim3(kThreadsMax), 0, stream, p, scores, spans, best);
+        hipLaunchKernelGGL((cky_kernel<true, false>), dim3(qc.n_spill), dim3(kThreadsMax), 0, stream, p, scores, spans,
+                           best, nullptr);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     return hipSuccess;

@@ -423,7 +423,35 @@ int crf_plan_create(crf_plan **out, const int32_t *lengths_host, int32_t batch, 
         for (int q = 0; q < bd.count; ++q) uses_ws[sc.order[bd.first + q]] = 1;
     }
     sc.ws_bytes = split_cursor - si.ws_bytes;
-    p->ws_bytes = si.ws_bytes + sc.ws_bytes;
+
+    // MBR decoding (unlabelled plans): bundles whose workgroup holds the
+    // inside chart and then, in the same LDS, the CKY chart over the
+    // marginals, so a bundle's LDS is the larger of the two.  Sentences past
+    // LDS run on the inside and CKY workspace kernels, which must then list
+    // the same sentences; if they do not, or no bundle is left, MBR decoding
+    // runs as separate launches.
+    HostSchedule sm;
+    bool mbr_fused = num_labels == 1;
+    if (mbr_fused) {
+        auto mbr_bytes = [=](int n, int64_t count) {
+            return std::max(inside_bundle_bytes(n, count), cky_bundle_bytes(n, count));
+        };
+        sm = make_schedule(order, lengths_host, lds_cap, force, 0, mbr_bytes, [](int) { return (int64_t)0; },
+                           kCkyTargetScale);
+        auto sorted = [](std::vector<int32_t> v) {
+            std::sort(v.begin(), v.end());
+            return v;
+        };
+        const std::vector<int32_t> ms = sorted(sm.spill);
+        mbr_fused = !sm.bundles.empty() && ms == sorted(si.spill) && ms == sorted(sc.spill);
+        if (mbr_fused)
+            for (crf::Bundle &bd : sm.bundles) {
+                if (split_in_lds(bd.n)) continue;
+                bd.split_ws = (int32_t)(split_cursor / 256);
+                split_cursor += (bd.count * crf::cky_split_count(bd.n) + 255) / 256 * 256;
+            }
+    }
+    p->ws_bytes = split_cursor;
     p->workspace_users = (int32_t)std::count(uses_ws.begin(), uses_ws.end(), 1);
 
     std::vector<int32_t> len(lengths_host, lengths_host + batch);
@@ -453,35 +481,55 @@ int crf_plan_create(crf_plan **out, const int32_t *lengths_host, int32_t batch, 
     int max_count = 1;
     for (const crf::Bundle &bd : si.bundles) max_count = std::max(max_count, (int)bd.count);
     for (const crf::Bundle &bd : sc.bundles) max_count = std::max(max_count, (int)bd.count);
+    if (mbr_fused)
+        for (const crf::Bundle &bd : sm.bundles) max_count = std::max(max_count, (int)bd.count);
     const int stride = crf::kRecHeader + max_count;
     kp.rec_stride = stride;
-    auto records = [&](const HostSchedule &h, bool inside) {
+    auto put_inside_layout = [&](int32_t *q, int n, int count, int off) {
+        const crf::InsideLayout l = crf::inside_layout(n, count, inside_strict(n, count));
+        q[crf::kRecE + off] = l.e;
+        q[crf::kRecLd + off] = l.ld;
+        q[crf::kRecCs + off] = l.cs;
+    };
+    auto put_cky_layout = [&](int32_t *q, int n, int count, int off) {
+        const crf::CkyLayout l = crf::cky_layout(n, count, split_in_lds(n) ? 1 : 0, cky_strict(n, count));
+        q[crf::kRecE + off] = l.e;
+        q[crf::kRecLd + off] = l.ld;
+        q[crf::kRecCs + off] = l.cs;
+    };
+    constexpr int kSecond = crf::kRecE2 - crf::kRecE;   // offset of the second layout's fields
+    auto records = [&](const HostSchedule &h, int kind) {
         std::vector<int32_t> r((size_t)h.bundles.size() * stride, 0);
         for (size_t b = 0; b < h.bundles.size(); ++b) {
             const crf::Bundle &bd = h.bundles[b];
             int32_t *q = r.data() + b * stride;
             q[crf::kRecN] = bd.n;
             q[crf::kRecCount] = bd.count;
-            q[crf::kRecSplitWs] = inside ? -1 : bd.split_ws;
-            q[crf::kRecKind] = inside ? 1 : 0;
-            if (inside) {
-                const crf::InsideLayout l = crf::inside_layout(bd.n, bd.count, inside_strict(bd.n, bd.count));
-                q[crf::kRecE] = l.e;
-                q[crf::kRecLd] = l.ld;
-                q[crf::kRecCs] = l.cs;
+            q[crf::kRecSplitWs] = kind == crf::kKindInside ? -1 : bd.split_ws;
+            q[crf::kRecKind] = kind;
+            if (kind == crf::kKindCky) {
+                put_cky_layout(q, bd.n, bd.count, 0);
             } else {
-                const crf::CkyLayout l =
-                    crf::cky_layout(bd.n, bd.count, split_in_lds(bd.n) ? 1 : 0, cky_strict(bd.n, bd.count));
-                q[crf::kRecE] = l.e;
-                q[crf::kRecLd] = l.ld;
-                q[crf::kRecCs] = l.cs;
+                put_inside_layout(q, bd.n, bd.count, 0);
+                if (kind == crf::kKindMbr) put_cky_layout(q, bd.n, bd.count, kSecond);
             }
             q[crf::kRecMagic] = (int32_t)crf::div_magic(bd.count);
             for (int t = 0; t < bd.count; ++t) q[crf::kRecHeader + t] = h.order[bd.first + t];
         }
         return r;
     };
-    const std::vector<int32_t> rec_in = records(si, true), rec_ck = records(sc, false);
+    const std::vector<int32_t> rec_in = records(si, crf::kKindInside), rec_ck = records(sc, crf::kKindCky);
+    const std::vector<int32_t> rec_mbr = mbr_fused ? records(sm, crf::kKindMbr) : std::vector<int32_t>();
+    kp.n_mbr = mbr_fused ? (int32_t)sm.bundles.size() : 0;
+    kp.mbr_lds = mbr_fused ? sm.lds_bytes : 0;
+    kp.mbr_grid = 0;
+    if (mbr_fused) {
+        int cus = 0;
+        if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, p->device) != hipSuccess || cus < 1)
+            cus = 256;
+        const int per_cu = std::min(4, std::max(1, (int)(lds_cap / std::max(1, sm.lds_bytes))));
+        kp.mbr_grid = std::min<int32_t>(kp.n_mbr, cus * per_cu);
+    }
     std::vector<int32_t> rec_mix;
     rec_mix.reserve(mix.size() * stride);
     for (int32_t e : mix) {
@@ -504,7 +552,8 @@ int crf_plan_create(crf_plan **out, const int32_t *lengths_host, int32_t batch, 
         (e = upload(p, rec_ck, &kp.cky.recs)) != hipSuccess ||
         (e = upload(p, sc.spill, &kp.cky.order_spill)) != hipSuccess ||
         (e = upload(p, sc.off, &kp.cky.ws_off)) != hipSuccess ||
-        (e = upload(p, rec_mix, &kp.mix)) != hipSuccess) {
+        (e = upload(p, rec_mix, &kp.mix)) != hipSuccess ||
+        (e = upload(p, rec_mbr, &kp.mbr)) != hipSuccess) {
         const int code = (e == hipErrorOutOfMemory) ? CRF_ENOMEM : CRF_EHIP;
         release(p);
         delete p;
@@ -512,7 +561,7 @@ int crf_plan_create(crf_plan **out, const int32_t *lengths_host, int32_t batch, 
                                   : hip_fail(e, "schedule upload");
     }
     kp.counter = nullptr;
-    if (kp.fused_grid > 0) {
+    if (kp.fused_grid > 0 || kp.mbr_grid > 0) {
         void *c = nullptr;
         if ((e = hipMalloc(&c, 256)) != hipSuccess || (p->allocations.push_back(c), false) ||
             (e = hipMemset(c, 0, 256)) != hipSuccess) {
@@ -537,7 +586,7 @@ int crf_plan_create(crf_plan **out, const int32_t *lengths_host, int32_t batch, 
     }
     // Best effort: ROCm launches with any dynamic LDS up to the per-block
     // limit without this attribute; a real shortfall surfaces as a launch error.
-    if (crf::set_kernel_attributes(std::max(si.lds_bytes, sc.lds_bytes)) != hipSuccess)
+    if (crf::set_kernel_attributes(std::max(std::max(si.lds_bytes, sc.lds_bytes), kp.mbr_lds)) != hipSuccess)
         (void)hipGetLastError();
     // Resolve this device's scratch address for the no-allocation entry
     // point now (it retries, and reports a failure, on its first call).
@@ -575,6 +624,7 @@ int crf_plan_info(const crf_plan *plan, crf_plan_stats *out) {
     out->split_ws_count = plan->split_ws_count;
     out->workspace_users = plan->workspace_users;
     out->fused_queue = plan->kp.counter != nullptr ? 1 : 0;
+    out->mbr_fused = plan->kp.mbr != nullptr ? 1 : 0;
     return ok();
 }
 
@@ -651,6 +701,58 @@ int crf_inside_fwd_bwd_cky_noalloc(const crf_plan *plan, const float *scores, co
     e = crf::launch_parse_scratch(plan->kp, scr, scores, grad_logZ, logZ, marginals, spans, best,
                                   static_cast<hipStream_t>(stream));
     return e == hipSuccess ? ok() : hip_fail(e, "crf_inside_fwd_bwd_cky_noalloc launch");
+}
+
+int crf_mbr_decode(const crf_plan *plan, const float *scores, float *logZ, float *marginals, int32_t *spans,
+                   float *best, void *stream) {
+    if (plan == nullptr) return fail(CRF_EINVAL, "plan is NULL");
+    if (scores == nullptr || marginals == nullptr || spans == nullptr)
+        return fail(CRF_EINVAL, "scores/marginals/spans is NULL");
+    if (scores == marginals) return fail(CRF_EINVAL, "marginals must not alias scores");
+    if (plan->L != 1) return fail(CRF_EUNSUPPORTED, "MBR decoding of labelled scores (L = %d)", plan->L);
+    int rc = check_device(plan);
+    if (rc != CRF_OK) return rc;
+    hipError_t e = crf::launch_mbr(plan->kp, scores, logZ, marginals, spans, best, static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? ok() : hip_fail(e, "crf_mbr_decode launch");
+}
+
+int crf_gold_loss(const crf_plan *plan, const float *scores, const int32_t *gold_spans, const float *grad_loss,
+                  float *loss, float *grad_scores, void *stream) {
+    if (plan == nullptr) return fail(CRF_EINVAL, "plan is NULL");
+    if (scores == nullptr || gold_spans == nullptr || loss == nullptr || grad_scores == nullptr)
+        return fail(CRF_EINVAL, "scores/gold_spans/loss/grad_scores is NULL");
+    if (scores == grad_scores) return fail(CRF_EINVAL, "grad_scores must not alias scores");
+    if (plan->L != 1) return fail(CRF_EUNSUPPORTED, "gold-tree loss of labelled scores (L = %d)", plan->L);
+    int rc = check_device(plan);
+    if (rc != CRF_OK) return rc;
+    hipError_t e = crf::launch_loss(plan->kp, scores, gold_spans, grad_loss, loss, grad_scores,
+                                    static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? ok() : hip_fail(e, "crf_gold_loss launch");
+}
+
+int crf_cky_decode_labeled(const crf_plan *plan, const float *scores, int32_t *spans, int32_t *labels, float *best,
+                           void *stream) {
+    if (plan == nullptr) return fail(CRF_EINVAL, "plan is NULL");
+    if (scores == nullptr || spans == nullptr || labels == nullptr)
+        return fail(CRF_EINVAL, "scores/spans/labels is NULL");
+    int rc = check_device(plan);
+    if (rc != CRF_OK) return rc;
+    hipError_t e = crf::launch_cky(plan->kp, scores, spans, best, static_cast<hipStream_t>(stream), labels);
+    return e == hipSuccess ? ok() : hip_fail(e, "crf_cky_decode_labeled launch");
+}
+
+int crf_label_spans(const crf_plan *plan, const float *label_scores, int32_t num_labels, const int32_t *spans,
+                    int32_t *labels, void *stream) {
+    if (plan == nullptr) return fail(CRF_EINVAL, "plan is NULL");
+    if (label_scores == nullptr || spans == nullptr || labels == nullptr)
+        return fail(CRF_EINVAL, "label_scores/spans/labels is NULL");
+    if (num_labels < 1 || num_labels > CRF_MAX_LABELS)
+        return fail(CRF_EINVAL, "num_labels %d outside [1, %d]", num_labels, CRF_MAX_LABELS);
+    int rc = check_device(plan);
+    if (rc != CRF_OK) return rc;
+    hipError_t e = crf::launch_label_spans(plan->kp, label_scores, num_labels, spans, labels,
+                                           static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? ok() : hip_fail(e, "crf_label_spans launch");
 }
 
 int crf_cky_decode(const crf_plan *plan, const float *scores, int32_t *spans, float *best,

@@ -48,7 +48,17 @@ namespace crf {
 hipError_t launch_inside(const KernelPlan &, const float *, const float *, float *, float *, hipStream_t) {
     return hipErrorNotSupported;
 }
-hipError_t launch_cky(const KernelPlan &, const float *, int32_t *, float *, hipStream_t) {
+hipError_t launch_cky(const KernelPlan &, const float *, int32_t *, float *, hipStream_t, int32_t *) {
+    return hipErrorNotSupported;
+}
+hipError_t launch_mbr(const KernelPlan &, const float *, float *, float *, int32_t *, float *, hipStream_t) {
+    return hipErrorNotSupported;
+}
+hipError_t launch_loss(const KernelPlan &, const float *, const int32_t *, const float *, float *, float *,
+                       hipStream_t) {
+    return hipErrorNotSupported;
+}
+hipError_t launch_label_spans(const KernelPlan &, const float *, int, const int32_t *, int32_t *, hipStream_t) {
     return hipErrorNotSupported;
 }
 hipError_t launch_parse(const KernelPlan &, const float *, const float *, float *, float *, int32_t *, float *,
@@ -113,6 +123,24 @@ int main(int argc, char **argv) {
             strict = l.ld == ld && l.cs == cs && l.e == e;
         }
         std::printf("R %d %d %d %d %d %d %d %d %lld", kind, n, count, split_ws, strict, ld, cs, e, bytes);
+        for (int t = 0; t < count; ++t) std::printf(" %d", r[crf::kRecHeader + t]);
+        std::printf("\n");
+    }
+    // MBR bundles, as
+    //   M n count split_ws inside_strict cky_strict mbr_grid mbr_lds id...
+    for (int b = 0; b < kp.n_mbr; ++b) {
+        const int32_t *r = kp.mbr + (size_t)b * kp.rec_stride;
+        const int n = r[crf::kRecN], count = r[crf::kRecCount];
+        const crf::InsideLayout li = crf::inside_layout(n, count, true);
+        const crf::CkyLayout lc = crf::cky_layout(n, count, r[crf::kRecSplitWs] < 0 ? 1 : 0, true);
+        const int si = li.ld == r[crf::kRecLd] && li.cs == r[crf::kRecCs] && li.e == r[crf::kRecE];
+        const int sc = lc.ld == r[crf::kRecLd2] && lc.cs == r[crf::kRecCs2] && lc.e == r[crf::kRecE2];
+        if (r[crf::kRecKind] != crf::kKindMbr) {
+            std::printf("E kind\n");
+            return 1;
+        }
+        const long long ib = crf::inside_bundle_bytes(n, count, si != 0);
+        std::printf("M %d %d %d %d %d %d %d %lld", n, count, r[crf::kRecSplitWs], si, sc, kp.mbr_grid, kp.mbr_lds, ib);
         for (int t = 0; t < count; ++t) std::printf(" %d", r[crf::kRecHeader + t]);
         std::printf("\n");
     }

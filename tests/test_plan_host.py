@@ -55,6 +55,11 @@ def plan_of(harness, tmp_path, lengths, labels=None):
         elif t[0] == "I":
             v = list(map(int, t[1:]))
             recs.append(dict(kind=1, n=v[0], count=v[1], ids=v[2:]))
+        elif t[0] == "M":
+            v = list(map(int, t[1:]))
+            head.setdefault("mbr", []).append(dict(n=v[0], count=v[1], split_ws=v[2], inside_strict=v[3],
+                                                   cky_strict=v[4], grid=v[5], lds=v[6], inside_bytes=v[7],
+                                                   ids=v[8:]))
     return head, recs
 
 
@@ -152,3 +157,28 @@ def test_workspace_users_reported(harness, tmp_path):
     # sentences past the LDS limit use it for both charts
     head, _ = plan_of(harness, tmp_path, [200, 150, 10])
     assert head["spill"] == 2 and head["cky_spill"] == 2 and head["ws_users"] == 2
+
+
+@pytest.mark.parametrize("name", ["tiny", "mixed", "longer"])
+def test_mbr_bundles(harness, tmp_path, name):
+    # MBR bundles: every sentence in exactly one, of its own length, within
+    # the launch's LDS with either chart; split tables of long sentences in
+    # the workspace; one workgroup slot per CU per bundle LDS that fits
+    b = W.make(name)
+    head, _ = plan_of(harness, tmp_path, b.lengths)
+    mb = head["mbr"]
+    ids = sorted(i for r in mb for i in r["ids"])
+    assert ids == list(range(b.B))
+    lds = mb[0]["lds"]
+    for r in mb:
+        assert r["count"] == len(r["ids"]) and all(b.lengths[i] == r["n"] for i in r["ids"])
+        assert r["inside_bytes"] <= lds
+        assert (r["split_ws"] >= 0) == (r["n"] >= 97)
+        assert r["grid"] == min(len(mb), 256 * min(4, max(1, 163840 // lds)))
+    if name == "mixed":
+        assert lds <= head["half_cu"]          # two workgroups per CU
+
+
+def test_mbr_not_fused_when_all_in_workspace(harness, tmp_path):
+    head, _ = plan_of(harness, tmp_path, [200, 150])
+    assert "mbr" not in head
