@@ -174,6 +174,9 @@ def main():
                     help="after timing, run a plain device copy of this many MiB a few times "
                          "(a known-size kernel to scale HBM counters by)")
     ap.add_argument("--ceilings", action="store_true", help="measure the ALU / LDS ceilings and exit")
+    ap.add_argument("--profile", choices=["parse", "fwd_bwd", "cky", "mbr", "loss", "lcky", "label_spans"],
+                    help="launch only this entry point (warmup + steps launches, then exit): the program "
+                         "that rocprofv3 summaries under profiles/ are taken on")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); "
@@ -224,7 +227,60 @@ def main():
         if rc:
             raise B.CrfError(rc, "crf_inside_fwd_bwd_cky")
 
+    def mbr():
+        rc = lib.crf_mbr_decode(h, a_scores, a_logz, a_marg, a_spans, a_best, sp)
+        if rc:
+            raise B.CrfError(rc, "crf_mbr_decode")
+
+    # gold trees for the loss: right-branching (any tree will do for timing)
+    gold_np = np.full((batch.B, R, 2), -1, np.int32)
+    for bi, nn in enumerate(batch.lengths):
+        nn = int(nn)
+        rows = [(i, nn) for i in range(nn - 1)]
+        g2 = np.empty((2 * nn - 1, 2), np.int32)
+        g2[0:2 * nn - 2:2] = rows
+        g2[1:2 * nn - 2:2] = [(i, i + 1) for i in range(nn - 1)]
+        g2[2 * nn - 2] = (nn - 1, nn)
+        gold_np[bi, :2 * nn - 1] = g2
+    gold = torch.from_numpy(gold_np).to(dev)
+    labels_out = torch.empty((batch.B, R), dtype=torch.int32, device=dev)
+    a_gold, a_labels = P(gold.data_ptr()), P(labels_out.data_ptr())
+
+    def loss():
+        rc = lib.crf_gold_loss(h, a_scores, a_gold, None, a_logz, a_marg, sp)
+        if rc:
+            raise B.CrfError(rc, "crf_gold_loss")
+
+    def lcky():
+        rc = lib.crf_cky_decode_labeled(h, a_scores, a_spans, a_labels, a_best, sp)
+        if rc:
+            raise B.CrfError(rc, "crf_cky_decode_labeled")
+
+    def label_spans():
+        rc = lib.crf_label_spans(h, a_scores, labels, a_spans, a_labels, sp)
+        if rc:
+            raise B.CrfError(rc, "crf_label_spans")
+
     step = parse if decode else fwd_bwd
+    passes = {"parse": parse, "fwd_bwd": fwd_bwd, "cky": cky, "mbr": mbr, "loss": loss, "lcky": lcky,
+              "label_spans": label_spans}
+    if args.profile is not None:
+        if args.profile == "label_spans":
+            lcky()                       # spans to label
+        fn = passes[args.profile]
+        for _ in range(args.warmup + args.steps):
+            fn()
+        torch.cuda.synchronize()
+        print(json.dumps({"profile": args.profile, "workload": batch.name, "launches": args.warmup + args.steps,
+                          "warmup": args.warmup}), flush=True)
+        if args.copy_mib > 0:
+            src = torch.empty(args.copy_mib << 18, dtype=torch.float32, device=dev).fill_(1.0)
+            dst = torch.empty_like(src)
+            for _ in range(3):
+                dst.copy_(src)
+            torch.cuda.synchronize()
+        plan.close()
+        return
 
     for _ in range(args.warmup):
         step()
@@ -260,6 +316,9 @@ def main():
     t_step = per_launch(step, reps)
     t_inside = per_launch(fwd_bwd, reps) if decode else t_step
     t_cky = per_launch(cky, reps) if decode else None
+    # the other entry points on the same batch (median launch, microseconds)
+    others = ["mbr", "loss"] if decode else ["lcky"]
+    t_other = {k: per_launch(passes[k], reps) for k in others}
 
     # The longest sentence alone: the dependency chain no batch can beat.
     longest = int(np.argmax(batch.lengths))
@@ -302,6 +361,10 @@ def main():
     if decode:
         extra["decode_ms"] = t_cky
         extra["decode_sentences_per_s"] = round(batch.B / (t_cky["median"] * 1e-3), 1)
+    names = {"mbr": "mbr_decode", "loss": "gold_loss", "lcky": "labeled_decode"}
+    for k, t in t_other.items():
+        extra[names[k] + "_ms"] = t
+        extra[names[k] + "_sentences_per_s"] = round(batch.B / (t["median"] * 1e-3), 1)
 
     if args.copy_mib > 0:
         src = torch.empty(args.copy_mib << 18, dtype=torch.float32, device=dev).fill_(1.0)
