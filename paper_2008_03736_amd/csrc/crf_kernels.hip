@@ -209,6 +209,7 @@ struct Bundle_ctx {
     int n, ld, nb;
     uint32_t mnb;   // div_magic(nb)
     int e;          // the inside layout's bank exponent (inside_layout); 5 on the workspace
+    int *ovf;       // linear-domain sweeps: set to 1 (LDS) when a value leaves float32's range
 };
 
 
@@ -330,11 +331,41 @@ __device__ __forceinline__ float span_lse(const T *a, const T *b, int kl, float 
     return mg + fast_log2(sg) + own;
 }
 
+// The same sum in the linear domain (the chart holding exp2 of the values
+// above): one span's sum over its K split terms is the dot product of its
+// two runs, sum_k a_k b_k, one FMA per term.  Terms c >= MF past K are
+// dropped by a select on the accumulator, so whatever the masked reads find
+// (other spans' scores, padding) never reaches the sum.  Two accumulators
+// halve the dependent chain.  The group's sum is returned to every lane.
+template <int G, int C, int MF, typename T>
+__device__ __forceinline__ float span_dot(const T *a, const T *b, int kl) {
+    float xa[C], xb[C];
+#pragma unroll
+    for (int c = 0; c < C; ++c) {
+        xa[c] = a[c * G];
+        xb[c] = b[c * G];
+    }
+    __builtin_amdgcn_sched_barrier(0);   // every load in flight before the first use
+    float acc[2] = {0.f, 0.f};
+#pragma unroll
+    for (int c = 0; c < C; ++c) {
+        const float t = __builtin_fmaf(xa[c], xb[c], acc[c & 1]);
+        acc[c & 1] = (c < MF || c * G < kl) ? t : acc[c & 1];
+    }
+    return grp_sum<G>(acc[0] + acc[1]);
+}
+
+// Bound of a stored linear-domain value: anything above it (infinity, NaN
+// or a value whose products could overflow) sends the bundle to the
+// log-domain sweep.
+constexpr float kLinMax = 0x1p+100f;
+
 // One span of a width-w inside step (K = w - 1 splits):
 // alpha(i,j) = s(i,j) + d + log2 sum_k exp2(alpha(i,k) + alpha(k,j)), d the
 // sentence's score shift (see rescale_chart); the root's own term is not
-// shifted.
-template <int G, int C, int MF, bool IL, typename T>
+// shifted.  LIN: the chart holds exp2 of these values, and the span's value
+// is exp2(own) * sum_k alpha(i,k) alpha(k,j).
+template <bool LIN, int G, int C, int MF, bool IL, typename T>
 __device__ __forceinline__ void inside_span(const Bundle_ctx<T> &bx, int w, int nsp, int f, const float *dsh) {
     const int ld = bx.ld, n = bx.n, K = w - 1;
     const Lane_at at = lane_at<G, IL>(f, nsp, bx.nb, bx.mnb);
@@ -344,20 +375,26 @@ __device__ __forceinline__ void inside_span(const Bundle_ctx<T> &bx, int w, int 
     const int rq = (int)__umul24((uint32_t)(i + ld + w), (uint32_t)ld);   // Q row j
     const int pa = rp + rot_alpha_p(w), qa = rq + n + 1 - w;                   // alpha(i,j) cells
     const float own = pq[pa] + (w < n ? dsh[at.sb] : 0.f);
-    const float v = span_lse<G, C, MF>(pq + rp + l, pq + rq + (n + 2 - w) + l, K - l, own);
+    float v;
+    if constexpr (LIN)
+        v = fast_exp2(own) * span_dot<G, C, MF>(pq + rp + l, pq + rq + (n + 2 - w) + l, K - l);
+    else
+        v = span_lse<G, C, MF>(pq + rp + l, pq + rq + (n + 2 - w) + l, K - l, own);
     // An unconditional use keeps the score load in the load block, where it
     // is issued with the operand loads instead of after the reductions.
     asm volatile("" ::"v"(v));
     if (at.act && l == 0) {
         pq[pa] = v;
         pq[qa] = v;
+        if constexpr (LIN)
+            if (!(v <= kLinMax)) *bx.ovf = 1;
     }
 }
 
 // One span (i,j) of a width-v outside step: K = n - v parent terms, every
 // operand a parent of width > v or a sibling of width <= n - v, so this step
 // runs beside the inside step of width n - v + 1.
-template <int G, int C, int MF, bool IL, typename T>
+template <bool LIN, int G, int C, int MF, bool IL, typename T>
 __device__ __forceinline__ void outside_span(const Bundle_ctx<T> &bx, int v, int nsp, int f, const float *dsh) {
     const int ld = bx.ld, n = bx.n, K = n - v;
     const Lane_at at = lane_at<G, IL>(f, nsp, bx.nb, bx.mnb);
@@ -367,16 +404,22 @@ __device__ __forceinline__ void outside_span(const Bundle_ctx<T> &bx, int v, int
     const int rq = (int)__umul24((uint32_t)(i + ld), (uint32_t)ld);   // Q row i
     const int po = rp + n - v, qo = rq + v;                          // O'(i,j) cells
     const float own = pq[po] + dsh[at.sb];
-    const float o = span_lse<G, C, MF>(pq + rp + l, pq + rq + v + 1 + l, K - l, own);
+    float o;
+    if constexpr (LIN)
+        o = fast_exp2(own) * span_dot<G, C, MF>(pq + rp + l, pq + rq + v + 1 + l, K - l);
+    else
+        o = span_lse<G, C, MF>(pq + rp + l, pq + rq + v + 1 + l, K - l, own);
     asm volatile("" ::"v"(o));
     if (at.act && l == 0) {
         pq[qo] = o;
         pq[po] = o;
+        if constexpr (LIN)
+            if (!(o <= kLinMax)) *bx.ovf = 1;
     }
 }
 
 // Forward-only width step: every span of width w of every sentence.
-template <int G, int C, int MF, bool IL, typename T>
+template <bool LIN, int G, int C, int MF, bool IL, typename T>
 __device__ __forceinline__ void fwd_step(const Bundle_ctx<T> &bx, int w, const float *dsh) {
     const int tid = threadIdx.x, nt = blockDim.x;
     const int nsp = bx.nb * (bx.n - w + 1);
@@ -385,7 +428,7 @@ __device__ __forceinline__ void fwd_step(const Bundle_ctx<T> &bx, int w, const f
     for (int f0 = 0; f0 < total; f0 += nt) {
         const int fw = f0 + wq0;
         if (fw >= total) break;   // no span for this wavefront in this pass or later
-        if (wave_has_span<G, IL>(fw, nsp)) inside_span<G, C, MF, IL>(bx, w, nsp, f0 + tid, dsh);
+        if (wave_has_span<G, IL>(fw, nsp)) inside_span<LIN, G, C, MF, IL>(bx, w, nsp, f0 + tid, dsh);
     }
 }
 
@@ -393,7 +436,7 @@ __device__ __forceinline__ void fwd_step(const Bundle_ctx<T> &bx, int w, const f
 // >= 2), both with K = t terms per span, so one step shape serves both.
 // Inside spans take the first threads, outside spans start at the next
 // wavefront boundary, so every wavefront runs one kind.
-template <int G, int C, int MF, bool IL, typename T>
+template <bool LIN, int G, int C, int MF, bool IL, typename T>
 __device__ __forceinline__ void io_step(const Bundle_ctx<T> &bx, int t, const float *dsh) {
     const int tid = threadIdx.x, nt = blockDim.x;
     const int n = bx.n, w = t + 1, v = n - t;
@@ -405,30 +448,30 @@ __device__ __forceinline__ void io_step(const Bundle_ctx<T> &bx, int t, const fl
         const int fw = f0 + wq0;
         if (fw >= total) break;
         if (fw < obase) {
-            if (wave_has_span<G, IL>(fw, nin)) inside_span<G, C, MF, IL>(bx, w, nin, f0 + tid, dsh);
+            if (wave_has_span<G, IL>(fw, nin)) inside_span<LIN, G, C, MF, IL>(bx, w, nin, f0 + tid, dsh);
         } else {
             if (wave_has_span<G, IL>(fw - obase, nout))
-                outside_span<G, C, MF, IL>(bx, v, nout, f0 + tid - obase, dsh);
+                outside_span<LIN, G, C, MF, IL>(bx, v, nout, f0 + tid - obase, dsh);
         }
     }
 }
 
 // A run of forward widths [w0, w1) sharing one step shape: a tight loop with
 // no dispatch.
-template <int G, int C, int MF, bool IL, typename T>
+template <bool LIN, int G, int C, int MF, bool IL, typename T>
 __device__ __forceinline__ void fwd_run(const Bundle_ctx<T> &bx, int w0, int w1, const float *dsh) {
     for (int w = w0; w < w1; ++w) {
-        fwd_step<G, C, MF, IL>(bx, w, dsh);
+        fwd_step<LIN, G, C, MF, IL>(bx, w, dsh);
         __syncthreads();
     }
 }
 
 // A run of joint steps [t0, t1) sharing one step shape.  Span counts are
 // n - t (inside) and t + 1 (outside), both in [1, n+1].
-template <int G, int C, int MF, bool IL, typename T>
+template <bool LIN, int G, int C, int MF, bool IL, typename T>
 __device__ __forceinline__ void io_run(const Bundle_ctx<T> &bx, int t0, int t1, const float *dsh) {
     for (int t = t0; t < t1; ++t) {
-        io_step<G, C, MF, IL>(bx, t, dsh);
+        io_step<LIN, G, C, MF, IL>(bx, t, dsh);
         __syncthreads();
     }
 }
@@ -453,24 +496,53 @@ __device__ __forceinline__ void io_run(const Bundle_ctx<T> &bx, int t0, int t1, 
         }                                                    \
     } while (0)
 
-// The forward sweep alone: widths 2..n, one dispatch per run of widths
-// sharing a step shape.
+// Where a sweep stops for a rescale of the chart: after step t, the first
+// rescale point >= lo, or 0 when no rescale is left.  One after step n/4
+// (n >= 8).  The linear domain, whose shift starts from an estimate (see
+// inside_block_impl), adds one after step 16 for sentences of 100 words or
+// more, before a poor estimate can drift a whole width out of float32's
+// range, and one after step n/2 for sentences of more than 128 words.
+template <bool LIN>
+__device__ __forceinline__ int next_rescale(int lo, int n) {
+    if constexpr (LIN)
+        if (n >= 100 && lo <= 16) return 16;
+    const int t0 = n >= 8 ? n / 4 : 0;
+    if (t0 >= lo) return t0;
+    if constexpr (LIN)
+        if (n > 128 && n / 2 >= lo) return n / 2;
+    return 0;
+}
+
+template <bool LIN, bool REV, typename T>
+__device__ void rescale_chart(const Bundle_ctx<T> &bx, int t0, float *dsh, float *dl);
+
+// The forward sweep alone: steps t = 1..n-1 (widths 2..n), one dispatch per
+// run of steps sharing a step shape; the linear domain cuts the runs for its
+// rescales (the log domain needs none here).
 // WIDE: workspace charts (longer sentences), which may need 16 terms per lane.
 // IL: interleaved span numbering (lane_at).
-template <bool WIDE, bool IL, typename T>
-__device__ __forceinline__ void fwd_sweep(const Bundle_ctx<T> &bx, const float *dsh) {
+// dl: per-sentence scratch for the rescales.
+template <bool LIN, bool WIDE, bool IL, typename T>
+__device__ __forceinline__ void fwd_sweep(const Bundle_ctx<T> &bx, float *dsh, float *dl) {
     const int n = bx.n;
-#define CRF_FWD_FIXED(LO, HI, GG, CC, MM) \
-    if (n >= LO + 1) fwd_run<GG, CC, MM, IL>(bx, LO + 1, min(HI + 2, n + 1), dsh);
-    CRF_FIXED_RUNS(CRF_FWD_FIXED)
+    for (int lo = 1; lo < n;) {
+        const int tr = LIN ? next_rescale<true>(lo, n) : 0;
+        const int hi = tr > 0 ? tr + 1 : n;   // steps [lo, hi), widths [lo + 1, hi + 1)
+#define CRF_FWD_FIXED(LO, HI, GG, CC, MM)                                                  \
+        if (max(lo, LO) < min(hi, HI + 1))                                                 \
+            fwd_run<LIN, GG, CC, MM, IL>(bx, max(lo, LO) + 1, min(hi, HI + 1) + 1, dsh);
+        CRF_FIXED_RUNS(CRF_FWD_FIXED)
 #undef CRF_FWD_FIXED
-    for (int w = kFixedRunsMaxK + 2; w <= n;) {
-        const StepShape sh = step_shape_k(w - 1);
-        const int w2 = min(shape_run_end(w - 1) + 1, n + 1);
-#define CRF_FWD_RUN(GG, CC, MM) fwd_run<GG, CC, MM, IL>(bx, w, w2, dsh)
-        CRF_DISPATCH_WIDE_SHAPE(sh, CRF_FWD_RUN);
+        for (int t = max(lo, kFixedRunsMaxK + 1); t < hi;) {
+            const StepShape sh = step_shape_k(t);
+            const int t2 = min(shape_run_end(t), hi);
+#define CRF_FWD_RUN(GG, CC, MM) fwd_run<LIN, GG, CC, MM, IL>(bx, t + 1, t2 + 1, dsh)
+            CRF_DISPATCH_WIDE_SHAPE(sh, CRF_FWD_RUN);
 #undef CRF_FWD_RUN
-        w = w2;
+            t = t2;
+        }
+        if (tr > 0) rescale_chart<LIN, false>(bx, tr, dsh, dl);
+        lo = hi;
     }
 }
 
@@ -507,28 +579,39 @@ constexpr float kShiftBand = 30.0f;
 // Score shift.  Adding one constant d to every non-forced score adds d times
 // their number, n - 2, to the log score of every tree: log Z moves by
 // (n-2) d and no marginal changes.  Chart values grow about linearly with the
-// span width, and float32 rounding of alpha + O - log Z, the exponent of a
-// marginal, grows with them; d = minus the typical growth per internal node
-// keeps both near zero.  After joint step t0 (inside widths <= t0+1 done,
-// outside widths >= n-t0 done) the growth is estimated from alpha at width
-// w0 = t0+1, and the stored values are moved to the shifted problem:
-//   alpha(i,j) += d (w-1)   (w-1 non-forced nodes below and at (i,j))
-//   O'(i,j)    += d (n-w)   (n-1-w above it, plus its own score)
-// Later steps add d to each score as they read it; the root's O' stays 0.
-template <typename T>
-__device__ void rescale_chart(const Bundle_ctx<T> &bx, int t0, float *dsh) {
+// span width; the shift keeps them near zero (log domain: so that the
+// float32 rounding of alpha + O - log Z, the exponent of a marginal, stays
+// small; linear domain: so that exp2 of them stays in float32's range).
+// After step t0 (inside widths <= t0+1 done, outside widths >= n-t0 done) a
+// further shift delta is estimated from alpha at width w0 = t0+1 -- log
+// domain: minus the mean growth per node of the spans within kShiftBand of
+// the largest; linear domain: minus the midpoint of that mean and the
+// largest, which keeps the largest values further from float32's limit --
+// and the stored values move to the shifted problem:
+//   alpha(i,j) += delta (w-1)   (w-1 non-forced nodes below and at (i,j))
+//   O'(i,j)    += delta (n-w)   (n-1-w above it, plus its own score)
+// (times exp2 of these in the linear domain), d += delta.  Later steps add d
+// to each score as they read it; the root's O' stays 0.  dl holds delta per
+// sentence meanwhile.
+template <bool LIN, bool REV, typename T>
+__device__ void rescale_chart(const Bundle_ctx<T> &bx, int t0, float *dsh, float *dl) {
     const int n = bx.n, ld = bx.ld, nb = bx.nb, w0 = t0 + 1, S = n - t0;
     const int tid = threadIdx.x;
     by_sentence_groups(S, nb, [&](auto gs, int sb, int gl, bool valid) {
         constexpr int GS = decltype(gs)::value;
         const T *P = bx.chart0 + (size_t)sb * bx.cstride;
+        auto val = [&](int i) {
+            const float a = P[i * ld + w0 - 1];
+            if constexpr (LIN) return fast_log2(a);   // (0 gives -inf, below NEG)
+            else return a;
+        };
         float m = NEG;
-        for (int i = gl; i < S; i += GS) m = fmax_nn(m, P[i * ld + w0 - 1]);
+        for (int i = gl; i < S; i += GS) m = fmax_nn(m, val(i));
         m = grp_max<GS>(m);
         const float floor_v = m - kShiftBand * (float)(w0 - 1);
         float acc = 0.f, cnt = 0.f;
         for (int i = gl; i < S; i += GS) {
-            const float a = P[i * ld + w0 - 1];
+            const float a = val(i);
             if (a >= floor_v) {
                 acc += a;
                 cnt += 1.f;
@@ -536,9 +619,25 @@ __device__ void rescale_chart(const Bundle_ctx<T> &bx, int t0, float *dsh) {
         }
         acc = grp_sum<GS>(acc);
         cnt = grp_sum<GS>(cnt);
-        if (valid && gl == 0) dsh[sb] = -acc / (cnt * (float)(w0 - 1));
+        float delta;
+        if constexpr (LIN)   // (every value 0: no shift)
+            delta = m > 0.5f * NEG ? -0.5f * (m + acc / cnt) / (float)(w0 - 1) : 0.f;
+        else
+            delta = -acc / (cnt * (float)(w0 - 1));
+        if (valid && gl == 0) dl[sb] = delta;
     });
     __syncthreads();
+    auto moved = [&](float x, float dk) {
+        // linear domain: x exp2(dk), as ldexp by the integer part of dk times
+        // exp2 of the rest, so that a factor beyond float32's range (dk can
+        // exceed 128 when x is small) never forms on its own
+        if constexpr (LIN) {
+            const float k = floorf(dk);
+            return __builtin_amdgcn_ldexpf(x * fast_exp2(dk - k), (int)k);
+        } else {
+            return x + dk;
+        }
+    };
     // alpha of widths 2..w0: per sentence n rows x (w0-1) widths
     {
         const int A = w0 - 1, per = n * A, total = nb * per;
@@ -550,14 +649,14 @@ __device__ void rescale_chart(const Bundle_ctx<T> &bx, int t0, float *dsh) {
             const int w = 2 + r - i * A, j = i + w;
             if (j <= n) {
                 T *P = bx.chart0 + (size_t)sb * bx.cstride, *Q = P + (size_t)ld * ld;
-                const float a = P[i * ld + w - 1] + dsh[sb] * (float)(w - 1);
+                const float a = moved(P[i * ld + w - 1], dl[sb] * (float)(w - 1));
                 P[i * ld + w - 1] = a;
                 Q[j * ld + n + 1 - w] = a;
             }
         }
     }
     // O' of widths n-t0..n-1: spans (i, i+v) with i + (v - (n-t0)) <= t0
-    {
+    if constexpr (REV) {
         const int per = (t0 + 1) * t0, total = nb * per;
         const float inv_per = 1.0f / (float)per, inv_t = 1.0f / (float)t0;
         for (int f = tid; f < total; f += blockDim.x) {
@@ -567,39 +666,41 @@ __device__ void rescale_chart(const Bundle_ctx<T> &bx, int t0, float *dsh) {
             const int e = r - i * t0, v = n - t0 + e, j = i + v;
             if (i + e <= t0) {
                 T *P = bx.chart0 + (size_t)sb * bx.cstride, *Q = P + (size_t)ld * ld;
-                const float o = Q[i * ld + v] + dsh[sb] * (float)(n - v);
+                const float o = moved(Q[i * ld + v], dl[sb] * (float)(n - v));
                 Q[i * ld + v] = o;
                 P[j * ld + n - v] = o;
             }
         }
     }
+    for (int sb = tid; sb < nb; sb += blockDim.x) dsh[sb] += dl[sb];
     __syncthreads();
 }
 
 // The joint sweep: steps t = 1..n-1 (inside widths 2..n, outside widths
 // n-1..2), one dispatch per run of steps sharing a step shape; the runs are
-// cut after step t0 for the rescale (t0 = 0: none).
-template <bool WIDE, bool IL, typename T>
-__device__ __forceinline__ void io_sweep(const Bundle_ctx<T> &bx, float *dsh, int t0) {
+// cut at the rescale points (next_rescale), each phase running the fixed list
+// of runs, so that each run and the rescale appear once in the code.
+template <bool LIN, bool WIDE, bool IL, typename T>
+__device__ __forceinline__ void io_sweep(const Bundle_ctx<T> &bx, float *dsh, float *dl) {
     const int n = bx.n;
-    // two phases, steps [1, t0] and [t0+1, n-1], with the rescale between
-    // (one copy of each run in the code)
-    for (int ph = 0; ph < 2; ++ph) {
-        const int lo = ph == 0 ? 1 : t0 + 1, hi = ph == 0 ? t0 + 1 : n;   // steps [lo, hi)
+    for (int lo = 1; lo < n;) {
+        const int tr = next_rescale<LIN>(lo, n);
+        const int hi = tr > 0 ? tr + 1 : n;   // steps [lo, hi)
 #define CRF_IO_FIXED(LO, HI, GG, CC, MM)                              \
         if (max(lo, LO) < min(hi, HI + 1))                            \
-            io_run<GG, CC, MM, IL>(bx, max(lo, LO), min(hi, HI + 1), dsh);
+            io_run<LIN, GG, CC, MM, IL>(bx, max(lo, LO), min(hi, HI + 1), dsh);
         CRF_FIXED_RUNS(CRF_IO_FIXED)
 #undef CRF_IO_FIXED
         for (int t = max(lo, kFixedRunsMaxK + 1); t < hi;) {
             const StepShape sh = step_shape_k(t);
             const int t2 = min(shape_run_end(t), hi);
-#define CRF_IO_RUN(GG, CC, MM) io_run<GG, CC, MM, IL>(bx, t, t2, dsh)
+#define CRF_IO_RUN(GG, CC, MM) io_run<LIN, GG, CC, MM, IL>(bx, t, t2, dsh)
             CRF_DISPATCH_WIDE_SHAPE(sh, CRF_IO_RUN);
 #undef CRF_IO_RUN
             t = t2;
         }
-        if (ph == 0 && t0 > 0) rescale_chart(bx, t0, dsh);
+        if (tr > 0) rescale_chart<LIN, true>(bx, tr, dsh, dl);
+        lo = hi;
     }
 }
 
@@ -788,14 +889,24 @@ __device__ __forceinline__ int label_argmax(const float *s, int L) {
 //   which nothing reads once the sweep is done, so the epilogue subtracts g
 //   once per distinct span.
 constexpr int kGoldMark = 0x7FBADBAD;   // a NaN bit pattern: no finite chart value has it
-template <bool REV, bool LAB, bool SPILL, bool GOLD = false>
-__device__ __forceinline__ void inside_block(const KernelPlan &p, int block, const int32_t *rec, char *smem_raw,
-                                             const float *__restrict__ scores,
-                                             const float *__restrict__ grad,
-                                             float *__restrict__ logZ, float *__restrict__ marg,
-                                             const int32_t *__restrict__ gold = nullptr,
-                                             float *__restrict__ loss = nullptr) {
+//
+// LIN: the sweeps run in the linear domain -- the chart holds exp2 of the
+// (shifted, log2-scaled) inside and outside values, a span's sum over its
+// splits is a dot product (span_dot), and rescales at doubling steps keep the
+// values near 1.  A value that leaves float32's range (or a root below
+// kLinMin) sets the bundle's overflow flag, and the bundle returns false
+// before it has written any output: the caller then runs it again in the log
+// domain (LIN = false, max-shifted log-sum-exp per span).
+constexpr float kLinMin = 0x1p-100f;
+template <bool LIN, bool REV, bool LAB, bool SPILL, bool GOLD>
+__device__ __forceinline__ bool inside_block_impl(const KernelPlan &p, int block, const int32_t *rec, char *smem_raw,
+                                                  const float *__restrict__ scores,
+                                                  const float *__restrict__ grad,
+                                                  float *__restrict__ logZ, float *__restrict__ marg,
+                                                  const int32_t *__restrict__ gold,
+                                                  float *__restrict__ loss) {
     static_assert(!GOLD || (REV && !LAB), "the gold-tree loss is unlabelled and needs the marginals");
+    __shared__ int lin_ovf;
     __shared__ double spill_forced[1];
     __shared__ float spill_gv[1];
     __shared__ int spill_id[1];
@@ -842,19 +953,19 @@ __device__ __forceinline__ void inside_block(const KernelPlan &p, int block, con
         if (tid < nb) sid[tid] = id0;
     }
     const int ld = lay.ld;
-    const Bundle_ctx<float> bx{chart0, cstride, n, ld, nb, mnb, lay.e};
+    const Bundle_ctx<float> bx{chart0, cstride, n, ld, nb, mnb, lay.e, LIN ? &lin_ovf : nullptr};
+    if (tid == 0) lin_ovf = 0;
     __syncthreads();
-    for (int t = tid; t < nb; t += NT) {
-        gv[t] = grad ? grad[sid[t]] : 1.0f;
-        dsh[t] = 0.f;
-    }
+    // (gv holds the rescales' per-sentence shifts during the sweep and the
+    // upstream gradients after it)
+    for (int t = tid; t < nb; t += NT) dsh[t] = 0.f;
 
     const size_t row_stride = LAB ? (size_t)N1 * L : (size_t)N1;
     const size_t sent_stride = (size_t)N1 * row_stride;
 
     // Prologue: scores of every valid cell into the charts (log2-scaled, in
     // the cells of alpha and, for the outside, of O'); forced spans get 0 in
-    // alpha and park their natural-unit score.
+    // alpha (1 in the linear domain) and park their natural-unit score.
     auto score_at = [&](int sb, int i, int j) -> const float * {
         return scores + (size_t)sid[sb] * sent_stride + (size_t)i * row_stride + (size_t)j * (LAB ? L : 1);
     };
@@ -871,16 +982,17 @@ __device__ __forceinline__ void inside_block(const KernelPlan &p, int block, con
     auto put_score = [&](int sb, int i, int j, float s) {
         float *P = chart0 + (size_t)sb * cstride, *Q = P + (size_t)ld * ld;
         const int w = j - i;
+        const float zero = LIN ? 1.f : 0.f;   // log2 value 0
         if (w == 1) {   // forced: alpha 0, score parked in the O' cell no sweep uses
-            P[i * ld] = 0.f;
-            Q[j * ld + n] = 0.f;
+            P[i * ld] = zero;
+            Q[j * ld + n] = zero;
             P[j * ld + n - 1] = s;
-        } else if (i == 0 && j == n) {   // the root: own term 0, O' 0, score parked
+        } else if (i == 0 && j == n) {   // the root: own term 0 (a log2 score), O' 0, score parked
             P[n - 1] = 0.f;
             P[n] = s;
             if constexpr (REV) {
-                Q[n] = 0.f;
-                P[n * ld] = 0.f;
+                Q[n] = zero;
+                P[n * ld] = zero;
             }
         } else {
             const float s2 = s * LOG2E_F;
@@ -891,6 +1003,12 @@ __device__ __forceinline__ void inside_block(const KernelPlan &p, int block, con
     for_cells_loaded<LAB ? 1 : 8>(nb, n, score_at, load_score, put_score);
     __syncthreads();
     // Forced-span sums, a lane group per sentence, fixed order (deterministic).
+    // The linear domain also seeds each sentence's shift d from its scores:
+    // for independent scores of mean m and variance v (log2 units) the
+    // expected tree weight grows by 4 (Catalan) times E[exp2(s)] =
+    // exp2(m + v ln2 / 2) per node, so d = -(m + v ln2 / 2 + 2), from the
+    // non-forced spans of widths 2..9 (near-forbidden scores left out); the
+    // rescales then correct it from the chart itself.
     by_sentence_groups(n, nb, [&](auto gs, int sb, int gl, bool valid) {
         constexpr int GS = decltype(gs)::value;
         const float *P = chart0 + (size_t)sb * cstride;
@@ -899,30 +1017,62 @@ __device__ __forceinline__ void inside_block(const KernelPlan &p, int block, con
         if (gl == 0 && n >= 2) acc += (double)P[n];
         acc = grp_sum_d<GS>(acc);
         if (valid && gl == 0) forced[sb] = acc;
+        if constexpr (LIN) {
+            float s1 = 0.f, s2 = 0.f, c = 0.f;
+            for (int i = gl; i < n - 1; i += GS)
+                for (int w = 2; w <= 9 && i + w <= n; ++w) {
+                    if (i == 0 && w == n) continue;   // the root: forced
+                    const float x = P[i * ld + w - 1];
+                    if (x > -1000.f) {
+                        s1 += x;
+                        s2 += x * x;
+                        c += 1.f;
+                    }
+                }
+            s1 = grp_sum<GS>(s1);
+            s2 = grp_sum<GS>(s2);
+            c = grp_sum<GS>(c);
+            if (valid && gl == 0 && c > 0.f) {
+                const float mean = s1 / c, var = fmaxf(s2 / c - mean * mean, 0.f);
+                dsh[sb] = -(mean + 0.5f * (float)LN2_D * var + 2.0f);
+            }
+        }
     });
+    if constexpr (LIN) __syncthreads();   // the seeds are read by the first step
 
     // Workspace charts lay spans side by side; LDS charts interleave them
     // when their layout allows (e = 0).
     if constexpr (!REV) {
-        if constexpr (SPILL) fwd_sweep<true, false>(bx, dsh);
-        else if (lay.e == 0) fwd_sweep<false, true>(bx, dsh);
-        else fwd_sweep<false, false>(bx, dsh);
+        if constexpr (SPILL) fwd_sweep<LIN, true, false>(bx, dsh, gv);
+        else if (lay.e == 0) fwd_sweep<LIN, false, true>(bx, dsh, gv);
+        else fwd_sweep<LIN, false, false>(bx, dsh, gv);
     } else {
-        // The rescale needs a few widths of alpha to estimate the growth;
-        // short sentences keep small magnitudes and skip it.
-        const int t0 = n >= 8 ? n / 4 : 0;
-        if constexpr (SPILL) io_sweep<true, false>(bx, dsh, t0);
-        else if (lay.e == 0) io_sweep<false, true>(bx, dsh, t0);
-        else io_sweep<false, false>(bx, dsh, t0);
+        if constexpr (SPILL) io_sweep<LIN, true, false>(bx, dsh, gv);
+        else if (lay.e == 0) io_sweep<LIN, false, true>(bx, dsh, gv);
+        else io_sweep<LIN, false, false>(bx, dsh, gv);
     }
-    // log Z = (alpha~(0,n) - (n-2) d) ln 2 + forced sum.
+    // (the sweep's last barrier published the chart and the flag)
+    if constexpr (LIN) {
+        for (int sb = tid; sb < nb; sb += NT) {
+            const float r = chart0[(size_t)sb * cstride + n - 1];
+            if (!(r >= kLinMin && r <= kLinMax)) lin_ovf = 1;
+        }
+        __syncthreads();
+        if (lin_ovf) return false;   // nothing written yet: the log domain redoes the bundle
+    }
+    for (int t = tid; t < nb; t += NT) gv[t] = grad ? grad[sid[t]] : 1.0f;
+    __syncthreads();
+    // log Z = (alpha~(0,n) - (n-2) d) ln 2 + forced sum, alpha~(0,n) the
+    // root's log2 value.
     auto log_z = [&](int sb) {
-        const double z2 = (double)chart0[(size_t)sb * cstride + n - 1] - (double)dsh[sb] * (n >= 2 ? n - 2 : 0);
+        const float r = chart0[(size_t)sb * cstride + n - 1];
+        const double lr = LIN ? log2((double)r) : (double)r;
+        const double z2 = lr - (double)dsh[sb] * (n >= 2 ? n - 2 : 0);
         return z2 * LN2_D + forced[sb];
     };
     if (logZ != nullptr)
         for (int sb = tid; sb < nb; sb += NT) logZ[sid[sb]] = (float)log_z(sb);
-    if constexpr (!REV) return;
+    if constexpr (!REV) return true;
 
     if constexpr (GOLD) {
         // Gold rows of each sentence: mark the span, sum its score (float64,
@@ -950,12 +1100,16 @@ __device__ __forceinline__ void inside_block(const KernelPlan &p, int block, con
     //   mu(i,j) = g exp2(alpha~(i,j) + O'(i,j) - (s(i,j) + d) - alpha~(0,n)),
     // and exactly g on forced spans.
     // mu of a valid cell whose own score (log2 units) is own2
+    auto lg = [](float x) {   // a chart value as its log2 value
+        if constexpr (LIN) return fast_log2(x);   // (0 gives -inf, and exp2 of the exponent 0)
+        else return x;
+    };
     auto span_mu = [&](int sb, int i, int j, float own2) {
         const float *P = chart0 + (size_t)sb * cstride, *Q = P + (size_t)ld * ld;
         const bool forced_span = (j == i + 1) || (i == 0 && j == n);
         const int w = j - i;
         float mu = gv[sb];
-        if (!forced_span) mu *= fast_exp2(((P[i * ld + w - 1] - P[n - 1]) + Q[i * ld + w]) - (own2 + dsh[sb]));
+        if (!forced_span) mu *= fast_exp2(((lg(P[i * ld + w - 1]) - lg(P[n - 1])) + lg(Q[i * ld + w])) - (own2 + dsh[sb]));
         if constexpr (GOLD)
             if (__builtin_bit_cast(int, P[j * ld + n - w]) == kGoldMark) mu -= gv[sb];
         return mu;
@@ -1013,6 +1167,22 @@ __device__ __forceinline__ void inside_block(const KernelPlan &p, int block, con
             marg[(size_t)sid[sb] * sent_stride + (size_t)i * row_stride + j] = span_mu(sb, i, j, s * LOG2E_F);
         });
     }
+    return true;
+}
+
+// A bundle (or a workspace sentence): the linear-domain sweeps, and the log
+// domain if they leave float32's range (see inside_block_impl).
+template <bool REV, bool LAB, bool SPILL, bool GOLD = false>
+__device__ __forceinline__ void inside_block(const KernelPlan &p, int block, const int32_t *rec, char *smem_raw,
+                                             const float *__restrict__ scores,
+                                             const float *__restrict__ grad,
+                                             float *__restrict__ logZ, float *__restrict__ marg,
+                                             const int32_t *__restrict__ gold = nullptr,
+                                             float *__restrict__ loss = nullptr) {
+    if (inside_block_impl<true, REV, LAB, SPILL, GOLD>(p, block, rec, smem_raw, scores, grad, logZ, marg, gold, loss))
+        return;
+    __syncthreads();   // every thread has left the linear attempt
+    inside_block_impl<false, REV, LAB, SPILL, GOLD>(p, block, rec, smem_raw, scores, grad, logZ, marg, gold, loss);
 }
 
 // ---------------------------------------------------------------------------

@@ -173,6 +173,20 @@ def test_short_and_padded(torch):
     full_check(torch, b)
 
 
+@pytest.mark.parametrize("sd,mean", [(10.0, 0.0), (1.0, -60.0), (1.0, 60.0)])
+def test_scores_beyond_the_linear_range(torch, sd, mean):
+    # sd 10: a spread that a float32 chart of exp2 values cannot hold past a
+    # few words -- the sweeps detect it and redo those bundles in the log
+    # domain, on LDS charts (n <= 142) and workspace charts alike (every
+    # sentence but the 3-word one, measured with a build that skips the redo).
+    # Offsets of +-60 nats stay in the linear domain: the per-sentence shift,
+    # seeded from the scores' mean, absorbs them.
+    b = W.custom([3, 17, 40, 99, 130, 150], seed=78, sd=sd)
+    v = W.valid_mask(b.lengths, b.n1)
+    b.scores[v] += np.float32(mean)
+    full_check(torch, b)
+
+
 def test_all_zero_scores(torch):
     # every tree ties: right-branching tree, Catalan-ratio marginals
     b = W.custom([1, 2, 5, 40, 99], sd=0.0)
