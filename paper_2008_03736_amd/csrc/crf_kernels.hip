@@ -875,7 +875,8 @@ __device__ __forceinline__ int label_argmax(const float *s, int L) {
 // Inside (+ marginals).  One workgroup per bundle (or, SPILL, per long
 // sentence with its chart in the workspace).
 //   REV: also compute the marginals (joint inside/outside sweep) and write them.
-//   LAB: labelled scores [B][N1][N1][L].
+//   (Labelled scores run the same code on their label log-sum-exps, which
+//   label_reduce_kernel writes beforehand; see launch_inside.)
 // Dynamic LDS (bundled): nb charts (chart stride from inside_layout), then
 // nb x {forced (f64), grad (f32), id (i32), shift (f32)}, then the room
 // bundle_extra_bytes gives every bundle.
@@ -898,14 +899,14 @@ constexpr int kGoldMark = 0x7FBADBAD;   // a NaN bit pattern: no finite chart va
 // before it has written any output: the caller then runs it again in the log
 // domain (LIN = false, max-shifted log-sum-exp per span).
 constexpr float kLinMin = 0x1p-100f;
-template <bool LIN, bool REV, bool LAB, bool SPILL, bool GOLD>
+template <bool LIN, bool REV, bool SPILL, bool GOLD>
 __device__ __forceinline__ bool inside_block_impl(const KernelPlan &p, int block, const int32_t *rec, char *smem_raw,
                                                   const float *__restrict__ scores,
                                                   const float *__restrict__ grad,
                                                   float *__restrict__ logZ, float *__restrict__ marg,
                                                   const int32_t *__restrict__ gold,
                                                   float *__restrict__ loss) {
-    static_assert(!GOLD || (REV && !LAB), "the gold-tree loss is unlabelled and needs the marginals");
+    static_assert(!GOLD || REV, "the gold-tree loss needs the marginals");
     __shared__ int lin_ovf;
     __shared__ double spill_forced[1];
     __shared__ float spill_gv[1];
@@ -913,7 +914,7 @@ __device__ __forceinline__ bool inside_block_impl(const KernelPlan &p, int block
     __shared__ float spill_dsh[1];
     const int NT = blockDim.x;
     const int tid = threadIdx.x;
-    const int N1 = p.n1, L = p.L;
+    const int N1 = p.n1;
 
     int n, nb;
     float *chart0;
@@ -960,24 +961,16 @@ __device__ __forceinline__ bool inside_block_impl(const KernelPlan &p, int block
     // upstream gradients after it)
     for (int t = tid; t < nb; t += NT) dsh[t] = 0.f;
 
-    const size_t row_stride = LAB ? (size_t)N1 * L : (size_t)N1;
+    const size_t row_stride = (size_t)N1;
     const size_t sent_stride = (size_t)N1 * row_stride;
 
     // Prologue: scores of every valid cell into the charts (log2-scaled, in
     // the cells of alpha and, for the outside, of O'); forced spans get 0 in
     // alpha (1 in the linear domain) and park their natural-unit score.
     auto score_at = [&](int sb, int i, int j) -> const float * {
-        return scores + (size_t)sid[sb] * sent_stride + (size_t)i * row_stride + (size_t)j * (LAB ? L : 1);
+        return scores + (size_t)sid[sb] * sent_stride + (size_t)i * row_stride + (size_t)j;
     };
-    // 8-byte label accesses: an even label count on 8-byte aligned tensors
-    const bool wide_in = LAB && (L & 1) == 0 && ((uintptr_t)scores & 7) == 0;
-    const bool wide_out = wide_in && ((uintptr_t)marg & 7) == 0;
-    auto load_score = [&](const float *q) -> float {
-        if constexpr (LAB)
-            return label_lse2(q, L, wide_in) * (float)LN2_D;   // the label log-sum-exp is the span's score
-        else
-            return *q;
-    };
+    auto load_score = [](const float *q) -> float { return *q; };
     // (cells of the rotated P / Q squares, see the inside chart layout)
     auto put_score = [&](int sb, int i, int j, float s) {
         float *P = chart0 + (size_t)sb * cstride, *Q = P + (size_t)ld * ld;
@@ -1000,7 +993,7 @@ __device__ __forceinline__ bool inside_block_impl(const KernelPlan &p, int block
             if constexpr (REV) P[j * ld + n - w] = s2;
         }
     };
-    for_cells_loaded<LAB ? 1 : 8>(nb, n, score_at, load_score, put_score);
+    for_cells_loaded<8>(nb, n, score_at, load_score, put_score);
     __syncthreads();
     // Forced-span sums, a lane group per sentence, fixed order (deterministic).
     // The linear domain also seeds each sentence's shift d from its scores:
@@ -1114,75 +1107,25 @@ __device__ __forceinline__ bool inside_block_impl(const KernelPlan &p, int block
             if (__builtin_bit_cast(int, P[j * ld + n - w]) == kGoldMark) mu -= gv[sb];
         return mu;
     };
-    if constexpr (LAB) {
-        // Up to 32 labels: one load of a span's labels serves its log-sum-exp
-        // (the same arithmetic as the prologue's, so the same own score) and
-        // its per-label marginals, two spans per thread at a time.
-        if (L <= 32) {
-            const Cell_walk cw(nb, n);
-            for (int c0 = tid; c0 < cw.total; c0 += NT * 2) {
-                Cell e[2];
-                const float *q[2];
-                float v[2][32];
-#pragma unroll
-                for (int u = 0; u < 2; ++u) {
-                    e[u] = cw.at(c0 + u * NT);
-                    q[u] = score_at(e[u].sb, e[u].i, e[u].j);
-                }
-#pragma unroll
-                for (int u = 0; u < 2; ++u) label_load32(q[u], L, wide_in, v[u]);
-                __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-                for (int u = 0; u < 2; ++u) {
-                    float m = -INFINITY, acc = 0.f;
-                    label_block(v[u], 0, L, m, acc);
-                    const float own2 = ((m + fast_log2(acc)) * (float)LN2_D) * LOG2E_F;   // as the chart holds it
-                    const float mu = span_mu(e[u].sb, e[u].i, e[u].j, own2);
-                    if (e[u].ok) {
-                        float *o = marg + (q[u] - scores);
-                        if (wide_out) {   // 8-byte stores
-                            float2 *o2 = reinterpret_cast<float2 *>(o);
-#pragma unroll
-                            for (int k = 0; k < 16; ++k)
-                                if (2 * k < L)
-                                    o2[k] = make_float2(mu * fast_exp2(v[u][2 * k] * LOG2E_F - own2),
-                                                        mu * fast_exp2(v[u][2 * k + 1] * LOG2E_F - own2));
-                        } else {
-#pragma unroll
-                            for (int k = 0; k < 32; ++k)
-                                if (k < L) o[k] = mu * fast_exp2(v[u][k] * LOG2E_F - own2);
-                        }
-                    }
-                }
-            }
-        } else {
-            for_cells_loaded<1>(nb, n, score_at, load_score, [&](int sb, int i, int j, float s) {
-                const float mu = span_mu(sb, i, j, s * LOG2E_F);
-                const size_t cell = (size_t)sid[sb] * sent_stride + (size_t)i * row_stride + (size_t)j * L;
-                label_marginals(scores + cell, L, mu, s * LOG2E_F, marg + cell);
-            });
-        }
-    } else {
-        for_cells_loaded<8>(nb, n, score_at, load_score, [&](int sb, int i, int j, float s) {
-            marg[(size_t)sid[sb] * sent_stride + (size_t)i * row_stride + j] = span_mu(sb, i, j, s * LOG2E_F);
-        });
-    }
+    for_cells_loaded<8>(nb, n, score_at, load_score, [&](int sb, int i, int j, float s) {
+        marg[(size_t)sid[sb] * sent_stride + (size_t)i * row_stride + j] = span_mu(sb, i, j, s * LOG2E_F);
+    });
     return true;
 }
 
 // A bundle (or a workspace sentence): the linear-domain sweeps, and the log
 // domain if they leave float32's range (see inside_block_impl).
-template <bool REV, bool LAB, bool SPILL, bool GOLD = false>
+template <bool REV, bool SPILL, bool GOLD = false>
 __device__ __forceinline__ void inside_block(const KernelPlan &p, int block, const int32_t *rec, char *smem_raw,
                                              const float *__restrict__ scores,
                                              const float *__restrict__ grad,
                                              float *__restrict__ logZ, float *__restrict__ marg,
                                              const int32_t *__restrict__ gold = nullptr,
                                              float *__restrict__ loss = nullptr) {
-    if (inside_block_impl<true, REV, LAB, SPILL, GOLD>(p, block, rec, smem_raw, scores, grad, logZ, marg, gold, loss))
+    if (inside_block_impl<true, REV, SPILL, GOLD>(p, block, rec, smem_raw, scores, grad, logZ, marg, gold, loss))
         return;
     __syncthreads();   // every thread has left the linear attempt
-    inside_block_impl<false, REV, LAB, SPILL, GOLD>(p, block, rec, smem_raw, scores, grad, logZ, marg, gold, loss);
+    inside_block_impl<false, REV, SPILL, GOLD>(p, block, rec, smem_raw, scores, grad, logZ, marg, gold, loss);
 }
 
 // ---------------------------------------------------------------------------
@@ -1492,14 +1435,70 @@ __device__ __forceinline__ void cky_block(const KernelPlan &p, int block, const 
 
 // Workgroups of 256, 512 or 1024 threads (the plan's choice) share one
 // build of each kernel.
-template <bool REV, bool LAB, bool SPILL>
+template <bool REV, bool SPILL>
 __global__ __launch_bounds__(kThreadsMax) void inside_kernel(KernelPlan p, const float *__restrict__ scores,
                                                              const float *__restrict__ grad,
                                                              float *__restrict__ logZ,
                                                              float *__restrict__ marg) {
     extern __shared__ __align__(16) char smem_raw[];
-    inside_block<REV, LAB, SPILL>(p, blockIdx.x, SPILL ? nullptr : p.inside.recs + (size_t)blockIdx.x * p.rec_stride,
-                                  smem_raw, scores, grad, logZ, marg);
+    inside_block<REV, SPILL>(p, blockIdx.x, SPILL ? nullptr : p.inside.recs + (size_t)blockIdx.x * p.rec_stride,
+                             smem_raw, scores, grad, logZ, marg);
+}
+
+// Labelled scores [B][N1][N1][L], spread over the whole chip: a workgroup per
+// chunk of kLabelChunk slots of one sentence's cell walk (Cell_walk), a cell
+// per thread.  label_reduce_kernel writes each valid cell's label
+// log-sum-exp s'(i,j) = log sum_l exp s(i,j,l) (Sec. 4.2, Eq. tree-label-score:
+// the one-stage Z sums exp of the labelled score over labels per span) into
+// sp [B][N1][N1]; the unlabelled kernels then run on sp; label_expand_kernel
+// writes the per-label marginals mu(i,j) exp(s(i,j,l) - s'(i,j)) from their
+// marginals mu [B][N1][N1].  Only valid cells are read or written.
+__device__ __forceinline__ bool label_cell(const KernelPlan &p, int *b, int *i, int *j) {
+    const int2 ch = reinterpret_cast<const int2 *>(p.lab_chunks)[blockIdx.x];   // (sentence, first slot)
+    *b = ch.x;
+    const int n = p.len[ch.x];
+    const Cell_walk cw(1, n);
+    const Cell e = cw.at(ch.y + (int)threadIdx.x);
+    *i = e.i;
+    *j = e.j;
+    return e.ok;
+}
+__global__ __launch_bounds__(kLabelChunk) void label_reduce_kernel(KernelPlan p, const float *__restrict__ s4,
+                                                                   float *__restrict__ sp) {
+    int b, i, j;
+    const bool ok = label_cell(p, &b, &i, &j);
+    const int N1 = p.n1, L = p.L;
+    const size_t cell = ((size_t)b * N1 + i) * N1 + j;
+    const bool wide = (L & 1) == 0 && ((uintptr_t)s4 & 7) == 0;   // 8-byte loads: an even count, aligned
+    const float v = label_lse2(s4 + cell * L, L, wide) * (float)LN2_D;   // (reads a valid cell even when !ok)
+    if (ok) sp[cell] = v;
+}
+// label_expand_kernel runs over the contiguous label blocks of the rows: row
+// i of sentence b holds the labels of cells (i, i+1..n) back to back, and a
+// workgroup takes kLabelRowChunk consecutive floats of one row (p.lab_rows:
+// sentence, row, first float), kLabelRowChunk / kLabelChunk per thread with
+// consecutive threads on consecutive floats, so reads and writes are whole
+// cache lines; each float gathers its cell's marginal and log-sum-exp.
+__global__ __launch_bounds__(kLabelChunk) void label_expand_kernel(KernelPlan p, const float *__restrict__ s4,
+                                                                   const float *__restrict__ sp,
+                                                                   const float *__restrict__ mu,
+                                                                   float *__restrict__ marg) {
+    const int4 rc = reinterpret_cast<const int4 *>(p.lab_rows)[blockIdx.x];   // (sentence, row, first float)
+    const int N1 = p.n1, L = p.L, n = p.len[rc.x], i = rc.y;
+    const int len = (n - i) * L;                       // floats of the row's label block
+    const size_t cell0 = ((size_t)rc.x * N1 + i) * N1 + i + 1;
+    const float *src = s4 + cell0 * L;
+    float *dst = marg + cell0 * L;
+    const float invL = 1.0f / (float)L;
+#pragma unroll
+    for (int u = 0; u < kLabelRowChunk / kLabelChunk; ++u) {
+        const int f = rc.z + u * kLabelChunk + (int)threadIdx.x;
+        if (f < len) {
+            const int c = div_small(f, L, invL);           // cell (i, i+1+c)
+            const float m = mu[cell0 + c], own2 = sp[cell0 + c] * LOG2E_F;
+            dst[f] = m * fast_exp2(src[f] * LOG2E_F - own2);
+        }
+    }
 }
 
 // The gold-tree loss: the inside kernel with marginals, minus the gold
@@ -1511,7 +1510,7 @@ __global__ __launch_bounds__(kThreadsMax) void loss_kernel(KernelPlan p, const f
                                                            float *__restrict__ loss,
                                                            float *__restrict__ marg) {
     extern __shared__ __align__(16) char smem_raw[];
-    inside_block<true, false, SPILL, true>(p, blockIdx.x,
+    inside_block<true, SPILL, true>(p, blockIdx.x,
                                            SPILL ? nullptr : p.inside.recs + (size_t)blockIdx.x * p.rec_stride,
                                            smem_raw, scores, grad, nullptr, marg, gold, loss);
 }
@@ -1555,7 +1554,7 @@ __global__ __launch_bounds__(kThreadsMax) void mbr_kernel(KernelPlan p, const fl
     int cur = blockIdx.x;
     for (;;) {
         const int32_t *rec = p.mbr + (size_t)cur * p.rec_stride;
-        inside_block<true, false, false>(p, 0, rec, smem_raw, scores, nullptr, logZ, marg);
+        inside_block<true, false>(p, 0, rec, smem_raw, scores, nullptr, logZ, marg);
         __syncthreads();   // the marginals are written and the inside charts are free
         cky_block<false>(p, 0, rec, smem_raw, marg, spans, best, nullptr, true);
         if ((int)gridDim.x >= p.n_mbr) break;
@@ -1623,7 +1622,7 @@ __global__ __launch_bounds__(kThreadsMax) void parse_kernel(KernelPlan p, const 
     for (;;) {
         const int32_t *rec = p.mix + (size_t)cur * p.rec_stride;
         if (rec[kRecKind] == kKindInside)
-            inside_block<true, false, false>(p, 0, rec, smem_raw, scores, grad, logZ, marg);
+            inside_block<true, false>(p, 0, rec, smem_raw, scores, grad, logZ, marg);
         else
             cky_block<false>(p, 0, rec, smem_raw, scores, spans, best);
         if ((int)gridDim.x >= p.n_mix) break;   // one bundle per workgroup: no claims at all
@@ -1678,8 +1677,7 @@ hipError_t launch_parse_scratch(const KernelPlan &p, char *scr, const float *sco
 
 hipError_t set_kernel_attributes(int max_lds_bytes) {
     const void *fns[] = {
-        (const void *)inside_kernel<false, false, false>, (const void *)inside_kernel<true, false, false>,
-        (const void *)inside_kernel<false, true, false>,  (const void *)inside_kernel<true, true, false>,
+        (const void *)inside_kernel<false, false>,        (const void *)inside_kernel<true, false>,
         (const void *)cky_kernel<false, false>,           (const void *)cky_kernel<false, true>,
         (const void *)loss_kernel<false>,                 (const void *)parse_kernel,
         (const void *)mbr_kernel,
@@ -1694,18 +1692,31 @@ hipError_t set_kernel_attributes(int max_lds_bytes) {
 template <bool SPILL>
 static void launch_inside_k(const KernelPlan &p, dim3 grid, int threads, size_t lds, hipStream_t s,
                             const float *scores, const float *grad, float *logZ, float *marg) {
-    const bool rev = marg != nullptr, lab = p.L > 1;
     const dim3 block(threads);
-    if (rev && lab) hipLaunchKernelGGL((inside_kernel<true, true, SPILL>), grid, block, lds, s, p, scores, grad, logZ, marg);
-    else if (rev) hipLaunchKernelGGL((inside_kernel<true, false, SPILL>), grid, block, lds, s, p, scores, grad, logZ, marg);
-    else if (lab) hipLaunchKernelGGL((inside_kernel<false, true, SPILL>), grid, block, lds, s, p, scores, grad, logZ, marg);
-    else hipLaunchKernelGGL((inside_kernel<false, false, SPILL>), grid, block, lds, s, p, scores, grad, logZ, marg);
+    if (marg != nullptr) hipLaunchKernelGGL((inside_kernel<true, SPILL>), grid, block, lds, s, p, scores, grad, logZ, marg);
+    else hipLaunchKernelGGL((inside_kernel<false, SPILL>), grid, block, lds, s, p, scores, grad, logZ, marg);
 }
 
 hipError_t launch_inside(const KernelPlan &p, const float *scores, const float *grad, float *logZ,
                          float *marg, hipStream_t stream) {
     const Schedule &q = p.inside;
     hipError_t e;
+    if (p.L > 1) {
+        // labelled: label log-sum-exps into the workspace, the unlabelled
+        // sweeps on them (their marginals into the workspace too), then the
+        // per-label marginals
+        float *sp = reinterpret_cast<float *>(p.ws + p.lab_sp_off);
+        float *mu = reinterpret_cast<float *>(p.ws + p.lab_mu_off);
+        hipLaunchKernelGGL(label_reduce_kernel, dim3(p.n_lab_chunks), dim3(kLabelChunk), 0, stream, p, scores, sp);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        KernelPlan u = p;
+        u.L = 1;
+        if ((e = launch_inside(u, sp, grad, logZ, marg != nullptr ? mu : nullptr, stream)) != hipSuccess) return e;
+        if (marg == nullptr) return hipSuccess;
+        hipLaunchKernelGGL(label_expand_kernel, dim3(p.n_lab_rows), dim3(kLabelChunk), 0, stream, p, scores, sp, mu,
+                           marg);
+        return hipGetLastError();
+    }
     if (q.n_bundles > 0) {
         launch_inside_k<false>(p, dim3(q.n_bundles), q.threads, q.lds_bytes, stream, scores, grad, logZ, marg);
         if ((e = hipGetLastError()) != hipSuccess) return e;

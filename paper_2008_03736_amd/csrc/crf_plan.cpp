@@ -90,14 +90,11 @@ struct HostSchedule {
 };
 
 // Cost model of one sentence for sizing bundles: split points plus a latency
-// term per width step, plus, for labelled scores, a term per label of every
-// span (each is read twice and written once, 32 labels of a span per lane
-// group; about 30 split points' worth, measured on 26 labels).
-constexpr double kLabelCellCost = 30.0;
-inline double sentence_cost(int n, int labels = 1) {
+// term per width step.  (Labelled scores are reduced over their labels
+// before the bundles run, so the bundles' work is the same.)
+inline double sentence_cost(int n) {
     const double T = (double)(n + 1) * n * (n - 1) / 6.0;
-    const double cells = labels > 1 ? (double)n * (n + 1) / 2.0 * labels : 0.0;
-    return T + 200.0 * (n - 1) + kLabelCellCost * cells;
+    return T + 200.0 * (n - 1);
 }
 
 // Predicted duration (microseconds on MI355X, two workgroups per CU) of a
@@ -225,9 +222,6 @@ void plan_fused_launch(std::vector<crf::Bundle> &in, std::vector<crf::Bundle> &c
 // little, and fewer, fuller bundles measured 3-5% faster on the 5,000-sentence
 // mixed batch than an even share; CKY bundles take the share.
 constexpr double kInsideTargetScale = 2.0, kCkyTargetScale = 1.0;
-// Labelled bundles spend most of their time reading and writing labels, a
-// latency-bound pass per bundle: they aim at one slot's share.
-constexpr double kLabelTargetScale = 1.0;
 
 // `order` is sorted by decreasing length.  `bundle_bytes(n, count)` is the
 // LDS of a bundle of `count` sentences of n words, `spill_chart(n)` a
@@ -238,7 +232,7 @@ constexpr double kLabelTargetScale = 1.0;
 template <typename BB, typename FS>
 HostSchedule make_schedule(const std::vector<int32_t> &order, const int32_t *len, int lds_cap,
                            bool force_spill, int64_t ws_base, BB &&bundle_bytes, FS &&spill_chart,
-                           double target_scale, int labels = 1) {
+                           double target_scale) {
     HostSchedule s;
     s.threads = crf::kThreadsDefault;
     // Workgroup LDS budget: half the CU when every eligible sentence fits in
@@ -269,7 +263,7 @@ HostSchedule make_schedule(const std::vector<int32_t> &order, const int32_t *len
     // Target cost per bundle: spread the total over the workgroup slots, but
     // never split below one sentence.
     double total = 0.0;
-    for (int32_t b : eligible) total += sentence_cost(len[b], labels);
+    for (int32_t b : eligible) total += sentence_cost(len[b]);
     const double target = std::max(total / slots, 1.0) * target_scale;
 
     struct Tmp { crf::Bundle bd; double cost; };
@@ -282,7 +276,7 @@ HostSchedule make_schedule(const std::vector<int32_t> &order, const int32_t *len
         const int count = (int)(e - a);
         int by_lds = 1;
         while (by_lds < crf::kMaxBundle && bundle_bytes(n, by_lds + 1) <= budget) ++by_lds;
-        const int by_cost = std::max(1, (int)(target / sentence_cost(n, labels)));
+        const int by_cost = std::max(1, (int)(target / sentence_cost(n)));
         const int per = std::min(by_lds, std::max(1, by_cost));
         const int nbund = (count + per - 1) / per;
         for (int q = 0; q < nbund; ++q) {
@@ -292,7 +286,7 @@ HostSchedule make_schedule(const std::vector<int32_t> &order, const int32_t *len
             t.bd.count = hi - lo;
             t.bd.n = n;
             t.bd.split_ws = -1;
-            t.cost = (hi - lo) * (sentence_cost(n, labels) - 200.0 * (n - 1)) + 200.0 * (n - 1);
+            t.cost = (hi - lo) * (sentence_cost(n) - 200.0 * (n - 1)) + 200.0 * (n - 1);
             tmp.push_back(t);
             s.lds_bytes = std::max<int32_t>(s.lds_bytes, (int32_t)bundle_bytes(n, hi - lo));
         }
@@ -407,8 +401,7 @@ int crf_plan_create(crf_plan **out, const int32_t *lengths_host, int32_t batch, 
     };
     auto cky_bundle_bytes = [=](int n, int64_t count) { return cky_bytes_with(n, count, cky_strict(n, count)); };
     HostSchedule si = make_schedule(order, lengths_host, lds_cap, force, 0, inside_bundle_bytes,
-                                    inside_spill_bytes, num_labels > 1 ? kLabelTargetScale : kInsideTargetScale,
-                                    num_labels);
+                                    inside_spill_bytes, kInsideTargetScale);
     HostSchedule sc = make_schedule(order, lengths_host, lds_cap, force, si.ws_bytes, cky_bundle_bytes,
                                     cky_spill_bytes, kCkyTargetScale);
     int64_t split_cursor = si.ws_bytes + sc.ws_bytes;
@@ -450,6 +443,31 @@ int crf_plan_create(crf_plan **out, const int32_t *lengths_host, int32_t batch, 
                 bd.split_ws = (int32_t)(split_cursor / 256);
                 split_cursor += (bd.count * crf::cky_split_count(bd.n) + 255) / 256 * 256;
             }
+    }
+    // Labelled plans: the label log-sum-exps and their marginals, [B][N1][N1]
+    // float32 each, and the chunks of the label passes.
+    std::vector<int32_t> lab_chunks, lab_rows;
+    int64_t lab_sp_off = 0, lab_mu_off = 0;
+    if (num_labels > 1) {
+        const int64_t plane = (int64_t)batch * n1 * n1 * 4;
+        lab_sp_off = (split_cursor + 255) / 256 * 256;
+        lab_mu_off = (lab_sp_off + plane + 255) / 256 * 256;
+        split_cursor = lab_mu_off + plane;
+        for (int32_t b = 0; b < batch; ++b) {
+            const int n = lengths_host[b];
+            for (int64_t c0 = 0; c0 < crf::cell_walk_slots(n); c0 += crf::kLabelChunk) {
+                lab_chunks.push_back(b);
+                lab_chunks.push_back((int32_t)c0);
+            }
+            for (int i = 0; i < n; ++i)
+                for (int64_t f0 = 0; f0 < (int64_t)(n - i) * num_labels; f0 += crf::kLabelRowChunk) {
+                    lab_rows.push_back(b);
+                    lab_rows.push_back(i);
+                    lab_rows.push_back((int32_t)f0);
+                    lab_rows.push_back(0);
+                }
+        }
+        std::fill(uses_ws.begin(), uses_ws.end(), 1);
     }
     p->ws_bytes = split_cursor;
     p->workspace_users = (int32_t)std::count(uses_ws.begin(), uses_ws.end(), 1);
@@ -520,6 +538,10 @@ int crf_plan_create(crf_plan **out, const int32_t *lengths_host, int32_t batch, 
     };
     const std::vector<int32_t> rec_in = records(si, crf::kKindInside), rec_ck = records(sc, crf::kKindCky);
     const std::vector<int32_t> rec_mbr = mbr_fused ? records(sm, crf::kKindMbr) : std::vector<int32_t>();
+    kp.n_lab_chunks = (int32_t)(lab_chunks.size() / 2);
+    kp.n_lab_rows = (int32_t)(lab_rows.size() / 4);
+    kp.lab_sp_off = lab_sp_off;
+    kp.lab_mu_off = lab_mu_off;
     kp.n_mbr = mbr_fused ? (int32_t)sm.bundles.size() : 0;
     kp.mbr_lds = mbr_fused ? sm.lds_bytes : 0;
     kp.mbr_grid = 0;
@@ -553,7 +575,9 @@ int crf_plan_create(crf_plan **out, const int32_t *lengths_host, int32_t batch, 
         (e = upload(p, sc.spill, &kp.cky.order_spill)) != hipSuccess ||
         (e = upload(p, sc.off, &kp.cky.ws_off)) != hipSuccess ||
         (e = upload(p, rec_mix, &kp.mix)) != hipSuccess ||
-        (e = upload(p, rec_mbr, &kp.mbr)) != hipSuccess) {
+        (e = upload(p, rec_mbr, &kp.mbr)) != hipSuccess ||
+        (e = upload(p, lab_chunks, &kp.lab_chunks)) != hipSuccess ||
+        (e = upload(p, lab_rows, &kp.lab_rows)) != hipSuccess) {
         const int code = (e == hipErrorOutOfMemory) ? CRF_ENOMEM : CRF_EHIP;
         release(p);
         delete p;
