@@ -132,3 +132,62 @@ def subset(batch, idx):
     n1 = int(lengths.max()) + 1
     scores = np.ascontiguousarray(batch.scores[idx][:, :n1, :n1])
     return Batch(batch.name, lengths, scores, batch.sd)
+
+
+# --------------------------------------------------------------------------
+# Boundary representations for the biaffine span scorer (Sec. 2.2,
+# Eq. biaffine), stored as bfloat16 bit patterns (uint16).
+
+
+def to_bf16(x):
+    """float32 array -> bfloat16 bit patterns (uint16), rounded to nearest even."""
+    b = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
+    b = b + (np.uint32(0x7FFF) + ((b >> np.uint32(16)) & np.uint32(1)))
+    return (b >> np.uint32(16)).astype(np.uint16)
+
+
+def from_bf16(h):
+    """bfloat16 bit patterns (uint16) -> float32."""
+    return (np.asarray(h, dtype=np.uint16).astype(np.uint32) << np.uint32(16)).view(np.float32)
+
+
+@dataclass
+class BiaffineInputs:
+    lengths: np.ndarray      # int32 [B]
+    rl: np.ndarray           # uint16 (bf16) [B, N1, d]: left boundary representations r^l_i
+    rr: np.ndarray           # uint16 (bf16) [B, N1, d]: right boundary representations r^r_j
+    wt: np.ndarray           # uint16 (bf16) [L, d, d+1]: wt[l, c, a] = W_l[a, c]; a = d is the bias row
+
+    @property
+    def B(self):
+        return int(self.lengths.shape[0])
+
+    @property
+    def n1(self):
+        return int(self.rl.shape[1])
+
+    @property
+    def d(self):
+        return int(self.rl.shape[2])
+
+    @property
+    def num_labels(self):
+        return int(self.wt.shape[0])
+
+
+def biaffine_inputs(lengths, d, labels=1, seed=0, score_sd=2.0, n1=None):
+    """Seeded representations and weights: r ~ N(0,1), W ~ N(0, (score_sd/d)^2),
+    so that a span score sums d products of d products and has sd about
+    score_sd (as the span scores of the CRF workloads).  Rows past each
+    sentence hold NaN (never read).  Draw order: rl, rr, wt."""
+    rng = np.random.default_rng(seed)
+    lengths = np.asarray(lengths, np.int32)
+    B = lengths.shape[0]
+    n1 = int(lengths.max()) + 1 if n1 is None else int(n1)
+    rl = rng.standard_normal((B, n1, d), dtype=np.float32)
+    rr = rng.standard_normal((B, n1, d), dtype=np.float32)
+    wt = rng.standard_normal((labels, d, d + 1), dtype=np.float32) * np.float32(score_sd / d)
+    rows = np.arange(n1)[None, :] > lengths[:, None]
+    rl[rows] = np.nan
+    rr[rows] = np.nan
+    return BiaffineInputs(lengths, to_bf16(rl), to_bf16(rr), to_bf16(wt))

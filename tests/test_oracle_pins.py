@@ -460,3 +460,73 @@ def test_mbr_invariants():
         assert n + 1 - 1e-5 <= best[bi] <= 2 * n - 1 + 1e-5
         cky_sum = sum(float(mu32[bi, i, j]) for i, j in sp_cky[bi, : 2 * n - 1])
         assert best[bi] >= cky_sum - 1e-9
+
+
+# --------------------------------------------------------------------------
+# Biaffine span scorer (Sec. 2.2, Eq. biaffine)
+
+
+def _bf(x):
+    return W.to_bf16(np.asarray(x, np.float32))
+
+
+def test_biaffine_bias_row_is_on_the_left():
+    # W zero but its last row: the appended 1 of [r^l_i ; 1] picks that row,
+    # so s(i,j) = bias . r^r_j, the same for every i (a bias on the right
+    # representation); placing the 1 on the right instead would make it
+    # depend on i only
+    from oracle import biaffine as obi
+
+    rng = np.random.default_rng(1)
+    d, n = 6, 5
+    inp = W.biaffine_inputs([n], d, seed=2)
+    w = np.zeros((1, d, d + 1), np.float32)
+    bias = rng.standard_normal(d).astype(np.float32)
+    w[0, :, d] = bias
+    s, _ = obi.biaffine(inp.rl, inp.rr, _bf(w), [n])
+    rr = W.from_bf16(inp.rr).astype(np.float64)
+    bq = W.from_bf16(_bf(bias)).astype(np.float64)
+    for i in range(n):
+        for j in range(i + 1, n + 1):
+            assert abs(s[0, i, j] - float(np.dot(bq, rr[0, j]))) <= 1e-12
+
+
+def test_biaffine_rank_one_weight_factorises():
+    # W = u v^T: s(i,j) = ([r^l_i;1] . u) (v . r^r_j) -- a transposed W, a
+    # swapped pair of representations or a misplaced bias all break it.
+    # Small integers keep u, v and every u_a v_c exact in bfloat16.
+    from oracle import biaffine as obi
+
+    rng = np.random.default_rng(3)
+    d, n = 5, 4
+    inp = W.biaffine_inputs([n], d, seed=4)
+    u = rng.integers(-3, 4, d + 1).astype(np.float64)
+    v = rng.integers(-3, 4, d).astype(np.float64)
+    w = np.outer(v, u)[None]                         # wt[0, c, a] = W[a, c] = u_a v_c
+    assert np.array_equal(W.from_bf16(_bf(w)).astype(np.float64), w)
+    s, _ = obi.biaffine(inp.rl, inp.rr, _bf(w), [n])
+    rl = W.from_bf16(inp.rl).astype(np.float64)[0]
+    rr = W.from_bf16(inp.rr).astype(np.float64)[0]
+    for i in range(n):
+        for j in range(i + 1, n + 1):
+            ref = float(np.dot(np.append(rl[i], 1.0), u)) * float(np.dot(v, rr[j]))
+            assert abs(s[0, i, j] - ref) <= 1e-9 * max(1.0, abs(ref))
+
+
+def test_biaffine_labels_use_their_own_weights():
+    # label l's scores come from W_l alone: permuting the weights permutes
+    # the labels; one weight per label equals the unlabelled scorer
+    from oracle import biaffine as obi
+
+    d, L = 8, 3
+    lengths = [3, 6]
+    inp = W.biaffine_inputs(lengths, d, labels=L, seed=5)
+    s, bound = obi.biaffine(inp.rl, inp.rr, inp.wt, lengths)
+    perm = [2, 0, 1]
+    s2, _ = obi.biaffine(inp.rl, inp.rr, inp.wt[perm], lengths)
+    v = W.valid_mask(np.asarray(lengths), inp.n1)
+    assert np.array_equal(s2[v], s[v][:, perm])
+    for l in range(L):
+        s1, _ = obi.biaffine(inp.rl, inp.rr, inp.wt[l:l + 1], lengths)
+        assert np.array_equal(s1[v], s[v][:, l])
+    assert np.all(bound[v] >= np.abs(s[v]) - 1e-12)
