@@ -146,6 +146,44 @@ def stats_ms(samples):
             "n": int(a.size)}
 
 
+BF16_PEAK = 2.5e15   # dense bf16 MFMA FLOP/s
+
+
+def bench_biaffine(torch, B, batch, dev, reps, d=500):
+    """The biaffine span scorer (Eq. biaffine) that produces this batch's
+    scores from boundary representations of the paper's size, d = 500: median
+    launch time and MFMA roofline.  Algorithmic FLOPs per sentence of n words:
+    the n left rows' [r^l;1]^T W (2 n (d+1) d) and the valid cells' inner
+    products (2 d n(n+1)/2).  Inputs: seeded N(0,1) representations, W of sd
+    2/d (scores of sd ~2, as the batch's), bf16."""
+    g = torch.Generator(device=dev)
+    g.manual_seed(0)
+    shape = (batch.B, batch.n1, d)
+    rl = torch.randn(shape, generator=g, device=dev).to(torch.bfloat16).view(torch.int16)
+    rr = torch.randn(shape, generator=g, device=dev).to(torch.bfloat16).view(torch.int16)
+    ldw = (d + 1 + 3) // 4 * 4
+    w = (torch.randn((1, d, ldw), generator=g, device=dev) * (2.0 / d)).to(torch.bfloat16).view(torch.int16)
+    scores = torch.empty((batch.B, batch.n1, batch.n1), dtype=torch.float32, device=dev)
+    with B.Plan(batch.lengths, n1=batch.n1, device=dev) as plan:
+        fn = lambda: plan.biaffine_scores(rl, rr, w, scores=scores)
+        fn()
+        torch.cuda.synchronize()
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+        for a, b in evs:
+            a.record()
+            fn()
+            b.record()
+        torch.cuda.synchronize()
+        t = stats_ms([a.elapsed_time(b) for a, b in evs])
+    n = batch.lengths.astype(np.int64)
+    flops = int((2 * n * (d + 1) * d + d * n * (n + 1)).sum())
+    ach = flops / (t["mean"] * 1e-3)
+    return {"entry": "crf_biaffine_scores", "d": d, "launch_ms": t,
+            "sentences_per_s": round(batch.B / (t["median"] * 1e-3), 1),
+            "roofline": {"bound": "mfma", "achieved": round(ach / 1e12, 2), "peak": BF16_PEAK / 1e12,
+                         "unit": "TFLOP/s", "frac": round(ach / BF16_PEAK, 4), "algorithmic_flops": flops}}
+
+
 def run_ceilings():
     """Microbenchmarked ceilings of gfx950 (lane-operations per second)."""
     import torch
@@ -174,7 +212,7 @@ def main():
                     help="after timing, run a plain device copy of this many MiB a few times "
                          "(a known-size kernel to scale HBM counters by)")
     ap.add_argument("--ceilings", action="store_true", help="measure the ALU / LDS ceilings and exit")
-    ap.add_argument("--profile", choices=["parse", "fwd_bwd", "cky", "mbr", "loss", "lcky", "label_spans"],
+    ap.add_argument("--profile", choices=["parse", "fwd_bwd", "cky", "mbr", "loss", "lcky", "label_spans", "biaffine"],
                     help="launch only this entry point (warmup + steps launches, then exit): the program "
                          "that rocprofv3 summaries under profiles/ are taken on")
     args = ap.parse_args()
@@ -264,6 +302,10 @@ def main():
     step = parse if decode else fwd_bwd
     passes = {"parse": parse, "fwd_bwd": fwd_bwd, "cky": cky, "mbr": mbr, "loss": loss, "lcky": lcky,
               "label_spans": label_spans}
+    if args.profile == "biaffine":
+        bench_biaffine(torch, B, batch, dev, args.warmup + args.steps)
+        print(json.dumps({"profile": "biaffine", "workload": batch.name}), flush=True)
+        return
     if args.profile is not None:
         if args.profile == "label_spans":
             lcky()                       # spans to label
@@ -365,6 +407,8 @@ def main():
     for k, t in t_other.items():
         extra[names[k] + "_ms"] = t
         extra[names[k] + "_sentences_per_s"] = round(batch.B / (t["median"] * 1e-3), 1)
+
+    extra["biaffine_scorer"] = bench_biaffine(torch, B, batch, dev, reps) if decode else None
 
     if args.copy_mib > 0:
         src = torch.empty(args.copy_mib << 18, dtype=torch.float32, device=dev).fill_(1.0)

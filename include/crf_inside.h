@@ -17,7 +17,9 @@
  *     labelled tree;
  *   - MBR decoding over the marginals (Sec. 3.3), the gold-tree CRF loss
  *     and its gradient (Sec. 2.3, Eq. bracket-loss), and the labelling stage
- *     of the two-stage parser (Sec. 2.1, Eq. label-argmax).
+ *     of the two-stage parser (Sec. 2.1, Eq. label-argmax);
+ *   - the span (and label) scores themselves, from boundary representations
+ *     by the biaffine scorer (Sec. 2.2, Eq. biaffine).
  *
  * Conventions
  *   Fence posts.  A sentence of n words has boundaries 0..n; span (i,j),
@@ -239,6 +241,32 @@ int crf_cky_decode_labeled(const crf_plan *plan, const float *scores, int32_t *s
  */
 int crf_label_spans(const crf_plan *plan, const float *label_scores, int32_t num_labels, const int32_t *spans,
                     int32_t *labels, void *stream);
+
+/*
+ * crf_biaffine_scores -- the biaffine span scorer that produces the span
+ * scores (Sec. 2.2, Eq. biaffine): s(i,j) = [r^l_i ; 1]^T W r^r_j from the
+ * left boundary representation of fence post i and the right one of fence
+ * post j, W of (d+1) x d entries (the appended 1 makes its last row a bias on
+ * r^r_j); one W per label for label scores (Sec. 2.2, label scoring):
+ * s(i,j,l) = [r^l_i ; 1]^T W_l r^r_j.  bf16 inputs, fp32 products and sums
+ * on the matrix cores (MFMA); the inner (d x d) product stays on chip.
+ *   rl, rr      device bf16 bit patterns [B][N1][d]: r^l_i and r^r_i of
+ *               sentence b at [(b*N1 + i)*d]; rows past n_b are not read.
+ *               8-byte aligned.
+ *   w           device bf16 bit patterns [num_labels][d][ldw], W transposed:
+ *               w[(l*d + c)*ldw + a] = W_l[a][c] for a <= d (a = d is the bias
+ *               row); entries a > d are not read.  8-byte aligned.
+ *   d           4 <= d <= 508, a multiple of 4 (the paper's d is 500, and
+ *               100 for the label scorer).
+ *   ldw         row stride of w, >= d+1 and a multiple of 4.
+ *   num_labels  number of W (1 for span scores).
+ *   scores      device float32, [B][N1][N1] when num_labels = 1 (the layout
+ *               the CRF calls take), else [B][N1][N1][num_labels]; only cells
+ *               0 <= i < j <= n_b are written.
+ * B, N1 and the lengths are the plan's (its own num_labels is not used).
+ */
+int crf_biaffine_scores(const crf_plan *plan, const uint16_t *rl, const uint16_t *rr, const uint16_t *w,
+                        int32_t d, int32_t ldw, int32_t num_labels, float *scores, void *stream);
 
 /*
  * crf_inside_fwd_bwd_cky_noalloc -- crf_inside_fwd_bwd_cky for callers that

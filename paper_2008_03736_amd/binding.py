@@ -37,6 +37,7 @@ SIGNATURES = {
     "crf_gold_loss": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P]),
     "crf_cky_decode_labeled": (ctypes.c_int, [_P, _P, _P, _P, _P, _P]),
     "crf_label_spans": (ctypes.c_int, [_P, _P, _I32, _P, _P, _P]),
+    "crf_biaffine_scores": (ctypes.c_int, [_P, _P, _P, _P, _I32, _I32, _I32, _P, _P]),
     "crf_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "crf_last_error": (ctypes.c_char_p, []),
 }
@@ -155,6 +156,11 @@ def crf_cky_decode_labeled(plan, scores, spans, labels, best, stream):
 
 def crf_label_spans(plan, label_scores, num_labels, spans, labels, stream):
     _check(load().crf_label_spans(plan, label_scores, num_labels, spans, labels, stream), "crf_label_spans")
+
+
+def crf_biaffine_scores(plan, rl, rr, w, d, ldw, num_labels, scores, stream):
+    _check(load().crf_biaffine_scores(plan, rl, rr, w, d, ldw, num_labels, scores, stream),
+           "crf_biaffine_scores")
 
 
 def crf_status_string(status):
@@ -386,6 +392,31 @@ class Plan:
         crf_label_spans(self._handle, label_scores.data_ptr(), int(label_scores.shape[3]), spans.data_ptr(),
                         labels.data_ptr(), _stream_ptr(t, self.device))
         return labels
+
+    def biaffine_scores(self, rl, rr, w, scores=None):
+        """Span (or label) scores from boundary representations (Sec. 2.2,
+        Eq. biaffine).  rl, rr: bf16 bit patterns as int16/uint16 tensors
+        [B, N1, d]; w: [L, d, ldw] (W transposed, bias at index d).  Returns
+        float32 [B, N1, N1] (L = 1) or [B, N1, N1, L]; a fresh buffer is
+        NaN-filled, and only valid cells are written."""
+        t = self._torch
+        if rl.dim() != 3 or tuple(rl.shape[:2]) != (self.B, self.n1) or tuple(rr.shape) != tuple(rl.shape):
+            raise ValueError(f"rl and rr must be [{self.B}, {self.n1}, d]")
+        d = int(rl.shape[2])
+        if w.dim() != 3 or int(w.shape[1]) != d:
+            raise ValueError("w must be [L, d, ldw]")
+        for x in (rl, rr, w):
+            if x.dtype not in (t.int16, t.uint16) or not x.is_contiguous() or x.device != self.device:
+                raise ValueError("rl, rr and w must be contiguous 16-bit tensors on the plan's device")
+        L = int(w.shape[0])
+        shape = (self.B, self.n1, self.n1) if L == 1 else (self.B, self.n1, self.n1, L)
+        if scores is None:
+            scores = t.full(shape, float("nan"), dtype=t.float32, device=self.device)
+        elif tuple(scores.shape) != shape or scores.dtype != t.float32 or not scores.is_contiguous():
+            raise ValueError(f"scores must be contiguous float32 {shape}")
+        crf_biaffine_scores(self._handle, rl.data_ptr(), rr.data_ptr(), w.data_ptr(), d, int(w.shape[2]), L,
+                            scores.data_ptr(), _stream_ptr(t, self.device))
+        return scores
 
     def cky_decode(self, scores, spans=None, best=None):
         """(spans int32 [B, 2(N1-1)-1, 2] preorder padded with -1, best float32 [B])."""

@@ -6,7 +6,8 @@ import sys
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
-SOURCES = [os.path.join(CSRC, "crf_kernels.hip"), os.path.join(CSRC, "crf_plan.cpp")]
+SOURCES = [os.path.join(CSRC, "crf_kernels.hip"), os.path.join(CSRC, "crf_biaffine.hip"),
+           os.path.join(CSRC, "crf_plan.cpp")]
 LIB = os.path.join(PKG, "libcrfinside.so")
 # microbenchmarks of the ceilings behind the roofline (bench.py --ceilings)
 CEIL_SOURCES = [os.path.join(CSRC, "crf_ceilings.hip")]

@@ -273,6 +273,12 @@ __host__ __device__ inline int masked_reach(int n) {
     return (sh.C - sh.MF) * sh.G;
 }
 
+// Biaffine scorer tiles: rows (left fence posts) and columns (right fence
+// posts) per tile, representation dimensions per chunk of the inner product,
+// and the largest d whose staged rows fit in LDS beside a chunk of W.
+constexpr int kBiaRows = 64, kBiaCols = 64, kBiaChunk = 64;
+constexpr int kBiaMaxD = 508;
+
 // Cell-walk slots per workgroup of the label reduction (one per thread,
 // which is also the workgroup size of the label passes), and floats per
 // workgroup of the label expansion.
@@ -351,6 +357,10 @@ struct KernelPlan {
     // (sentence, row, first float, 0)
     const int32_t *lab_rows;
     int32_t n_lab_rows;
+    // biaffine scorer tiles: kBiaRows row ids then kBiaCols column ids each
+    // (b N1 + fence post, or -1)
+    const int32_t *bia_tiles;
+    int32_t n_bia_tiles;
     int64_t lab_sp_off, lab_mu_off;
     int32_t rec_stride;          // ints per record: kRecHeader + the largest bundle
     int32_t B, n1, L;
@@ -389,5 +399,11 @@ hipError_t launch_label_spans(const KernelPlan &p, const float *label_scores, in
 hipError_t launch_parse(const KernelPlan &p, const float *scores, const float *grad, float *logZ,
                         float *marg, int32_t *spans, float *best, hipStream_t stream);
 hipError_t set_kernel_attributes(int max_lds_bytes);
+// The biaffine scorer (crf_biaffine.hip): dynamic LDS per workgroup for d,
+// and the launch over the plan's tiles and L labels.
+int64_t biaffine_lds_bytes(int d);
+hipError_t set_biaffine_attributes();   // once per plan: the LDS of the largest d
+hipError_t launch_biaffine(const KernelPlan &p, const uint16_t *rl, const uint16_t *rr, const uint16_t *w, int d,
+                           int ldw, int L, float *scores, hipStream_t stream);
 
 }  // namespace crf

@@ -472,6 +472,42 @@ int crf_plan_create(crf_plan **out, const int32_t *lengths_host, int32_t batch, 
     p->ws_bytes = split_cursor;
     p->workspace_users = (int32_t)std::count(uses_ws.begin(), uses_ws.end(), 1);
 
+    // Biaffine scorer tiles: sentences of up to kBiaRows - 1 words packed
+    // whole into tiles of kBiaRows fence posts (longest first, next fit;
+    // their scores are the tile's diagonal blocks), longer ones cut into
+    // blocks of fence posts with a tile per pair of row block <= column block.
+    std::vector<int32_t> bia;
+    {
+        std::vector<int32_t> ids;
+        auto flush = [&]() {
+            if (ids.empty()) return;
+            for (int h = 0; h < 2; ++h)
+                for (int r = 0; r < crf::kBiaRows; ++r) bia.push_back(r < (int)ids.size() ? ids[r] : -1);
+            ids.clear();
+        };
+        for (int32_t b : order) {
+            const int n = lengths_host[b];
+            if (n + 1 <= crf::kBiaRows) {
+                if ((int)ids.size() + n + 1 > crf::kBiaRows) flush();
+                for (int i = 0; i <= n; ++i) ids.push_back(b * n1 + i);
+                continue;
+            }
+            const int nblk = (n + 1 + crf::kBiaRows - 1) / crf::kBiaRows;
+            for (int rb = 0; rb < nblk; ++rb)
+                for (int cb = rb; cb < nblk; ++cb) {
+                    for (int r = 0; r < crf::kBiaRows; ++r) {
+                        const int i = rb * crf::kBiaRows + r;
+                        bia.push_back(i <= n ? b * n1 + i : -1);
+                    }
+                    for (int c = 0; c < crf::kBiaCols; ++c) {
+                        const int j = cb * crf::kBiaCols + c;
+                        bia.push_back(j <= n ? b * n1 + j : -1);
+                    }
+                }
+        }
+        flush();
+    }
+
     std::vector<int32_t> len(lengths_host, lengths_host + batch);
     crf::KernelPlan &kp = p->kp;
     kp.B = batch;
@@ -540,6 +576,7 @@ int crf_plan_create(crf_plan **out, const int32_t *lengths_host, int32_t batch, 
     const std::vector<int32_t> rec_mbr = mbr_fused ? records(sm, crf::kKindMbr) : std::vector<int32_t>();
     kp.n_lab_chunks = (int32_t)(lab_chunks.size() / 2);
     kp.n_lab_rows = (int32_t)(lab_rows.size() / 4);
+    kp.n_bia_tiles = (int32_t)(bia.size() / (crf::kBiaRows + crf::kBiaCols));
     kp.lab_sp_off = lab_sp_off;
     kp.lab_mu_off = lab_mu_off;
     kp.n_mbr = mbr_fused ? (int32_t)sm.bundles.size() : 0;
@@ -577,7 +614,8 @@ int crf_plan_create(crf_plan **out, const int32_t *lengths_host, int32_t batch, 
         (e = upload(p, rec_mix, &kp.mix)) != hipSuccess ||
         (e = upload(p, rec_mbr, &kp.mbr)) != hipSuccess ||
         (e = upload(p, lab_chunks, &kp.lab_chunks)) != hipSuccess ||
-        (e = upload(p, lab_rows, &kp.lab_rows)) != hipSuccess) {
+        (e = upload(p, lab_rows, &kp.lab_rows)) != hipSuccess ||
+        (e = upload(p, bia, &kp.bia_tiles)) != hipSuccess) {
         const int code = (e == hipErrorOutOfMemory) ? CRF_ENOMEM : CRF_EHIP;
         release(p);
         delete p;
@@ -612,6 +650,7 @@ int crf_plan_create(crf_plan **out, const int32_t *lengths_host, int32_t batch, 
     // limit without this attribute; a real shortfall surfaces as a launch error.
     if (crf::set_kernel_attributes(std::max(std::max(si.lds_bytes, sc.lds_bytes), kp.mbr_lds)) != hipSuccess)
         (void)hipGetLastError();
+    if (crf::set_biaffine_attributes() != hipSuccess) (void)hipGetLastError();
     // Resolve this device's scratch address for the no-allocation entry
     // point now (it retries, and reports a failure, on its first call).
     char *scr = nullptr;
@@ -777,6 +816,25 @@ int crf_label_spans(const crf_plan *plan, const float *label_scores, int32_t num
     hipError_t e = crf::launch_label_spans(plan->kp, label_scores, num_labels, spans, labels,
                                            static_cast<hipStream_t>(stream));
     return e == hipSuccess ? ok() : hip_fail(e, "crf_label_spans launch");
+}
+
+int crf_biaffine_scores(const crf_plan *plan, const uint16_t *rl, const uint16_t *rr, const uint16_t *w,
+                        int32_t d, int32_t ldw, int32_t num_labels, float *scores, void *stream) {
+    if (plan == nullptr) return fail(CRF_EINVAL, "plan is NULL");
+    if (rl == nullptr || rr == nullptr || w == nullptr || scores == nullptr)
+        return fail(CRF_EINVAL, "rl/rr/w/scores is NULL");
+    if (d < 4 || d > crf::kBiaMaxD || d % 4 != 0)
+        return fail(CRF_EINVAL, "d %d is not a multiple of 4 in [4, %d]", d, crf::kBiaMaxD);
+    if (ldw < d + 1 || ldw % 4 != 0) return fail(CRF_EINVAL, "ldw %d < d+1 or not a multiple of 4", ldw);
+    if (num_labels < 1 || num_labels > CRF_MAX_LABELS)
+        return fail(CRF_EINVAL, "num_labels %d outside [1, %d]", num_labels, CRF_MAX_LABELS);
+    if (((uintptr_t)rl | (uintptr_t)rr | (uintptr_t)w) & 7)
+        return fail(CRF_EINVAL, "rl/rr/w must be 8-byte aligned");
+    int rc = check_device(plan);
+    if (rc != CRF_OK) return rc;
+    hipError_t e = crf::launch_biaffine(plan->kp, rl, rr, w, d, ldw, num_labels, scores,
+                                        static_cast<hipStream_t>(stream));
+    return e == hipSuccess ? ok() : hip_fail(e, "crf_biaffine_scores launch");
 }
 
 int crf_cky_decode(const crf_plan *plan, const float *scores, int32_t *spans, float *best,

@@ -66,6 +66,12 @@ hipError_t launch_parse(const KernelPlan &, const float *, const float *, float 
     return hipErrorNotSupported;
 }
 hipError_t set_kernel_attributes(int) { return hipSuccess; }
+int64_t biaffine_lds_bytes(int) { return 0; }
+hipError_t set_biaffine_attributes() { return hipSuccess; }
+hipError_t launch_biaffine(const KernelPlan &, const uint16_t *, const uint16_t *, const uint16_t *, int, int, int,
+                           float *, hipStream_t) {
+    return hipErrorNotSupported;
+}
 hipError_t scratch_address(int, char **out) {
     *out = nullptr;
     return hipErrorNotSupported;
