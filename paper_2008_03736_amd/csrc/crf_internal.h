@@ -276,8 +276,9 @@ __host__ __device__ inline int masked_reach(int n) {
 // Biaffine scorer tiles: rows (left fence posts) and columns (right fence
 // posts) per tile, representation dimensions per chunk of the inner product,
 // and the largest d whose staged rows fit in LDS beside a chunk of W.
-constexpr int kBiaRows = 64, kBiaCols = 64, kBiaChunk = 64;
+constexpr int kBiaRows = 64, kBiaCols = 64, kBiaChunk = 32;
 constexpr int kBiaMaxD = 508;
+static_assert(kBiaRows == kBiaCols, "packed tiles use their fence posts as both rows and columns");
 
 // Cell-walk slots per workgroup of the label reduction (one per thread,
 // which is also the workgroup size of the label passes), and floats per

@@ -473,23 +473,31 @@ int crf_plan_create(crf_plan **out, const int32_t *lengths_host, int32_t batch, 
     p->workspace_users = (int32_t)std::count(uses_ws.begin(), uses_ws.end(), 1);
 
     // Biaffine scorer tiles: sentences of up to kBiaRows - 1 words packed
-    // whole into tiles of kBiaRows fence posts (longest first, next fit;
-    // their scores are the tile's diagonal blocks), longer ones cut into
-    // blocks of fence posts with a tile per pair of row block <= column block.
+    // whole into tiles of kBiaRows fence posts (their scores are the tile's
+    // diagonal blocks; longest first, each into the open tile with the least
+    // room that still holds it, found through lists of open tiles by free
+    // rows), longer ones cut into blocks of fence posts with a tile per pair
+    // of row block <= column block.
     std::vector<int32_t> bia;
     {
-        std::vector<int32_t> ids;
-        auto flush = [&]() {
-            if (ids.empty()) return;
-            for (int h = 0; h < 2; ++h)
-                for (int r = 0; r < crf::kBiaRows; ++r) bia.push_back(r < (int)ids.size() ? ids[r] : -1);
-            ids.clear();
-        };
+        std::vector<std::vector<int32_t>> packed;
+        std::vector<std::vector<int32_t>> by_free(crf::kBiaRows + 1);
         for (int32_t b : order) {
             const int n = lengths_host[b];
             if (n + 1 <= crf::kBiaRows) {
-                if ((int)ids.size() + n + 1 > crf::kBiaRows) flush();
-                for (int i = 0; i <= n; ++i) ids.push_back(b * n1 + i);
+                int t = -1;
+                for (int f = n + 1; f <= crf::kBiaRows && t < 0; ++f)
+                    if (!by_free[f].empty()) {
+                        t = by_free[f].back();
+                        by_free[f].pop_back();
+                    }
+                if (t < 0) {
+                    t = (int)packed.size();
+                    packed.emplace_back();
+                }
+                for (int i = 0; i <= n; ++i) packed[t].push_back(b * n1 + i);
+                const int room = crf::kBiaRows - (int)packed[t].size();
+                if (room > 0) by_free[room].push_back(t);
                 continue;
             }
             const int nblk = (n + 1 + crf::kBiaRows - 1) / crf::kBiaRows;
@@ -505,7 +513,9 @@ int crf_plan_create(crf_plan **out, const int32_t *lengths_host, int32_t batch, 
                     }
                 }
         }
-        flush();
+        for (const auto &ids : packed)
+            for (int h = 0; h < 2; ++h)
+                for (int r = 0; r < crf::kBiaRows; ++r) bia.push_back(r < (int)ids.size() ? ids[r] : -1);
     }
 
     std::vector<int32_t> len(lengths_host, lengths_host + batch);
