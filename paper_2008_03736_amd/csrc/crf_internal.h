@@ -280,14 +280,10 @@ constexpr int kBiaRows = 64, kBiaCols = 64, kBiaChunk = 32;
 constexpr int kBiaMaxD = 508;
 static_assert(kBiaRows == kBiaCols, "packed tiles use their fence posts as both rows and columns");
 
-// Cell-walk slots per workgroup of the label reduction (one per thread,
-// which is also the workgroup size of the label passes), and floats per
-// workgroup of the label expansion.
+// Threads per workgroup of the label passes, and floats of a row's label
+// block per workgroup.
 constexpr int kLabelChunk = 256;
 constexpr int kLabelRowChunk = 1024;
-// Slots of a sentence's cell walk (Cell_walk): rows r and n-1-r share one of
-// n+1 slots, ceil(n/2) rows.
-__host__ __device__ inline int64_t cell_walk_slots(int n) { return (int64_t)((n + 1) / 2) * (n + 1); }
 
 // Longest sentence whose CKY chart could sit in one CU's LDS (160 KiB):
 // 8 (n+1)^2 <= 163840 (with row padding, its split table and tables the
@@ -349,13 +345,9 @@ struct KernelPlan {
     const int32_t *mbr;
     int32_t n_mbr, mbr_grid, mbr_lds;
     int32_t *counter;            // the fused kernels' bundle claims; zero between launches
-    // labelled plans: chunks of kLabelChunk cell-walk slots, (sentence, first
-    // slot) pairs, and the workspace offsets of the label log-sum-exps and of
-    // their marginals ([B][N1][N1] float32 each)
-    const int32_t *lab_chunks;
-    int32_t n_lab_chunks;
-    // and chunks of kLabelRowChunk floats of the rows' label blocks:
-    // (sentence, row, first float, 0)
+    // labelled plans: chunks of kLabelRowChunk floats of the rows' label
+    // blocks, (sentence, row, first float, 0), and the workspace offsets of
+    // the label log-sum-exps and of their marginals ([B][N1][N1] float32 each)
     const int32_t *lab_rows;
     int32_t n_lab_rows;
     // biaffine scorer tiles: kBiaRows row ids then kBiaCols column ids each

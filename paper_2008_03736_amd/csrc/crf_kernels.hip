@@ -774,20 +774,6 @@ __device__ __forceinline__ void for_cells_loaded(int nb, int n, AD &&addr, LD &&
     }
 }
 
-// Log-sum-exp (log2 units) of the L label scores of one span at s: blocks
-// of 32 labels, each block's loads issued together (clamped to the last
-// label, so every load is in bounds) and its terms kept in registers;
-// label_block folds one block into the running max m and sum acc.
-__device__ __forceinline__ void label_block(const float (&v)[32], int q0, int L, float &m, float &acc) {
-    float mb = -INFINITY;
-#pragma unroll
-    for (int k = 0; k < 32; ++k) mb = q0 + k < L ? fmax_nn(mb, v[k]) : mb;
-    const float mn = fmax_nn(m, mb * LOG2E_F);
-    acc *= fast_exp2(m - mn);   // (0 * exp2(-inf) = 0 on the first block)
-#pragma unroll
-    for (int k = 0; k < 32; ++k) acc += q0 + k < L ? fast_exp2(v[k] * LOG2E_F - mn) : 0.f;
-    m = mn;
-}
 // The first 32 labels of a span into v (clamped to the last label), with
 // 8-byte loads when `wide`: an even count on an 8-byte aligned score tensor
 // (every span's offset is then a multiple of 2 floats).  The values are the
@@ -807,33 +793,6 @@ __device__ __forceinline__ void label_load32(const float *s, int L, bool wide, f
         for (int k = 0; k < 32; ++k) v[k] = s[min(k, L - 1)];
     }
 }
-__device__ __forceinline__ float label_lse2(const float *s, int L, bool wide) {
-    float m = -INFINITY, acc = 0.f;
-    for (int q0 = 0; q0 < L; q0 += 32) {
-        float v[32];
-        if (q0 == 0) {
-            label_load32(s, L, wide, v);
-        } else {
-#pragma unroll
-            for (int k = 0; k < 32; ++k) v[k] = s[min(q0 + k, L - 1)];
-        }
-        label_block(v, q0, L, m, acc);
-    }
-    return m + fast_log2(acc);
-}
-// o[q] = mu exp2(s[q] log2e - lse2) for the L labels of one span, in blocks
-// of 32 as above.
-__device__ __forceinline__ void label_marginals(const float *s, int L, float mu, float lse2, float *o) {
-    for (int q0 = 0; q0 < L; q0 += 32) {
-        float v[32];
-#pragma unroll
-        for (int k = 0; k < 32; ++k) v[k] = s[min(q0 + k, L - 1)];
-#pragma unroll
-        for (int k = 0; k < 32; ++k)
-            if (q0 + k < L) o[q0 + k] = mu * fast_exp2(v[k] * LOG2E_F - lse2);
-    }
-}
-
 // Max over the L labels of one span at s (an exact float32 max), for the
 // one-stage labelled CKY: blocks of 32 labels, each block's loads issued
 // together (clamped to the last label).
@@ -1445,58 +1404,107 @@ __global__ __launch_bounds__(kThreadsMax) void inside_kernel(KernelPlan p, const
                              smem_raw, scores, grad, logZ, marg);
 }
 
-// Labelled scores [B][N1][N1][L], spread over the whole chip: a workgroup per
-// chunk of kLabelChunk slots of one sentence's cell walk (Cell_walk), a cell
-// per thread.  label_reduce_kernel writes each valid cell's label
-// log-sum-exp s'(i,j) = log sum_l exp s(i,j,l) (Sec. 4.2, Eq. tree-label-score:
-// the one-stage Z sums exp of the labelled score over labels per span) into
-// sp [B][N1][N1]; the unlabelled kernels then run on sp; label_expand_kernel
+// Labelled scores [B][N1][N1][L], spread over the whole chip.
+// label_reduce_kernel writes each valid cell's label log-sum-exp
+// s'(i,j) = log sum_l exp s(i,j,l) (Sec. 4.2, Eq. tree-label-score: the
+// one-stage Z sums exp of the labelled score over labels per span) into sp
+// [B][N1][N1]; the unlabelled kernels then run on sp; label_expand_kernel
 // writes the per-label marginals mu(i,j) exp(s(i,j,l) - s'(i,j)) from their
 // marginals mu [B][N1][N1].  Only valid cells are read or written.
-__device__ __forceinline__ bool label_cell(const KernelPlan &p, int *b, int *i, int *j) {
-    const int2 ch = reinterpret_cast<const int2 *>(p.lab_chunks)[blockIdx.x];   // (sentence, first slot)
-    *b = ch.x;
-    const int n = p.len[ch.x];
-    const Cell_walk cw(1, n);
-    const Cell e = cw.at(ch.y + (int)threadIdx.x);
-    *i = e.i;
-    *j = e.j;
-    return e.ok;
+// Both passes run over the contiguous label blocks of the rows: row i of
+// sentence b holds the labels of cells (i, i+1..n) back to back, and a
+// wavefront takes a chunk of at most kLabelRowChunk consecutive floats of one
+// row (p.lab_rows: sentence, row, first float), its lanes on consecutive
+// floats, so that every global access is a whole cache line, and every load
+// of a chunk is issued before the first use (a chunk is a few hundred floats:
+// serial round trips to memory, not bandwidth, would bound it otherwise).
+constexpr int kLabelWaves = kLabelChunk / 64;          // chunks per workgroup, a wavefront each
+constexpr int kLabelPer = kLabelRowChunk / 64;         // floats of a chunk per lane
+struct Label_row {
+    size_t cell0;   // the row's first cell (i, i+1)
+    int f0, len;    // the chunk's first float, the row block's floats
+};
+__device__ __forceinline__ bool label_row(const KernelPlan &p, int r, Label_row *o) {
+    if (r >= p.n_lab_rows) return false;
+    const int4 rc = reinterpret_cast<const int4 *>(p.lab_rows)[r];   // (sentence, row, first float)
+    const int N1 = p.n1, n = p.len[rc.x], i = rc.y;
+    o->cell0 = ((size_t)rc.x * N1 + i) * N1 + i + 1;
+    o->f0 = rc.z;
+    o->len = (n - i) * p.L;
+    return true;
 }
+
+// The reduction stages the cells that start in its chunk (their labels run
+// up to L - 1 floats past it) in LDS, then folds a cell per lane from there:
+// the max, then the sum of exp2 of the shifted terms, label by label.
 __global__ __launch_bounds__(kLabelChunk) void label_reduce_kernel(KernelPlan p, const float *__restrict__ s4,
                                                                    float *__restrict__ sp) {
-    int b, i, j;
-    const bool ok = label_cell(p, &b, &i, &j);
-    const int N1 = p.n1, L = p.L;
-    const size_t cell = ((size_t)b * N1 + i) * N1 + j;
-    const bool wide = (L & 1) == 0 && ((uintptr_t)s4 & 7) == 0;   // 8-byte loads: an even count, aligned
-    const float v = label_lse2(s4 + cell * L, L, wide) * (float)LN2_D;   // (reads a valid cell even when !ok)
-    if (ok) sp[cell] = v;
+    extern __shared__ float lab_stage[];   // kLabelWaves x (kLabelRowChunk + L) floats
+    const int wave = (int)threadIdx.x >> 6, lane = (int)threadIdx.x & 63, L = p.L;
+    float *stage = lab_stage + wave * (kLabelRowChunk + L);
+    Label_row rw{};
+    int c0 = 0, c1 = 0;
+    if (label_row(p, (int)blockIdx.x * kLabelWaves + wave, &rw)) {
+        c0 = (rw.f0 + L - 1) / L;                                     // first cell starting in the chunk
+        c1 = min((rw.f0 + kLabelRowChunk - 1) / L + 1, rw.len / L);   // one past the last
+        const int a = c0 * L, e = c1 * L;                             // its floats, e - a < kLabelRowChunk + L
+        const float *src = s4 + rw.cell0 * L;
+        for (int base = a; base < e; base += 64 * kLabelPer) {
+            float v[kLabelPer];
+#pragma unroll
+            for (int k = 0; k < kLabelPer; ++k) v[k] = src[min(base + 64 * k + lane, e - 1)];
+#pragma unroll
+            for (int k = 0; k < kLabelPer; ++k)
+                if (base + 64 * k + lane < e) stage[base + 64 * k + lane - a] = v[k];
+        }
+    }
+    __syncthreads();
+    for (int c = c0 + lane; c < c1; c += 64) {
+        const float *row = stage + (c - c0) * L;
+        float m = -INFINITY;
+        for (int k = 0; k < L; ++k) m = fmax_nn(m, row[k]);
+        const float m2 = m * LOG2E_F;
+        float acc = 0.f;
+        for (int k = 0; k < L; ++k) acc += fast_exp2(row[k] * LOG2E_F - m2);
+        sp[rw.cell0 + c] = (m2 + fast_log2(acc)) * (float)LN2_D;
+    }
 }
-// label_expand_kernel runs over the contiguous label blocks of the rows: row
-// i of sentence b holds the labels of cells (i, i+1..n) back to back, and a
-// workgroup takes kLabelRowChunk consecutive floats of one row (p.lab_rows:
-// sentence, row, first float), kLabelRowChunk / kLabelChunk per thread with
-// consecutive threads on consecutive floats, so reads and writes are whole
-// cache lines; each float gathers its cell's marginal and log-sum-exp.
+
+// The expansion: the chunk's cells' marginals and log-sum-exps (log2 units)
+// are staged in LDS, a cell per lane, and each float of the chunk takes its
+// cell's pair from there.
 __global__ __launch_bounds__(kLabelChunk) void label_expand_kernel(KernelPlan p, const float *__restrict__ s4,
                                                                    const float *__restrict__ sp,
                                                                    const float *__restrict__ mu,
                                                                    float *__restrict__ marg) {
-    const int4 rc = reinterpret_cast<const int4 *>(p.lab_rows)[blockIdx.x];   // (sentence, row, first float)
-    const int N1 = p.n1, L = p.L, n = p.len[rc.x], i = rc.y;
-    const int len = (n - i) * L;                       // floats of the row's label block
-    const size_t cell0 = ((size_t)rc.x * N1 + i) * N1 + i + 1;
-    const float *src = s4 + cell0 * L;
-    float *dst = marg + cell0 * L;
+    extern __shared__ float lab_cells[];   // kLabelWaves x 2 x (kLabelRowChunk / 2 + 2) floats
+    constexpr int kCells = kLabelRowChunk / 2 + 2;   // cells a chunk can touch (L >= 2)
+    const int wave = (int)threadIdx.x >> 6, lane = (int)threadIdx.x & 63, L = p.L;
+    float *cm = lab_cells + wave * 2 * kCells, *co = cm + kCells;
+    Label_row rw{};
+    const bool have = label_row(p, (int)blockIdx.x * kLabelWaves + wave, &rw);
+    const int end = have ? min(rw.f0 + kLabelRowChunk, rw.len) : 0;   // the chunk's floats [f0, end)
+    const int c0 = have ? rw.f0 / L : 0, nc = have ? (end - 1) / L + 1 - c0 : 0;
+    const float *src = s4 + rw.cell0 * L;
+    float x[kLabelPer];
+    if (have) {
+#pragma unroll
+        for (int k = 0; k < kLabelPer; ++k) x[k] = src[min(rw.f0 + 64 * k + lane, end - 1)];
+        for (int c = lane; c < nc; c += 64) {
+            cm[c] = mu[rw.cell0 + c0 + c];
+            co[c] = sp[rw.cell0 + c0 + c] * LOG2E_F;
+        }
+    }
+    __syncthreads();
+    if (!have) return;
+    float *dst = marg + rw.cell0 * L;
     const float invL = 1.0f / (float)L;
 #pragma unroll
-    for (int u = 0; u < kLabelRowChunk / kLabelChunk; ++u) {
-        const int f = rc.z + u * kLabelChunk + (int)threadIdx.x;
-        if (f < len) {
-            const int c = div_small(f, L, invL);           // cell (i, i+1+c)
-            const float m = mu[cell0 + c], own2 = sp[cell0 + c] * LOG2E_F;
-            dst[f] = m * fast_exp2(src[f] * LOG2E_F - own2);
+    for (int k = 0; k < kLabelPer; ++k) {
+        const int f = rw.f0 + 64 * k + lane;
+        if (f < end) {
+            const int c = div_small(f, L, invL) - c0;   // cell (i, i+1+c0+c)
+            dst[f] = cm[c] * fast_exp2(x[k] * LOG2E_F - co[c]);
         }
     }
 }
@@ -1686,7 +1694,9 @@ hipError_t set_kernel_attributes(int max_lds_bytes) {
         hipError_t e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, max_lds_bytes);
         if (e != hipSuccess) return e;
     }
-    return hipSuccess;
+    // the label reduction's staging at the most labels a plan accepts
+    return hipFuncSetAttribute((const void *)label_reduce_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
+                               (int)(kLabelWaves * (kLabelRowChunk + CRF_MAX_LABELS) * sizeof(float)));
 }
 
 template <bool SPILL>
@@ -1707,14 +1717,17 @@ hipError_t launch_inside(const KernelPlan &p, const float *scores, const float *
         // per-label marginals
         float *sp = reinterpret_cast<float *>(p.ws + p.lab_sp_off);
         float *mu = reinterpret_cast<float *>(p.ws + p.lab_mu_off);
-        hipLaunchKernelGGL(label_reduce_kernel, dim3(p.n_lab_chunks), dim3(kLabelChunk), 0, stream, p, scores, sp);
+        const dim3 lab_grid((p.n_lab_rows + kLabelWaves - 1) / kLabelWaves);
+        hipLaunchKernelGGL(label_reduce_kernel, lab_grid, dim3(kLabelChunk),
+                           (size_t)kLabelWaves * (kLabelRowChunk + p.L) * sizeof(float), stream, p, scores, sp);
         if ((e = hipGetLastError()) != hipSuccess) return e;
         KernelPlan u = p;
         u.L = 1;
         if ((e = launch_inside(u, sp, grad, logZ, marg != nullptr ? mu : nullptr, stream)) != hipSuccess) return e;
         if (marg == nullptr) return hipSuccess;
-        hipLaunchKernelGGL(label_expand_kernel, dim3(p.n_lab_rows), dim3(kLabelChunk), 0, stream, p, scores, sp, mu,
-                           marg);
+        hipLaunchKernelGGL(label_expand_kernel, lab_grid, dim3(kLabelChunk),
+                           (size_t)kLabelWaves * 2 * (kLabelRowChunk / 2 + 2) * sizeof(float), stream, p, scores, sp,
+                           mu, marg);
         return hipGetLastError();
     }
     if (q.n_bundles > 0) {

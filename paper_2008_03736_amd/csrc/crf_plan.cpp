@@ -446,7 +446,7 @@ int crf_plan_create(crf_plan **out, const int32_t *lengths_host, int32_t batch, 
     }
     // Labelled plans: the label log-sum-exps and their marginals, [B][N1][N1]
     // float32 each, and the chunks of the label passes.
-    std::vector<int32_t> lab_chunks, lab_rows;
+    std::vector<int32_t> lab_rows;
     int64_t lab_sp_off = 0, lab_mu_off = 0;
     if (num_labels > 1) {
         const int64_t plane = (int64_t)batch * n1 * n1 * 4;
@@ -455,10 +455,6 @@ int crf_plan_create(crf_plan **out, const int32_t *lengths_host, int32_t batch, 
         split_cursor = lab_mu_off + plane;
         for (int32_t b = 0; b < batch; ++b) {
             const int n = lengths_host[b];
-            for (int64_t c0 = 0; c0 < crf::cell_walk_slots(n); c0 += crf::kLabelChunk) {
-                lab_chunks.push_back(b);
-                lab_chunks.push_back((int32_t)c0);
-            }
             for (int i = 0; i < n; ++i)
                 for (int64_t f0 = 0; f0 < (int64_t)(n - i) * num_labels; f0 += crf::kLabelRowChunk) {
                     lab_rows.push_back(b);
@@ -584,7 +580,6 @@ int crf_plan_create(crf_plan **out, const int32_t *lengths_host, int32_t batch, 
     };
     const std::vector<int32_t> rec_in = records(si, crf::kKindInside), rec_ck = records(sc, crf::kKindCky);
     const std::vector<int32_t> rec_mbr = mbr_fused ? records(sm, crf::kKindMbr) : std::vector<int32_t>();
-    kp.n_lab_chunks = (int32_t)(lab_chunks.size() / 2);
     kp.n_lab_rows = (int32_t)(lab_rows.size() / 4);
     kp.n_bia_tiles = (int32_t)(bia.size() / (crf::kBiaRows + crf::kBiaCols));
     kp.lab_sp_off = lab_sp_off;
@@ -623,7 +618,6 @@ int crf_plan_create(crf_plan **out, const int32_t *lengths_host, int32_t batch, 
         (e = upload(p, sc.off, &kp.cky.ws_off)) != hipSuccess ||
         (e = upload(p, rec_mix, &kp.mix)) != hipSuccess ||
         (e = upload(p, rec_mbr, &kp.mbr)) != hipSuccess ||
-        (e = upload(p, lab_chunks, &kp.lab_chunks)) != hipSuccess ||
         (e = upload(p, lab_rows, &kp.lab_rows)) != hipSuccess ||
         (e = upload(p, bia, &kp.bia_tiles)) != hipSuccess) {
         const int code = (e == hipErrorOutOfMemory) ? CRF_ENOMEM : CRF_EHIP;
