@@ -51,8 +51,14 @@ HBM_PEAK = 8.0e12               # bytes per second
 # while that source is unchanged (else null).  `profile` names the committed
 # summary that holds the counters and the scaling.
 MEASURED_TRAFFIC = {
-    "mixed": {"bytes": 76.01e6, "source_sha16": "dd5a193d65ff39e9",
+    "mixed": {"bytes": 85.09e6, "source_sha16": "fa73431a51438dba",
               "profile": "profiles/parse_kernel_mixed5000.txt"},
+    "longer": {"bytes": 36.80e6, "source_sha16": "fa73431a51438dba",
+               "profile": "profiles/parse_kernel_longer2000.txt"},
+    "labeled": {"bytes": 143.10e6, "source_sha16": "fa73431a51438dba",
+                "profile": "profiles/inside_kernel_labeled1000.txt"},
+    "stress": {"bytes": 1391.86e6, "source_sha16": "fa73431a51438dba",
+               "profile": "profiles/spill_kernels_stress64.txt"},
 }
 METRIC = "sentences/sec for inside fwd+bwd and CKY decode; % of binding roofline"
 
@@ -382,7 +388,7 @@ def main():
     hbm = wm["bytes_inside"] + (wm["bytes_cky"] if decode else 0)
     avg_s = t_step["mean"] * 1e-3
     ach = slots / avg_s
-    traffic, traffic_src = measured_traffic(batch.name) if decode else (None, None)
+    traffic, traffic_src = measured_traffic(batch.name)
     roof = {"bound": "alu",
             "kernel": "parse_kernel (inside + marginals + CKY, one launch)" if decode
             else "inside_kernel (inside + marginals)",
