@@ -336,23 +336,29 @@ __device__ __forceinline__ float span_lse(const T *a, const T *b, int kl, float 
 // two runs, sum_k a_k b_k, one FMA per term.  Terms c >= MF past K are
 // dropped by a select on the accumulator, so whatever the masked reads find
 // (other spans' scores, padding) never reaches the sum.  Two accumulators
-// halve the dependent chain.  The group's sum is returned to every lane.
+// halve the dependent chain.  The span's own score (at po, log2 units) and
+// its sentence's shift (at pd, added when `shifted`) are loaded with the
+// operands, so that a step pays one LDS round trip; the group's sum times
+// exp2(own + shift) is returned to every lane.
 template <int G, int C, int MF, typename T>
-__device__ __forceinline__ float span_dot(const T *a, const T *b, int kl) {
+__device__ __forceinline__ float span_dot(const T *a, const T *b, int kl, const T *po, const float *pd,
+                                          bool shifted) {
     float xa[C], xb[C];
 #pragma unroll
     for (int c = 0; c < C; ++c) {
         xa[c] = a[c * G];
         xb[c] = b[c * G];
     }
+    const float own = *po, sh = *pd;
     __builtin_amdgcn_sched_barrier(0);   // every load in flight before the first use
+    const float e = fast_exp2(shifted ? own + sh : own);
     float acc[2] = {0.f, 0.f};
 #pragma unroll
     for (int c = 0; c < C; ++c) {
         const float t = __builtin_fmaf(xa[c], xb[c], acc[c & 1]);
         acc[c & 1] = (c < MF || c * G < kl) ? t : acc[c & 1];
     }
-    return grp_sum<G>(acc[0] + acc[1]);
+    return e * grp_sum<G>(acc[0] + acc[1]);
 }
 
 // Bound of a stored linear-domain value: anything above it (infinity, NaN
@@ -374,12 +380,12 @@ __device__ __forceinline__ void inside_span(const Bundle_ctx<T> &bx, int w, int 
     const int rp = (int)__umul24((uint32_t)i, (uint32_t)ld);              // P row i
     const int rq = (int)__umul24((uint32_t)(i + ld + w), (uint32_t)ld);   // Q row j
     const int pa = rp + rot_alpha_p(w), qa = rq + n + 1 - w;                   // alpha(i,j) cells
-    const float own = pq[pa] + (w < n ? dsh[at.sb] : 0.f);
     float v;
     if constexpr (LIN)
-        v = fast_exp2(own) * span_dot<G, C, MF>(pq + rp + l, pq + rq + (n + 2 - w) + l, K - l);
+        v = span_dot<G, C, MF>(pq + rp + l, pq + rq + (n + 2 - w) + l, K - l, pq + pa, dsh + at.sb, w < n);
     else
-        v = span_lse<G, C, MF>(pq + rp + l, pq + rq + (n + 2 - w) + l, K - l, own);
+        v = span_lse<G, C, MF>(pq + rp + l, pq + rq + (n + 2 - w) + l, K - l,
+                               pq[pa] + (w < n ? dsh[at.sb] : 0.f));
     // An unconditional use keeps the score load in the load block, where it
     // is issued with the operand loads instead of after the reductions.
     asm volatile("" ::"v"(v));
@@ -403,12 +409,11 @@ __device__ __forceinline__ void outside_span(const Bundle_ctx<T> &bx, int v, int
     const int rp = (int)__umul24((uint32_t)(i + v), (uint32_t)ld);    // P row j
     const int rq = (int)__umul24((uint32_t)(i + ld), (uint32_t)ld);   // Q row i
     const int po = rp + n - v, qo = rq + v;                          // O'(i,j) cells
-    const float own = pq[po] + dsh[at.sb];
     float o;
     if constexpr (LIN)
-        o = fast_exp2(own) * span_dot<G, C, MF>(pq + rp + l, pq + rq + v + 1 + l, K - l);
+        o = span_dot<G, C, MF>(pq + rp + l, pq + rq + v + 1 + l, K - l, pq + po, dsh + at.sb, true);
     else
-        o = span_lse<G, C, MF>(pq + rp + l, pq + rq + v + 1 + l, K - l, own);
+        o = span_lse<G, C, MF>(pq + rp + l, pq + rq + v + 1 + l, K - l, pq[po] + dsh[at.sb]);
     asm volatile("" ::"v"(o));
     if (at.act && l == 0) {
         pq[qo] = o;
