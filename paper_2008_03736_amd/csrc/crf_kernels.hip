@@ -1552,6 +1552,22 @@ __device__ __forceinline__ int claim_next(int32_t *counter, int n_rec, int *slot
     return cur;
 }
 
+// The workspace-chart sentences of the fused pass in one launch: workgroup
+// b < inside.n_spill runs the inside sweep with the marginals of the b-th
+// such sentence, the others run CKY, so that a long sentence's two passes
+// run side by side on two CUs (their workspace charts are disjoint: the CKY
+// schedule's follow the inside schedule's).
+__global__ __launch_bounds__(kThreadsMax) void spill_parse_kernel(KernelPlan p, const float *__restrict__ scores,
+                                                                  const float *__restrict__ grad,
+                                                                  float *__restrict__ logZ, float *__restrict__ marg,
+                                                                  int32_t *__restrict__ spans,
+                                                                  float *__restrict__ best) {
+    extern __shared__ __align__(16) char smem_raw[];
+    const int b = (int)blockIdx.x;
+    if (b < p.inside.n_spill) inside_block<true, true>(p, b, nullptr, smem_raw, scores, grad, logZ, marg);
+    else cky_block<true>(p, b - p.inside.n_spill, nullptr, smem_raw, scores, spans, best);
+}
+
 // MBR decoding (Sec. 3.3) in one launch: each bundle runs the inside sweep
 // with the outside and writes the marginals, then CKY with the marginals in
 // place of the scores, in the same workgroup.  The CKY prologue reads back
@@ -1825,23 +1841,27 @@ hipError_t launch_label_spans(const KernelPlan &p, const float *label_scores, in
 hipError_t launch_parse(const KernelPlan &p, const float *scores, const float *grad, float *logZ,
                         float *marg, int32_t *spans, float *best, hipStream_t stream) {
     const Schedule &qi = p.inside, &qc = p.cky;
-    if (p.mix == nullptr || p.counter == nullptr || p.fused_grid < 1 || p.n_mix != qi.n_bundles + qc.n_bundles) {
-        hipError_t e = launch_inside(p, scores, grad, logZ, marg, stream);
-        if (e != hipSuccess) return e;
-        return launch_cky(p, scores, spans, best, stream);
-    }
-    const size_t lds = (size_t)(qi.lds_bytes > qc.lds_bytes ? qi.lds_bytes : qc.lds_bytes);
-    hipLaunchKernelGGL(parse_kernel, dim3(p.fused_grid), dim3(qi.threads), lds, stream, p,
-                       scores, grad, logZ, marg, spans, best);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    if (qi.n_spill > 0) {
-        launch_inside_k<true>(p, dim3(qi.n_spill), kThreadsMax, 0, stream, scores, grad, logZ, marg);
+    hipError_t e;
+    if (p.mix != nullptr && p.counter != nullptr && p.fused_grid >= 1 && p.n_mix == qi.n_bundles + qc.n_bundles) {
+        const size_t lds = (size_t)(qi.lds_bytes > qc.lds_bytes ? qi.lds_bytes : qc.lds_bytes);
+        hipLaunchKernelGGL(parse_kernel, dim3(p.fused_grid), dim3(qi.threads), lds, stream, p,
+                           scores, grad, logZ, marg, spans, best);
         if ((e = hipGetLastError()) != hipSuccess) return e;
+    } else {
+        // the LDS bundles of each pass as its own launch
+        if (qi.n_bundles > 0) {
+            launch_inside_k<false>(p, dim3(qi.n_bundles), qi.threads, qi.lds_bytes, stream, scores, grad, logZ, marg);
+            if ((e = hipGetLastError()) != hipSuccess) return e;
+        }
+        if (qc.n_bundles > 0) {
+            hipLaunchKernelGGL((cky_kernel<false, false>), dim3(qc.n_bundles), dim3(qc.threads), (size_t)qc.lds_bytes,
+                               stream, p, scores, spans, best, nullptr);
+            if ((e = hipGetLastError()) != hipSuccess) return e;
+        }
     }
-    if (qc.n_spill > 0) {
-        hipLaunchKernelGGL((cky_kernel<true, false>), dim3(qc.n_spill), dim3(kThreadsMax), 0, stream, p, scores, spans,
-                           best, nullptr);
+    if (qi.n_spill + qc.n_spill > 0) {
+        hipLaunchKernelGGL(spill_parse_kernel, dim3(qi.n_spill + qc.n_spill), dim3(kThreadsMax), 0, stream, p, scores,
+                           grad, logZ, marg, spans, best);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     return hipSuccess;
