@@ -31,6 +31,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "crf_internal.h"
 
 namespace crf {
@@ -62,39 +64,55 @@ __host__ __device__ inline int bia_kp(int d) { return d + 1 <= 128 ? 128 : d + 1
 // padding, ldw >= d + 4), and the masks are applied when the chunk is
 // stored: a load whose result were used at once would wait out its whole L2
 // latency there.  Rows are wave-uniform (scalar addresses).
-template <int KS>
+// P = 4 or 8: bf16 per piece (8-byte or 16-byte loads; 16-byte pieces need
+// 16-byte aligned rows, ldw a multiple of 8).
+template <int KS, int P>
 struct WChunk {
-    static constexpr int H = (8 * KS + 63) / 64;   // pieces of 4 per lane and row
-    uint2 v[kWRows][H];
+    static constexpr int H = (32 * KS / P + 63) / 64;   // pieces per lane and row
+    using V = typename std::conditional<P == 8, uint4, uint2>::type;
+    V v[kWRows][H];
 };
-template <int KS>
-__device__ __forceinline__ void load_w(WChunk<KS> &r, const uint16_t *wl, int c0, int d, int ldw, int wv, int lane) {
-    // scalar row base + one 32-bit lane offset per piece (saddr form)
-    uint32_t ko[WChunk<KS>::H];
+template <int KS, int P>
+__device__ __forceinline__ void load_w(WChunk<KS, P> &r, const uint16_t *wl, int c0, int d, int ldw, int wv,
+                                       int lane) {
+    using V = typename WChunk<KS, P>::V;
+    // scalar row base + one 32-bit lane offset per piece (saddr form); the
+    // last piece is the one holding k = d (the bias), inside the row since
+    // ldw >= d + 1 is a multiple of P
+    const int dp = d - d % P;
+    uint32_t ko[WChunk<KS, P>::H];
 #pragma unroll
-    for (int h = 0; h < WChunk<KS>::H; ++h) ko[h] = 2u * (uint32_t)min(4 * (lane + 64 * h), d);   // bytes
+    for (int h = 0; h < WChunk<KS, P>::H; ++h) ko[h] = 2u * (uint32_t)min(P * (lane + 64 * h), dp);   // bytes
 #pragma unroll
     for (int rr_ = 0; rr_ < kWRows; ++rr_) {
         const char *row = reinterpret_cast<const char *>(wl + (size_t)min(c0 + kWRows * wv + rr_, d - 1) * ldw);
 #pragma unroll
-        for (int h = 0; h < WChunk<KS>::H; ++h) r.v[rr_][h] = *reinterpret_cast<const uint2 *>(row + ko[h]);
+        for (int h = 0; h < WChunk<KS, P>::H; ++h) r.v[rr_][h] = *reinterpret_cast<const V *>(row + ko[h]);
     }
 }
-template <int KS>
-__device__ __forceinline__ void store_w(const WChunk<KS> &r, uint16_t *Ws, int lda, int c0, int d, int wv,
+// Keep the bf16 at k .. k+1 of a 32-bit word when each is <= d (k = d: the bias).
+__device__ __forceinline__ uint32_t keep2(uint32_t x, int k, int d) {
+    return x & ((k <= d ? 0x0000FFFFu : 0u) | (k + 1 <= d ? 0xFFFF0000u : 0u));
+}
+template <int KS, int P>
+__device__ __forceinline__ void store_w(const WChunk<KS, P> &r, uint16_t *Ws, int lda, int c0, int d, int wv,
                                         int lane) {
+    using V = typename WChunk<KS, P>::V;
 #pragma unroll
-    for (int h = 0; h < WChunk<KS>::H; ++h) {
-        const int k = 4 * (lane + 64 * h);
+    for (int h = 0; h < WChunk<KS, P>::H; ++h) {
+        const int k = P * (lane + 64 * h);
         if (k >= 32 * KS) continue;
-        const uint32_t mx = k < d ? 0xFFFFFFFFu : k == d ? 0x0000FFFFu : 0u, my = k < d ? 0xFFFFFFFFu : 0u;
 #pragma unroll
         for (int rr_ = 0; rr_ < kWRows; ++rr_) {
             const bool row = c0 + kWRows * wv + rr_ < d;
-            uint2 v = r.v[rr_][h];
-            v.x = row ? v.x & mx : 0u;
-            v.y = row ? v.y & my : 0u;
-            *reinterpret_cast<uint2 *>(Ws + (kWRows * wv + rr_) * lda + k) = v;
+            V v = r.v[rr_][h];
+            v.x = row ? keep2(v.x, k, d) : 0u;
+            v.y = row ? keep2(v.y, k + 2, d) : 0u;
+            if constexpr (P == 8) {
+                v.z = row ? keep2(v.z, k + 4, d) : 0u;
+                v.w = row ? keep2(v.w, k + 6, d) : 0u;
+            }
+            *reinterpret_cast<V *>(Ws + (kWRows * wv + rr_) * lda + k) = v;
         }
     }
 }
@@ -104,7 +122,8 @@ __device__ __forceinline__ void store_w(const WChunk<KS> &r, uint16_t *Ws, int l
 // (K = d + 1 padded to 128, 256 or 512), taken in groups of kGrp steps whose
 // fragments are read from LDS while the previous group is multiplied.
 constexpr int kGrp = 2;
-template <int KS>
+constexpr int kRAhead = 3;   // chunks of r^r in flight
+template <int KS, int P>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void biaffine_kernel(
     const int32_t *__restrict__ tiles, const int32_t *__restrict__ len, int N1, int d, int ldw, int L,
     const uint16_t *__restrict__ rl, const uint16_t *__restrict__ rr, const uint16_t *__restrict__ w,
@@ -129,17 +148,23 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     const uint16_t *wl = w + (size_t)l * d * ldw;
 
     // Issue the first W chunk's loads before anything waits.
-    WChunk<KS> wn;
-    load_w<KS>(wn, wl, 0, d, ldw, wv, lane);
+    WChunk<KS, P> wn;
+    load_w<KS, P>(wn, wl, 0, d, ldw, wv, lane);
 
     // r^r of the tile's columns: thread t stages column t/4, dimensions
-    // 8 (t%4) .. +7 of each chunk (two loads of four: rows are 8-byte aligned).
+    // 8 (t%4) .. +7 of each chunk (two loads of four: rows are 8-byte
+    // aligned).  These are scattered pieces of rows in HBM, whose latency is
+    // longer than a chunk's products: they are loaded kRAhead chunks ahead
+    // (rn[c % kRAhead] holds chunk c's pieces).
     const int sj = tid >> 2, sk = 8 * (tid & 3);
     const int cid = rec[kBiaRows + sj];
     const uint16_t *crow = rr + (size_t)(cid >= 0 ? cid : 0) * d;
-    uint2 rn[2];
+    uint2 rn[kRAhead][2];
 #pragma unroll
-    for (int h = 0; h < 2; ++h) rn[h] = *reinterpret_cast<const uint2 *>(crow + min(sk + 4 * h, d - 4));
+    for (int a = 0; a < kRAhead; ++a)
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+            rn[a][h] = *reinterpret_cast<const uint2 *>(crow + min(kBiaChunk * a + sk + 4 * h, d - 4));
 
     // This wave's rows [r^l_i ; 1 ; 0 ...] as MFMA fragments, in registers
     // for the whole tile: row 16 wave + lane%16, K offsets k0 + 8 (lane/16).
@@ -178,19 +203,26 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
 #pragma unroll
     for (int c = 0; c < kBiaCols / 16; ++c) acc[c] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    for (int c0 = 0; c0 < d; c0 += kBiaChunk) {
+    // (the chunk loop runs in steps of kRAhead chunks so that the slot of
+    // rn each chunk uses is a compile-time index)
+    for (int cb = 0; cb < d; cb += kRAhead * kBiaChunk) {
+#pragma unroll
+    for (int a = 0; a < kRAhead; ++a) {
+        const int c0 = cb + a * kBiaChunk;
+        if (c0 >= d) break;
         __syncthreads();   // the previous chunk's readers are done
-        store_w<KS>(wn, Ws, lda, c0, d, wv, lane);
+        store_w<KS, P>(wn, Ws, lda, c0, d, wv, lane);
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
-            const uint2 v = cid >= 0 && c0 + sk + 4 * h < d ? rn[h] : make_uint2(0u, 0u);
+            const uint2 v = cid >= 0 && c0 + sk + 4 * h < d ? rn[a][h] : make_uint2(0u, 0u);
             *reinterpret_cast<uint2 *>(Rs + sj * kUStride + sk + 4 * h) = v;
         }
-        if (c0 + kBiaChunk < d) {   // the next chunk's loads fly during this one's products
-            load_w<KS>(wn, wl, c0 + kBiaChunk, d, ldw, wv, lane);
+        if (c0 + kBiaChunk < d)   // the next chunk's W flies during this one's products
+            load_w<KS, P>(wn, wl, c0 + kBiaChunk, d, ldw, wv, lane);
+        if (c0 + kRAhead * kBiaChunk < d) {   // and r^r kRAhead chunks ahead
 #pragma unroll
             for (int h = 0; h < 2; ++h)
-                rn[h] = *reinterpret_cast<const uint2 *>(crow + min(c0 + kBiaChunk + sk + 4 * h, d - 4));
+                rn[a][h] = *reinterpret_cast<const uint2 *>(crow + min(c0 + kRAhead * kBiaChunk + sk + 4 * h, d - 4));
         }
         __syncthreads();
 
@@ -260,6 +292,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
                 acc[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al[k], br[k][c], acc[c], 0, 0, 0);
             }
     }
+    }
 
     // The valid cells: row and column of one sentence, i < j <= n_b.
 #pragma unroll
@@ -277,11 +310,12 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
 }  // namespace
 
 hipError_t set_biaffine_attributes() {
-    const void *fns[] = {(const void *)biaffine_kernel<4>, (const void *)biaffine_kernel<8>,
-                         (const void *)biaffine_kernel<16>};
+    const void *fns[] = {(const void *)biaffine_kernel<4, 4>,  (const void *)biaffine_kernel<8, 4>,
+                         (const void *)biaffine_kernel<16, 4>, (const void *)biaffine_kernel<4, 8>,
+                         (const void *)biaffine_kernel<8, 8>,  (const void *)biaffine_kernel<16, 8>};
     const int lds[] = {(int)biaffine_lds_bytes(127), (int)biaffine_lds_bytes(255), (int)biaffine_lds_bytes(kBiaMaxD)};
-    for (int k = 0; k < 3; ++k) {
-        const hipError_t e = hipFuncSetAttribute(fns[k], hipFuncAttributeMaxDynamicSharedMemorySize, lds[k]);
+    for (int k = 0; k < 6; ++k) {
+        const hipError_t e = hipFuncSetAttribute(fns[k], hipFuncAttributeMaxDynamicSharedMemorySize, lds[k % 3]);
         if (e != hipSuccess) return e;
     }
     return hipSuccess;
@@ -293,18 +327,32 @@ int64_t biaffine_lds_bytes(int d) {
            4 * (2 * (kBiaRows + kBiaCols) + kBiaRows);
 }
 
+template <int P>
+static void launch_biaffine_p(const KernelPlan &p, dim3 grid, size_t lds, hipStream_t stream, const uint16_t *rl,
+                              const uint16_t *rr, const uint16_t *w, int d, int ldw, int L, float *scores) {
+    const dim3 block(256);
+    const int kp = bia_kp(d);
+    if (kp == 128)
+        hipLaunchKernelGGL((biaffine_kernel<4, P>), grid, block, lds, stream, p.bia_tiles, p.len, p.n1, d, ldw, L, rl,
+                           rr, w, scores);
+    else if (kp == 256)
+        hipLaunchKernelGGL((biaffine_kernel<8, P>), grid, block, lds, stream, p.bia_tiles, p.len, p.n1, d, ldw, L, rl,
+                           rr, w, scores);
+    else
+        hipLaunchKernelGGL((biaffine_kernel<16, P>), grid, block, lds, stream, p.bia_tiles, p.len, p.n1, d, ldw, L, rl,
+                           rr, w, scores);
+}
+
 hipError_t launch_biaffine(const KernelPlan &p, const uint16_t *rl, const uint16_t *rr, const uint16_t *w, int d,
                            int ldw, int L, float *scores, hipStream_t stream) {
     if (p.n_bia_tiles < 1) return hipSuccess;
     const size_t lds = (size_t)biaffine_lds_bytes(d);
-    const dim3 grid(p.n_bia_tiles, L), block(256);
-    const int kp = bia_kp(d);
-    if (kp == 128)
-        hipLaunchKernelGGL(biaffine_kernel<4>, grid, block, lds, stream, p.bia_tiles, p.len, p.n1, d, ldw, L, rl, rr, w, scores);
-    else if (kp == 256)
-        hipLaunchKernelGGL(biaffine_kernel<8>, grid, block, lds, stream, p.bia_tiles, p.len, p.n1, d, ldw, L, rl, rr, w, scores);
+    const dim3 grid(p.n_bia_tiles, L);
+    // 16-byte W pieces when every row starts 16-byte aligned
+    if (ldw % 8 == 0 && ((uintptr_t)w & 15) == 0)
+        launch_biaffine_p<8>(p, grid, lds, stream, rl, rr, w, d, ldw, L, scores);
     else
-        hipLaunchKernelGGL(biaffine_kernel<16>, grid, block, lds, stream, p.bia_tiles, p.len, p.n1, d, ldw, L, rl, rr, w, scores);
+        launch_biaffine_p<4>(p, grid, lds, stream, rl, rr, w, d, ldw, L, scores);
     return hipGetLastError();
 }
 
