@@ -4,7 +4,9 @@
 //   P n_mix fused_grid lds_inside lds_cky half_cu
 //   W spill cky_spill split_ws workspace_users workspace_bytes fused_queue
 //   R kind n count split_ws strict ld cs e bytes id...
-// one R line per record of the fused queue, in queue order.  Arguments: a file
+// one R line per record of the fused queue, in queue order; M lines for the
+// MBR bundles, I lines for labelled plans' inside bundles, T lines for the
+// biaffine scorer's tiles.  Arguments: a file
 // of sentence lengths, and optionally the number of labels.
 #include <cstdio>
 #include <cstdlib>
@@ -156,6 +158,14 @@ int main(int argc, char **argv) {
         const int32_t *r = kp.inside.recs + (size_t)b * kp.rec_stride;
         std::printf("I %d %d", r[crf::kRecN], r[crf::kRecCount]);
         for (int t = 0; t < r[crf::kRecCount]; ++t) std::printf(" %d", r[crf::kRecHeader + t]);
+        std::printf("\n");
+    }
+    // Biaffine scorer tiles, as
+    //   T n1 row_id x kBiaRows col_id x kBiaCols   (b n1 + fence post, or -1)
+    for (int t = 0; t < kp.n_bia_tiles; ++t) {
+        const int32_t *r = kp.bia_tiles + (size_t)t * (crf::kBiaRows + crf::kBiaCols);
+        std::printf("T %d", n1);
+        for (int k = 0; k < crf::kBiaRows + crf::kBiaCols; ++k) std::printf(" %d", r[k]);
         std::printf("\n");
     }
     crf_plan_destroy(p);

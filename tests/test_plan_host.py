@@ -55,6 +55,10 @@ def plan_of(harness, tmp_path, lengths, labels=None):
         elif t[0] == "I":
             v = list(map(int, t[1:]))
             recs.append(dict(kind=1, n=v[0], count=v[1], ids=v[2:]))
+        elif t[0] == "T":
+            v = list(map(int, t[1:]))
+            head["n1"] = v[0]
+            head.setdefault("tiles", []).append(v[1:])
         elif t[0] == "M":
             v = list(map(int, t[1:]))
             head.setdefault("mbr", []).append(dict(n=v[0], count=v[1], split_ws=v[2], inside_strict=v[3],
@@ -182,3 +186,56 @@ def test_mbr_bundles(harness, tmp_path, name):
 def test_mbr_not_fused_when_all_in_workspace(harness, tmp_path):
     head, _ = plan_of(harness, tmp_path, [200, 150])
     assert "mbr" not in head
+
+
+def check_tiles(head, lengths, rows=64):
+    """The scorer's tiles cover every valid cell (i < j <= n_b) of every
+    sentence exactly once; a tile's rows and columns are fence posts of the
+    batch (or -1); a tile that packs whole sentences uses its fence posts as
+    both its rows and its columns."""
+    lengths = np.asarray(lengths, np.int64)
+    n1 = head["n1"]
+    t = np.asarray(head["tiles"], np.int64)
+    assert t.shape[1] == 2 * rows
+    r, c = t[:, :rows], t[:, rows:]
+    for ids in (r, c):
+        v = ids[ids >= 0]
+        assert np.all(v % n1 <= lengths[v // n1]), "a tile names a fence post past its sentence"
+    rr = np.repeat(r[:, :, None], rows, axis=2)
+    cc = np.repeat(c[:, None, :], rows, axis=1)
+    ok = (rr >= 0) & (cc >= 0) & (rr // n1 == cc // n1) & (rr % n1 < cc % n1)
+    cells = rr[ok] * n1 + cc[ok] % n1                       # (b n1 + i) n1 + j
+    got = np.bincount(cells, minlength=len(lengths) * n1 * n1)
+    b, i, j = np.unravel_index(np.arange(len(lengths) * n1 * n1), (len(lengths), n1, n1))
+    want = ((i < j) & (j <= lengths[b])).astype(np.int64)
+    assert np.array_equal(got, want), "valid cells covered exactly once, nothing else"
+    # a sentence of up to rows - 1 words sits whole in one tile, whose rows
+    # are also its columns
+    short = np.flatnonzero(lengths + 1 <= rows)
+    for k in range(len(t)):
+        row = r[k][r[k] >= 0]
+        for b in np.unique(row // n1):
+            if lengths[b] + 1 <= rows:
+                assert np.array_equal(np.sort(row[row // n1 == b] % n1), np.arange(lengths[b] + 1)), (k, b)
+                assert np.array_equal(r[k], c[k])
+    seen = np.unique(r[r >= 0] // n1)
+    assert np.all(np.isin(short, seen))
+    tile_idx = np.arange(len(t))[:, None].repeat(rows, 1)
+    pairs = np.unique(np.stack([tile_idx[r >= 0], r[r >= 0] // n1], -1), axis=0)   # (tile, sentence)
+    tiles_of = np.bincount(pairs[:, 1], minlength=len(lengths))
+    assert np.all(tiles_of[short] == 1), "a short sentence in more than one tile"
+
+
+@pytest.mark.parametrize("name", ["tiny", "mixed", "longer", "stress"])
+def test_biaffine_tiles_cover_every_cell_once(harness, tmp_path, name):
+    lengths = W.make(name, 0).lengths
+    head, _ = plan_of(harness, tmp_path, lengths)
+    check_tiles(head, lengths)
+
+
+def test_biaffine_tiles_edge_lengths(harness, tmp_path):
+    # one word, exactly a tile's rows (63 words: 64 fence posts), one past it,
+    # two and three blocks, and many short sentences that fill tiles unevenly
+    lengths = [1, 63, 64, 127, 128, 129, 200, 2, 3, 5, 7, 11, 13] + [4] * 40
+    head, _ = plan_of(harness, tmp_path, lengths)
+    check_tiles(head, lengths)
