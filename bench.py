@@ -223,8 +223,8 @@ def main():
                          "that rocprofv3 summaries under profiles/ are taken on")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); "
-              "sentences are independent and would be sharded by sentence, see DESIGN.md",
+        print(f"bench.py: runs on one GPU only (asked for --gpus {args.gpus}); sentences are "
+              "independent, so more GPUs would each take a share of the batch by sentence",
               file=sys.stderr)
         sys.exit(2)
     if args.ceilings:
