@@ -84,3 +84,11 @@ def test_biaffine_mixed_batch_sample(torch):
     idx = np.unique(np.concatenate([order[:6], order[-6:], np.arange(0, m.B, 211)]))
     sub = W.BiaffineInputs(inp.lengths[idx], inp.rl[idx], inp.rr[idx], inp.wt)
     check(got[idx], sub)
+
+
+@pytest.mark.parametrize("d,ldw,labels", [(100, 112, 3), (64, 68, 2), (500, 520, 1), (12, 20, 5)])
+def test_biaffine_row_strides(torch, d, ldw, labels):
+    # weight rows wider than d + 1 (NaN padding never read), on both load
+    # widths: 16-byte pieces when ldw is a multiple of 8, 8-byte ones else
+    inp = W.biaffine_inputs([1, 9, 40, 66], d, labels=labels, seed=ldw)
+    check(run(torch, inp, ldw=ldw), inp)
