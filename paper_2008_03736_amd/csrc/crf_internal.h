@@ -283,6 +283,11 @@ static_assert(kBiaRows == kBiaCols, "packed tiles use their fence posts as both 
 // Threads per workgroup of the label passes, and floats of a row's label
 // block per workgroup.
 constexpr int kLabelChunk = 256;
+// Labelled bundles of sentences of up to this many words read their label
+// scores and write their per-label marginals themselves (in the inside
+// kernel's prologue and epilogue); longer sentences, whose bundles set the
+// launch's critical path, leave both to the chip-wide label passes.
+constexpr int kLabInBundleMaxN = 48;
 constexpr int kLabelRowChunk = 1024;
 
 // Longest sentence whose CKY chart could sit in one CU's LDS (160 KiB):
@@ -311,7 +316,10 @@ struct Bundle {
 // count sentence ids -- so that its sentence ids arrive with its shape, one
 // memory round trip before its scores, and the workgroup computes none of it.
 constexpr int kRecHeader = 12;
-enum RecField { kRecN = 0, kRecCount, kRecSplitWs, kRecKind, kRecE, kRecLd, kRecCs, kRecMagic, kRecE2, kRecLd2, kRecCs2 };
+enum RecField {
+    kRecN = 0, kRecCount, kRecSplitWs, kRecKind, kRecE, kRecLd, kRecCs, kRecMagic, kRecE2, kRecLd2, kRecCs2,
+    kRecLab   // labelled inside bundles: 1 when the bundle reads and writes its own label scores
+};
 enum RecKind { kKindCky = 0, kKindInside = 1, kKindMbr = 2 };
 // g / S by multiply-high: 2^32 / S + 1, exact for g < 2^18, 2 <= S <= 1024;
 // 0 for S = 1 (the caller takes g itself).
@@ -345,9 +353,10 @@ struct KernelPlan {
     const int32_t *mbr;
     int32_t n_mbr, mbr_grid, mbr_lds;
     int32_t *counter;            // the fused kernels' bundle claims; zero between launches
-    // labelled plans: chunks of kLabelRowChunk floats of the rows' label
-    // blocks, (sentence, row, first float, 0), and the workspace offsets of
-    // the label log-sum-exps and of their marginals ([B][N1][N1] float32 each)
+    // labelled plans: chunks of kLabelRowChunk floats of the label blocks of
+    // the rows of the sentences whose label passes run chip-wide, (sentence,
+    // row, first float, 0), and the workspace offsets of their label
+    // log-sum-exps and marginals ([B][N1][N1] float32 each)
     const int32_t *lab_rows;
     int32_t n_lab_rows;
     // biaffine scorer tiles: kBiaRows row ids then kBiaCols column ids each
@@ -355,6 +364,12 @@ struct KernelPlan {
     const int32_t *bia_tiles;
     int32_t n_bia_tiles;
     int64_t lab_sp_off, lab_mu_off;
+    // set per labelled inside launch: the label scores [B][N1][N1][L], the
+    // per-label marginals out (NULL for the forward pass) and L, for the
+    // bundles that do their own label I/O (kRecLab)
+    const float *lab_s4;
+    float *lab_out;
+    int32_t lab_L;
     int32_t rec_stride;          // ints per record: kRecHeader + the largest bundle
     int32_t B, n1, L;
 };

@@ -779,6 +779,20 @@ __device__ __forceinline__ void for_cells_loaded(int nb, int n, AD &&addr, LD &&
     }
 }
 
+// Log-sum-exp (log2 units) of the L label scores of one span at s: blocks
+// of 32 labels, each block's loads issued together (clamped to the last
+// label, so every load is in bounds) and its terms kept in registers;
+// label_block folds one block into the running max m and sum acc.
+__device__ __forceinline__ void label_block(const float (&v)[32], int q0, int L, float &m, float &acc) {
+    float mb = -INFINITY;
+#pragma unroll
+    for (int k = 0; k < 32; ++k) mb = q0 + k < L ? fmax_nn(mb, v[k]) : mb;
+    const float mn = fmax_nn(m, mb * LOG2E_F);
+    acc *= fast_exp2(m - mn);   // (0 * exp2(-inf) = 0 on the first block)
+#pragma unroll
+    for (int k = 0; k < 32; ++k) acc += q0 + k < L ? fast_exp2(v[k] * LOG2E_F - mn) : 0.f;
+    m = mn;
+}
 // The first 32 labels of a span into v (clamped to the last label), with
 // 8-byte loads when `wide`: an even count on an 8-byte aligned score tensor
 // (every span's offset is then a multiple of 2 floats).  The values are the
@@ -798,6 +812,33 @@ __device__ __forceinline__ void label_load32(const float *s, int L, bool wide, f
         for (int k = 0; k < 32; ++k) v[k] = s[min(k, L - 1)];
     }
 }
+__device__ __forceinline__ float label_lse2(const float *s, int L, bool wide) {
+    float m = -INFINITY, acc = 0.f;
+    for (int q0 = 0; q0 < L; q0 += 32) {
+        float v[32];
+        if (q0 == 0) {
+            label_load32(s, L, wide, v);
+        } else {
+#pragma unroll
+            for (int k = 0; k < 32; ++k) v[k] = s[min(q0 + k, L - 1)];
+        }
+        label_block(v, q0, L, m, acc);
+    }
+    return m + fast_log2(acc);
+}
+// o[q] = mu exp2(s[q] log2e - lse2) for the L labels of one span, in blocks
+// of 32 as above.
+__device__ __forceinline__ void label_marginals(const float *s, int L, float mu, float lse2, float *o) {
+    for (int q0 = 0; q0 < L; q0 += 32) {
+        float v[32];
+#pragma unroll
+        for (int k = 0; k < 32; ++k) v[k] = s[min(q0 + k, L - 1)];
+#pragma unroll
+        for (int k = 0; k < 32; ++k)
+            if (q0 + k < L) o[q0 + k] = mu * fast_exp2(v[k] * LOG2E_F - lse2);
+    }
+}
+
 // Max over the L labels of one span at s (an exact float32 max), for the
 // one-stage labelled CKY: blocks of 32 labels, each block's loads issued
 // together (clamped to the last label).
@@ -957,7 +998,23 @@ __device__ __forceinline__ bool inside_block_impl(const KernelPlan &p, int block
             if constexpr (REV) P[j * ld + n - w] = s2;
         }
     };
-    for_cells_loaded<8>(nb, n, score_at, load_score, put_score);
+    // A labelled bundle that does its own label I/O (kRecLab) reads each
+    // span's labels and takes their log-sum-exp (Sec. 4.2, Eq.
+    // tree-label-score: the span's score in the one-stage Z); the others
+    // read the [B][N1][N1] scores (the label passes' log-sum-exps for a
+    // labelled plan).
+    const bool lab = !SPILL && p.lab_L > 1 && rec[kRecLab] != 0;   // (uniform)
+    const int L = p.lab_L;
+    const size_t lab_sent = (size_t)N1 * N1 * (size_t)L;
+    auto lab_at = [&](int sb, int i, int j) -> const float * {
+        return p.lab_s4 + (size_t)sid[sb] * lab_sent + ((size_t)i * N1 + (size_t)j) * (size_t)L;
+    };
+    const bool wide_in = (L & 1) == 0 && ((uintptr_t)p.lab_s4 & 7) == 0;   // 8-byte label loads
+    auto lab_lse = [&](const float *q) -> float { return label_lse2(q, L, wide_in) * (float)LN2_D; };
+    if (lab)
+        for_cells_loaded<1>(nb, n, lab_at, lab_lse, put_score);
+    else
+        for_cells_loaded<8>(nb, n, score_at, load_score, put_score);
     __syncthreads();
     // Forced-span sums, a lane group per sentence, fixed order (deterministic).
     // The linear domain also seeds each sentence's shift d from its scores:
@@ -1071,6 +1128,58 @@ __device__ __forceinline__ bool inside_block_impl(const KernelPlan &p, int block
             if (__builtin_bit_cast(int, P[j * ld + n - w]) == kGoldMark) mu -= gv[sb];
         return mu;
     };
+    if (lab) {
+        // per-label marginals mu(i,j) exp(s(i,j,l) - s'(i,j)).  Up to 32
+        // labels: one load of a span's labels serves its log-sum-exp (the
+        // prologue's arithmetic, so the same own score as the chart's) and
+        // its outputs, two spans per thread at a time.
+        float *const out0 = p.lab_out;
+        const bool wide_out = wide_in && ((uintptr_t)out0 & 7) == 0;
+        if (L <= 32) {
+            const Cell_walk cw(nb, n);
+            for (int c0 = tid; c0 < cw.total; c0 += NT * 2) {
+                Cell e[2];
+                const float *q[2];
+                float v[2][32];
+#pragma unroll
+                for (int u = 0; u < 2; ++u) {
+                    e[u] = cw.at(c0 + u * NT);
+                    q[u] = lab_at(e[u].sb, e[u].i, e[u].j);
+                }
+#pragma unroll
+                for (int u = 0; u < 2; ++u) label_load32(q[u], L, wide_in, v[u]);
+                __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                for (int u = 0; u < 2; ++u) {
+                    float m = -INFINITY, acc = 0.f;
+                    label_block(v[u], 0, L, m, acc);
+                    const float own2 = ((m + fast_log2(acc)) * (float)LN2_D) * LOG2E_F;   // as the chart holds it
+                    const float mu = span_mu(e[u].sb, e[u].i, e[u].j, own2);
+                    if (e[u].ok) {
+                        float *o = out0 + (q[u] - p.lab_s4);
+                        if (wide_out) {   // 8-byte stores
+                            float2 *o2 = reinterpret_cast<float2 *>(o);
+#pragma unroll
+                            for (int k = 0; k < 16; ++k)
+                                if (2 * k < L)
+                                    o2[k] = make_float2(mu * fast_exp2(v[u][2 * k] * LOG2E_F - own2),
+                                                        mu * fast_exp2(v[u][2 * k + 1] * LOG2E_F - own2));
+                        } else {
+#pragma unroll
+                            for (int k = 0; k < 32; ++k)
+                                if (k < L) o[k] = mu * fast_exp2(v[u][k] * LOG2E_F - own2);
+                        }
+                    }
+                }
+            }
+        } else {
+            for_cells_loaded<1>(nb, n, lab_at, lab_lse, [&](int sb, int i, int j, float s) {
+                const float *q = lab_at(sb, i, j);
+                label_marginals(q, L, span_mu(sb, i, j, s * LOG2E_F), s * LOG2E_F, out0 + (q - p.lab_s4));
+            });
+        }
+        return true;
+    }
     for_cells_loaded<8>(nb, n, score_at, load_score, [&](int sb, int i, int j, float s) {
         marg[(size_t)sid[sb] * sent_stride + (size_t)i * row_stride + j] = span_mu(sb, i, j, s * LOG2E_F);
     });
@@ -1733,19 +1842,26 @@ hipError_t launch_inside(const KernelPlan &p, const float *scores, const float *
     const Schedule &q = p.inside;
     hipError_t e;
     if (p.L > 1) {
-        // labelled: label log-sum-exps into the workspace, the unlabelled
-        // sweeps on them (their marginals into the workspace too), then the
+        // labelled: the label log-sum-exps of the sentences whose label
+        // passes run chip-wide into the workspace, the sweeps (on those, and
+        // on their own label scores for the bundles marked kRecLab; the
+        // former's marginals into the workspace too), then those sentences'
         // per-label marginals
         float *sp = reinterpret_cast<float *>(p.ws + p.lab_sp_off);
         float *mu = reinterpret_cast<float *>(p.ws + p.lab_mu_off);
         const dim3 lab_grid((p.n_lab_rows + kLabelWaves - 1) / kLabelWaves);
-        hipLaunchKernelGGL(label_reduce_kernel, lab_grid, dim3(kLabelChunk),
-                           (size_t)kLabelWaves * (kLabelRowChunk + p.L) * sizeof(float), stream, p, scores, sp);
-        if ((e = hipGetLastError()) != hipSuccess) return e;
+        if (p.n_lab_rows > 0) {
+            hipLaunchKernelGGL(label_reduce_kernel, lab_grid, dim3(kLabelChunk),
+                               (size_t)kLabelWaves * (kLabelRowChunk + p.L) * sizeof(float), stream, p, scores, sp);
+            if ((e = hipGetLastError()) != hipSuccess) return e;
+        }
         KernelPlan u = p;
         u.L = 1;
+        u.lab_s4 = scores;
+        u.lab_out = marg;
+        u.lab_L = p.L;
         if ((e = launch_inside(u, sp, grad, logZ, marg != nullptr ? mu : nullptr, stream)) != hipSuccess) return e;
-        if (marg == nullptr) return hipSuccess;
+        if (marg == nullptr || p.n_lab_rows < 1) return hipSuccess;
         hipLaunchKernelGGL(label_expand_kernel, lab_grid, dim3(kLabelChunk),
                            (size_t)kLabelWaves * 2 * (kLabelRowChunk / 2 + 2) * sizeof(float), stream, p, scores, sp,
                            mu, marg);

@@ -449,12 +449,15 @@ int crf_plan_create(crf_plan **out, const int32_t *lengths_host, int32_t batch, 
     std::vector<int32_t> lab_rows;
     int64_t lab_sp_off = 0, lab_mu_off = 0;
     if (num_labels > 1) {
+        std::vector<char> in_ws(batch, 0);   // inside charts in the workspace: never in a bundle
+        for (int32_t b : si.spill) in_ws[b] = 1;
         const int64_t plane = (int64_t)batch * n1 * n1 * 4;
         lab_sp_off = (split_cursor + 255) / 256 * 256;
         lab_mu_off = (lab_sp_off + plane + 255) / 256 * 256;
         split_cursor = lab_mu_off + plane;
         for (int32_t b = 0; b < batch; ++b) {
             const int n = lengths_host[b];
+            if (n <= crf::kLabInBundleMaxN && !in_ws[b]) continue;   // its bundle does its own label I/O
             for (int i = 0; i < n; ++i)
                 for (int64_t f0 = 0; f0 < (int64_t)(n - i) * num_labels; f0 += crf::kLabelRowChunk) {
                     lab_rows.push_back(b);
@@ -567,6 +570,7 @@ int crf_plan_create(crf_plan **out, const int32_t *lengths_host, int32_t batch, 
             q[crf::kRecCount] = bd.count;
             q[crf::kRecSplitWs] = kind == crf::kKindInside ? -1 : bd.split_ws;
             q[crf::kRecKind] = kind;
+            q[crf::kRecLab] = kind == crf::kKindInside && num_labels > 1 && bd.n <= crf::kLabInBundleMaxN;
             if (kind == crf::kKindCky) {
                 put_cky_layout(q, bd.n, bd.count, 0);
             } else {

@@ -160,6 +160,20 @@ def test_labeled_many_labels(torch, labels):
     print(f"L = {labels}: max |marginal error| {worst:.2e}")
 
 
+@pytest.mark.parametrize("spill", [False, True])
+def test_labeled_in_bundle_boundary(torch, spill):
+    # sentences on both sides of the longest length whose bundles read their
+    # label scores and write their per-label marginals themselves (48 words),
+    # and the same batch with every chart in the workspace, where the label
+    # work always runs chip-wide; NaN-filled outputs show any cell left unwritten
+    b = W.custom([1, 3, 47, 48, 49, 50, 48, 2], seed=77, sd=1.0, labels=5)
+    flags = B.CRF_FORCE_SPILL if spill else 0
+    out = gpu_run(torch, b, flags=flags, decode=False, marg_fill=float("nan"))
+    assert out["info"]["spill_count"] == (b.B if spill else 0)
+    worst = check_labeled_chunks(out, b, chunk=b.B)
+    print(f"labelled around the in-bundle cutoff (spill={spill}): max |marginal error| {worst:.2e}")
+
+
 # --------------------------------------------------------------------------
 # Edge cases
 
@@ -248,8 +262,9 @@ def test_labeled_alignment(torch, offset, labels):
     # labelled scores and marginals 8-byte aligned (offset 0) or only 4-byte
     # aligned (offset 1 float), with an even and an odd label count: the
     # 8-byte label accesses are taken only for even counts on aligned
-    # tensors, and every case gives the same results
-    b = W.custom([5, 12, 30, 31], seed=41 + labels, sd=1.0, labels=labels)
+    # tensors, and every case gives the same results, both in the bundles
+    # that do their own label work and in the chip-wide label passes
+    b = W.custom([5, 12, 30, 31, 49, 60], seed=41 + labels, sd=1.0, labels=labels)
     dev = torch.device("cuda", 0)
     size = b.scores.size
     s = torch.empty(size + 1, dtype=torch.float32, device=dev)[offset:offset + size].view(b.scores.shape)
