@@ -47,17 +47,18 @@ PEAK_SLOTS = 256 * 64 * 2.4e9   # VALU lane-slots per second
 HBM_PEAK = 8.0e12               # bytes per second
 # HBM bytes per launch of the timed kernel from rocprofv3 FETCH_SIZE /
 # WRITE_SIZE, each scaled by the same counter on a plain copy of known size,
-# keyed by workload and by the kernel source they were taken on: reported only
-# while that source is unchanged (else null).  `profile` names the committed
+# keyed by workload and by the sources they were taken on (source_sha16:
+# kernels, shared constants, plan): reported only while those are unchanged
+# (else null).  `profile` names the committed
 # summary that holds the counters and the scaling.
 MEASURED_TRAFFIC = {
-    "mixed": {"bytes": 85.32e6, "source_sha16": "bf51439bd164cf54",
+    "mixed": {"bytes": 85.59e6, "source_sha16": "c958cf87b9655ef7",
               "profile": "profiles/parse_kernel_mixed5000.txt"},
-    "longer": {"bytes": 36.69e6, "source_sha16": "bf51439bd164cf54",
+    "longer": {"bytes": 36.75e6, "source_sha16": "c958cf87b9655ef7",
                "profile": "profiles/parse_kernel_longer2000.txt"},
-    "labeled": {"bytes": 143.11e6, "source_sha16": "bf51439bd164cf54",
+    "labeled": {"bytes": 119.09e6, "source_sha16": "c958cf87b9655ef7",
                 "profile": "profiles/inside_kernel_labeled1000.txt"},
-    "stress": {"bytes": 4910.45e6, "source_sha16": "bf51439bd164cf54",
+    "stress": {"bytes": 4906.55e6, "source_sha16": "c958cf87b9655ef7",
                "profile": "profiles/spill_kernels_stress64.txt"},
 }
 METRIC = "sentences/sec for inside fwd+bwd and CKY decode; % of binding roofline"
@@ -81,11 +82,15 @@ def work_model(lengths, labels=1, trans_slots=4):
 
 
 def source_sha16():
+    """Hash of the sources that decide what the CRF kernels do: the kernels,
+    the shared constants and records, and the plan that lays out the launches."""
     import hashlib
 
-    src = os.path.join(ROOT, "paper_2008_03736_amd", "csrc", "crf_kernels.hip")
-    with open(src, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    h = hashlib.sha256()
+    for name in ("crf_kernels.hip", "crf_internal.h", "crf_plan.cpp"):
+        with open(os.path.join(ROOT, "paper_2008_03736_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
 
 
 def measured_traffic(workload):

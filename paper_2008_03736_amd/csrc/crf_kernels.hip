@@ -779,62 +779,65 @@ __device__ __forceinline__ void for_cells_loaded(int nb, int n, AD &&addr, LD &&
     }
 }
 
-// Log-sum-exp (log2 units) of the L label scores of one span at s: blocks
-// of 32 labels, each block's loads issued together (clamped to the last
-// label, so every load is in bounds) and its terms kept in registers;
-// label_block folds one block into the running max m and sum acc.
-__device__ __forceinline__ void label_block(const float (&v)[32], int q0, int L, float &m, float &acc) {
+// In-bundle label work takes a span's labels kLabBlk at a time: each block's
+// loads issued together (clamped to the last label, so every load is in
+// bounds) and its terms kept in registers.  Sixteen fits in what the inside
+// kernels have to spare at their prologue; 32 made them spill.
+constexpr int kLabBlk = 16;
+// Folds labels q0 .. q0+kLabBlk-1 of a span (v) into the running max m
+// (log2 units) and sum acc of its log-sum-exp.
+__device__ __forceinline__ void label_block(const float *v, int q0, int L, float &m, float &acc) {
     float mb = -INFINITY;
 #pragma unroll
-    for (int k = 0; k < 32; ++k) mb = q0 + k < L ? fmax_nn(mb, v[k]) : mb;
+    for (int k = 0; k < kLabBlk; ++k) mb = q0 + k < L ? fmax_nn(mb, v[k]) : mb;
     const float mn = fmax_nn(m, mb * LOG2E_F);
     acc *= fast_exp2(m - mn);   // (0 * exp2(-inf) = 0 on the first block)
 #pragma unroll
-    for (int k = 0; k < 32; ++k) acc += q0 + k < L ? fast_exp2(v[k] * LOG2E_F - mn) : 0.f;
+    for (int k = 0; k < kLabBlk; ++k) acc += q0 + k < L ? fast_exp2(v[k] * LOG2E_F - mn) : 0.f;
     m = mn;
 }
-// The first 32 labels of a span into v (clamped to the last label), with
-// 8-byte loads when `wide`: an even count on an 8-byte aligned score tensor
-// (every span's offset is then a multiple of 2 floats).  The values are the
-// same either way.
-__device__ __forceinline__ void label_load32(const float *s, int L, bool wide, float (&v)[32]) {
+// Labels q0 .. q0+kLabBlk-1 of a span into v (clamped to the last label),
+// with 8-byte loads when `wide`: an even count on an 8-byte aligned score
+// tensor (every span's offset is then a multiple of 2 floats; q0 is even).
+// The values at valid labels are the same either way.
+__device__ __forceinline__ void label_load_blk(const float *s, int q0, int L, bool wide, float *v) {
     if (wide) {
         const float2 *s2 = reinterpret_cast<const float2 *>(s);
         const int last = L / 2 - 1;
 #pragma unroll
-        for (int k = 0; k < 16; ++k) {
-            const float2 x = s2[min(k, last)];
+        for (int k = 0; k < kLabBlk / 2; ++k) {
+            const float2 x = s2[min(q0 / 2 + k, last)];
             v[2 * k] = x.x;
             v[2 * k + 1] = x.y;
         }
     } else {
 #pragma unroll
-        for (int k = 0; k < 32; ++k) v[k] = s[min(k, L - 1)];
+        for (int k = 0; k < kLabBlk; ++k) v[k] = s[min(q0 + k, L - 1)];
     }
 }
+// The first 32 labels of a span into v (clamped), 8-byte loads when `wide`.
+__device__ __forceinline__ void label_load32(const float *s, int L, bool wide, float (&v)[32]) {
+    label_load_blk(s, 0, L, wide, v);
+    label_load_blk(s, kLabBlk, L, wide, v + kLabBlk);
+}
+// Log-sum-exp (log2 units) of the L label scores of one span at s.
 __device__ __forceinline__ float label_lse2(const float *s, int L, bool wide) {
     float m = -INFINITY, acc = 0.f;
-    for (int q0 = 0; q0 < L; q0 += 32) {
-        float v[32];
-        if (q0 == 0) {
-            label_load32(s, L, wide, v);
-        } else {
-#pragma unroll
-            for (int k = 0; k < 32; ++k) v[k] = s[min(q0 + k, L - 1)];
-        }
+    for (int q0 = 0; q0 < L; q0 += kLabBlk) {
+        float v[kLabBlk];
+        label_load_blk(s, q0, L, wide, v);
         label_block(v, q0, L, m, acc);
     }
     return m + fast_log2(acc);
 }
-// o[q] = mu exp2(s[q] log2e - lse2) for the L labels of one span, in blocks
-// of 32 as above.
-__device__ __forceinline__ void label_marginals(const float *s, int L, float mu, float lse2, float *o) {
-    for (int q0 = 0; q0 < L; q0 += 32) {
-        float v[32];
+// o[q] = mu exp2(s[q] log2e - lse2) for the L labels of one span, a block
+// at a time.
+__device__ __forceinline__ void label_marginals(const float *s, int L, bool wide, float mu, float lse2, float *o) {
+    for (int q0 = 0; q0 < L; q0 += kLabBlk) {
+        float v[kLabBlk];
+        label_load_blk(s, q0, L, wide, v);
 #pragma unroll
-        for (int k = 0; k < 32; ++k) v[k] = s[min(q0 + k, L - 1)];
-#pragma unroll
-        for (int k = 0; k < 32; ++k)
+        for (int k = 0; k < kLabBlk; ++k)
             if (q0 + k < L) o[q0 + k] = mu * fast_exp2(v[k] * LOG2E_F - lse2);
     }
 }
@@ -904,7 +907,7 @@ constexpr int kGoldMark = 0x7FBADBAD;   // a NaN bit pattern: no finite chart va
 // before it has written any output: the caller then runs it again in the log
 // domain (LIN = false, max-shifted log-sum-exp per span).
 constexpr float kLinMin = 0x1p-100f;
-template <bool LIN, bool REV, bool SPILL, bool GOLD>
+template <bool LIN, bool REV, bool SPILL, bool GOLD, bool LAB>
 __device__ __forceinline__ bool inside_block_impl(const KernelPlan &p, int block, const int32_t *rec, char *smem_raw,
                                                   const float *__restrict__ scores,
                                                   const float *__restrict__ grad,
@@ -912,6 +915,7 @@ __device__ __forceinline__ bool inside_block_impl(const KernelPlan &p, int block
                                                   const int32_t *__restrict__ gold,
                                                   float *__restrict__ loss) {
     static_assert(!GOLD || REV, "the gold-tree loss needs the marginals");
+    static_assert(!LAB || (!SPILL && !GOLD), "label I/O is for labelled bundles in LDS");
     __shared__ int lin_ovf;
     __shared__ double spill_forced[1];
     __shared__ float spill_gv[1];
@@ -1002,8 +1006,9 @@ __device__ __forceinline__ bool inside_block_impl(const KernelPlan &p, int block
     // span's labels and takes their log-sum-exp (Sec. 4.2, Eq.
     // tree-label-score: the span's score in the one-stage Z); the others
     // read the [B][N1][N1] scores (the label passes' log-sum-exps for a
-    // labelled plan).
-    const bool lab = !SPILL && p.lab_L > 1 && rec[kRecLab] != 0;   // (uniform)
+    // labelled plan).  Only the LAB build holds this code: its register
+    // blocks would otherwise raise every other kernel's register pressure.
+    const bool lab = LAB && rec[kRecLab] != 0;   // (uniform)
     const int L = p.lab_L;
     const size_t lab_sent = (size_t)N1 * N1 * (size_t)L;
     auto lab_at = [&](int sb, int i, int j) -> const float * {
@@ -1011,10 +1016,14 @@ __device__ __forceinline__ bool inside_block_impl(const KernelPlan &p, int block
     };
     const bool wide_in = (L & 1) == 0 && ((uintptr_t)p.lab_s4 & 7) == 0;   // 8-byte label loads
     auto lab_lse = [&](const float *q) -> float { return label_lse2(q, L, wide_in) * (float)LN2_D; };
-    if (lab)
-        for_cells_loaded<1>(nb, n, lab_at, lab_lse, put_score);
-    else
+    if constexpr (LAB) {
+        if (lab)
+            for_cells_loaded<1>(nb, n, lab_at, lab_lse, put_score);
+        else
+            for_cells_loaded<8>(nb, n, score_at, load_score, put_score);
+    } else {
         for_cells_loaded<8>(nb, n, score_at, load_score, put_score);
+    }
     __syncthreads();
     // Forced-span sums, a lane group per sentence, fixed order (deterministic).
     // The linear domain also seeds each sentence's shift d from its scores:
@@ -1128,54 +1137,45 @@ __device__ __forceinline__ bool inside_block_impl(const KernelPlan &p, int block
             if (__builtin_bit_cast(int, P[j * ld + n - w]) == kGoldMark) mu -= gv[sb];
         return mu;
     };
-    if (lab) {
+    if constexpr (LAB) if (lab) {
         // per-label marginals mu(i,j) exp(s(i,j,l) - s'(i,j)).  Up to 32
         // labels: one load of a span's labels serves its log-sum-exp (the
-        // prologue's arithmetic, so the same own score as the chart's) and
-        // its outputs, two spans per thread at a time.
+        // prologue's blocks and arithmetic, so the same own score as the
+        // chart's) and its outputs.
         float *const out0 = p.lab_out;
         const bool wide_out = wide_in && ((uintptr_t)out0 & 7) == 0;
-        if (L <= 32) {
+        if (L <= 2 * kLabBlk) {
             const Cell_walk cw(nb, n);
-            for (int c0 = tid; c0 < cw.total; c0 += NT * 2) {
-                Cell e[2];
-                const float *q[2];
-                float v[2][32];
-#pragma unroll
-                for (int u = 0; u < 2; ++u) {
-                    e[u] = cw.at(c0 + u * NT);
-                    q[u] = lab_at(e[u].sb, e[u].i, e[u].j);
-                }
-#pragma unroll
-                for (int u = 0; u < 2; ++u) label_load32(q[u], L, wide_in, v[u]);
+            for (int c = tid; c < cw.total; c += NT) {
+                const Cell e = cw.at(c);
+                const float *q = lab_at(e.sb, e.i, e.j);
+                float v[2 * kLabBlk];
+                label_load32(q, L, wide_in, v);
                 __builtin_amdgcn_sched_barrier(0);
+                float m = -INFINITY, acc = 0.f;
+                label_block(v, 0, L, m, acc);
+                if (L > kLabBlk) label_block(v + kLabBlk, kLabBlk, L, m, acc);
+                const float own2 = ((m + fast_log2(acc)) * (float)LN2_D) * LOG2E_F;   // as the chart holds it
+                const float mu = span_mu(e.sb, e.i, e.j, own2);
+                if (!e.ok) continue;
+                float *o = out0 + (q - p.lab_s4);
+                if (wide_out) {   // 8-byte stores
+                    float2 *o2 = reinterpret_cast<float2 *>(o);
 #pragma unroll
-                for (int u = 0; u < 2; ++u) {
-                    float m = -INFINITY, acc = 0.f;
-                    label_block(v[u], 0, L, m, acc);
-                    const float own2 = ((m + fast_log2(acc)) * (float)LN2_D) * LOG2E_F;   // as the chart holds it
-                    const float mu = span_mu(e[u].sb, e[u].i, e[u].j, own2);
-                    if (e[u].ok) {
-                        float *o = out0 + (q[u] - p.lab_s4);
-                        if (wide_out) {   // 8-byte stores
-                            float2 *o2 = reinterpret_cast<float2 *>(o);
+                    for (int k = 0; k < kLabBlk; ++k)
+                        if (2 * k < L)
+                            o2[k] = make_float2(mu * fast_exp2(v[2 * k] * LOG2E_F - own2),
+                                                mu * fast_exp2(v[2 * k + 1] * LOG2E_F - own2));
+                } else {
 #pragma unroll
-                            for (int k = 0; k < 16; ++k)
-                                if (2 * k < L)
-                                    o2[k] = make_float2(mu * fast_exp2(v[u][2 * k] * LOG2E_F - own2),
-                                                        mu * fast_exp2(v[u][2 * k + 1] * LOG2E_F - own2));
-                        } else {
-#pragma unroll
-                            for (int k = 0; k < 32; ++k)
-                                if (k < L) o[k] = mu * fast_exp2(v[u][k] * LOG2E_F - own2);
-                        }
-                    }
+                    for (int k = 0; k < 2 * kLabBlk; ++k)
+                        if (k < L) o[k] = mu * fast_exp2(v[k] * LOG2E_F - own2);
                 }
             }
         } else {
             for_cells_loaded<1>(nb, n, lab_at, lab_lse, [&](int sb, int i, int j, float s) {
                 const float *q = lab_at(sb, i, j);
-                label_marginals(q, L, span_mu(sb, i, j, s * LOG2E_F), s * LOG2E_F, out0 + (q - p.lab_s4));
+                label_marginals(q, L, wide_in, span_mu(sb, i, j, s * LOG2E_F), s * LOG2E_F, out0 + (q - p.lab_s4));
             });
         }
         return true;
@@ -1188,17 +1188,17 @@ __device__ __forceinline__ bool inside_block_impl(const KernelPlan &p, int block
 
 // A bundle (or a workspace sentence): the linear-domain sweeps, and the log
 // domain if they leave float32's range (see inside_block_impl).
-template <bool REV, bool SPILL, bool GOLD = false>
+template <bool REV, bool SPILL, bool GOLD = false, bool LAB = false>
 __device__ __forceinline__ void inside_block(const KernelPlan &p, int block, const int32_t *rec, char *smem_raw,
                                              const float *__restrict__ scores,
                                              const float *__restrict__ grad,
                                              float *__restrict__ logZ, float *__restrict__ marg,
                                              const int32_t *__restrict__ gold = nullptr,
                                              float *__restrict__ loss = nullptr) {
-    if (inside_block_impl<true, REV, SPILL, GOLD>(p, block, rec, smem_raw, scores, grad, logZ, marg, gold, loss))
+    if (inside_block_impl<true, REV, SPILL, GOLD, LAB>(p, block, rec, smem_raw, scores, grad, logZ, marg, gold, loss))
         return;
     __syncthreads();   // every thread has left the linear attempt
-    inside_block_impl<false, REV, SPILL, GOLD>(p, block, rec, smem_raw, scores, grad, logZ, marg, gold, loss);
+    inside_block_impl<false, REV, SPILL, GOLD, LAB>(p, block, rec, smem_raw, scores, grad, logZ, marg, gold, loss);
 }
 
 // ---------------------------------------------------------------------------
@@ -1507,15 +1507,17 @@ __device__ __forceinline__ void cky_block(const KernelPlan &p, int block, const 
 }
 
 // Workgroups of 256, 512 or 1024 threads (the plan's choice) share one
-// build of each kernel.
-template <bool REV, bool SPILL>
+// build of each kernel.  LAB: the labelled plans' bundle kernel, whose
+// bundles marked kRecLab read and write their own label scores.
+template <bool REV, bool SPILL, bool LAB = false>
 __global__ __launch_bounds__(kThreadsMax) void inside_kernel(KernelPlan p, const float *__restrict__ scores,
                                                              const float *__restrict__ grad,
                                                              float *__restrict__ logZ,
                                                              float *__restrict__ marg) {
     extern __shared__ __align__(16) char smem_raw[];
-    inside_block<REV, SPILL>(p, blockIdx.x, SPILL ? nullptr : p.inside.recs + (size_t)blockIdx.x * p.rec_stride,
-                             smem_raw, scores, grad, logZ, marg);
+    inside_block<REV, SPILL, false, LAB>(p, blockIdx.x,
+                                         SPILL ? nullptr : p.inside.recs + (size_t)blockIdx.x * p.rec_stride,
+                                         smem_raw, scores, grad, logZ, marg);
 }
 
 // Labelled scores [B][N1][N1][L], spread over the whole chip.
@@ -1816,6 +1818,7 @@ hipError_t launch_parse_scratch(const KernelPlan &p, char *scr, const float *sco
 hipError_t set_kernel_attributes(int max_lds_bytes) {
     const void *fns[] = {
         (const void *)inside_kernel<false, false>,        (const void *)inside_kernel<true, false>,
+        (const void *)inside_kernel<false, false, true>,  (const void *)inside_kernel<true, false, true>,
         (const void *)cky_kernel<false, false>,           (const void *)cky_kernel<false, true>,
         (const void *)loss_kernel<false>,                 (const void *)parse_kernel,
         (const void *)mbr_kernel,
@@ -1829,17 +1832,35 @@ hipError_t set_kernel_attributes(int max_lds_bytes) {
                                (int)(kLabelWaves * (kLabelRowChunk + CRF_MAX_LABELS) * sizeof(float)));
 }
 
-template <bool SPILL>
+template <bool SPILL, bool LAB = false>
 static void launch_inside_k(const KernelPlan &p, dim3 grid, int threads, size_t lds, hipStream_t s,
                             const float *scores, const float *grad, float *logZ, float *marg) {
     const dim3 block(threads);
-    if (marg != nullptr) hipLaunchKernelGGL((inside_kernel<true, SPILL>), grid, block, lds, s, p, scores, grad, logZ, marg);
-    else hipLaunchKernelGGL((inside_kernel<false, SPILL>), grid, block, lds, s, p, scores, grad, logZ, marg);
+    if (marg != nullptr)
+        hipLaunchKernelGGL((inside_kernel<true, SPILL, LAB>), grid, block, lds, s, p, scores, grad, logZ, marg);
+    else
+        hipLaunchKernelGGL((inside_kernel<false, SPILL, LAB>), grid, block, lds, s, p, scores, grad, logZ, marg);
+}
+
+// The bundles' launch and the workspace sentences' launch of one inside pass.
+template <bool LAB>
+static hipError_t launch_inside_sweeps(const KernelPlan &p, const float *scores, const float *grad, float *logZ,
+                                       float *marg, hipStream_t stream) {
+    const Schedule &q = p.inside;
+    hipError_t e;
+    if (q.n_bundles > 0) {
+        launch_inside_k<false, LAB>(p, dim3(q.n_bundles), q.threads, q.lds_bytes, stream, scores, grad, logZ, marg);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    if (q.n_spill > 0) {
+        launch_inside_k<true>(p, dim3(q.n_spill), kThreadsMax, 0, stream, scores, grad, logZ, marg);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    return hipSuccess;
 }
 
 hipError_t launch_inside(const KernelPlan &p, const float *scores, const float *grad, float *logZ,
                          float *marg, hipStream_t stream) {
-    const Schedule &q = p.inside;
     hipError_t e;
     if (p.L > 1) {
         // labelled: the label log-sum-exps of the sentences whose label
@@ -1860,22 +1881,15 @@ hipError_t launch_inside(const KernelPlan &p, const float *scores, const float *
         u.lab_s4 = scores;
         u.lab_out = marg;
         u.lab_L = p.L;
-        if ((e = launch_inside(u, sp, grad, logZ, marg != nullptr ? mu : nullptr, stream)) != hipSuccess) return e;
+        if ((e = launch_inside_sweeps<true>(u, sp, grad, logZ, marg != nullptr ? mu : nullptr, stream)) != hipSuccess)
+            return e;
         if (marg == nullptr || p.n_lab_rows < 1) return hipSuccess;
         hipLaunchKernelGGL(label_expand_kernel, lab_grid, dim3(kLabelChunk),
                            (size_t)kLabelWaves * 2 * (kLabelRowChunk / 2 + 2) * sizeof(float), stream, p, scores, sp,
                            mu, marg);
         return hipGetLastError();
     }
-    if (q.n_bundles > 0) {
-        launch_inside_k<false>(p, dim3(q.n_bundles), q.threads, q.lds_bytes, stream, scores, grad, logZ, marg);
-        if ((e = hipGetLastError()) != hipSuccess) return e;
-    }
-    if (q.n_spill > 0) {
-        launch_inside_k<true>(p, dim3(q.n_spill), kThreadsMax, 0, stream, scores, grad, logZ, marg);
-        if ((e = hipGetLastError()) != hipSuccess) return e;
-    }
-    return hipSuccess;
+    return launch_inside_sweeps<false>(p, scores, grad, logZ, marg, stream);
 }
 
 template <bool LAB>
