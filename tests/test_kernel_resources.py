@@ -1,0 +1,74 @@
+"""Register budgets of the HIP kernels, from the resource report that the
+build writes beside the library (the compiler's per-kernel figures).
+
+A kernel that runs out of registers spills to scratch memory: the spill
+reloads then sit on the sweeps' dependent chain of steps and the spills add
+HBM traffic (label code once compiled into the shared inside body pushed
+every inside kernel past its 128 VGPRs and slowed the fused launch by a
+fifth).  These tests hold every kernel to the scratch it uses now, so such a
+change fails on the CPU, at build time, rather than in a profile."""
+import csv
+import os
+
+import pytest
+
+from paper_2008_03736_amd import build as BLD
+
+# scratch bytes per lane each kernel may use; every other kernel none.  The
+# fused and MBR kernels (both the inside and the CKY body in one kernel, at
+# 128 VGPRs) keep a few loop-invariant values there, reloaded once per
+# rescale segment; the labelled workspace CKY a few more.
+ALLOWED_SCRATCH = {
+    "parse_kernel": 24,
+    "mbr_kernel": 24,
+    "cky_kernel<true, true>": 12,
+}
+# every kernel the library launches (short names)
+EXPECTED = [
+    "inside_kernel<false, false, false>", "inside_kernel<true, false, false>",
+    "inside_kernel<false, false, true>", "inside_kernel<true, false, true>",
+    "inside_kernel<false, true, false>", "inside_kernel<true, true, false>",
+    "cky_kernel<false, false>", "cky_kernel<false, true>", "cky_kernel<true, false>", "cky_kernel<true, true>",
+    "loss_kernel<false>", "loss_kernel<true>",
+    "parse_kernel", "spill_parse_kernel", "mbr_kernel",
+    "label_reduce_kernel", "label_expand_kernel", "label_spans_kernel",
+]
+
+
+def short(name):
+    name = name.replace("crf::(anonymous namespace)::", "").replace("crf::", "")
+    if name.startswith("void "):
+        name = name[5:]
+    return name.split("(")[0]
+
+
+@pytest.fixture(scope="module")
+def report():
+    if not os.path.exists(BLD.RESOURCES):
+        pytest.fail("no kernel resource report: build the library (__graft_entry__.build())")
+    with open(BLD.RESOURCES) as f:
+        rows = list(csv.DictReader(f, delimiter="\t"))
+    return {short(r["kernel"]): r for r in rows}
+
+
+def test_report_lists_every_kernel(report):
+    missing = [k for k in EXPECTED if k not in report]
+    assert not missing, f"kernels missing from the resource report: {missing}"
+    assert any(k.startswith("biaffine_kernel<") for k in report)
+
+
+def test_no_kernel_spills_beyond_its_budget(report):
+    over = []
+    for k, r in report.items():
+        scratch = int(r["ScratchSize [bytes/lane]"])
+        if scratch > ALLOWED_SCRATCH.get(k, 0):
+            over.append(f"{k}: {scratch} bytes/lane of scratch ({r['VGPRs Spill']} VGPRs spilled)")
+    assert not over, "kernels spill to scratch: " + "; ".join(over)
+
+
+def test_inside_kernels_keep_their_occupancy(report):
+    # the forward-only inside kernels fit five waves per SIMD, the others four
+    for k in ("inside_kernel<false, false, false>", "inside_kernel<false, false, true>"):
+        assert int(report[k]["Occupancy [waves/SIMD]"]) >= 5, k
+    for k in ("inside_kernel<true, false, false>", "inside_kernel<true, false, true>", "parse_kernel"):
+        assert int(report[k]["Occupancy [waves/SIMD]"]) >= 4, k
