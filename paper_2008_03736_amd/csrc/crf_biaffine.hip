@@ -8,26 +8,27 @@
 // contraction of the parser, so it runs on MFMA (bf16 inputs, fp32
 // accumulation).
 //
-// Design.  A workgroup (four wavefronts, sixteen rows each) takes a tile of
-// kBiaRows rows (left fence posts) and kBiaCols columns (right fence posts)
-// -- short sentences packed whole into one tile (their scores are the tile's
-// diagonal blocks), longer ones cut into row and column blocks -- and one
-// label.  For each chunk of kBiaChunk of the d output dimensions of W it
-// computes U = [R^l ; 1] W[:, chunk] (MFMA over K = d+1; each wavefront
-// keeps its rows, with the 1 and the zero padding of K, as fragments in
-// registers for the whole tile, and W's chunk is staged in LDS while the
-// next one is loaded into registers), keeps U on chip as bf16 hi + lo parts
-// (a 16-bit mantissa in all), and accumulates S += U R^r[:, chunk]^T (MFMA,
-// two products for hi and lo).  U never leaves the CU; W is read once per
-// tile from L2.  The chunk is narrow so that two workgroups share a CU and
-// one's barriers and load latencies hide behind the other's products.  Only
-// the valid cells 0 <= i < j <= n_b of S are written.
+// Design.  A workgroup (four wavefronts) takes a tile of kBiaRows rows (left
+// fence posts) and kBiaCols columns (right fence posts) -- short sentences
+// packed whole into one tile (their scores are the tile's diagonal blocks),
+// longer ones cut into row and column blocks -- and one label.  For each
+// chunk of kBiaChunk of the d output dimensions of W it computes
+// U = [R^l ; 1] W[:, chunk] on MFMA with K = d+1 split four ways: wavefront w
+// keeps the tile's 64 rows over its quarter of K (with the 1 and the zero
+// padding) as fragments in registers for the whole tile, loads its quarter of
+// W's chunk straight from L2 into registers (each W fragment feeds four
+// products, and W never passes through LDS), and the four partial sums meet
+// in LDS.  U stays on chip as bf16 hi + lo parts (a 16-bit mantissa in all),
+// and S += U R^r[:, chunk]^T (MFMA, two products for hi and lo) accumulates
+// sixteen rows per wavefront.  Only the valid cells 0 <= i < j <= n_b of S
+// are written.
 //
 // MFMA v_mfma_f32_16x16x32_bf16 (gfx950): A 16 x 32, B 32 x 16, D 16 x 16;
 // lane l supplies A row l%16 and B column l%16 at K offsets 8(l/16)..+7, and
 // holds D rows 4(l/16)..+3 of column l%16.  The first product is taken as
-// U^T = W^T [R^l ; 1]^T, so that a lane holds four consecutive columns of
-// one row of U and stores them with one 8-byte write.
+// U^T = W^T [R^l ; 1]^T: W is stored transposed, so an A fragment is eight
+// consecutive entries of one stored row, and a lane's D holds four
+// consecutive columns of one row of U.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -44,100 +45,67 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kPad = 8;                       // bf16 of padding per staged row (keeps 16-byte reads conflict-free)
 constexpr int kUStride = kBiaChunk + kPad;    // row stride of the staged U and R^r chunks
-constexpr int kWRows = kBiaChunk / 4;         // rows of a W chunk each wavefront stages
+constexpr int kPStride = kBiaChunk + 4;       // row stride (floats) of the staged partial sums of U
+constexpr int kNM = kBiaChunk / 16;           // 16-column blocks of U in a chunk
+constexpr int kNN = kBiaRows / 16;            // 16-row blocks of the tile
 
 // Eight consecutive bf16 of a staged row as an MFMA operand.
 __device__ __forceinline__ bf16x8 frag(const uint16_t *p) {
     return __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4 *>(p));
 }
+__device__ __forceinline__ bf16x8 frag(const uint4 &v) { return __builtin_bit_cast(bf16x8, v); }
 
 // K of the first product: d + 1 padded to 128, 256 or 512.
 __host__ __device__ inline int bia_kp(int d) { return d + 1 <= 128 ? 128 : d + 1 <= 256 ? 256 : 512; }
 
-// One chunk of W[:, c0 .. c0 + kBiaChunk)^T as this thread's share of the
-// staged rows (wave w: rows kWRows w .. +kWRows; lane: pieces of four at
-// lane, lane + 64): row c holds W[k][c0 + c] for k <= d (k = d: the bias),
-// zeros after.  Loaded into registers, stored to LDS separately, so that the
-// next chunk's loads fly while the current one is multiplied.  The loads are
-// unconditional, from addresses clamped into the weights (row min(c, d-1),
-// column min(k, d): at k = d the bias and three entries of the row's
-// padding, ldw >= d + 4), and the masks are applied when the chunk is
-// stored: a load whose result were used at once would wait out its whole L2
-// latency there.  Rows are wave-uniform (scalar addresses).
-// P = 4 or 8: bf16 per piece (8-byte or 16-byte loads; 16-byte pieces need
-// 16-byte aligned rows, ldw a multiple of 8).
-template <int KS, int P>
-struct WChunk {
-    static constexpr int H = (32 * KS / P + 63) / 64;   // pieces per lane and row
-    using V = typename std::conditional<P == 8, uint4, uint2>::type;
-    V v[kWRows][H];
-};
-template <int KS, int P>
-__device__ __forceinline__ void load_w(WChunk<KS, P> &r, const uint16_t *wl, int c0, int d, int ldw, int wv,
-                                       int lane) {
-    using V = typename WChunk<KS, P>::V;
-    // scalar row base + one 32-bit lane offset per piece (saddr form); the
-    // last piece is the one holding k = d (the bias), inside the row since
-    // ldw >= d + 1 is a multiple of P
-    const int dp = d - d % P;
-    uint32_t ko[WChunk<KS, P>::H];
-#pragma unroll
-    for (int h = 0; h < WChunk<KS, P>::H; ++h) ko[h] = 2u * (uint32_t)min(P * (lane + 64 * h), dp);   // bytes
-#pragma unroll
-    for (int rr_ = 0; rr_ < kWRows; ++rr_) {
-        const char *row = reinterpret_cast<const char *>(wl + (size_t)min(c0 + kWRows * wv + rr_, d - 1) * ldw);
-#pragma unroll
-        for (int h = 0; h < WChunk<KS, P>::H; ++h) r.v[rr_][h] = *reinterpret_cast<const V *>(row + ko[h]);
-    }
-}
-// Keep the bf16 at k .. k+1 of a 32-bit word when each is <= d (k = d: the bias).
-__device__ __forceinline__ uint32_t keep2(uint32_t x, int k, int d) {
-    return x & ((k <= d ? 0x0000FFFFu : 0u) | (k + 1 <= d ? 0xFFFF0000u : 0u));
-}
-template <int KS, int P>
-__device__ __forceinline__ void store_w(const WChunk<KS, P> &r, uint16_t *Ws, int lda, int c0, int d, int wv,
+// This wavefront's A fragments of one chunk: W^T rows c0 + 16 m + lane%16
+// (clamped to row d-1: the columns of U past d meet zero r^r entries), K
+// offsets kq0 + 32 s + 8 (lane/16) .. +7.  P = 8 or 4: one 16-byte load or
+// two 8-byte loads (16-byte pieces need 16-byte aligned rows, ldw a multiple
+// of 8).  Offsets are clamped to the piece that holds k = d (the bias), which
+// lies inside the row since ldw >= d + 1 is a multiple of P; what a clamped
+// or partial piece brings past k = d is masked off at use (wmask).
+template <int KQ, int P>
+__device__ __forceinline__ void load_wq(uint4 (&f)[kNM][KQ], const uint16_t *wl, int c0, int d, int ldw, int kq0,
                                         int lane) {
-    using V = typename WChunk<KS, P>::V;
+    const int dp = d - d % P;
 #pragma unroll
-    for (int h = 0; h < WChunk<KS, P>::H; ++h) {
-        const int k = P * (lane + 64 * h);
-        if (k >= 32 * KS) continue;
+    for (int m = 0; m < kNM; ++m) {
+        const uint16_t *row = wl + (size_t)min(c0 + 16 * m + (lane & 15), d - 1) * ldw;
 #pragma unroll
-        for (int rr_ = 0; rr_ < kWRows; ++rr_) {
-            const bool row = c0 + kWRows * wv + rr_ < d;
-            V v = r.v[rr_][h];
-            v.x = row ? keep2(v.x, k, d) : 0u;
-            v.y = row ? keep2(v.y, k + 2, d) : 0u;
+        for (int s = 0; s < KQ; ++s) {
+            const int k = kq0 + 32 * s + 8 * (lane >> 4);
             if constexpr (P == 8) {
-                v.z = row ? keep2(v.z, k + 4, d) : 0u;
-                v.w = row ? keep2(v.w, k + 6, d) : 0u;
+                f[m][s] = *reinterpret_cast<const uint4 *>(row + min(k, dp));
+            } else {
+                const uint2 a = *reinterpret_cast<const uint2 *>(row + min(k, dp));
+                const uint2 b = *reinterpret_cast<const uint2 *>(row + min(k + 4, dp));
+                f[m][s] = make_uint4(a.x, a.y, b.x, b.y);
             }
-            *reinterpret_cast<V *>(Ws + (kWRows * wv + rr_) * lda + k) = v;
         }
     }
+}
+// Bits of a fragment's four words that hold entries k <= d (k: its first entry).
+__device__ __forceinline__ uint32_t keep_word(int k, int d) {
+    return (k <= d ? 0x0000FFFFu : 0u) | (k + 1 <= d ? 0xFFFF0000u : 0u);
 }
 
 // Tile record: kBiaRows row ids then kBiaCols column ids, each b * N1 + i
 // (sentence b, fence post i) or -1.  KS = K / 32 steps of the first product
-// (K = d + 1 padded to 128, 256 or 512), taken in groups of kGrp steps whose
-// fragments are read from LDS while the previous group is multiplied.
-constexpr int kGrp = 2;
+// (K = d + 1 padded to 128, 256 or 512); each wavefront takes KS / 4 of them.
 constexpr int kRAhead = 3;   // chunks of r^r in flight
 template <int KS, int P>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) void biaffine_kernel(
     const int32_t *__restrict__ tiles, const int32_t *__restrict__ len, int N1, int d, int ldw, int L,
     const uint16_t *__restrict__ rl, const uint16_t *__restrict__ rr, const uint16_t *__restrict__ w,
     float *__restrict__ scores) {
+    static_assert(KS % 4 == 0, "K splits four ways");
+    constexpr int KQ = KS / 4;               // steps of this wavefront's quarter of K
     extern __shared__ __align__(16) char smem_raw[];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wv = __builtin_amdgcn_readfirstlane(wave);
-    constexpr int Kp = 32 * KS;              // K of the first product
-    constexpr int NC = kBiaChunk / 16;       // 16-column blocks of a chunk
-    constexpr int NG = KS / kGrp < 1 ? 1 : KS / kGrp;
-    constexpr int GS = KS / NG;              // steps per group
-    const int lda = Kp + kPad;
-    uint16_t *Ws = reinterpret_cast<uint16_t *>(smem_raw);   // [kBiaChunk][lda]: W[:, chunk]^T
-    uint16_t *Rs = Ws + kBiaChunk * lda;                     // [kBiaCols][kUStride]: r^r[:, chunk]
+    const int kq0 = 32 * KQ * __builtin_amdgcn_readfirstlane(wave);   // first K of this wavefront
+    float *Ps = reinterpret_cast<float *>(smem_raw);                   // [4][kBiaRows][kPStride]: partial U
+    uint16_t *Rs = reinterpret_cast<uint16_t *>(Ps + 4 * kBiaRows * kPStride);   // [kBiaCols][kUStride]: r^r[:, chunk]
     uint16_t *Uh = Rs + kBiaCols * kUStride;                 // [kBiaRows][kUStride]: U hi
     uint16_t *Ul = Uh + kBiaRows * kUStride;                 // [kBiaRows][kUStride]: U lo
     int32_t *Ob = reinterpret_cast<int32_t *>(Ul + kBiaRows * kUStride);   // [kBiaRows + kBiaCols]
@@ -148,8 +116,14 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     const uint16_t *wl = w + (size_t)l * d * ldw;
 
     // Issue the first W chunk's loads before anything waits.
-    WChunk<KS, P> wn;
-    load_w<KS, P>(wn, wl, 0, d, ldw, wv, lane);
+    uint4 wf[kNM][KQ];
+    load_wq<KQ, P>(wf, wl, 0, d, ldw, kq0, lane);
+    uint4 wmask[KQ];
+#pragma unroll
+    for (int s = 0; s < KQ; ++s) {
+        const int k = kq0 + 32 * s + 8 * (lane >> 4);
+        wmask[s] = make_uint4(keep_word(k, d), keep_word(k + 2, d), keep_word(k + 4, d), keep_word(k + 6, d));
+    }
 
     // r^r of the tile's columns: thread t stages column t/4, dimensions
     // 8 (t%4) .. +7 of each chunk (two loads of four: rows are 8-byte
@@ -166,26 +140,31 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
         for (int h = 0; h < 2; ++h)
             rn[a][h] = *reinterpret_cast<const uint2 *>(crow + min(kBiaChunk * a + sk + 4 * h, d - 4));
 
-    // This wave's rows [r^l_i ; 1 ; 0 ...] as MFMA fragments, in registers
-    // for the whole tile: row 16 wave + lane%16, K offsets k0 + 8 (lane/16).
-    uint2 afr[KS][2];
-    {
-        const int id = rec[16 * wave + (lane & 15)];
-        const uint16_t *row = rl + (size_t)(id >= 0 ? id : 0) * d;
+    // The tile's rows [r^l_i ; 1 ; 0 ...] over this wavefront's quarter of K
+    // as MFMA fragments, in registers for the whole tile: row 16 n + lane%16,
+    // K offsets kq0 + 32 s + 8 (lane/16) .. +7 (two pieces of four).
+    uint4 rf[kNN][KQ];
 #pragma unroll
-        for (int s = 0; s < KS; ++s)
+    for (int n = 0; n < kNN; ++n) {
+        const int id = rec[16 * n + (lane & 15)];
+        const uint16_t *row = rl + (size_t)(id >= 0 ? id : 0) * d;
+        uint2 v[KQ][2];
+#pragma unroll
+        for (int s = 0; s < KQ; ++s)
 #pragma unroll
             for (int h = 0; h < 2; ++h)
-                afr[s][h] = *reinterpret_cast<const uint2 *>(row + min(32 * s + 8 * (lane >> 4) + 4 * h, d - 4));
+                v[s][h] = *reinterpret_cast<const uint2 *>(row + min(kq0 + 32 * s + 8 * (lane >> 4) + 4 * h, d - 4));
 #pragma unroll
-        for (int s = 0; s < KS; ++s)
+        for (int s = 0; s < KQ; ++s) {
+            uint2 q[2];
 #pragma unroll
             for (int h = 0; h < 2; ++h) {
-                const int k = 32 * s + 8 * (lane >> 4) + 4 * h;
-                uint2 v = id >= 0 && k < d ? afr[s][h] : make_uint2(0u, 0u);
-                if (k == d) v.x = 0x3F80u;                   // the appended 1 (k = d, a multiple of 4)
-                afr[s][h] = v;
+                const int k = kq0 + 32 * s + 8 * (lane >> 4) + 4 * h;   // a multiple of 4, as d is
+                q[h] = id >= 0 && k < d ? v[s][h] : make_uint2(0u, 0u);
+                if (k == d) q[h].x = 0x3F80u;                            // the appended 1
             }
+            rf[n][s] = make_uint4(q[0].x, q[0].y, q[1].x, q[1].y);
+        }
     }
 
     // Where the tile's cells of S go, decoded once into LDS (read back by the
@@ -210,66 +189,64 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) voi
     for (int a = 0; a < kRAhead; ++a) {
         const int c0 = cb + a * kBiaChunk;
         if (c0 >= d) break;
-        __syncthreads();   // the previous chunk's readers are done
-        store_w<KS, P>(wn, Ws, lda, c0, d, wv, lane);
+        __syncthreads();   // the previous chunk's readers of Ps, Rs, Uh and Ul are done
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
             const uint2 v = cid >= 0 && c0 + sk + 4 * h < d ? rn[a][h] : make_uint2(0u, 0u);
             *reinterpret_cast<uint2 *>(Rs + sj * kUStride + sk + 4 * h) = v;
         }
-        if (c0 + kBiaChunk < d)   // the next chunk's W flies during this one's products
-            load_w<KS, P>(wn, wl, c0 + kBiaChunk, d, ldw, wv, lane);
-        if (c0 + kRAhead * kBiaChunk < d) {   // and r^r kRAhead chunks ahead
+        if (c0 + kRAhead * kBiaChunk < d) {   // r^r kRAhead chunks ahead
 #pragma unroll
             for (int h = 0; h < 2; ++h)
                 rn[a][h] = *reinterpret_cast<const uint2 *>(crow + min(c0 + kRAhead * kBiaChunk + sk + 4 * h, d - 4));
         }
-        __syncthreads();
 
-        // U^T[chunk][16 wave .. +16] = W[:, chunk]^T [r^l ; 1]^T
-        f32x4 u[NC];
+        // U^T[chunk][tile rows], this wavefront's quarter of K
+        f32x4 u[kNM][kNN];
 #pragma unroll
-        for (int c = 0; c < NC; ++c) u[c] = f32x4{0.f, 0.f, 0.f, 0.f};
-        const uint16_t *wrow = Ws + (lane & 15) * lda + 8 * (lane >> 4);
-        bf16x8 bw[2][GS][NC];
+        for (int m = 0; m < kNM; ++m)
 #pragma unroll
-        for (int s = 0; s < GS; ++s)
+            for (int n = 0; n < kNN; ++n) u[m][n] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-            for (int c = 0; c < NC; ++c) bw[0][s][c] = frag(wrow + 16 * c * lda + 32 * s);
+        for (int s = 0; s < KQ; ++s)
 #pragma unroll
-        for (int g = 0; g < NG; ++g) {
-            if (g + 1 < NG) {
+            for (int m = 0; m < kNM; ++m) {
+                const uint4 wv = wf[m][s];
+                const bf16x8 af = frag(make_uint4(wv.x & wmask[s].x, wv.y & wmask[s].y, wv.z & wmask[s].z,
+                                                  wv.w & wmask[s].w));
 #pragma unroll
-                for (int s = 0; s < GS; ++s)
-#pragma unroll
-                    for (int c = 0; c < NC; ++c)
-                        bw[(g + 1) & 1][s][c] = frag(wrow + 16 * c * lda + 32 * ((g + 1) * GS + s));
+                for (int n = 0; n < kNN; ++n)
+                    u[m][n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af, frag(rf[n][s]), u[m][n], 0, 0, 0);
             }
-            // keep the next group's reads ahead of this group's products (the
-            // scheduler would otherwise pair each read with its product and
-            // wait out the LDS latency at every one)
-            __builtin_amdgcn_sched_barrier(0);
+        // the next chunk's W flies while this one's sums meet and its second
+        // product runs
+        if (c0 + kBiaChunk < d) load_wq<KQ, P>(wf, wl, c0 + kBiaChunk, d, ldw, kq0, lane);
+        // partial sums to LDS: row 16 n + lane%16, columns 16 m + 4 (lane/16) .. +3
 #pragma unroll
-            for (int s = 0; s < GS; ++s) {
-                const int ks = g * GS + s;
-                const bf16x8 a =
-                    __builtin_bit_cast(bf16x8, make_uint4(afr[ks][0].x, afr[ks][0].y, afr[ks][1].x, afr[ks][1].y));
+        for (int m = 0; m < kNM; ++m)
 #pragma unroll
-                for (int c = 0; c < NC; ++c)
-                    u[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bw[g & 1][s][c], a, u[c], 0, 0, 0);
+            for (int n = 0; n < kNN; ++n)
+                *reinterpret_cast<f32x4 *>(Ps + (wave * kBiaRows + 16 * n + (lane & 15)) * kPStride + 16 * m +
+                                           4 * (lane >> 4)) = u[m][n];
+        __syncthreads();
+        // the four quarters summed, to bf16 hi + lo: thread t takes row t/4,
+        // columns 8 (t%4) .. +7
+        {
+            const int r = tid >> 2, c = 8 * (tid & 3);
+            f32x4 s0 = f32x4{0.f, 0.f, 0.f, 0.f}, s1 = s0;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const float *src = Ps + (q * kBiaRows + r) * kPStride + c;
+                s0 += *reinterpret_cast<const f32x4 *>(src);
+                s1 += *reinterpret_cast<const f32x4 *>(src + 4);
             }
-            __builtin_amdgcn_sched_barrier(0);
-        }
-        // U to LDS as bf16 hi + lo: row 16 wave + lane%16, columns
-        // 16 c + 4 (lane/16) .. +3
-#pragma unroll
-        for (int c = 0; c < NC; ++c) {
-            const bf16x4 hi = __builtin_convertvector(u[c], bf16x4);
-            const f32x4 rest = u[c] - __builtin_convertvector(hi, f32x4);
-            const bf16x4 lo = __builtin_convertvector(rest, bf16x4);
-            const int o = (16 * wave + (lane & 15)) * kUStride + 16 * c + 4 * (lane >> 4);
-            *reinterpret_cast<bf16x4 *>(Uh + o) = hi;
-            *reinterpret_cast<bf16x4 *>(Ul + o) = lo;
+            const bf16x4 h0 = __builtin_convertvector(s0, bf16x4), h1 = __builtin_convertvector(s1, bf16x4);
+            const bf16x4 l0 = __builtin_convertvector(s0 - __builtin_convertvector(h0, f32x4), bf16x4);
+            const bf16x4 l1 = __builtin_convertvector(s1 - __builtin_convertvector(h1, f32x4), bf16x4);
+            *reinterpret_cast<bf16x4 *>(Uh + r * kUStride + c) = h0;
+            *reinterpret_cast<bf16x4 *>(Uh + r * kUStride + c + 4) = h1;
+            *reinterpret_cast<bf16x4 *>(Ul + r * kUStride + c) = l0;
+            *reinterpret_cast<bf16x4 *>(Ul + r * kUStride + c + 4) = l1;
         }
         __syncthreads();
 
@@ -321,9 +298,8 @@ hipError_t set_biaffine_attributes() {
     return hipSuccess;
 }
 
-int64_t biaffine_lds_bytes(int d) {
-    const int64_t lda = bia_kp(d) + kPad;
-    return 2 * (kBiaChunk * lda + (kBiaCols + 2 * kBiaRows) * (int64_t)kUStride) +
+int64_t biaffine_lds_bytes(int) {
+    return 4 * (4 * kBiaRows * (int64_t)kPStride) + 2 * ((kBiaCols + 2 * kBiaRows) * (int64_t)kUStride) +
            4 * (2 * (kBiaRows + kBiaCols) + kBiaRows);
 }
 
