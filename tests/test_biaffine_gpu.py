@@ -57,11 +57,14 @@ def check(got, inp):
     return float(err.max())
 
 
-@pytest.mark.parametrize("d", [500, 100, 4, 64, 508])
+@pytest.mark.parametrize("d", [500, 100, 4, 64, 508, 124, 128, 252, 256])
 def test_biaffine_span_scores(torch, d):
     # lengths across the packing (short sentences packed into one tile) and
     # the blocking (sentences of 64 or more fence posts), d = 500 (the
-    # paper's), 100 (its label scorer), and the limits
+    # paper's), 100 (its label scorer), the limits, and the K paddings'
+    # edges: d + 1 just under and over 128 and 256, which put the appended
+    # 1 (and the end of W's rows) in the third or fourth quarter of K, the
+    # quarter each wavefront of the first product takes
     lengths = [1, 2, 5, 30, 62, 63, 64, 99, 130, 20, 7]
     inp = W.biaffine_inputs(lengths, d, seed=d)
     worst = check(run(torch, inp), inp)
