@@ -883,8 +883,11 @@ __device__ __forceinline__ int label_argmax(const float *s, int L) {
 // Inside (+ marginals).  One workgroup per bundle (or, SPILL, per long
 // sentence with its chart in the workspace).
 //   REV: also compute the marginals (joint inside/outside sweep) and write them.
-//   (Labelled scores run the same code on their label log-sum-exps, which
-//   label_reduce_kernel writes beforehand; see launch_inside.)
+//   LAB: a labelled plan's bundles.  Bundles of sentences of up to
+//   kLabInBundleMaxN words (kRecLab) read their label scores and take each
+//   span's log-sum-exp in the prologue and write the per-label marginals in
+//   the epilogue; the others run on the label log-sum-exps that
+//   label_reduce_kernel wrote beforehand (see launch_inside).
 // Dynamic LDS (bundled): nb charts (chart stride from inside_layout), then
 // nb x {forced (f64), grad (f32), id (i32), shift (f32)}, then the room
 // bundle_extra_bytes gives every bundle.
@@ -1520,7 +1523,9 @@ __global__ __launch_bounds__(kThreadsMax) void inside_kernel(KernelPlan p, const
                                          smem_raw, scores, grad, logZ, marg);
 }
 
-// Labelled scores [B][N1][N1][L], spread over the whole chip.
+// Labelled scores [B][N1][N1][L] of the sentences whose bundles leave their
+// label work to these passes (longer than kLabInBundleMaxN words, or with
+// their chart in the workspace), spread over the whole chip.
 // label_reduce_kernel writes each valid cell's label log-sum-exp
 // s'(i,j) = log sum_l exp s(i,j,l) (Sec. 4.2, Eq. tree-label-score: the
 // one-stage Z sums exp of the labelled score over labels per span) into sp
