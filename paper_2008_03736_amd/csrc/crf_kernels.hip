@@ -1353,7 +1353,7 @@ __device__ __forceinline__ void cky_sweep(const Cky_ctx<SP> &cx) {
     const int n = cx.n;
 #define CRF_CKY_FIXED(LO, HI, GG, CC, MM) \
     if (n >= LO + 1) cky_run<GG, CC, MM, IL>(cx, LO + 1, min(HI + 2, n + 1));
-    CRF_FIXED_RUNS(CRF_CKY_FIXED)
+    CRF_CKY_FIXED_RUNS(CRF_CKY_FIXED)
 #undef CRF_CKY_FIXED
     for (int w = kFixedRunsMaxK + 2; w <= n;) {
         const StepShape sh = step_shape_k(w - 1);
