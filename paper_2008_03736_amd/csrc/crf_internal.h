@@ -223,9 +223,11 @@ __host__ __device__ constexpr StepShape step_shape_k(int K) {
 // R(LO, HI, G, C, MF).  The sweeps call these runs one after the other,
 // with no shape dispatch (sentences of up to 129 words); steps of more
 // splits go through step_shape_k.
-#define CRF_FIXED_RUNS(R) \
-    R(1, 1, 1, 1, 0) R(2, 2, 1, 2, 1) R(3, 4, 1, 4, 2) R(5, 8, 1, 8, 4) R(9, 16, 2, 8, 4) R(17, 32, 4, 8, 4) \
+#define CRF_FIXED_RUNS_LOW(R) R(1, 1, 1, 1, 0) R(2, 2, 1, 2, 1) R(3, 4, 1, 4, 2) R(5, 8, 1, 8, 4)
+#define CRF_FIXED_RUNS_MID(R) R(9, 16, 2, 8, 4) R(17, 32, 4, 8, 4)
+#define CRF_FIXED_RUNS_HIGH(R) \
     R(33, 48, 4, 12, 8) R(49, 64, 4, 16, 12) R(65, 96, 4, 24, 16) R(97, 128, 4, 32, 24)
+#define CRF_FIXED_RUNS(R) CRF_FIXED_RUNS_LOW(R) CRF_FIXED_RUNS_MID(R) CRF_FIXED_RUNS_HIGH(R)
 constexpr int kFixedRunsMaxK = 128;
 constexpr bool fixed_runs_match_step_shapes() {
     int next = 1;
@@ -278,6 +280,39 @@ constexpr bool cky_runs_match_step_shapes() {
 }
 static_assert(cky_runs_match_step_shapes(),
               "CRF_CKY_FIXED_RUNS must list step_shape_cky's runs, with step_shape_k's reach");
+
+// The joint sweep's shapes for bundles of sentences of at most
+// kShortBundleMaxN words.  Such a bundle holds several sentences of one
+// length, so at step_shape_k's lanes per span a step takes several passes of
+// the workgroup; from 9 to 32 splits these shapes give each span half the
+// lanes with twice the splits each (C G, and so the reach of the masked reads
+// (C - MF) G, kept): fewer passes and one group-reduction level less per
+// step.  Outside 9..32 both lists run the same code (a CU running short and
+// long bundles side by side fetches one copy of it).
+constexpr int kShortBundleMaxN = 40;
+__host__ __device__ constexpr StepShape step_shape_short(int K) {
+    if (K <= 8 || K > 32) return step_shape_k(K);
+    return K <= 16 ? StepShape{1, 16, 8} : StepShape{2, 16, 8};
+}
+#define CRF_SHORT_RUNS_MID(R) R(9, 16, 1, 16, 8) R(17, 32, 2, 16, 8)
+#define CRF_SHORT_FIXED_RUNS(R) CRF_FIXED_RUNS_LOW(R) CRF_SHORT_RUNS_MID(R) CRF_FIXED_RUNS_HIGH(R)
+constexpr bool short_runs_match_step_shapes() {
+    int next = 1;
+#define CRF_CHECK_SHORT_RUN(LO, HI, GG, CC, MM)                                              \
+    if (LO != next) return false;                                                          \
+    for (int K = LO; K <= HI; ++K) {                                                       \
+        const StepShape s = step_shape_short(K), r = step_shape_k(K);                      \
+        if (s.G != GG || s.C != CC || s.MF != MM) return false;                            \
+        if (s.MF * s.G > K || s.C * s.G < K || s.C * s.G != r.C * r.G) return false;       \
+        if ((s.C - s.MF) * s.G != (r.C - r.MF) * r.G) return false;                        \
+    }                                                                                      \
+    next = HI + 1;
+    CRF_SHORT_FIXED_RUNS(CRF_CHECK_SHORT_RUN)
+#undef CRF_CHECK_SHORT_RUN
+    return next == kFixedRunsMaxK + 1;
+}
+static_assert(short_runs_match_step_shapes(),
+              "CRF_SHORT_FIXED_RUNS must list step_shape_short's runs, with step_shape_k's reach");
 
 // The first K' > K whose step shape differs from K's (the sweeps run the
 // steps of one shape as one loop; a closed form, since a scan over the

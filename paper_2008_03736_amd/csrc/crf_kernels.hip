@@ -684,7 +684,9 @@ __device__ void rescale_chart(const Bundle_ctx<T> &bx, int t0, float *dsh, float
 // The joint sweep: steps t = 1..n-1 (inside widths 2..n, outside widths
 // n-1..2), one dispatch per run of steps sharing a step shape; the runs are
 // cut at the rescale points (next_rescale), each phase running the fixed list
-// of runs, so that each run and the rescale appear once in the code.
+// of runs (with the short-bundle runs of 9..32 splits for bundles of at most
+// kShortBundleMaxN words), so that each run and the rescale appear once in
+// the code.
 template <bool LIN, bool WIDE, bool IL, typename T>
 __device__ __forceinline__ void io_sweep(const Bundle_ctx<T> &bx, float *dsh, float *dl) {
     const int n = bx.n;
@@ -694,7 +696,13 @@ __device__ __forceinline__ void io_sweep(const Bundle_ctx<T> &bx, float *dsh, fl
 #define CRF_IO_FIXED(LO, HI, GG, CC, MM)                              \
         if (max(lo, LO) < min(hi, HI + 1))                            \
             io_run<LIN, GG, CC, MM, IL>(bx, max(lo, LO), min(hi, HI + 1), dsh);
-        CRF_FIXED_RUNS(CRF_IO_FIXED)
+        CRF_FIXED_RUNS_LOW(CRF_IO_FIXED)
+        if (!WIDE && n <= kShortBundleMaxN) {
+            CRF_SHORT_RUNS_MID(CRF_IO_FIXED)
+        } else {
+            CRF_FIXED_RUNS_MID(CRF_IO_FIXED)
+        }
+        CRF_FIXED_RUNS_HIGH(CRF_IO_FIXED)
 #undef CRF_IO_FIXED
         for (int t = max(lo, kFixedRunsMaxK + 1); t < hi;) {
             const StepShape sh = step_shape_k(t);
