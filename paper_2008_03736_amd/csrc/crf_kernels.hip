@@ -180,6 +180,13 @@ __device__ __forceinline__ int grp_min_i(int v) {
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 __device__ __forceinline__ float fast_log2(float x) { return __builtin_amdgcn_logf(x); }
+// log2 of a positive normal float, in float64: the exact binary exponent plus
+// the float32 log2 of the mantissa in [0.5, 1) (good to about 1e-7 absolute
+// at any exponent).  No float64 log: its polynomial's coefficients would be
+// kept in a dozen VGPRs across a persistent kernel's loop.
+__device__ __forceinline__ double log2_split(float x) {
+    return (double)__builtin_amdgcn_frexp_expf(x) + (double)fast_log2(__builtin_amdgcn_frexp_mantf(x));
+}
 
 // a / d for 0 <= a < 2^24, 1 <= d, with inv = 1.0f / d: the float quotient is
 // within one of the truth and is corrected exactly.
@@ -1100,7 +1107,7 @@ __device__ __forceinline__ bool inside_block_impl(const KernelPlan &p, int block
     // root's log2 value.
     auto log_z = [&](int sb) {
         const float r = chart0[(size_t)sb * cstride + n - 1];
-        const double lr = LIN ? log2((double)r) : (double)r;
+        const double lr = LIN ? log2_split(r) : (double)r;
         const double z2 = lr - (double)dsh[sb] * (n >= 2 ? n - 2 : 0);
         return z2 * LN2_D + forced[sb];
     };
