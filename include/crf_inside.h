@@ -38,18 +38,28 @@
  *   Memory.  Every float/int pointer passed to a compute call is device memory
  *   owned by the caller; the library never frees it.  lengths_host in
  *   crf_plan_create is host memory, read only during the call.  The plan owns
- *   its device copies of the lengths and schedule and a workspace for
- *   sentences whose chart does not fit in LDS; they are allocated by
- *   crf_plan_create and freed by crf_plan_destroy.  Compute calls allocate
- *   nothing.
+ *   its device copies of the lengths and schedule, a workspace for
+ *   sentences whose chart does not fit in LDS and, with such sentences, a
+ *   257 KB area for the teams below; they are allocated by crf_plan_create
+ *   and freed by crf_plan_destroy.  Compute calls allocate nothing.
+ *
+ *   Teams.  When a call has only a few workspace sentences (at most 32
+ *   sentence passes in one launch), each pass runs on a team of 8 or 16
+ *   workgroups of one XCD that wait for each other at every width step.
+ *   Such a launch waits until all its workgroups are resident at once (it
+ *   is sized to fit an otherwise idle device); work from other streams
+ *   delays it.  A wait that lasts about 2^24 polls ends the launch, and the
+ *   log Z (and best score) of its workspace sentences are NaN.  Results are
+ *   bit-identical to those of one workgroup per pass.
  *
  *   Streams.  `stream` is a hipStream_t (NULL = the null stream).  Compute
  *   calls only enqueue work and never synchronise.  Calls on one plan must
  *   not overlap on the device: issue them on one stream, or order them with
  *   events.  A plan owns device state that its calls use while they run --
- *   the fused launches' work counter, and the workspace that holds the charts
+ *   the fused launches' work counter, the workspace that holds the charts
  *   and CKY split tables of sentences too long for LDS (crf_plan_info:
- *   workspace_users) -- and two overlapping calls would share it.  Different
+ *   workspace_users) and the team area -- and two overlapping calls would
+ *   share it.  Different
  *   plans share nothing and may run concurrently on any streams.
  *
  *   Errors.  Every call returns a status (CRF_OK = 0).  Arguments are checked
@@ -277,7 +287,8 @@ int crf_biaffine_scores(const crf_plan *plan, const uint16_t *rl, const uint16_t
  * used: the call takes them from a static scratch array of the library,
  * 8 MiB per GPU, held from the library's first use on a device until the
  * process ends.  It calls no allocation routine; it enqueues a small kernel
- * that clears the array's counter, then the launches of the fused call.
+ * that clears the array's counter, then the launches of the fused call
+ * (with one workgroup per workspace sentence pass: no teams).
  *   Returns CRF_EINVAL when the plan needs more workspace than the array
  *   holds (8 MiB less 256 bytes; crf_plan_info: workspace_bytes), e.g. a
  *   batch with many sentences longer than 142 words.

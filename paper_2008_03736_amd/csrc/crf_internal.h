@@ -444,7 +444,33 @@ struct KernelPlan {
     int32_t lab_L;
     int32_t rec_stride;          // ints per record: kRecHeader + the largest bundle
     int32_t B, n1, L;
+    // Workspace launches by teams: the team area (kTeamAreaBytes, zeroed
+    // before each team launch), how many workspace workgroups the device
+    // holds at once, and the team size of the launch at hand (set by the
+    // launcher; 1: a workgroup per sentence pass, no team area used).
+    int32_t *team_area;
+    int32_t team_cap, team_k;
 };
+
+// Teams for workspace sentences: up to kTeamMaxK workgroups of one XCD run a
+// sentence's pass together.  The team area holds kTeamHeaderWords words
+// (arrivals per XCD at [0, 16), all arrivals at 16, the abort flag at 17)
+// and kTeamLineWords words per team (its barrier's arrivals at 0, at 1 the
+// last of its jobs, plus one, whose linear-domain sweep left float32's range).
+constexpr int kTeamMaxK = 16;
+// Smallest team a launch forms.  A workspace step is bound by its memory
+// round trips (operand loads, store acknowledgements, the team's arrival),
+// not by one CU's issue, and a team reads the chart past its L1: teams pay
+// where a few long sentences leave most of the chip idle (a lone 512-word
+// sentence 7.1 -> 2.2 ms at k = 8), not on batches that fill it (64 sentences
+// of 256 words: 1.7 ms alone, 2.7 ms in teams of two).
+constexpr int kTeamMinK = 8;
+constexpr int kTeamHeaderWords = 64, kTeamLineWords = 64;
+constexpr int kTeamMaxTeams = 1024;
+constexpr int64_t kTeamAreaBytes = 4 * (int64_t)(kTeamHeaderWords + kTeamLineWords * kTeamMaxTeams);
+// Workgroups of kThreadsMax threads of the workspace kernels one CU holds at
+// once (the least over those kernels; 0 on error).
+int spill_blocks_per_cu();
 
 // The no-allocation entry point's scratch: a file-scope device array of
 // kScratchBytes per GPU (the first kScratchCounterBytes hold the fused

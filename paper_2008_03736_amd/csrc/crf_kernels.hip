@@ -206,6 +206,147 @@ __device__ __forceinline__ int next_pow2(int x) { return x <= 1 ? 1 : 1 << (32 -
 __device__ __forceinline__ int floor_pow2(int x) { return x <= 1 ? 1 : 1 << (31 - __builtin_clz(x)); }
 
 // ---------------------------------------------------------------------------
+// Teams.  A workspace sentence's pass can run on k workgroups of one XCD:
+// member `rank` takes virtual threads rank * blockDim.x + threadIdx.x of
+// k * blockDim.x in every step, and a team barrier replaces the workgroup
+// barrier between steps.  The chart goes through the XCD's L2, which the
+// members share: a member's stores are in L2 before its arrival is counted,
+// and the members read the chart with device-coherent loads (chart_ld),
+// which a CU's stale L1 lines cannot serve.  The arrival counters are
+// updated by atomics and polled the same way.  k = 1: a lone workgroup,
+// whose barriers are __syncthreads.
+struct Team {
+    int k = 1, rank = 0;
+    int32_t *line = nullptr;   // the team's words: [0] arrivals, [1] last job (+1) that left float32's range
+    int32_t *err = nullptr;    // the launch's abort flag
+    int *ep = nullptr;         // (LDS) team barriers this workgroup has passed
+    int job = 0;               // jobs this team has started
+};
+
+// A wait that lasts this many polls sets the abort flag; from then on no team
+// barrier of the launch waits (the outputs of its workspace sentences are
+// NaN).  Only a grid that is not resident at once can take that long.
+constexpr int kTeamSpin = 1 << 24;
+
+__device__ __forceinline__ int load_coherent(const int32_t *q) {
+    return __hip_atomic_load(q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ bool team_aborted(const Team &tm) { return tm.k > 1 && load_coherent(tm.err) != 0; }
+
+__device__ __forceinline__ void team_sync(const Team &tm) {
+    if (tm.k == 1) {
+        __syncthreads();
+        return;
+    }
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // this wave's stores are in L2
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        const int target = tm.k * ++*tm.ep;
+        atomicAdd(tm.line, 1);
+        for (int s = 0; load_coherent(tm.line) < target; ++s)
+            if ((s & 63) == 63 && (s >= kTeamSpin || load_coherent(tm.err) != 0)) {
+                atomicOr(tm.err, 1);
+                break;
+            }
+    }
+    __syncthreads();
+}
+
+// Barrier after a sweep step: the team's, or the workgroup's.
+template <bool TEAM>
+__device__ __forceinline__ void step_sync(const Team &tm) {
+    if constexpr (TEAM) team_sync(tm);
+    else __syncthreads();
+}
+
+// A chart read.  A team's members read each other's stores through device-
+// coherent loads: they skip this CU's L1 (which nothing short of dropping
+// the XCD's whole L2 invalidates) and are served by the XCD's L2.  Plain
+// loads otherwise.
+template <bool TEAM, typename T>
+__device__ __forceinline__ T chart_ld(const T *q) {
+    if constexpr (TEAM) return __hip_atomic_load(q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    else return *q;
+}
+
+// The same with the choice made at run time (reads outside the steps).
+template <typename T>
+__device__ __forceinline__ T chart_ld_if(const T *q, bool coherent) {
+    return coherent ? __hip_atomic_load(q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : *q;
+}
+
+// Virtual thread index and count of a step's lanes.
+template <bool TEAM>
+__device__ __forceinline__ int team_tid(const Team &tm) {
+    if constexpr (TEAM) return tm.rank * (int)blockDim.x + (int)threadIdx.x;
+    else return (int)threadIdx.x;
+}
+template <bool TEAM>
+__device__ __forceinline__ int team_nt(const Team &tm) {
+    if constexpr (TEAM) return tm.k * (int)blockDim.x;
+    else return (int)blockDim.x;
+}
+
+// Joins the launch's teams (thread 0; every workgroup of the grid resident
+// at once, the team area zeroed before the launch).  Each workgroup counts
+// itself on its XCD (the XCC_ID hardware register) and waits for the whole
+// grid; then the workgroups of each XCD form teams of k in arrival order.
+// Returns the team (-1: left over, or the grid never assembled), the
+// member's rank and the number of teams.
+struct Team_slot {
+    int team, rank, teams;
+};
+__device__ Team_slot join_team(int32_t *area, int k) {
+    const int xcc = __builtin_amdgcn_s_getreg((3 << 11) | 20) & 15;   // hwreg(HW_REG_XCC_ID, 0, 4)
+    const int slot = atomicAdd(area + xcc, 1);
+    atomicAdd(area + 16, 1);
+    for (int s = 0; load_coherent(area + 16) < (int)gridDim.x; ++s)
+        if ((s & 63) == 63 && (s >= kTeamSpin || load_coherent(area + 17) != 0)) {
+            atomicOr(area + 17, 1);
+            return Team_slot{-1, 0, 0};
+        }
+    int before = 0, teams = 0;
+    for (int x = 0; x < 16; ++x) {
+        const int c = load_coherent(area + x) / k;
+        if (x < xcc) before += c;
+        teams += c;
+    }
+    if (slot >= (load_coherent(area + xcc) / k) * k) return Team_slot{-1, 0, teams};
+    return Team_slot{before + slot / k, slot % k, teams};
+}
+
+// The jobs of a workspace launch by teams (sentence passes 0, 1, ...;
+// launched when p.team_k > 1; otherwise each workgroup takes the job of its
+// index): team t takes jobs t, t + T, ...  Sets this workgroup's team, first
+// job and stride; false: it takes no job.  (The callers loop over the jobs
+// themselves, with a barrier between jobs and ++tm.job.)  tm.k is at least 2,
+// as the compiler can see, so a team build holds only the team sweeps (and a
+// lone build, whose Team is the default, only the others).
+__device__ __forceinline__ bool spill_jobs(const KernelPlan &p, Team &tm, int &first, int &stride) {
+    __shared__ int slot[3];
+    __shared__ int ep;
+    tm = Team{};
+    if (threadIdx.x == 0) {
+        const Team_slot ts = join_team(p.team_area, p.team_k);
+        slot[0] = ts.team;
+        slot[1] = ts.rank;
+        slot[2] = ts.teams;
+        ep = 0;
+    }
+    __syncthreads();
+    if (slot[0] < 0) return false;
+    tm.k = max(2, p.team_k);
+    tm.rank = slot[1];
+    tm.line = p.team_area + kTeamHeaderWords + slot[0] * kTeamLineWords;
+    tm.err = p.team_area + 17;
+    tm.ep = &ep;
+    first = slot[0];
+    stride = slot[2];
+    return true;
+}
+
+// ---------------------------------------------------------------------------
 // Per-bundle context: nb sentences of length n; sentence sb's chart starts at
 // chart0 + sb * cstride (elements).
 
@@ -217,6 +358,7 @@ struct Bundle_ctx {
     uint32_t mnb;   // div_magic(nb)
     int e;          // the inside layout's bank exponent (inside_layout); 5 on the workspace
     int *ovf;       // linear-domain sweeps: set to 1 (LDS) when a value leaves float32's range
+    Team tm;        // workspace sentences: the team running the pass
 };
 
 
@@ -314,13 +456,13 @@ __device__ __forceinline__ T *sq_p(const Bundle_ctx<T> &bx, int sb) {   // (sb <
 // (terms c >= MF may fall past K: they count as exp2(-inf) = 0 and read at
 // most (C - MF)*G cells past the run); the group's result plus `own` is
 // returned to every lane of the group.
-template <int G, int C, int MF, typename T>
+template <int G, int C, int MF, bool TEAM, typename T>
 __device__ __forceinline__ float span_lse(const T *a, const T *b, int kl, float own) {
     float x[C], xa[C], xb[C];
 #pragma unroll
     for (int c = 0; c < C; ++c) {
-        xa[c] = a[c * G];
-        xb[c] = b[c * G];
+        xa[c] = chart_ld<TEAM>(&a[c * G]);
+        xb[c] = chart_ld<TEAM>(&b[c * G]);
     }
     __builtin_amdgcn_sched_barrier(0);   // every load in flight before the first use
 #pragma unroll
@@ -347,16 +489,16 @@ __device__ __forceinline__ float span_lse(const T *a, const T *b, int kl, float 
 // its sentence's shift (at pd, added when `shifted`) are loaded with the
 // operands, so that a step pays one LDS round trip; the group's sum times
 // exp2(own + shift) is returned to every lane.
-template <int G, int C, int MF, typename T>
+template <int G, int C, int MF, bool TEAM, typename T>
 __device__ __forceinline__ float span_dot(const T *a, const T *b, int kl, const T *po, const float *pd,
                                           bool shifted) {
     float xa[C], xb[C];
 #pragma unroll
     for (int c = 0; c < C; ++c) {
-        xa[c] = a[c * G];
-        xb[c] = b[c * G];
+        xa[c] = chart_ld<TEAM>(&a[c * G]);
+        xb[c] = chart_ld<TEAM>(&b[c * G]);
     }
-    const float own = *po, sh = *pd;
+    const float own = chart_ld<TEAM>(po), sh = *pd;
     __builtin_amdgcn_sched_barrier(0);   // every load in flight before the first use
     const float e = fast_exp2(shifted ? own + sh : own);
     float acc[2] = {0.f, 0.f};
@@ -378,7 +520,7 @@ constexpr float kLinMax = 0x1p+100f;
 // sentence's score shift (see rescale_chart); the root's own term is not
 // shifted.  LIN: the chart holds exp2 of these values, and the span's value
 // is exp2(own) * sum_k alpha(i,k) alpha(k,j).
-template <bool LIN, int G, int C, int MF, bool IL, typename T>
+template <bool LIN, int G, int C, int MF, bool IL, bool TEAM, typename T>
 __device__ __forceinline__ void inside_span(const Bundle_ctx<T> &bx, int w, int nsp, int f, const float *dsh) {
     const int ld = bx.ld, n = bx.n, K = w - 1;
     const Lane_at at = lane_at<G, IL>(f, nsp, bx.nb, bx.mnb);
@@ -389,10 +531,10 @@ __device__ __forceinline__ void inside_span(const Bundle_ctx<T> &bx, int w, int 
     const int pa = rp + rot_alpha_p(w), qa = rq + n + 1 - w;                   // alpha(i,j) cells
     float v;
     if constexpr (LIN)
-        v = span_dot<G, C, MF>(pq + rp + l, pq + rq + (n + 2 - w) + l, K - l, pq + pa, dsh + at.sb, w < n);
+        v = span_dot<G, C, MF, TEAM>(pq + rp + l, pq + rq + (n + 2 - w) + l, K - l, pq + pa, dsh + at.sb, w < n);
     else
-        v = span_lse<G, C, MF>(pq + rp + l, pq + rq + (n + 2 - w) + l, K - l,
-                               pq[pa] + (w < n ? dsh[at.sb] : 0.f));
+        v = span_lse<G, C, MF, TEAM>(pq + rp + l, pq + rq + (n + 2 - w) + l, K - l,
+                                     chart_ld<TEAM>(&pq[pa]) + (w < n ? dsh[at.sb] : 0.f));
     // An unconditional use keeps the score load in the load block, where it
     // is issued with the operand loads instead of after the reductions.
     asm volatile("" ::"v"(v));
@@ -407,7 +549,7 @@ __device__ __forceinline__ void inside_span(const Bundle_ctx<T> &bx, int w, int 
 // One span (i,j) of a width-v outside step: K = n - v parent terms, every
 // operand a parent of width > v or a sibling of width <= n - v, so this step
 // runs beside the inside step of width n - v + 1.
-template <bool LIN, int G, int C, int MF, bool IL, typename T>
+template <bool LIN, int G, int C, int MF, bool IL, bool TEAM, typename T>
 __device__ __forceinline__ void outside_span(const Bundle_ctx<T> &bx, int v, int nsp, int f, const float *dsh) {
     const int ld = bx.ld, n = bx.n, K = n - v;
     const Lane_at at = lane_at<G, IL>(f, nsp, bx.nb, bx.mnb);
@@ -418,9 +560,9 @@ __device__ __forceinline__ void outside_span(const Bundle_ctx<T> &bx, int v, int
     const int po = rp + n - v, qo = rq + v;                          // O'(i,j) cells
     float o;
     if constexpr (LIN)
-        o = span_dot<G, C, MF>(pq + rp + l, pq + rq + v + 1 + l, K - l, pq + po, dsh + at.sb, true);
+        o = span_dot<G, C, MF, TEAM>(pq + rp + l, pq + rq + v + 1 + l, K - l, pq + po, dsh + at.sb, true);
     else
-        o = span_lse<G, C, MF>(pq + rp + l, pq + rq + v + 1 + l, K - l, pq[po] + dsh[at.sb]);
+        o = span_lse<G, C, MF, TEAM>(pq + rp + l, pq + rq + v + 1 + l, K - l, chart_ld<TEAM>(&pq[po]) + dsh[at.sb]);
     asm volatile("" ::"v"(o));
     if (at.act && l == 0) {
         pq[qo] = o;
@@ -431,16 +573,16 @@ __device__ __forceinline__ void outside_span(const Bundle_ctx<T> &bx, int v, int
 }
 
 // Forward-only width step: every span of width w of every sentence.
-template <bool LIN, int G, int C, int MF, bool IL, typename T>
+template <bool LIN, int G, int C, int MF, bool IL, bool TEAM, typename T>
 __device__ __forceinline__ void fwd_step(const Bundle_ctx<T> &bx, int w, const float *dsh) {
-    const int tid = threadIdx.x, nt = blockDim.x;
+    const int tid = team_tid<TEAM>(bx.tm), nt = team_nt<TEAM>(bx.tm);
     const int nsp = bx.nb * (bx.n - w + 1);
     const int total = region_lanes<G, IL>(nsp);
     const int wq0 = __builtin_amdgcn_readfirstlane(tid & ~63);   // this wavefront's first thread
     for (int f0 = 0; f0 < total; f0 += nt) {
         const int fw = f0 + wq0;
         if (fw >= total) break;   // no span for this wavefront in this pass or later
-        if (wave_has_span<G, IL>(fw, nsp)) inside_span<LIN, G, C, MF, IL>(bx, w, nsp, f0 + tid, dsh);
+        if (wave_has_span<G, IL>(fw, nsp)) inside_span<LIN, G, C, MF, IL, TEAM>(bx, w, nsp, f0 + tid, dsh);
     }
 }
 
@@ -448,9 +590,9 @@ __device__ __forceinline__ void fwd_step(const Bundle_ctx<T> &bx, int w, const f
 // >= 2), both with K = t terms per span, so one step shape serves both.
 // Inside spans take the first threads, outside spans start at the next
 // wavefront boundary, so every wavefront runs one kind.
-template <bool LIN, int G, int C, int MF, bool IL, typename T>
+template <bool LIN, int G, int C, int MF, bool IL, bool TEAM, typename T>
 __device__ __forceinline__ void io_step(const Bundle_ctx<T> &bx, int t, const float *dsh) {
-    const int tid = threadIdx.x, nt = blockDim.x;
+    const int tid = team_tid<TEAM>(bx.tm), nt = team_nt<TEAM>(bx.tm);
     const int n = bx.n, w = t + 1, v = n - t;
     const int nin = bx.nb * (n - t), nout = v >= 2 ? bx.nb * (t + 1) : 0;
     const int obase = (region_lanes<G, IL>(nin) + 63) & ~63;
@@ -460,31 +602,31 @@ __device__ __forceinline__ void io_step(const Bundle_ctx<T> &bx, int t, const fl
         const int fw = f0 + wq0;
         if (fw >= total) break;
         if (fw < obase) {
-            if (wave_has_span<G, IL>(fw, nin)) inside_span<LIN, G, C, MF, IL>(bx, w, nin, f0 + tid, dsh);
+            if (wave_has_span<G, IL>(fw, nin)) inside_span<LIN, G, C, MF, IL, TEAM>(bx, w, nin, f0 + tid, dsh);
         } else {
             if (wave_has_span<G, IL>(fw - obase, nout))
-                outside_span<LIN, G, C, MF, IL>(bx, v, nout, f0 + tid - obase, dsh);
+                outside_span<LIN, G, C, MF, IL, TEAM>(bx, v, nout, f0 + tid - obase, dsh);
         }
     }
 }
 
 // A run of forward widths [w0, w1) sharing one step shape: a tight loop with
 // no dispatch.
-template <bool LIN, int G, int C, int MF, bool IL, typename T>
+template <bool LIN, int G, int C, int MF, bool IL, bool TEAM, typename T>
 __device__ __forceinline__ void fwd_run(const Bundle_ctx<T> &bx, int w0, int w1, const float *dsh) {
     for (int w = w0; w < w1; ++w) {
-        fwd_step<LIN, G, C, MF, IL>(bx, w, dsh);
-        __syncthreads();
+        fwd_step<LIN, G, C, MF, IL, TEAM>(bx, w, dsh);
+        step_sync<TEAM>(bx.tm);
     }
 }
 
 // A run of joint steps [t0, t1) sharing one step shape.  Span counts are
 // n - t (inside) and t + 1 (outside), both in [1, n+1].
-template <bool LIN, int G, int C, int MF, bool IL, typename T>
+template <bool LIN, int G, int C, int MF, bool IL, bool TEAM, typename T>
 __device__ __forceinline__ void io_run(const Bundle_ctx<T> &bx, int t0, int t1, const float *dsh) {
     for (int t = t0; t < t1; ++t) {
-        io_step<LIN, G, C, MF, IL>(bx, t, dsh);
-        __syncthreads();
+        io_step<LIN, G, C, MF, IL, TEAM>(bx, t, dsh);
+        step_sync<TEAM>(bx.tm);
     }
 }
 
@@ -525,7 +667,7 @@ __device__ __forceinline__ int next_rescale(int lo, int n) {
     return 0;
 }
 
-template <bool LIN, bool REV, typename T>
+template <bool LIN, bool REV, bool TEAM, typename T>
 __device__ void rescale_chart(const Bundle_ctx<T> &bx, int t0, float *dsh, float *dl);
 
 // The forward sweep alone: steps t = 1..n-1 (widths 2..n), one dispatch per
@@ -534,7 +676,7 @@ __device__ void rescale_chart(const Bundle_ctx<T> &bx, int t0, float *dsh, float
 // WIDE: workspace charts (longer sentences), which may need 16 terms per lane.
 // IL: interleaved span numbering (lane_at).
 // dl: per-sentence scratch for the rescales.
-template <bool LIN, bool WIDE, bool IL, typename T>
+template <bool LIN, bool WIDE, bool IL, bool TEAM, typename T>
 __device__ __forceinline__ void fwd_sweep(const Bundle_ctx<T> &bx, float *dsh, float *dl) {
     const int n = bx.n;
     for (int lo = 1; lo < n;) {
@@ -542,18 +684,18 @@ __device__ __forceinline__ void fwd_sweep(const Bundle_ctx<T> &bx, float *dsh, f
         const int hi = tr > 0 ? tr + 1 : n;   // steps [lo, hi), widths [lo + 1, hi + 1)
 #define CRF_FWD_FIXED(LO, HI, GG, CC, MM)                                                  \
         if (max(lo, LO) < min(hi, HI + 1))                                                 \
-            fwd_run<LIN, GG, CC, MM, IL>(bx, max(lo, LO) + 1, min(hi, HI + 1) + 1, dsh);
+            fwd_run<LIN, GG, CC, MM, IL, TEAM>(bx, max(lo, LO) + 1, min(hi, HI + 1) + 1, dsh);
         CRF_FIXED_RUNS(CRF_FWD_FIXED)
 #undef CRF_FWD_FIXED
         for (int t = max(lo, kFixedRunsMaxK + 1); t < hi;) {
             const StepShape sh = step_shape_k(t);
             const int t2 = min(shape_run_end(t), hi);
-#define CRF_FWD_RUN(GG, CC, MM) fwd_run<LIN, GG, CC, MM, IL>(bx, t + 1, t2 + 1, dsh)
+#define CRF_FWD_RUN(GG, CC, MM) fwd_run<LIN, GG, CC, MM, IL, TEAM>(bx, t + 1, t2 + 1, dsh)
             CRF_DISPATCH_WIDE_SHAPE(sh, CRF_FWD_RUN);
 #undef CRF_FWD_RUN
             t = t2;
         }
-        if (tr > 0) rescale_chart<LIN, false>(bx, tr, dsh, dl);
+        if (tr > 0) rescale_chart<LIN, false, TEAM>(bx, tr, dsh, dl);
         lo = hi;
     }
 }
@@ -605,15 +747,17 @@ constexpr float kShiftBand = 30.0f;
 // (times exp2 of these in the linear domain), d += delta.  Later steps add d
 // to each score as they read it; the root's O' stays 0.  dl holds delta per
 // sentence meanwhile.
-template <bool LIN, bool REV, typename T>
+template <bool LIN, bool REV, bool TEAM, typename T>
 __device__ void rescale_chart(const Bundle_ctx<T> &bx, int t0, float *dsh, float *dl) {
     const int n = bx.n, ld = bx.ld, nb = bx.nb, w0 = t0 + 1, S = n - t0;
-    const int tid = threadIdx.x;
+    // (every member of a team estimates the shifts from the whole chart,
+    // the same figures in the same order, then moves its share of cells)
+    const int tid = team_tid<TEAM>(bx.tm), nt = team_nt<TEAM>(bx.tm);
     by_sentence_groups(S, nb, [&](auto gs, int sb, int gl, bool valid) {
         constexpr int GS = decltype(gs)::value;
         const T *P = bx.chart0 + (size_t)sb * bx.cstride;
         auto val = [&](int i) {
-            const float a = P[i * ld + w0 - 1];
+            const float a = chart_ld<TEAM>(&P[i * ld + w0 - 1]);
             if constexpr (LIN) return fast_log2(a);   // (0 gives -inf, below NEG)
             else return a;
         };
@@ -638,7 +782,7 @@ __device__ void rescale_chart(const Bundle_ctx<T> &bx, int t0, float *dsh, float
             delta = -acc / (cnt * (float)(w0 - 1));
         if (valid && gl == 0) dl[sb] = delta;
     });
-    __syncthreads();
+    step_sync<TEAM>(bx.tm);   // every member has read the chart before any cell moves
     auto moved = [&](float x, float dk) {
         // linear domain: x exp2(dk), as ldexp by the integer part of dk times
         // exp2 of the rest, so that a factor beyond float32's range (dk can
@@ -654,14 +798,14 @@ __device__ void rescale_chart(const Bundle_ctx<T> &bx, int t0, float *dsh, float
     {
         const int A = w0 - 1, per = n * A, total = nb * per;
         const float inv_per = 1.0f / (float)per, inv_a = 1.0f / (float)A;
-        for (int f = tid; f < total; f += blockDim.x) {
+        for (int f = tid; f < total; f += nt) {
             const int sb = div_small(f, per, inv_per);
             const int r = f - sb * per;
             const int i = div_small(r, A, inv_a);
             const int w = 2 + r - i * A, j = i + w;
             if (j <= n) {
                 T *P = bx.chart0 + (size_t)sb * bx.cstride, *Q = P + (size_t)ld * ld;
-                const float a = moved(P[i * ld + w - 1], dl[sb] * (float)(w - 1));
+                const float a = moved(chart_ld<TEAM>(&P[i * ld + w - 1]), dl[sb] * (float)(w - 1));
                 P[i * ld + w - 1] = a;
                 Q[j * ld + n + 1 - w] = a;
             }
@@ -671,21 +815,21 @@ __device__ void rescale_chart(const Bundle_ctx<T> &bx, int t0, float *dsh, float
     if constexpr (REV) {
         const int per = (t0 + 1) * t0, total = nb * per;
         const float inv_per = 1.0f / (float)per, inv_t = 1.0f / (float)t0;
-        for (int f = tid; f < total; f += blockDim.x) {
+        for (int f = tid; f < total; f += nt) {
             const int sb = div_small(f, per, inv_per);
             const int r = f - sb * per;
             const int i = div_small(r, t0, inv_t);
             const int e = r - i * t0, v = n - t0 + e, j = i + v;
             if (i + e <= t0) {
                 T *P = bx.chart0 + (size_t)sb * bx.cstride, *Q = P + (size_t)ld * ld;
-                const float o = moved(Q[i * ld + v], dl[sb] * (float)(n - v));
+                const float o = moved(chart_ld<TEAM>(&Q[i * ld + v]), dl[sb] * (float)(n - v));
                 Q[i * ld + v] = o;
                 P[j * ld + n - v] = o;
             }
         }
     }
-    for (int sb = tid; sb < nb; sb += blockDim.x) dsh[sb] += dl[sb];
-    __syncthreads();
+    for (int sb = threadIdx.x; sb < nb; sb += blockDim.x) dsh[sb] += dl[sb];   // (each member's own copy)
+    step_sync<TEAM>(bx.tm);
 }
 
 // The joint sweep: steps t = 1..n-1 (inside widths 2..n, outside widths
@@ -694,7 +838,7 @@ __device__ void rescale_chart(const Bundle_ctx<T> &bx, int t0, float *dsh, float
 // of runs (with the short-bundle runs of 9..32 splits for bundles of at most
 // kShortBundleMaxN words), so that each run and the rescale appear once in
 // the code.
-template <bool LIN, bool WIDE, bool IL, typename T>
+template <bool LIN, bool WIDE, bool IL, bool TEAM, typename T>
 __device__ __forceinline__ void io_sweep(const Bundle_ctx<T> &bx, float *dsh, float *dl) {
     const int n = bx.n;
     for (int lo = 1; lo < n;) {
@@ -702,7 +846,7 @@ __device__ __forceinline__ void io_sweep(const Bundle_ctx<T> &bx, float *dsh, fl
         const int hi = tr > 0 ? tr + 1 : n;   // steps [lo, hi)
 #define CRF_IO_FIXED(LO, HI, GG, CC, MM)                              \
         if (max(lo, LO) < min(hi, HI + 1))                            \
-            io_run<LIN, GG, CC, MM, IL>(bx, max(lo, LO), min(hi, HI + 1), dsh);
+            io_run<LIN, GG, CC, MM, IL, TEAM>(bx, max(lo, LO), min(hi, HI + 1), dsh);
         CRF_FIXED_RUNS_LOW(CRF_IO_FIXED)
         if (!WIDE && n <= kShortBundleMaxN) {
             CRF_SHORT_RUNS_MID(CRF_IO_FIXED)
@@ -714,12 +858,12 @@ __device__ __forceinline__ void io_sweep(const Bundle_ctx<T> &bx, float *dsh, fl
         for (int t = max(lo, kFixedRunsMaxK + 1); t < hi;) {
             const StepShape sh = step_shape_k(t);
             const int t2 = min(shape_run_end(t), hi);
-#define CRF_IO_RUN(GG, CC, MM) io_run<LIN, GG, CC, MM, IL>(bx, t, t2, dsh)
+#define CRF_IO_RUN(GG, CC, MM) io_run<LIN, GG, CC, MM, IL, TEAM>(bx, t, t2, dsh)
             CRF_DISPATCH_WIDE_SHAPE(sh, CRF_IO_RUN);
 #undef CRF_IO_RUN
             t = t2;
         }
-        if (tr > 0) rescale_chart<LIN, true>(bx, tr, dsh, dl);
+        if (tr > 0) rescale_chart<LIN, true, TEAM>(bx, tr, dsh, dl);
         lo = hi;
     }
 }
@@ -769,13 +913,14 @@ struct Cell_walk {
 // unconditional -- at() names a cell of the bundle even past the end -- so
 // that no branch separates them (a load inside a branch is waited for
 // before the branch joins).
+// A team's member walks its share: virtual threads t of NT.
 template <int U, typename AD, typename LD, typename F>
-__device__ __forceinline__ void for_cells_loaded(int nb, int n, AD &&addr, LD &&load, F &&use) {
-    const int NT = blockDim.x;
+__device__ __forceinline__ void for_cells_loaded(int nb, int n, AD &&addr, LD &&load, F &&use,
+                                                 int t = threadIdx.x, int NT = blockDim.x) {
     const Cell_walk cw(nb, n);
     using A = decltype(addr(0, 0, 1));
     using V = decltype(load(addr(0, 0, 1)));
-    for (int c0 = threadIdx.x; c0 < cw.total; c0 += NT * U) {
+    for (int c0 = t; c0 < cw.total; c0 += NT * U) {
         A a[U];
         V v[U];
         int cell[U];   // sb << 20 | i << 10 | j (sb < 256, i, j < 1024), or -1
@@ -931,7 +1076,7 @@ __device__ __forceinline__ bool inside_block_impl(const KernelPlan &p, int block
                                                   const float *__restrict__ grad,
                                                   float *__restrict__ logZ, float *__restrict__ marg,
                                                   const int32_t *__restrict__ gold,
-                                                  float *__restrict__ loss) {
+                                                  float *__restrict__ loss, const Team &tm) {
     static_assert(!GOLD || REV, "the gold-tree loss needs the marginals");
     static_assert(!LAB || (!SPILL && !GOLD), "label I/O is for labelled bundles in LDS");
     __shared__ int lin_ovf;
@@ -981,7 +1126,8 @@ __device__ __forceinline__ bool inside_block_impl(const KernelPlan &p, int block
         if (tid < nb) sid[tid] = id0;
     }
     const int ld = lay.ld;
-    const Bundle_ctx<float> bx{chart0, cstride, n, ld, nb, mnb, lay.e, LIN ? &lin_ovf : nullptr};
+    const Bundle_ctx<float> bx{chart0, cstride, n, ld, nb, mnb, lay.e, LIN ? &lin_ovf : nullptr, tm};
+    const bool coh = SPILL && tm.k > 1;   // a team's chart reads (chart_ld)
     if (tid == 0) lin_ovf = 0;
     __syncthreads();
     // (gv holds the rescales' per-sentence shifts during the sweep and the
@@ -1040,9 +1186,9 @@ __device__ __forceinline__ bool inside_block_impl(const KernelPlan &p, int block
         else
             for_cells_loaded<8>(nb, n, score_at, load_score, put_score);
     } else {
-        for_cells_loaded<8>(nb, n, score_at, load_score, put_score);
+        for_cells_loaded<8>(nb, n, score_at, load_score, put_score, team_tid<SPILL>(tm), team_nt<SPILL>(tm));
     }
-    __syncthreads();
+    step_sync<SPILL>(tm);
     // Forced-span sums, a lane group per sentence, fixed order (deterministic).
     // The linear domain also seeds each sentence's shift d from its scores:
     // for independent scores of mean m and variance v (log2 units) the
@@ -1054,8 +1200,8 @@ __device__ __forceinline__ bool inside_block_impl(const KernelPlan &p, int block
         constexpr int GS = decltype(gs)::value;
         const float *P = chart0 + (size_t)sb * cstride;
         double acc = 0.0;
-        for (int i = gl; i < n; i += GS) acc += (double)P[(i + 1) * ld + n - 1];
-        if (gl == 0 && n >= 2) acc += (double)P[n];
+        for (int i = gl; i < n; i += GS) acc += (double)chart_ld_if(&P[(i + 1) * ld + n - 1], coh);
+        if (gl == 0 && n >= 2) acc += (double)chart_ld_if(&P[n], coh);
         acc = grp_sum_d<GS>(acc);
         if (valid && gl == 0) forced[sb] = acc;
         if constexpr (LIN) {
@@ -1063,7 +1209,7 @@ __device__ __forceinline__ bool inside_block_impl(const KernelPlan &p, int block
             for (int i = gl; i < n - 1; i += GS)
                 for (int w = 2; w <= 9 && i + w <= n; ++w) {
                     if (i == 0 && w == n) continue;   // the root: forced
-                    const float x = P[i * ld + w - 1];
+                    const float x = chart_ld_if(&P[i * ld + w - 1], coh);
                     if (x > -1000.f) {
                         s1 += x;
                         s2 += x * x;
@@ -1084,21 +1230,38 @@ __device__ __forceinline__ bool inside_block_impl(const KernelPlan &p, int block
     // Workspace charts lay spans side by side; LDS charts interleave them
     // when their layout allows (e = 0).
     if constexpr (!REV) {
-        if constexpr (SPILL) fwd_sweep<LIN, true, false>(bx, dsh, gv);
-        else if (lay.e == 0) fwd_sweep<LIN, false, true>(bx, dsh, gv);
-        else fwd_sweep<LIN, false, false>(bx, dsh, gv);
+        if constexpr (SPILL) {
+            if (tm.k > 1) fwd_sweep<LIN, true, false, true>(bx, dsh, gv);
+            else fwd_sweep<LIN, true, false, false>(bx, dsh, gv);
+        } else if (lay.e == 0) fwd_sweep<LIN, false, true, false>(bx, dsh, gv);
+        else fwd_sweep<LIN, false, false, false>(bx, dsh, gv);
     } else {
-        if constexpr (SPILL) io_sweep<LIN, true, false>(bx, dsh, gv);
-        else if (lay.e == 0) io_sweep<LIN, false, true>(bx, dsh, gv);
-        else io_sweep<LIN, false, false>(bx, dsh, gv);
+        if constexpr (SPILL) {
+            if (tm.k > 1) io_sweep<LIN, true, false, true>(bx, dsh, gv);
+            else io_sweep<LIN, true, false, false>(bx, dsh, gv);
+        } else if (lay.e == 0) io_sweep<LIN, false, true, false>(bx, dsh, gv);
+        else io_sweep<LIN, false, false, false>(bx, dsh, gv);
     }
     // (the sweep's last barrier published the chart and the flag)
     if constexpr (LIN) {
         for (int sb = tid; sb < nb; sb += NT) {
-            const float r = chart0[(size_t)sb * cstride + n - 1];
+            const float r = chart_ld_if(&chart0[(size_t)sb * cstride + n - 1], coh);
             if (!(r >= kLinMin && r <= kLinMax)) lin_ovf = 1;
         }
         __syncthreads();
+        if constexpr (SPILL) {
+            if (tm.k > 1) {
+                // One decision for the team: a member that saw a value
+                // leave the range raises the team's word to this job + 1
+                // (later jobs raise it only after this barrier's readers
+                // are done, so the word needs no clearing).
+                int32_t *fl = tm.line + 1;
+                if (tid == 0 && lin_ovf) atomicMax(fl, tm.job + 1);
+                team_sync(tm);
+                if (tid == 0 && load_coherent(fl) > tm.job) lin_ovf = 1;
+                __syncthreads();
+            }
+        }
         if (lin_ovf) return false;   // nothing written yet: the log domain redoes the bundle
     }
     for (int t = tid; t < nb; t += NT) gv[t] = grad ? grad[sid[t]] : 1.0f;
@@ -1106,20 +1269,24 @@ __device__ __forceinline__ bool inside_block_impl(const KernelPlan &p, int block
     // log Z = (alpha~(0,n) - (n-2) d) ln 2 + forced sum, alpha~(0,n) the
     // root's log2 value.
     auto log_z = [&](int sb) {
-        const float r = chart0[(size_t)sb * cstride + n - 1];
+        const float r = chart_ld_if(&chart0[(size_t)sb * cstride + n - 1], coh);
         const double lr = LIN ? log2_split(r) : (double)r;
         const double z2 = lr - (double)dsh[sb] * (n >= 2 ? n - 2 : 0);
         return z2 * LN2_D + forced[sb];
     };
-    if (logZ != nullptr)
-        for (int sb = tid; sb < nb; sb += NT) logZ[sid[sb]] = (float)log_z(sb);
+    if (logZ != nullptr && tm.rank == 0) {
+        const bool aborted = SPILL && team_aborted(tm);
+        for (int sb = tid; sb < nb; sb += NT)
+            logZ[sid[sb]] = aborted ? __builtin_bit_cast(float, 0x7fc00000) : (float)log_z(sb);
+    }
     if constexpr (!REV) return true;
 
     if constexpr (GOLD) {
         // Gold rows of each sentence: mark the span, sum its score (float64,
         // a lane group per sentence in a fixed order), loss = log Z - sum.
+        // (a team's first member marks and sums)
         const int R = 2 * (N1 - 1) - 1, rows = 2 * n - 1;
-        by_sentence_groups(rows, nb, [&](auto gs, int sb, int gl, bool valid) {
+        if (tm.rank == 0) by_sentence_groups(rows, nb, [&](auto gs, int sb, int gl, bool valid) {
             constexpr int GS = decltype(gs)::value;
             float *P = chart0 + (size_t)sb * cstride;
             const int32_t *g2 = gold + (size_t)sid[sb] * R * 2;
@@ -1134,7 +1301,7 @@ __device__ __forceinline__ bool inside_block_impl(const KernelPlan &p, int block
             acc = grp_sum_d<GS>(acc);
             if (valid && gl == 0) loss[sid[sb]] = (float)(log_z(sb) - acc);
         });
-        __syncthreads();
+        step_sync<SPILL>(tm);
     }
 
     // Epilogue: marginals of the valid cells (coalesced stores along rows),
@@ -1150,9 +1317,11 @@ __device__ __forceinline__ bool inside_block_impl(const KernelPlan &p, int block
         const bool forced_span = (j == i + 1) || (i == 0 && j == n);
         const int w = j - i;
         float mu = gv[sb];
-        if (!forced_span) mu *= fast_exp2(((lg(P[i * ld + w - 1]) - lg(P[n - 1])) + lg(Q[i * ld + w])) - (own2 + dsh[sb]));
+        if (!forced_span)
+            mu *= fast_exp2(((lg(chart_ld_if(&P[i * ld + w - 1], coh)) - lg(chart_ld_if(&P[n - 1], coh))) +
+                             lg(chart_ld_if(&Q[i * ld + w], coh))) - (own2 + dsh[sb]));
         if constexpr (GOLD)
-            if (__builtin_bit_cast(int, P[j * ld + n - w]) == kGoldMark) mu -= gv[sb];
+            if (__builtin_bit_cast(int, chart_ld_if(&P[j * ld + n - w], coh)) == kGoldMark) mu -= gv[sb];
         return mu;
     };
     if constexpr (LAB) if (lab) {
@@ -1198,9 +1367,12 @@ __device__ __forceinline__ bool inside_block_impl(const KernelPlan &p, int block
         }
         return true;
     }
-    for_cells_loaded<8>(nb, n, score_at, load_score, [&](int sb, int i, int j, float s) {
-        marg[(size_t)sid[sb] * sent_stride + (size_t)i * row_stride + j] = span_mu(sb, i, j, s * LOG2E_F);
-    });
+    for_cells_loaded<8>(
+        nb, n, score_at, load_score,
+        [&](int sb, int i, int j, float s) {
+            marg[(size_t)sid[sb] * sent_stride + (size_t)i * row_stride + j] = span_mu(sb, i, j, s * LOG2E_F);
+        },
+        team_tid<SPILL>(tm), team_nt<SPILL>(tm));
     return true;
 }
 
@@ -1212,11 +1384,12 @@ __device__ __forceinline__ void inside_block(const KernelPlan &p, int block, con
                                              const float *__restrict__ grad,
                                              float *__restrict__ logZ, float *__restrict__ marg,
                                              const int32_t *__restrict__ gold = nullptr,
-                                             float *__restrict__ loss = nullptr) {
-    if (inside_block_impl<true, REV, SPILL, GOLD, LAB>(p, block, rec, smem_raw, scores, grad, logZ, marg, gold, loss))
+                                             float *__restrict__ loss = nullptr, const Team &tm = Team{}) {
+    if (inside_block_impl<true, REV, SPILL, GOLD, LAB>(p, block, rec, smem_raw, scores, grad, logZ, marg, gold, loss,
+                                                       tm))
         return;
     __syncthreads();   // every thread has left the linear attempt
-    inside_block_impl<false, REV, SPILL, GOLD, LAB>(p, block, rec, smem_raw, scores, grad, logZ, marg, gold, loss);
+    inside_block_impl<false, REV, SPILL, GOLD, LAB>(p, block, rec, smem_raw, scores, grad, logZ, marg, gold, loss, tm);
 }
 
 // ---------------------------------------------------------------------------
@@ -1232,6 +1405,7 @@ struct Cky_ctx {
     int n, ld, nb;
     uint32_t mnb;     // div_magic(nb)
     bool split_lds;   // split tables in LDS (else in global memory)
+    Team tm;          // workspace sentences: the team running the pass
     __device__ double *beta(int sb) const {   // (sb < 256, cstride < 2^24)
         return reinterpret_cast<double *>(chart0 + __umul24((uint32_t)sb, (uint32_t)cstride));
     }
@@ -1248,13 +1422,14 @@ struct Cky_ctx {
             *(__attribute__((address_space(1))) SP *)q = (SP)v;
         }
     }
-    __device__ int get_split(int sb, int e) const {
+    __device__ int get_split(int sb, int e, bool coherent = false) const {
         if (split_lds) {
             const uint32_t a = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char *)split0 +
                                __umul24((uint32_t)sb, (uint32_t)sstride) + (uint32_t)e * sizeof(SP);
             return (int)*(const __attribute__((address_space(3))) SP *)(uintptr_t)a;
         }
         const SP *q = reinterpret_cast<const SP *>(split0 + (size_t)sb * sstride) + e;
+        if (coherent) return (int)chart_ld<true>(q);
         return (int)*(const __attribute__((address_space(1))) SP *)q;
     }
 };
@@ -1283,9 +1458,9 @@ __device__ __forceinline__ Arg_max tree_arg_max(const double *x, int c0, int G) 
 // sp0 + i).  Each lane keeps its running max and the first of its terms to
 // reach it; the group then takes the lowest split among its lanes at the
 // group's max.
-template <int G, int C, int MF, bool IL, typename SP>
+template <int G, int C, int MF, bool IL, bool TEAM, typename SP>
 __device__ __forceinline__ void cky_step(const Cky_ctx<SP> &cx, int w, int sp0) {
-    const int tid = threadIdx.x, nt = blockDim.x;
+    const int tid = team_tid<TEAM>(cx.tm), nt = team_nt<TEAM>(cx.tm);
     const int n = cx.n, ld = cx.ld;
     const int K = w - 1, nsp = cx.nb * (n - w + 1);
     const int total = region_lanes<G, IL, 16>(nsp);
@@ -1300,7 +1475,7 @@ __device__ __forceinline__ void cky_step(const Cky_ctx<SP> &cx, int w, int sp0) 
         const int rb = (int)__umul24((uint32_t)i, (uint32_t)(ld + 1));   // [i][i]
         const int cb = rb + (int)__umul24((uint32_t)w, (uint32_t)ld);    // [j][i]
         const int rowo = rb + 1 + l, colo = cb + 1 + l;
-        const double sij = be[rb + w];
+        const double sij = chart_ld<TEAM>(&be[rb + w]);
         const int kl = K - l;
         // Terms in chunks of 16 (the last one shorter).  Up to 16 splits per
         // lane (one chunk), every float64 operand is loaded before the first
@@ -1314,8 +1489,8 @@ __device__ __forceinline__ void cky_step(const Cky_ctx<SP> &cx, int w, int sp0) 
             double xr[CN], xc[CN];
 #pragma unroll
             for (int c = 0; c < CN; ++c) {
-                xr[c] = be[rowo + (c0 + c) * G];
-                xc[c] = be[colo + (c0 + c) * G];
+                xr[c] = chart_ld<TEAM>(&be[rowo + (c0 + c) * G]);
+                xc[c] = chart_ld<TEAM>(&be[colo + (c0 + c) * G]);
             }
             if constexpr (C <= 16) __builtin_amdgcn_sched_barrier(0);
             double x[CN];
@@ -1355,25 +1530,25 @@ __device__ __forceinline__ void cky_step(const Cky_ctx<SP> &cx, int w, int sp0) 
     }
 }
 
-template <int G, int C, int MF, bool IL, typename SP>
+template <int G, int C, int MF, bool IL, bool TEAM, typename SP>
 __device__ __forceinline__ void cky_run(const Cky_ctx<SP> &cx, int w0, int w1) {
     for (int w = w0; w < w1; ++w) {
-        cky_step<G, C, MF, IL>(cx, w, cky_split_index(cx.n, w, 0));
-        __syncthreads();
+        cky_step<G, C, MF, IL, TEAM>(cx, w, cky_split_index(cx.n, w, 0));
+        step_sync<TEAM>(cx.tm);
     }
 }
 
-template <bool WIDE, bool IL, typename SP>
+template <bool WIDE, bool IL, bool TEAM, typename SP>
 __device__ __forceinline__ void cky_sweep(const Cky_ctx<SP> &cx) {
     const int n = cx.n;
 #define CRF_CKY_FIXED(LO, HI, GG, CC, MM) \
-    if (n >= LO + 1) cky_run<GG, CC, MM, IL>(cx, LO + 1, min(HI + 2, n + 1));
+    if (n >= LO + 1) cky_run<GG, CC, MM, IL, TEAM>(cx, LO + 1, min(HI + 2, n + 1));
     CRF_CKY_FIXED_RUNS(CRF_CKY_FIXED)
 #undef CRF_CKY_FIXED
     for (int w = kFixedRunsMaxK + 2; w <= n;) {
         const StepShape sh = step_shape_k(w - 1);
         const int w2 = min(shape_run_end(w - 1) + 1, n + 1);
-#define CRF_CKY_RUN(GG, CC, MM) cky_run<GG, CC, MM, IL>(cx, w, w2)
+#define CRF_CKY_RUN(GG, CC, MM) cky_run<GG, CC, MM, IL, TEAM>(cx, w, w2)
         CRF_DISPATCH_WIDE_SHAPE(sh, CRF_CKY_RUN);
 #undef CRF_CKY_RUN
         w = w2;
@@ -1383,7 +1558,7 @@ __device__ __forceinline__ void cky_sweep(const Cky_ctx<SP> &cx) {
 // Order one wavefront's LDS accesses across its lanes.
 template <typename SP>
 __device__ __forceinline__ int split_of(const Cky_ctx<SP> &cx, int sb, int i, int j) {
-    return i + 1 + cx.get_split(sb, cky_split_index(cx.n, j - i, i));
+    return i + 1 + cx.get_split(sb, cky_split_index(cx.n, j - i, i), cx.tm.k > 1);
 }
 
 // Write the trees of all the bundle's sentences in preorder (the 2n-1 rows
@@ -1439,7 +1614,8 @@ template <bool SPILL, bool LAB = false>
 __device__ __forceinline__ void cky_block(const KernelPlan &p, int block, const int32_t *rec, char *smem_raw,
                                           const float *__restrict__ scores,
                                           int32_t *__restrict__ spans, float *__restrict__ best,
-                                          int32_t *__restrict__ labels = nullptr, bool second = false) {
+                                          int32_t *__restrict__ labels = nullptr, bool second = false,
+                                          const Team &tm = Team{}) {
     __shared__ int spill_id[1];
     const int NT = blockDim.x;
     const int tid = threadIdx.x;
@@ -1480,7 +1656,8 @@ __device__ __forceinline__ void cky_block(const KernelPlan &p, int block, const 
     }
     const int ld = lay.ld;
     typedef typename std::conditional<SPILL, uint16_t, uint8_t>::type SP;
-    const Cky_ctx<SP> cx{chart0, cstride, split0, sstride, n, ld, nb, mnb, !SPILL && split_lds};
+    const Cky_ctx<SP> cx{chart0, cstride, split0, sstride, n, ld, nb, mnb, !SPILL && split_lds, tm};
+    const bool coh = SPILL && tm.k > 1;   // a team's chart reads (chart_ld)
     __syncthreads();
 
     auto score_at = [&](int sb, int i, int j) -> const float * {
@@ -1497,13 +1674,16 @@ __device__ __forceinline__ void cky_block(const KernelPlan &p, int block, const 
         be[i * ld + j] = s;
         if (j == i + 1) be[j * ld + i] = s;
     };
-    for_cells_loaded<LAB ? 1 : 8>(nb, n, score_at, load_score, put_score);
-    __syncthreads();
+    for_cells_loaded<LAB ? 1 : 8>(nb, n, score_at, load_score, put_score, team_tid<SPILL>(tm), team_nt<SPILL>(tm));
+    step_sync<SPILL>(tm);
     // Workspace charts lay spans side by side; LDS charts interleave them
     // when their layout allows (e = 0).
-    if constexpr (SPILL) cky_sweep<true, false>(cx);
-    else if (lay.e == 0) cky_sweep<false, true>(cx);
-    else cky_sweep<false, false>(cx);
+    if constexpr (SPILL) {
+        if (tm.k > 1) cky_sweep<true, false, true>(cx);
+        else cky_sweep<true, false, false>(cx);
+    } else if (lay.e == 0) cky_sweep<false, true, false>(cx);
+    else cky_sweep<false, false, false>(cx);
+    if (tm.rank != 0) return;   // a team's first member writes the outputs
 
     const int R = 2 * (N1 - 1) - 1;
     const int pad_rows = R - (2 * n - 1);   // rows past the tree are -1
@@ -1518,8 +1698,11 @@ __device__ __forceinline__ void cky_block(const KernelPlan &p, int block, const 
             if constexpr (LAB) labels[(size_t)sid[sbb] * R + r] = -1;
         }
     }
-    if (best != nullptr)
-        for (int sb = tid; sb < nb; sb += NT) best[sid[sb]] = (float)cx.beta(sb)[n];
+    if (best != nullptr) {
+        const bool aborted = SPILL && team_aborted(tm);
+        for (int sb = tid; sb < nb; sb += NT)
+            best[sid[sb]] = aborted ? __builtin_bit_cast(float, 0x7fc00000) : (float)chart_ld_if(&cx.beta(sb)[n], coh);
+    }
     // (the sweep's last barrier published the splits)
     walk_trees<LAB>(cx, sid, spans, R, labels, scores, N1, L);
 }
@@ -1527,15 +1710,26 @@ __device__ __forceinline__ void cky_block(const KernelPlan &p, int block, const 
 // Workgroups of 256, 512 or 1024 threads (the plan's choice) share one
 // build of each kernel.  LAB: the labelled plans' bundle kernel, whose
 // bundles marked kRecLab read and write their own label scores.
-template <bool REV, bool SPILL, bool LAB = false>
+template <bool REV, bool SPILL, bool LAB = false, bool TEAM = false>
 __global__ __launch_bounds__(kThreadsMax) void inside_kernel(KernelPlan p, const float *__restrict__ scores,
                                                              const float *__restrict__ grad,
                                                              float *__restrict__ logZ,
                                                              float *__restrict__ marg) {
     extern __shared__ __align__(16) char smem_raw[];
-    inside_block<REV, SPILL, false, LAB>(p, blockIdx.x,
-                                         SPILL ? nullptr : p.inside.recs + (size_t)blockIdx.x * p.rec_stride,
-                                         smem_raw, scores, grad, logZ, marg);
+    if constexpr (SPILL && !TEAM) {
+        inside_block<REV, true, false, LAB>(p, blockIdx.x, nullptr, smem_raw, scores, grad, logZ, marg);
+    } else if constexpr (SPILL) {
+        Team tm;
+        int job, stride;
+        if (!spill_jobs(p, tm, job, stride)) return;
+        for (; job < p.inside.n_spill; job += stride, ++tm.job) {
+            inside_block<REV, true, false, LAB>(p, job, nullptr, smem_raw, scores, grad, logZ, marg, nullptr, nullptr,
+                                                tm);
+            __syncthreads();
+        }
+    } else
+        inside_block<REV, false, false, LAB>(p, blockIdx.x, p.inside.recs + (size_t)blockIdx.x * p.rec_stride,
+                                             smem_raw, scores, grad, logZ, marg);
 }
 
 // Labelled scores [B][N1][N1][L] of the sentences whose bundles leave their
@@ -1647,26 +1841,47 @@ __global__ __launch_bounds__(kLabelChunk) void label_expand_kernel(KernelPlan p,
 
 // The gold-tree loss: the inside kernel with marginals, minus the gold
 // indicator (inside_block, GOLD).
-template <bool SPILL>
+template <bool SPILL, bool TEAM = false>
 __global__ __launch_bounds__(kThreadsMax) void loss_kernel(KernelPlan p, const float *__restrict__ scores,
                                                            const int32_t *__restrict__ gold,
                                                            const float *__restrict__ grad,
                                                            float *__restrict__ loss,
                                                            float *__restrict__ marg) {
     extern __shared__ __align__(16) char smem_raw[];
-    inside_block<true, SPILL, true>(p, blockIdx.x,
-                                           SPILL ? nullptr : p.inside.recs + (size_t)blockIdx.x * p.rec_stride,
-                                           smem_raw, scores, grad, nullptr, marg, gold, loss);
+    if constexpr (SPILL && !TEAM) {
+        inside_block<true, true, true>(p, blockIdx.x, nullptr, smem_raw, scores, grad, nullptr, marg, gold, loss);
+    } else if constexpr (SPILL) {
+        Team tm;
+        int job, stride;
+        if (!spill_jobs(p, tm, job, stride)) return;
+        for (; job < p.inside.n_spill; job += stride, ++tm.job) {
+            inside_block<true, true, true>(p, job, nullptr, smem_raw, scores, grad, nullptr, marg, gold, loss, tm);
+            __syncthreads();
+        }
+    } else
+        inside_block<true, false, true>(p, blockIdx.x, p.inside.recs + (size_t)blockIdx.x * p.rec_stride, smem_raw,
+                                        scores, grad, nullptr, marg, gold, loss);
 }
 
-template <bool SPILL, bool LAB>
+template <bool SPILL, bool LAB, bool TEAM = false>
 __global__ __launch_bounds__(kThreadsMax) void cky_kernel(KernelPlan p, const float *__restrict__ scores,
                                                           int32_t *__restrict__ spans,
                                                           float *__restrict__ best,
                                                           int32_t *__restrict__ labels) {
     extern __shared__ __align__(16) char smem_raw[];
-    cky_block<SPILL, LAB>(p, blockIdx.x, SPILL ? nullptr : p.cky.recs + (size_t)blockIdx.x * p.rec_stride,
-                          smem_raw, scores, spans, best, labels);
+    if constexpr (SPILL && !TEAM) {
+        cky_block<true, LAB>(p, blockIdx.x, nullptr, smem_raw, scores, spans, best, labels);
+    } else if constexpr (SPILL) {
+        Team tm;
+        int job, stride;
+        if (!spill_jobs(p, tm, job, stride)) return;
+        for (; job < p.cky.n_spill; job += stride, ++tm.job) {
+            cky_block<true, LAB>(p, job, nullptr, smem_raw, scores, spans, best, labels, false, tm);
+            __syncthreads();
+        }
+    } else
+        cky_block<false, LAB>(p, blockIdx.x, p.cky.recs + (size_t)blockIdx.x * p.rec_stride, smem_raw, scores, spans,
+                              best, labels);
 }
 
 // Claim the next bundle of a persistent launch over n_rec records (see
@@ -1683,20 +1898,34 @@ __device__ __forceinline__ int claim_next(int32_t *counter, int n_rec, int *slot
     return cur;
 }
 
-// The workspace-chart sentences of the fused pass in one launch: workgroup
+// The workspace-chart sentences of the fused pass in one launch: job
 // b < inside.n_spill runs the inside sweep with the marginals of the b-th
 // such sentence, the others run CKY, so that a long sentence's two passes
-// run side by side on two CUs (their workspace charts are disjoint: the CKY
-// schedule's follow the inside schedule's).
+// run side by side on different CUs (their workspace charts are disjoint:
+// the CKY schedule's follow the inside schedule's).
+template <bool TEAM>
 __global__ __launch_bounds__(kThreadsMax) void spill_parse_kernel(KernelPlan p, const float *__restrict__ scores,
                                                                   const float *__restrict__ grad,
                                                                   float *__restrict__ logZ, float *__restrict__ marg,
                                                                   int32_t *__restrict__ spans,
                                                                   float *__restrict__ best) {
     extern __shared__ __align__(16) char smem_raw[];
-    const int b = (int)blockIdx.x;
-    if (b < p.inside.n_spill) inside_block<true, true>(p, b, nullptr, smem_raw, scores, grad, logZ, marg);
-    else cky_block<true>(p, b - p.inside.n_spill, nullptr, smem_raw, scores, spans, best);
+    if constexpr (!TEAM) {   // a workgroup per job
+        const int b = (int)blockIdx.x;
+        if (b < p.inside.n_spill) inside_block<true, true>(p, b, nullptr, smem_raw, scores, grad, logZ, marg);
+        else cky_block<true>(p, b - p.inside.n_spill, nullptr, smem_raw, scores, spans, best);
+        return;
+    }
+    Team tm;
+    int job, stride;
+    if (!spill_jobs(p, tm, job, stride)) return;
+    for (; job < p.inside.n_spill + p.cky.n_spill; job += stride, ++tm.job) {
+        if (job < p.inside.n_spill)
+            inside_block<true, true>(p, job, nullptr, smem_raw, scores, grad, logZ, marg, nullptr, nullptr, tm);
+        else
+            cky_block<true>(p, job - p.inside.n_spill, nullptr, smem_raw, scores, spans, best, nullptr, false, tm);
+        __syncthreads();
+    }
 }
 
 // MBR decoding (Sec. 3.3) in one launch: each bundle runs the inside sweep
@@ -1829,10 +2058,29 @@ hipError_t launch_parse_scratch(const KernelPlan &p, char *scr, const float *sco
     KernelPlan q = p;
     q.counter = reinterpret_cast<int32_t *>(scr);
     q.ws = scr + kScratchCounterBytes;
+    q.team_area = nullptr;   // workspace sentences on lone workgroups: no memory beyond the scratch
     hipLaunchKernelGGL(zero_words, dim3(1), dim3(64), 0, stream, q.counter, (int)(kScratchCounterBytes / 4));
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     return launch_parse(q, scores, grad, logZ, marg, spans, best, stream);
+}
+
+int spill_blocks_per_cu() {
+    const void *fns[] = {
+        (const void *)inside_kernel<false, true, false, true>, (const void *)inside_kernel<true, true, false, true>,
+        (const void *)cky_kernel<true, false, true>,           (const void *)cky_kernel<true, true, true>,
+        (const void *)loss_kernel<true, true>,                 (const void *)spill_parse_kernel<true>,
+    };
+    int least = 1 << 30;
+    for (const void *f : fns) {
+        int nb = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, f, kThreadsMax, 0) != hipSuccess) {
+            (void)hipGetLastError();
+            return 0;
+        }
+        least = nb < least ? nb : least;
+    }
+    return least;
 }
 
 hipError_t set_kernel_attributes(int max_lds_bytes) {
@@ -1852,14 +2100,38 @@ hipError_t set_kernel_attributes(int max_lds_bytes) {
                                (int)(kLabelWaves * (kLabelRowChunk + CRF_MAX_LABELS) * sizeof(float)));
 }
 
-template <bool SPILL, bool LAB = false>
+template <bool SPILL, bool LAB = false, bool TEAM = false>
 static void launch_inside_k(const KernelPlan &p, dim3 grid, int threads, size_t lds, hipStream_t s,
                             const float *scores, const float *grad, float *logZ, float *marg) {
     const dim3 block(threads);
     if (marg != nullptr)
-        hipLaunchKernelGGL((inside_kernel<true, SPILL, LAB>), grid, block, lds, s, p, scores, grad, logZ, marg);
+        hipLaunchKernelGGL((inside_kernel<true, SPILL, LAB, TEAM>), grid, block, lds, s, p, scores, grad, logZ, marg);
     else
-        hipLaunchKernelGGL((inside_kernel<false, SPILL, LAB>), grid, block, lds, s, p, scores, grad, logZ, marg);
+        hipLaunchKernelGGL((inside_kernel<false, SPILL, LAB, TEAM>), grid, block, lds, s, p, scores, grad, logZ, marg);
+}
+
+// Shape of a workspace launch of `jobs` sentence passes.  With a team area,
+// teams of k workgroups, k a power of two up to kTeamMaxK: m = ceil(jobs / 8)
+// teams per XCD (workgroups go to the eight XCDs in turn), k as large as the
+// workgroups the device holds at once allow (a team barrier needs every
+// member resident; the grid joins first), and the team area cleared by a
+// kernel before the launch.  Otherwise (no area, or k below kTeamMinK: many
+// workspace sentences, which fill the chip without teams) a workgroup per
+// job.
+static hipError_t spill_launch_shape(KernelPlan &q, int jobs, hipStream_t stream, dim3 *grid) {
+    const int m = (jobs + 7) / 8;
+    int k = 1;
+    if (q.team_area != nullptr && jobs >= 1 && 8 * m <= kTeamMaxTeams)
+        while (2 * k <= kTeamMaxK && (int64_t)8 * m * 2 * k <= q.team_cap) k *= 2;
+    if (k < kTeamMinK) {
+        q.team_k = 1;
+        *grid = dim3(jobs);
+        return hipSuccess;
+    }
+    q.team_k = k;
+    *grid = dim3(8 * m * k);
+    hipLaunchKernelGGL(zero_words, dim3(1), dim3(256), 0, stream, q.team_area, kTeamHeaderWords + kTeamLineWords * 8 * m);
+    return hipGetLastError();
 }
 
 // The bundles' launch and the workspace sentences' launch of one inside pass.
@@ -1873,7 +2145,11 @@ static hipError_t launch_inside_sweeps(const KernelPlan &p, const float *scores,
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     if (q.n_spill > 0) {
-        launch_inside_k<true>(p, dim3(q.n_spill), kThreadsMax, 0, stream, scores, grad, logZ, marg);
+        KernelPlan t = p;
+        dim3 grid;
+        if ((e = spill_launch_shape(t, q.n_spill, stream, &grid)) != hipSuccess) return e;
+        if (t.team_k > 1) launch_inside_k<true, false, true>(t, grid, kThreadsMax, 0, stream, scores, grad, logZ, marg);
+        else launch_inside_k<true>(t, grid, kThreadsMax, 0, stream, scores, grad, logZ, marg);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     return hipSuccess;
@@ -1923,8 +2199,14 @@ static hipError_t launch_cky_k(const KernelPlan &p, const float *scores, int32_t
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     if (q.n_spill > 0) {
-        hipLaunchKernelGGL((cky_kernel<true, LAB>), dim3(q.n_spill), dim3(kThreadsMax), 0, stream, p, scores, spans,
-                           best, labels);
+        KernelPlan t = p;
+        dim3 grid;
+        if ((e = spill_launch_shape(t, q.n_spill, stream, &grid)) != hipSuccess) return e;
+        if (t.team_k > 1)
+            hipLaunchKernelGGL((cky_kernel<true, LAB, true>), grid, dim3(kThreadsMax), 0, stream, t, scores, spans, best,
+                               labels);
+        else
+            hipLaunchKernelGGL((cky_kernel<true, LAB>), grid, dim3(kThreadsMax), 0, stream, t, scores, spans, best, labels);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     return hipSuccess;
@@ -1953,10 +2235,18 @@ hipError_t launch_mbr(const KernelPlan &p, const float *scores, float *logZ, flo
     // CKY workspace lists hold the same sentences): their marginals, then
     // CKY over them
     if (p.inside.n_spill > 0) {
-        launch_inside_k<true>(p, dim3(p.inside.n_spill), kThreadsMax, 0, stream, scores, nullptr, logZ, marg);
+        KernelPlan t = p;
+        dim3 grid;
+        if ((e = spill_launch_shape(t, p.inside.n_spill, stream, &grid)) != hipSuccess) return e;
+        if (t.team_k > 1) launch_inside_k<true, false, true>(t, grid, kThreadsMax, 0, stream, scores, nullptr, logZ, marg);
+        else launch_inside_k<true>(t, grid, kThreadsMax, 0, stream, scores, nullptr, logZ, marg);
         if ((e = hipGetLastError()) != hipSuccess) return e;
-        hipLaunchKernelGGL((cky_kernel<true, false>), dim3(p.cky.n_spill), dim3(kThreadsMax), 0, stream, p, marg, spans,
-                           best, nullptr);
+        if ((e = spill_launch_shape(t, p.cky.n_spill, stream, &grid)) != hipSuccess) return e;
+        if (t.team_k > 1)
+            hipLaunchKernelGGL((cky_kernel<true, false, true>), grid, dim3(kThreadsMax), 0, stream, t, marg, spans, best,
+                               nullptr);
+        else
+            hipLaunchKernelGGL((cky_kernel<true, false>), grid, dim3(kThreadsMax), 0, stream, t, marg, spans, best, nullptr);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     return hipSuccess;
@@ -1972,8 +2262,15 @@ hipError_t launch_loss(const KernelPlan &p, const float *scores, const int32_t *
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     if (q.n_spill > 0) {
-        hipLaunchKernelGGL((loss_kernel<true>), dim3(q.n_spill), dim3(kThreadsMax), 0, stream, p, scores, gold, grad,
-                           loss, grad_scores);
+        KernelPlan t = p;
+        dim3 grid;
+        if ((e = spill_launch_shape(t, q.n_spill, stream, &grid)) != hipSuccess) return e;
+        if (t.team_k > 1)
+            hipLaunchKernelGGL((loss_kernel<true, true>), grid, dim3(kThreadsMax), 0, stream, t, scores, gold, grad, loss,
+                               grad_scores);
+        else
+            hipLaunchKernelGGL((loss_kernel<true>), grid, dim3(kThreadsMax), 0, stream, t, scores, gold, grad, loss,
+                               grad_scores);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     return hipSuccess;
@@ -2010,8 +2307,15 @@ hipError_t launch_parse(const KernelPlan &p, const float *scores, const float *g
         }
     }
     if (qi.n_spill + qc.n_spill > 0) {
-        hipLaunchKernelGGL(spill_parse_kernel, dim3(qi.n_spill + qc.n_spill), dim3(kThreadsMax), 0, stream, p, scores,
-                           grad, logZ, marg, spans, best);
+        KernelPlan t = p;
+        dim3 grid;
+        if ((e = spill_launch_shape(t, qi.n_spill + qc.n_spill, stream, &grid)) != hipSuccess) return e;
+        if (t.team_k > 1)
+            hipLaunchKernelGGL(spill_parse_kernel<true>, grid, dim3(kThreadsMax), 0, stream, t, scores, grad, logZ, marg,
+                               spans, best);
+        else
+            hipLaunchKernelGGL(spill_parse_kernel<false>, grid, dim3(kThreadsMax), 0, stream, t, scores, grad, logZ, marg,
+                               spans, best);
         if ((e = hipGetLastError()) != hipSuccess) return e;
     }
     return hipSuccess;

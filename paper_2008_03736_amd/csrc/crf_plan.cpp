@@ -641,6 +641,26 @@ int crf_plan_create(crf_plan **out, const int32_t *lengths_host, int32_t batch, 
         }
         kp.counter = static_cast<int32_t *>(c);
     }
+    // Teams for the workspace sentences: the workgroups the device holds at
+    // once, and the team area (none when no team of two fits).
+    kp.team_area = nullptr;
+    kp.team_cap = 0;
+    kp.team_k = 1;
+    if (!si.spill.empty() || !sc.spill.empty()) {
+        int cus = 0;
+        if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, p->device) != hipSuccess)
+            (void)hipGetLastError(), cus = 0;
+        kp.team_cap = std::max(0, cus) * crf::spill_blocks_per_cu();
+        if (kp.team_cap >= 16) {
+            void *a = nullptr;
+            if ((e = hipMalloc(&a, (size_t)crf::kTeamAreaBytes)) != hipSuccess || (p->allocations.push_back(a), false)) {
+                release(p);
+                delete p;
+                return hip_fail(e, "team area");
+            }
+            kp.team_area = static_cast<int32_t *>(a);
+        }
+    }
     kp.ws = nullptr;
     if (p->ws_bytes > 0) {
         void *ws = nullptr;

@@ -68,6 +68,7 @@ hipError_t launch_parse(const KernelPlan &, const float *, const float *, float 
     return hipErrorNotSupported;
 }
 hipError_t set_kernel_attributes(int) { return hipSuccess; }
+int spill_blocks_per_cu() { return 1; }
 int64_t biaffine_lds_bytes(int) { return 0; }
 hipError_t set_biaffine_attributes() { return hipSuccess; }
 hipError_t launch_biaffine(const KernelPlan &, const uint16_t *, const uint16_t *, const uint16_t *, int, int, int,

@@ -14,21 +14,28 @@ import pytest
 
 from paper_2008_03736_amd import build as BLD
 
-# scratch bytes per lane each kernel may use; every other kernel none.  None
-# uses any: the fused and MBR kernels (both the inside and the CKY body in one
-# persistent kernel) sit at 128 VGPRs with nothing spilled, since log Z is
-# taken without a float64 log, whose coefficients a persistent loop would
-# keep in registers (each spilled dword was stored once per lane, 1 MB of
-# HBM writes per launch).
-ALLOWED_SCRATCH = {}
+# scratch bytes per lane each kernel may use; every other kernel none.  The
+# fused and MBR kernels (both the inside and the CKY body in one persistent
+# kernel) sit at 128 VGPRs with nothing spilled, since log Z is taken without
+# a float64 log, whose coefficients a persistent loop would keep in registers
+# (each spilled dword was stored once per lane, 1 MB of HBM writes per
+# launch).  Only two team builds of the workspace kernels spill (their team
+# state and job loop beside two full sweeps); they run on launches of a few
+# long sentences, whose time is set by memory round trips.
+ALLOWED_SCRATCH = {"spill_parse_kernel<true>": 72, "loss_kernel<true, true>": 20}
 # every kernel the library launches (short names)
+# (the workspace kernels come in a lone-workgroup and a team build: the
+# last template argument)
 EXPECTED = [
-    "inside_kernel<false, false, false>", "inside_kernel<true, false, false>",
-    "inside_kernel<false, false, true>", "inside_kernel<true, false, true>",
-    "inside_kernel<false, true, false>", "inside_kernel<true, true, false>",
-    "cky_kernel<false, false>", "cky_kernel<false, true>", "cky_kernel<true, false>", "cky_kernel<true, true>",
-    "loss_kernel<false>", "loss_kernel<true>",
-    "parse_kernel", "spill_parse_kernel", "mbr_kernel",
+    "inside_kernel<false, false, false, false>", "inside_kernel<true, false, false, false>",
+    "inside_kernel<false, false, true, false>", "inside_kernel<true, false, true, false>",
+    "inside_kernel<false, true, false, false>", "inside_kernel<true, true, false, false>",
+    "inside_kernel<false, true, false, true>", "inside_kernel<true, true, false, true>",
+    "cky_kernel<false, false, false>", "cky_kernel<false, true, false>",
+    "cky_kernel<true, false, false>", "cky_kernel<true, true, false>",
+    "cky_kernel<true, false, true>", "cky_kernel<true, true, true>",
+    "loss_kernel<false, false>", "loss_kernel<true, false>", "loss_kernel<true, true>",
+    "parse_kernel", "spill_parse_kernel<false>", "spill_parse_kernel<true>", "mbr_kernel",
     "label_reduce_kernel", "label_expand_kernel", "label_spans_kernel",
 ]
 
@@ -66,7 +73,7 @@ def test_no_kernel_spills_beyond_its_budget(report):
 
 def test_inside_kernels_keep_their_occupancy(report):
     # the forward-only inside kernels fit five waves per SIMD, the others four
-    for k in ("inside_kernel<false, false, false>", "inside_kernel<false, false, true>"):
+    for k in ("inside_kernel<false, false, false, false>", "inside_kernel<false, false, true, false>"):
         assert int(report[k]["Occupancy [waves/SIMD]"]) >= 5, k
-    for k in ("inside_kernel<true, false, false>", "inside_kernel<true, false, true>", "parse_kernel"):
+    for k in ("inside_kernel<true, false, false, false>", "inside_kernel<true, false, true, false>", "parse_kernel"):
         assert int(report[k]["Occupancy [waves/SIMD]"]) >= 4, k

@@ -354,6 +354,18 @@ def test_longest_sentence(torch):
     print(f"n = 1023: max |marginal error| {worst:.2e}")
 
 
+def test_workspace_teams(torch):
+    # 16 sentences of 150..256 words: few enough that the workspace launches
+    # split each sentence pass over a team of 8 (fused, 32 passes) or 16
+    # workgroups of one XCD, several teams per XCD; every entry point against
+    # the oracle
+    lengths = [int(x) for x in np.random.default_rng(25).integers(150, 257, size=16)]
+    b = W.custom(lengths, seed=25, sd=2.0)
+    out, worst = full_check(torch, b)
+    assert out["info"]["spill_count"] == b.B
+    print(f"teams: max |marginal error| {worst:.2e}")
+
+
 def test_split_tables_in_workspace(torch):
     # sentences whose CKY chart leaves no room in half a CU for the split
     # table keep it in global memory; a longer one moves every bundle to a
