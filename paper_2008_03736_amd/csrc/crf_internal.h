@@ -472,6 +472,24 @@ constexpr int64_t kTeamAreaBytes = 4 * (int64_t)(kTeamHeaderWords + kTeamLineWor
 // once (the least over those kernels; 0 on error).
 int spill_blocks_per_cu();
 
+// Shape of a workspace launch of `jobs` sentence passes on a device that
+// holds `cap` such workgroups at once.  With a team area: m = ceil(jobs / 8)
+// teams per XCD (workgroups go to the eight XCDs in turn), k a power of two,
+// as large as cap allows up to kTeamMaxK, grid 8 m k <= cap (a team barrier
+// needs every member resident).  Without one, or with k below kTeamMinK:
+// k = 1, a workgroup per job.
+struct TeamShape {
+    int k, grid;
+};
+inline TeamShape team_shape(int jobs, int64_t cap, bool has_area) {
+    const int m = (jobs + 7) / 8;
+    int k = 1;
+    if (has_area && jobs >= 1 && 8 * m <= kTeamMaxTeams)
+        while (2 * k <= kTeamMaxK && (int64_t)8 * m * 2 * k <= cap) k *= 2;
+    if (k < kTeamMinK) return TeamShape{1, jobs};
+    return TeamShape{k, 8 * m * k};
+}
+
 // The no-allocation entry point's scratch: a file-scope device array of
 // kScratchBytes per GPU (the first kScratchCounterBytes hold the fused
 // launch's claim counter, the rest stands in for the plan's workspace).

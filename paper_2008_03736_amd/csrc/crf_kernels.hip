@@ -2110,27 +2110,15 @@ static void launch_inside_k(const KernelPlan &p, dim3 grid, int threads, size_t 
         hipLaunchKernelGGL((inside_kernel<false, SPILL, LAB, TEAM>), grid, block, lds, s, p, scores, grad, logZ, marg);
 }
 
-// Shape of a workspace launch of `jobs` sentence passes.  With a team area,
-// teams of k workgroups, k a power of two up to kTeamMaxK: m = ceil(jobs / 8)
-// teams per XCD (workgroups go to the eight XCDs in turn), k as large as the
-// workgroups the device holds at once allow (a team barrier needs every
-// member resident; the grid joins first), and the team area cleared by a
-// kernel before the launch.  Otherwise (no area, or k below kTeamMinK: many
-// workspace sentences, which fill the chip without teams) a workgroup per
-// job.
+// Sets the team size of a workspace launch (team_shape) and its grid; a
+// team launch gets its team area cleared by a kernel first.
 static hipError_t spill_launch_shape(KernelPlan &q, int jobs, hipStream_t stream, dim3 *grid) {
-    const int m = (jobs + 7) / 8;
-    int k = 1;
-    if (q.team_area != nullptr && jobs >= 1 && 8 * m <= kTeamMaxTeams)
-        while (2 * k <= kTeamMaxK && (int64_t)8 * m * 2 * k <= q.team_cap) k *= 2;
-    if (k < kTeamMinK) {
-        q.team_k = 1;
-        *grid = dim3(jobs);
-        return hipSuccess;
-    }
-    q.team_k = k;
-    *grid = dim3(8 * m * k);
-    hipLaunchKernelGGL(zero_words, dim3(1), dim3(256), 0, stream, q.team_area, kTeamHeaderWords + kTeamLineWords * 8 * m);
+    const TeamShape ts = team_shape(jobs, q.team_cap, q.team_area != nullptr);
+    q.team_k = ts.k;
+    *grid = dim3(ts.grid);
+    if (ts.k < 2) return hipSuccess;
+    hipLaunchKernelGGL(zero_words, dim3(1), dim3(256), 0, stream, q.team_area,
+                       kTeamHeaderWords + kTeamLineWords * (ts.grid / ts.k));
     return hipGetLastError();
 }
 

@@ -87,6 +87,16 @@ hipError_t launch_parse_scratch(const KernelPlan &, char *, const float *, const
 
 int main(int argc, char **argv) {
     if (argc < 2) return 2;
+    if (std::strcmp(argv[1], "teams") == 0) {   // S jobs cap k grid: the workspace launch shapes
+        for (int cap : {0, 8, 16, 32, 64, 256, 512, 1024})
+            for (int jobs = 0; jobs <= 300; ++jobs) {
+                const crf::TeamShape t = crf::team_shape(jobs, cap, true);
+                std::printf("S %d %d %d %d\n", jobs, cap, t.k, t.grid);
+            }
+        const crf::TeamShape t = crf::team_shape(5, 256, false);
+        std::printf("N %d %d\n", t.k, t.grid);
+        return 0;
+    }
     std::vector<int32_t> len;
     FILE *f = std::fopen(argv[1], "r");
     if (!f) return 2;
@@ -112,6 +122,7 @@ int main(int argc, char **argv) {
     }
     std::printf("W %d %d %d %d %lld %d\n", st.spill_count, st.cky_spill_count, st.split_ws_count, st.workspace_users,
                 (long long)st.workspace_bytes, st.fused_queue);
+    std::printf("Q %d %d\n", kp.team_cap, kp.team_area != nullptr ? 1 : 0);
     for (int b = 0; b < kp.n_mix; ++b) {
         const int32_t *r = kp.mix + (size_t)b * kp.rec_stride;
         const int n = r[crf::kRecN], count = r[crf::kRecCount], split_ws = r[crf::kRecSplitWs];

@@ -55,6 +55,8 @@ def plan_of(harness, tmp_path, lengths, labels=None):
         elif t[0] == "I":
             v = list(map(int, t[1:]))
             recs.append(dict(kind=1, n=v[0], count=v[1], ids=v[2:]))
+        elif t[0] == "Q":
+            head.update(zip(["team_cap", "team_area"], map(int, t[1:])))
         elif t[0] == "T":
             v = list(map(int, t[1:]))
             head["n1"] = v[0]
@@ -161,6 +163,38 @@ def test_workspace_users_reported(harness, tmp_path):
     # sentences past the LDS limit use it for both charts
     head, _ = plan_of(harness, tmp_path, [200, 150, 10])
     assert head["spill"] == 2 and head["cky_spill"] == 2 and head["ws_users"] == 2
+
+
+def test_team_area_only_with_workspace_sentences(harness, tmp_path):
+    # the team area (and the device's capacity for workspace workgroups: the
+    # stub's 256 CUs, one workgroup each) exists exactly when some sentence's
+    # chart is in the workspace
+    head, _ = plan_of(harness, tmp_path, [200, 150, 10])
+    assert head["team_area"] == 1 and head["team_cap"] == 256
+    head, _ = plan_of(harness, tmp_path, W.make("mixed").lengths)
+    assert head["team_area"] == 0
+
+
+def test_team_launch_shapes(harness):
+    # Every workspace launch shape: a team of k (a power of two in
+    # [kTeamMinK, kTeamMaxK] = [8, 16]) per job, m = ceil(jobs / 8) teams per
+    # XCD, the grid 8 m k within what the device holds at once; otherwise a
+    # workgroup per job.  Teams whenever the device has room for k >= 8.
+    res = subprocess.run([harness, "teams"], capture_output=True, text=True)
+    assert res.returncode == 0, res.stderr[-2000:]
+    rows = [tuple(map(int, l.split()[1:])) for l in res.stdout.splitlines() if l.startswith("S ")]
+    assert len(rows) == 8 * 301
+    for jobs, cap, k, grid in rows:
+        m = -(-jobs // 8)
+        if k == 1:
+            assert grid == jobs
+            assert jobs == 0 or 8 * m * 8 > cap        # no room for teams of 8
+        else:
+            assert k in (8, 16) and grid == 8 * m * k <= cap
+            assert 8 * m >= jobs and 8 * m <= 1024    # a team per job, within the team area
+            assert k == 16 or 8 * m * 16 > cap        # the largest team that fits
+    assert any(k > 1 for _, _, k, _ in rows)
+    assert res.stdout.splitlines()[-1] == "N 1 5"     # no team area: a workgroup per job
 
 
 @pytest.mark.parametrize("name", ["tiny", "mixed", "longer"])
