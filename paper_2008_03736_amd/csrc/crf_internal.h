@@ -281,15 +281,17 @@ constexpr bool cky_runs_match_step_shapes() {
 static_assert(cky_runs_match_step_shapes(),
               "CRF_CKY_FIXED_RUNS must list step_shape_cky's runs, with step_shape_k's reach");
 
-// The joint sweep's shapes for bundles of sentences of at most
-// kShortBundleMaxN words.  Such a bundle holds several sentences of one
-// length, so at step_shape_k's lanes per span a step takes several passes of
-// the workgroup; from 9 to 32 splits these shapes give each span half the
-// lanes with twice the splits each (C G, and so the reach of the masked reads
-// (C - MF) G, kept): fewer passes and one group-reduction level less per
-// step.  Outside 9..32 both lists run the same code (a CU running short and
-// long bundles side by side fetches one copy of it).
-constexpr int kShortBundleMaxN = 40;
+// The joint sweep's shapes for bundles whose steps take several passes of
+// the workgroup: a bundle of nb sentences of n words has nb (n + 1) spans in
+// a joint step, 4 lanes each at step_shape_k's shapes from 17 splits, and
+// short_bundle says when that exceeds the workgroup.  From 9 to 32 splits
+// these shapes give each span half the lanes with twice the splits each (C G,
+// and so the reach of the masked reads (C - MF) G, kept): fewer passes and one
+// group-reduction level less per step.  A bundle whose steps fit one pass (a
+// lone long sentence) keeps step_shape_k's shapes: its steps are latency-bound,
+// and shorter per-lane chains serve it better.  Outside 9..32 both lists run
+// the same code (a CU running both kinds of bundles fetches one copy of it).
+__host__ __device__ constexpr bool short_bundle(int nb, int n, int threads) { return nb * (n + 1) * 4 > threads; }
 __host__ __device__ constexpr StepShape step_shape_short(int K) {
     if (K <= 8 || K > 32) return step_shape_k(K);
     return K <= 16 ? StepShape{1, 16, 8} : StepShape{2, 16, 8};

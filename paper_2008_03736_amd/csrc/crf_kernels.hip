@@ -835,9 +835,9 @@ __device__ void rescale_chart(const Bundle_ctx<T> &bx, int t0, float *dsh, float
 // The joint sweep: steps t = 1..n-1 (inside widths 2..n, outside widths
 // n-1..2), one dispatch per run of steps sharing a step shape; the runs are
 // cut at the rescale points (next_rescale), each phase running the fixed list
-// of runs (with the short-bundle runs of 9..32 splits for bundles of at most
-// kShortBundleMaxN words), so that each run and the rescale appear once in
-// the code.
+// of runs (with the short-bundle runs of 9..32 splits for bundles whose
+// steps take several passes, short_bundle), so that each run and the
+// rescale appear once in the code.
 template <bool LIN, bool WIDE, bool IL, bool TEAM, typename T>
 __device__ __forceinline__ void io_sweep(const Bundle_ctx<T> &bx, float *dsh, float *dl) {
     const int n = bx.n;
@@ -848,7 +848,7 @@ __device__ __forceinline__ void io_sweep(const Bundle_ctx<T> &bx, float *dsh, fl
         if (max(lo, LO) < min(hi, HI + 1))                            \
             io_run<LIN, GG, CC, MM, IL, TEAM>(bx, max(lo, LO), min(hi, HI + 1), dsh);
         CRF_FIXED_RUNS_LOW(CRF_IO_FIXED)
-        if (!WIDE && n <= kShortBundleMaxN) {
+        if (!WIDE && short_bundle(bx.nb, n, (int)blockDim.x)) {
             CRF_SHORT_RUNS_MID(CRF_IO_FIXED)
         } else {
             CRF_FIXED_RUNS_MID(CRF_IO_FIXED)
