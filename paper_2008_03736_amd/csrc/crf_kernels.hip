@@ -685,7 +685,13 @@ __device__ __forceinline__ void fwd_sweep(const Bundle_ctx<T> &bx, float *dsh, f
 #define CRF_FWD_FIXED(LO, HI, GG, CC, MM)                                                  \
         if (max(lo, LO) < min(hi, HI + 1))                                                 \
             fwd_run<LIN, GG, CC, MM, IL, TEAM>(bx, max(lo, LO) + 1, min(hi, HI + 1) + 1, dsh);
-        CRF_FIXED_RUNS(CRF_FWD_FIXED)
+        CRF_FIXED_RUNS_LOW(CRF_FWD_FIXED)
+        if (!WIDE && short_bundle(bx.nb, n, (int)blockDim.x)) {
+            CRF_SHORT_RUNS_MID(CRF_FWD_FIXED)
+        } else {
+            CRF_FIXED_RUNS_MID(CRF_FWD_FIXED)
+        }
+        CRF_FIXED_RUNS_HIGH(CRF_FWD_FIXED)
 #undef CRF_FWD_FIXED
         for (int t = max(lo, kFixedRunsMaxK + 1); t < hi;) {
             const StepShape sh = step_shape_k(t);
