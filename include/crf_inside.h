@@ -90,6 +90,7 @@ enum {
 
 /* Plan flags. */
 #define CRF_FORCE_SPILL 0x1u  /* run every sentence on the workspace-chart kernels */
+#define CRF_NO_TEAMS 0x2u     /* one workgroup per workspace sentence pass, never teams */
 
 typedef struct crf_plan crf_plan;
 
@@ -121,7 +122,7 @@ typedef struct {
  *   batch        B >= 1.
  *   n1           padded side of the score block, 2 <= n1 <= CRF_MAX_LEN+1.
  *   num_labels   L, 1 <= L <= CRF_MAX_LABELS; 1 = unlabelled scores.
- *   flags        0 or CRF_FORCE_SPILL.
+ *   flags        0, or CRF_FORCE_SPILL and/or CRF_NO_TEAMS.
  * Uses the current HIP device; later calls must run with that device current.
  * Returns CRF_EINVAL (nothing allocated), CRF_ENOMEM or CRF_EHIP.
  */

@@ -19,6 +19,7 @@ CRF_OK, CRF_EINVAL, CRF_ENOMEM, CRF_EHIP, CRF_EUNSUPPORTED = 0, 1, 2, 3, 4
 CRF_MAX_LEN = 1023
 CRF_MAX_LABELS = 4096
 CRF_FORCE_SPILL = 0x1
+CRF_NO_TEAMS = 0x2
 
 # Every function the C header declares, with its ctypes signature.
 _P = ctypes.c_void_p

@@ -331,7 +331,7 @@ int crf_plan_create(crf_plan **out, const int32_t *lengths_host, int32_t batch, 
         return fail(CRF_EINVAL, "n1 %d outside [2, %d]", n1, CRF_MAX_LEN + 1);
     if (num_labels < 1 || num_labels > CRF_MAX_LABELS)
         return fail(CRF_EINVAL, "num_labels %d outside [1, %d]", num_labels, CRF_MAX_LABELS);
-    if (flags & ~CRF_FORCE_SPILL) return fail(CRF_EINVAL, "unknown flags 0x%x", flags);
+    if (flags & ~(CRF_FORCE_SPILL | CRF_NO_TEAMS)) return fail(CRF_EINVAL, "unknown flags 0x%x", flags);
     int32_t max_len = 0;
     for (int32_t b = 0; b < batch; ++b) {
         const int32_t n = lengths_host[b];
@@ -646,7 +646,7 @@ int crf_plan_create(crf_plan **out, const int32_t *lengths_host, int32_t batch, 
     kp.team_area = nullptr;
     kp.team_cap = 0;
     kp.team_k = 1;
-    if (!si.spill.empty() || !sc.spill.empty()) {
+    if ((!si.spill.empty() || !sc.spill.empty()) && !(flags & CRF_NO_TEAMS)) {
         int cus = 0;
         if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, p->device) != hipSuccess)
             (void)hipGetLastError(), cus = 0;

@@ -40,6 +40,7 @@ def test_constants_match_header():
     assert f"#define CRF_MAX_LEN {B.CRF_MAX_LEN}" in text
     assert f"#define CRF_MAX_LABELS {B.CRF_MAX_LABELS}" in text
     assert f"#define CRF_FORCE_SPILL 0x{B.CRF_FORCE_SPILL:x}u" in text
+    assert f"#define CRF_NO_TEAMS 0x{B.CRF_NO_TEAMS:x}u" in text
     for name, val in [("CRF_OK", 0), ("CRF_EINVAL", 1), ("CRF_ENOMEM", 2), ("CRF_EHIP", 3),
                       ("CRF_EUNSUPPORTED", 4)]:
         assert re.search(rf"\b{name} = {val}\b", text)

@@ -366,6 +366,33 @@ def test_workspace_teams(torch):
     print(f"teams: max |marginal error| {worst:.2e}")
 
 
+def test_workspace_teams_bit_identical(torch):
+    # teams split each step's lanes over workgroups but keep every span's
+    # arithmetic: every workspace entry point gives the same bits as with one
+    # workgroup per sentence pass (CRF_NO_TEAMS), LDS bundles beside them
+    b = W.custom([256, 201, 150, 143, 30, 7], seed=26, sd=2.0)
+    gold, _ = orc.cky(b.scores, b.lengths)
+    dev = torch.device("cuda", 0)
+    s = torch.from_numpy(b.scores).to(dev)
+    g = torch.from_numpy(np.ascontiguousarray(gold, np.int32)).to(dev)
+    grad = torch.tensor([1.0, -0.5, 2.0, 0.25, 1.0, 3.0], dtype=torch.float32, device=dev)
+
+    def run(flags):
+        with B.Plan(b.lengths, n1=b.n1, flags=flags, device=dev) as plan:
+            outs = [plan.inside_fwd(s), *plan.inside_fwd_bwd(s, grad_logZ=grad), *plan.cky_decode(s),
+                    *plan.parse(s), *plan.mbr_decode(s), *plan.gold_loss(s, g, grad_loss=grad)]
+            torch.cuda.synchronize()
+            info = plan.info
+        return [x.cpu().numpy() for x in outs], info
+
+    teams, info_t = run(0)
+    lone, info_l = run(B.CRF_NO_TEAMS)
+    assert info_t["spill_count"] == 4 and info_l["spill_count"] == 4
+    for i, (x, y) in enumerate(zip(teams, lone)):
+        assert np.array_equal(x, y, equal_nan=True), f"output {i} differs between teams and lone workgroups"
+    assert np.all(np.isfinite(teams[0]))
+
+
 def test_split_tables_in_workspace(torch):
     # sentences whose CKY chart leaves no room in half a CU for the split
     # table keep it in global memory; a longer one moves every bundle to a
