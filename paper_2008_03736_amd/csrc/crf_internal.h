@@ -330,14 +330,14 @@ __host__ __device__ inline int shape_run_end(int K) {
     if (K <= 64) return 65;
     if (K <= 96) return 97;
     if (K <= 128) return 129;
-    const StepShape s = step_shape_k(K);   // longer (workspace) sentences: scan
-    int k = K + 1;
-    while (k < (1 << 20)) {
-        const StepShape s2 = step_shape_k(k);
-        if (s2.G != s.G || s2.C != s.C) break;
-        ++k;
-    }
-    return k;
+    // workspace sentences: for g lanes per span (16 from 129 splits, doubling
+    // past 16 g, at most 64), 12 splits per lane up to 12 g, then 16; the
+    // widest shape never ends
+    int g = 16;
+    while (16 * g < K && g < 64) g <<= 1;
+    if (K <= 12 * g) return 12 * g + 1;
+    if (g < 64) return 16 * g + 1;
+    return 1 << 30;
 }
 
 // Cells past its span's last split that a masked split read may reach, at

@@ -87,6 +87,24 @@ hipError_t launch_parse_scratch(const KernelPlan &, char *, const float *, const
 
 int main(int argc, char **argv) {
     if (argc < 2) return 2;
+    if (std::strcmp(argv[1], "runs") == 0) {   // shape_run_end against step_shape_k, K = 1 .. 5000
+        const int top = 5000;
+        for (int K = 1; K <= top; ++K) {
+            const crf::StepShape s = crf::step_shape_k(K);
+            const int e = crf::shape_run_end(K);
+            if (e <= K) { std::printf("BAD %d end %d\n", K, e); return 1; }
+            for (int k = K; k < std::min(e, top + 1); ++k) {
+                const crf::StepShape t = crf::step_shape_k(k);
+                if (t.G != s.G || t.C != s.C || t.MF != s.MF) { std::printf("BAD %d end %d at %d\n", K, e, k); return 1; }
+            }
+            if (e <= top) {
+                const crf::StepShape t = crf::step_shape_k(e);
+                if (t.G == s.G && t.C == s.C) { std::printf("BAD %d end %d same shape\n", K, e); return 1; }
+            }
+        }
+        std::printf("RUNS OK\n");
+        return 0;
+    }
     if (std::strcmp(argv[1], "teams") == 0) {   // S jobs cap k grid: the workspace launch shapes
         for (int cap : {0, 8, 16, 32, 64, 256, 512, 1024})
             for (int jobs = 0; jobs <= 300; ++jobs) {

@@ -175,6 +175,14 @@ def test_team_area_only_with_workspace_sentences(harness, tmp_path):
     assert head["team_area"] == 0
 
 
+def test_step_shape_runs(harness):
+    # shape_run_end, the closed form the sweeps use to run a shape's steps as
+    # one loop, agrees with step_shape_k for every step up to 5000 splits:
+    # the shape holds from K to the run's end and changes there
+    res = subprocess.run([harness, "runs"], capture_output=True, text=True)
+    assert res.returncode == 0 and res.stdout.strip() == "RUNS OK", res.stdout[-500:]
+
+
 def test_team_launch_shapes(harness):
     # Every workspace launch shape: a team of k (a power of two in
     # [kTeamMinK, kTeamMaxK] = [8, 16]) per job, m = ceil(jobs / 8) teams per
