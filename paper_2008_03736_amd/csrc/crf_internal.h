@@ -463,9 +463,10 @@ constexpr int kTeamMaxK = 16;
 // Smallest team a launch forms.  A workspace step is bound by its memory
 // round trips (operand loads, store acknowledgements, the team's arrival),
 // not by one CU's issue, and a team reads the chart past its L1: teams pay
-// where a few long sentences leave most of the chip idle (a lone 512-word
-// sentence 7.1 -> 2.2 ms at k = 8), not on batches that fill it (64 sentences
-// of 256 words: 1.7 ms alone, 2.7 ms in teams of two).
+// where a few long sentences leave most of the chip idle (fused parse of a
+// lone 512-word sentence 7.0 -> 2.1 ms, of a 1023-word one 60 -> 7.6 ms, at
+// k = 16), not on batches that fill it (64 sentences of 256 words: 1.7 ms
+// alone, 2.7 ms in teams of two).
 constexpr int kTeamMinK = 8;
 constexpr int kTeamHeaderWords = 64, kTeamLineWords = 64;
 constexpr int kTeamMaxTeams = 1024;
