@@ -48,8 +48,11 @@
  *   workgroups of one XCD that wait for each other at every width step.
  *   Such a launch waits until all its workgroups are resident at once (it
  *   is sized to fit an otherwise idle device); work from other streams
- *   delays it.  A wait that lasts about 2^24 polls ends the launch, and the
- *   log Z (and best score) of its workspace sentences are NaN.  Results are
+ *   delays it.  A wait that lasts about 2^21 polls (a second or two) ends
+ *   the launch, and the log Z (and best score) of its workspace sentences
+ *   are NaN.  Two plans' team launches running at once on different streams
+ *   can hold each other's room that way: issue calls that may form teams on
+ *   one stream, or create the plans with CRF_NO_TEAMS.  Results are
  *   bit-identical to those of one workgroup per pass.
  *
  *   Streams.  `stream` is a hipStream_t (NULL = the null stream).  Compute
@@ -60,7 +63,8 @@
  *   and CKY split tables of sentences too long for LDS (crf_plan_info:
  *   workspace_users) and the team area -- and two overlapping calls would
  *   share it.  Different
- *   plans share nothing and may run concurrently on any streams.
+ *   plans share nothing and may run concurrently on any streams (but see
+ *   Teams below for calls with a few workspace sentences).
  *
  *   Errors.  Every call returns a status (CRF_OK = 0).  Arguments are checked
  *   on the host before any HIP call is made, so a rejected call has no effect

@@ -223,10 +223,11 @@ struct Team {
     int job = 0;               // jobs this team has started
 };
 
-// A wait that lasts this many polls sets the abort flag; from then on no team
-// barrier of the launch waits (the outputs of its workspace sentences are
-// NaN).  Only a grid that is not resident at once can take that long.
-constexpr int kTeamSpin = 1 << 24;
+// A wait that lasts this many polls (a second or two) sets the abort flag;
+// from then on no team barrier of the launch waits (the outputs of its
+// workspace sentences are NaN).  Only a grid that is not resident at once
+// can take that long.
+constexpr int kTeamSpin = 1 << 21;
 
 __device__ __forceinline__ int load_coherent(const int32_t *q) {
     return __hip_atomic_load(q, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
