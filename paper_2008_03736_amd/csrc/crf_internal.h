@@ -291,6 +291,8 @@ static_assert(cky_runs_match_step_shapes(),
 // lone long sentence) keeps step_shape_k's shapes: its steps are latency-bound,
 // and shorter per-lane chains serve it better.  Outside 9..32 both lists run
 // the same code (a CU running both kinds of bundles fetches one copy of it).
+// The labelled bundle kernel keeps step_shape_k's shapes throughout: beside
+// its bundles' own label work the multi-pass shapes measured 1% slower.
 __host__ __device__ constexpr bool short_bundle(int nb, int n, int threads) { return nb * (n + 1) * 4 > threads; }
 __host__ __device__ constexpr StepShape step_shape_short(int K) {
     if (K <= 8 || K > 32) return step_shape_k(K);

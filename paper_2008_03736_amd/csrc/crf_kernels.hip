@@ -677,7 +677,7 @@ __device__ void rescale_chart(const Bundle_ctx<T> &bx, int t0, float *dsh, float
 // WIDE: workspace charts (longer sentences), which may need 16 terms per lane.
 // IL: interleaved span numbering (lane_at).
 // dl: per-sentence scratch for the rescales.
-template <bool LIN, bool WIDE, bool IL, bool TEAM, typename T>
+template <bool LIN, bool WIDE, bool IL, bool TEAM, bool MULTI = true, typename T>
 __device__ __forceinline__ void fwd_sweep(const Bundle_ctx<T> &bx, float *dsh, float *dl) {
     const int n = bx.n;
     for (int lo = 1; lo < n;) {
@@ -687,7 +687,7 @@ __device__ __forceinline__ void fwd_sweep(const Bundle_ctx<T> &bx, float *dsh, f
         if (max(lo, LO) < min(hi, HI + 1))                                                 \
             fwd_run<LIN, GG, CC, MM, IL, TEAM>(bx, max(lo, LO) + 1, min(hi, HI + 1) + 1, dsh);
         CRF_FIXED_RUNS_LOW(CRF_FWD_FIXED)
-        if (!WIDE && short_bundle(bx.nb, n, (int)blockDim.x)) {
+        if (MULTI && !WIDE && short_bundle(bx.nb, n, (int)blockDim.x)) {
             CRF_SHORT_RUNS_MID(CRF_FWD_FIXED)
         } else {
             CRF_FIXED_RUNS_MID(CRF_FWD_FIXED)
@@ -845,7 +845,7 @@ __device__ void rescale_chart(const Bundle_ctx<T> &bx, int t0, float *dsh, float
 // of runs (with the short-bundle runs of 9..32 splits for bundles whose
 // steps take several passes, short_bundle), so that each run and the
 // rescale appear once in the code.
-template <bool LIN, bool WIDE, bool IL, bool TEAM, typename T>
+template <bool LIN, bool WIDE, bool IL, bool TEAM, bool MULTI = true, typename T>
 __device__ __forceinline__ void io_sweep(const Bundle_ctx<T> &bx, float *dsh, float *dl) {
     const int n = bx.n;
     for (int lo = 1; lo < n;) {
@@ -855,7 +855,7 @@ __device__ __forceinline__ void io_sweep(const Bundle_ctx<T> &bx, float *dsh, fl
         if (max(lo, LO) < min(hi, HI + 1))                            \
             io_run<LIN, GG, CC, MM, IL, TEAM>(bx, max(lo, LO), min(hi, HI + 1), dsh);
         CRF_FIXED_RUNS_LOW(CRF_IO_FIXED)
-        if (!WIDE && short_bundle(bx.nb, n, (int)blockDim.x)) {
+        if (MULTI && !WIDE && short_bundle(bx.nb, n, (int)blockDim.x)) {
             CRF_SHORT_RUNS_MID(CRF_IO_FIXED)
         } else {
             CRF_FIXED_RUNS_MID(CRF_IO_FIXED)
@@ -1240,14 +1240,14 @@ __device__ __forceinline__ bool inside_block_impl(const KernelPlan &p, int block
         if constexpr (SPILL) {
             if (tm.k > 1) fwd_sweep<LIN, true, false, true>(bx, dsh, gv);
             else fwd_sweep<LIN, true, false, false>(bx, dsh, gv);
-        } else if (lay.e == 0) fwd_sweep<LIN, false, true, false>(bx, dsh, gv);
-        else fwd_sweep<LIN, false, false, false>(bx, dsh, gv);
+        } else if (lay.e == 0) fwd_sweep<LIN, false, true, false, !LAB>(bx, dsh, gv);
+        else fwd_sweep<LIN, false, false, false, !LAB>(bx, dsh, gv);
     } else {
         if constexpr (SPILL) {
             if (tm.k > 1) io_sweep<LIN, true, false, true>(bx, dsh, gv);
             else io_sweep<LIN, true, false, false>(bx, dsh, gv);
-        } else if (lay.e == 0) io_sweep<LIN, false, true, false>(bx, dsh, gv);
-        else io_sweep<LIN, false, false, false>(bx, dsh, gv);
+        } else if (lay.e == 0) io_sweep<LIN, false, true, false, !LAB>(bx, dsh, gv);
+        else io_sweep<LIN, false, false, false, !LAB>(bx, dsh, gv);
     }
     // (the sweep's last barrier published the chart and the flag)
     if constexpr (LIN) {
