@@ -49,8 +49,9 @@
  *   Such a launch waits until all its workgroups are resident at once (it
  *   is sized to fit an otherwise idle device); work from other streams
  *   delays it.  A wait that lasts about 2^21 polls (a second or two) ends
- *   the launch, and the log Z (and best score) of its workspace sentences
- *   are NaN.  Two plans' team launches running at once on different streams
+ *   the launch, and the outputs of its workspace sentences are invalid: log
+ *   Z and best score NaN when a width step's wait ran out, left unwritten
+ *   when the launch's workgroups never were resident together.  Two plans' team launches running at once on different streams
  *   can hold each other's room that way: issue calls that may form teams on
  *   one stream, or create the plans with CRF_NO_TEAMS.  Results are
  *   bit-identical to those of one workgroup per pass.

@@ -224,9 +224,10 @@ struct Team {
 };
 
 // A wait that lasts this many polls (a second or two) sets the abort flag;
-// from then on no team barrier of the launch waits (the outputs of its
-// workspace sentences are NaN).  Only a grid that is not resident at once
-// can take that long.
+// from then on no team barrier of the launch waits (the log Z and best
+// score of its workspace sentences are NaN; a grid that never assembled
+// forms no team and writes nothing).  Only a grid that is not resident at
+// once can take that long.
 constexpr int kTeamSpin = 1 << 21;
 
 __device__ __forceinline__ int load_coherent(const int32_t *q) {
