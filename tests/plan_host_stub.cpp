@@ -125,7 +125,8 @@ int main(int argc, char **argv) {
     for (int v : len) n1 = std::max(n1, v + 1);
     crf_plan *p = nullptr;
     const int labels = argc > 2 ? std::atoi(argv[2]) : 1;
-    const int rc = crf_plan_create(&p, len.data(), (int32_t)len.size(), n1, labels, 0);
+    const uint32_t flags = argc > 3 ? (uint32_t)std::atoi(argv[3]) : 0u;
+    const int rc = crf_plan_create(&p, len.data(), (int32_t)len.size(), n1, labels, flags);
     if (rc != CRF_OK) {
         std::printf("E %d\n", rc);
         return 1;

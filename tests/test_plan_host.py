@@ -32,10 +32,10 @@ def harness(tmp_path_factory):
     return out
 
 
-def plan_of(harness, tmp_path, lengths, labels=None):
+def plan_of(harness, tmp_path, lengths, labels=None, flags=0):
     f = tmp_path / "lengths.txt"
     f.write_text("\n".join(str(int(v)) for v in lengths))
-    args = [harness, str(f)] + ([str(labels)] if labels is not None else [])
+    args = [harness, str(f), str(labels if labels is not None else 1), str(flags)]
     env = dict(os.environ, ASAN_OPTIONS="detect_leaks=1:abort_on_error=0", UBSAN_OPTIONS="print_stacktrace=1")
     res = subprocess.run(args, capture_output=True, text=True, env=env)
     assert res.returncode == 0, res.stdout[-2000:] + res.stderr[-4000:]
@@ -173,6 +173,9 @@ def test_team_area_only_with_workspace_sentences(harness, tmp_path):
     assert head["team_area"] == 1 and head["team_cap"] == 256
     head, _ = plan_of(harness, tmp_path, W.make("mixed").lengths)
     assert head["team_area"] == 0
+    # CRF_NO_TEAMS (0x2): workspace sentences, no team area
+    head, _ = plan_of(harness, tmp_path, [200, 150, 10], flags=2)
+    assert head["team_area"] == 0 and head["spill"] == 2
 
 
 def test_step_shape_runs(harness):
